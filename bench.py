@@ -1,0 +1,201 @@
+"""Benchmark: k-MIP attention forward + backward on one MI355X.
+
+Default workload: one graph of N = 500,000 nodes, H = 4 heads of d = 16,
+k = 32 (xyz point-cloud features), forward (score+select, then
+gather-softmax-aggregate) and backward (index set held fixed).  A step is one
+pass of all of it over the inputs, which are resident in HBM before the timed
+region starts.
+
+Prints ONE JSON line on stdout.  Extra detail goes to stderr.
+  value        whole-job node-queries per second (N / step time; every head)
+  roofline     the score+select kernel against the bf16 MFMA peak, from HIP
+               events recorded around it on its own stream
+  cpu_baseline the float64 CPU oracle on a bounded sample of the same
+               workload (not an optimisation target)
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "k-MIP attn fwd+bwd queries/s and score TFLOP/s (% bf16 MFMA peak) at N=500k"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=5)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--config", type=int, default=4, help="workload 1..5 (default 4: N=500k)")
+    p.add_argument("--n", type=int, default=None, help="override N (c2: number of graphs)")
+    p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--cpu-sample", type=int, default=2048, help="query-heads in the oracle sample")
+    return p.parse_args()
+
+
+def cpu_baseline(w, sample):
+    """Oracle on a seeded sample of query-heads: full-sort selection and the
+    aggregate for those rows, plus the backward over the whole batch on a
+    fixed index set (it is O(N H k d), a few seconds).  Returns queries/s."""
+    import numpy as np
+    import oracle
+
+    Qd, Kd, Vd, dOd = (oracle.from_bf16(getattr(w, n)) for n in ("q", "kk", "v", "dout"))
+    rng = np.random.default_rng(1)
+    m = min(sample, w.N * w.H)
+    sel = np.sort(rng.choice(w.N * w.H, size=m, replace=False))
+    t0 = time.perf_counter()
+    idx, _, _ = oracle.topk(Qd, Kd, w.k, offsets=w.offsets, sel=sel)
+    oracle.attend(Qd, Kd, Vd, idx, w.scale, sel=sel)
+    t_fwd = time.perf_counter() - t0
+    # backward on a fixed, valid index set for every query (the first k keys
+    # of each graph): its cost does not depend on which keys were selected
+    lo = np.zeros(w.N, np.int64) if w.offsets is None else np.repeat(
+        w.offsets[:-1].astype(np.int64), np.diff(w.offsets))
+    base = (lo[:, None, None] + np.arange(w.k)[None, None, :]).astype(np.int32)
+    full_idx = np.broadcast_to(base, (w.N, w.H, w.k)).copy()
+    t0 = time.perf_counter()
+    oracle.backward(Qd, Kd, Vd, dOd, full_idx, w.scale)
+    t_bwd = time.perf_counter() - t0
+    per_query = w.H * t_fwd / m + t_bwd / w.N
+    return {
+        "value": 1.0 / per_query, "unit": "queries/s", "cores": oracle.threads(), "kind": "oracle",
+        "sample": (f"full-sort top-k + aggregate on {m} seeded query-heads of the same workload "
+                   f"({t_fwd:.2f} s), backward on all {w.N * w.H} query-heads ({t_bwd:.2f} s); "
+                   f"per node-query cost = H*fwd/query-head + bwd/node"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the k-MIP path here is single-GPU; see DESIGN.md for how it would shard)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2604_03815_amd as kmip
+    import workloads
+
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    w = workloads.make(args.config, seed=args.seed, n=args.n)
+    log(f"[bench] workload c{args.config}: N={w.N} H={w.H} d={w.d} k={w.k} graphs={w.num_graphs} "
+        f"(generated in {time.perf_counter() - t0:.1f} s)")
+
+    def dev_t(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q, k, v = dev_t(w.q), dev_t(w.kk), dev_t(w.v)
+    g = dev_t(w.dout) if w.dout is not None else None
+    N, H, d, kk = w.N, w.H, w.d, w.k
+    idx = torch.empty((N, H, kk), dtype=torch.int32, device=dev)
+    out = torch.empty((N, H, d), dtype=torch.float32, device=dev)
+    lse = torch.empty((N, H), dtype=torch.float32, device=dev)
+    dq, dk, dv = (torch.empty((N, H, d), dtype=torch.float32, device=dev) for _ in range(3))
+    ws = kmip.Workspace(dev)
+    ws.get(kmip.topk_workspace_size(N, H, d, kk, w.num_graphs))
+    backward = w.backward and g is not None
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        kmip.topk(q, k, kk, graph_offsets=w.offsets, idx=idx, workspace=ws)
+        if ev is not None:
+            ev[1].record()
+        kmip.attend(q, k, v, idx, w.scale, out=out, lse=lse)
+        if ev is not None:
+            ev[2].record()
+        if backward:
+            kmip.bwd(q, k, v, g, idx, lse, w.scale, dq=dq, dk=dk, dv=dv)
+        if ev is not None:
+            ev[3].record()
+
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats(dev)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    t_total = time.perf_counter() - t0
+    peak_mem = torch.cuda.max_memory_allocated(dev)
+
+    t_sel = [e[0].elapsed_time(e[1]) for e in evs]
+    t_att = [e[1].elapsed_time(e[2]) for e in evs]
+    t_bwd = [e[2].elapsed_time(e[3]) for e in evs]
+    ms_step = 1e3 * t_total / args.steps
+    sel_ms = sum(t_sel) / len(t_sel)
+    pairs = w.score_pairs()
+    flops = 2.0 * H * pairs * d
+    tflops = flops / (sel_ms * 1e-3) / 1e12
+    log(f"[bench] per step: select {sel_ms:.3f} ms, attend {sum(t_att) / len(t_att):.3f} ms, "
+        f"backward {sum(t_bwd) / len(t_bwd):.3f} ms, wall {ms_step:.3f} ms")
+    log(f"[bench] score rate {tflops:.1f} TFLOP/s = {100 * tflops / PEAK_BF16_TFLOPS:.1f}% of bf16 peak; "
+        f"peak memory {peak_mem / 2**20:.1f} MiB ({peak_mem / N:.0f} B/node)")
+
+    cpu = None
+    if not args.no_cpu:
+        t0 = time.perf_counter()
+        cpu = cpu_baseline(w, args.cpu_sample)
+        log(f"[bench] cpu oracle baseline: {cpu['value']:.1f} queries/s on {cpu['cores']} threads "
+            f"({time.perf_counter() - t0:.1f} s)")
+
+    result = {
+        "metric": METRIC,
+        "value": N / (ms_step * 1e-3),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"c{args.config}: {w.notes}; single MI355X; "
+                         f"{'forward+backward' if backward else 'forward only'}"),
+            "N": N, "H": H, "d": d, "k": kk, "graphs": w.num_graphs, "score_pairs_per_head": pairs,
+            "seed": args.seed, "parallelism": "single GPU",
+        },
+        "score_tflops": tflops,
+        "score_pct_bf16_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
+        "kernel_ms": {"select": sel_ms, "attend": sum(t_att) / len(t_att),
+                      "backward": sum(t_bwd) / len(t_bwd) if backward else 0.0},
+        "peak_mem_bytes": peak_mem,
+        "roofline": {
+            "bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": tflops / PEAK_BF16_TFLOPS, "traffic": None,
+            "kernel": "select_kernel (score+select), incl. the K tiling pass in the timed call",
+            "algorithmic": f"2*H*sum(n_g^2)*d = {flops:.4g} FLOP per launch",
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,134 @@
+/*
+ * kmip.h -- C ABI of the MI355X (gfx950) k-MIP self-attention library.
+ *
+ * k-Maximum Inner Product attention (arXiv 2604.03815, Section 3.1, Eq. 1;
+ * Algorithm 1 in Appendix E): for every query node i and head h, score i
+ * against every key node j of the query's own graph (s_ij = q_i . k_j),
+ * keep the k largest scores, take a softmax over the k kept scores times
+ * `scale`, and sum the matching value rows.  The N x N score matrix is never
+ * stored (the symbolic-matrix idea of Appendix F): memory is linear in N.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Q, K, V, dOut: bfloat16, device memory, layout [N, H, d] row-major
+ *    (node-major: element (i, h, t) at ((i * H) + h) * d + t).
+ *  - out, dQ, dK, dV: float32, device memory, layout [N, H, d].
+ *  - topk_idx: int32, device memory, [N, H, k].  Global 0-based node ids,
+ *    ordered by (score descending, node id ascending).  When the query's
+ *    graph has n < k nodes, slots n..k-1 hold -1.
+ *  - lse: float32, device memory, [N, H]: natural log of
+ *    sum_{j kept} exp(scale * s_ij).
+ *  - graph_offsets: HOST memory, int32 [num_graphs + 1], o_0 = 0,
+ *    non-decreasing, o_G = N.  Query i of graph g attends only to keys in
+ *    [o_g, o_{g+1}) (block-diagonal batching of many graphs).  NULL means a
+ *    single graph of N nodes (num_graphs is then ignored).  Empty graphs are
+ *    allowed.
+ *  - Ties between equal scores go to the lower node id.  The query's own
+ *    key is a candidate.  `scale` must be finite and > 0; selection uses the
+ *    raw scores, which for scale > 0 is the same as the scaled scores.
+ *  - Supported sizes: d in {16, 32, 64}; 1 <= k <= 128; H >= 1;
+ *    0 <= N < 2^31 and N * H * max(d, k) < 2^31.
+ *  - stream: a hipStream_t (NULL = the default stream).  Every call is
+ *    asynchronous on `stream`; the caller synchronises.
+ *  - Ownership: the caller allocates every buffer (inputs, outputs and the
+ *    workspace); the library allocates no device memory and keeps no state
+ *    between calls.  Outputs are overwritten, never accumulated.
+ *  - Errors: arguments are validated on the host before any launch; on
+ *    error nothing is launched and outputs are untouched.  Index entries
+ *    read by kmip_attend / kmip_bwd that fall outside [0, N) are treated as
+ *    empty slots, never dereferenced.  NaN or Inf in the inputs, or scores
+ *    that overflow float32, give undefined (but memory-safe) results.
+ *    No exception crosses the ABI.
+ */
+#ifndef KMIP_H_
+#define KMIP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    KMIP_OK = 0,
+    KMIP_ERR_INVALID_ARG = 1, /* null buffer, bad size, bad offsets, bad scale */
+    KMIP_ERR_UNSUPPORTED = 2, /* d or k outside the compiled set */
+    KMIP_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
+    KMIP_ERR_HIP = 4          /* a HIP launch or copy failed; see kmip_last_error() */
+} kmip_status_t;
+
+#define KMIP_MAX_K 128
+
+/*
+ * Bytes of device workspace kmip_topk / kmip_fwd need for these sizes
+ * (0 if the sizes are invalid).  Holds a tiled copy of K and, for more than
+ * one graph, the work list.
+ */
+size_t kmip_topk_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t num_graphs);
+
+/*
+ * Score + select (Algorithm 1: SymbolicMultiply followed by RowwiseTopK;
+ * Appendix F).  For every query and head, streams the keys of the query's
+ * graph, forms bf16 score tiles on the matrix cores with fp32 accumulation,
+ * and keeps the k best (score, index) pairs on chip.
+ *   out: topk_idx [N, H, k].
+ *   workspace: device memory of at least kmip_topk_workspace_size() bytes,
+ *   256-byte aligned; its contents on entry do not matter.
+ */
+kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offsets,
+                        int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
+                        int32_t* topk_idx, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/*
+ * Gather-softmax-aggregate (Algorithm 1: GatherRows, softmax over the k kept
+ * scores divided by sqrt(d_K) -- here times `scale` -- and the einsum
+ * nk,nkv->nv).  Recomputes the k kept scores in fp32 from Q and the gathered
+ * K rows, then sums the gathered V rows.  Needs no workspace.
+ *   in:  topk_idx [N, H, k] (e.g. from kmip_topk; -1 marks an empty slot).
+ *   out: out [N, H, d], lse [N, H].  A query with no valid slot gets
+ *        out = 0 and lse = -inf.
+ */
+kmip_status_t kmip_attend(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
+                          int32_t d, int32_t k, float scale, const int32_t* topk_idx,
+                          float* out, float* lse, void* stream);
+
+/* kmip_topk followed by kmip_attend on the same stream; same workspace as kmip_topk. */
+size_t kmip_fwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t num_graphs);
+kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
+                       int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
+                       float scale, float* out, int32_t* topk_idx, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Backward with the forward's index set held fixed (Section 3.1, last
+ * paragraph, and Appendix E, last paragraph: the top-k indices are reused,
+ * so only the k selected pairs of each query carry gradient).  With p_j the
+ * softmax weights of query i (recomputed from Q, K, topk_idx and lse):
+ *   dp_j = dOut_i . v_j,  D_i = sum_j p_j dp_j,  g_j = p_j (dp_j - D_i),
+ *   dQ_i = scale sum_j g_j k_j,  dK_j += scale g_j q_i,  dV_j += p_j dOut_i.
+ *   in:  dOut bf16 [N, H, d]; topk_idx [N, H, k] and lse [N, H] as written
+ *        by the forward.
+ *   out: dQ, dK, dV float32 [N, H, d], overwritten.
+ *   variant: 0 = library's choice, 1 = scatter with fp32 atomics
+ *            (summation order not fixed), others reserved (UNSUPPORTED).
+ *   workspace: kmip_bwd_workspace_size() bytes (currently 0; may be NULL).
+ */
+size_t kmip_bwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t variant);
+kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* dOut,
+                       const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
+                       int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
+                       int32_t variant, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* kmip_status_string(kmip_status_t status);
+
+/* Detail of the last error on the calling host thread ("" if none). */
+const char* kmip_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KMIP_H_ */

@@ -48,7 +48,8 @@ def _load():
         lib.oracle_forward.argtypes = [P, P, P, P, i32, i64, i32, i32, i32, f64, P, P, P]
         lib.oracle_backward.argtypes = [P, P, P, P, i64, i32, i32, i32, f64, P, P, P, P]
         lib.oracle_check_set.argtypes = [P, P, P, i32, i64, i32, i32, i32, i64, P, P, P, P, P]
-        for f in ("oracle_topk", "oracle_attend", "oracle_forward", "oracle_backward",
+        lib.oracle_threads.argtypes = []
+        for f in ("oracle_threads", "oracle_topk", "oracle_attend", "oracle_forward", "oracle_backward",
                   "oracle_check_set"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
@@ -172,3 +173,8 @@ def check_set(Q, K, idx, offsets=None, sel=None):
     _load().oracle_check_set(_ptr(Q), _ptr(K), _ptr(o), G, N, H, d, k, n, _ptr(s), _ptr(idx),
                              _ptr(mn), _ptr(mx), _ptr(fl))
     return mn, mx, fl
+
+
+def threads() -> int:
+    """OpenMP threads the oracle runs on."""
+    return int(_load().oracle_threads())

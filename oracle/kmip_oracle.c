@@ -34,6 +34,7 @@
  * rounding, so the oracle sees the same numbers as the GPU path.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -355,3 +356,6 @@ int oracle_check_set(const double* Q, const double* K, const int32_t* offsets, i
     }
     return 0;
 }
+
+/* Number of OpenMP threads the functions above use. */
+int oracle_threads(void) { return omp_get_max_threads(); }

@@ -1,0 +1,235 @@
+// Host side of the kmip C ABI (declared in include/kmip.h): argument
+// validation, workspace layout, the block-diagonal work list and launches.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "kmip.h"
+#include "kmip_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+kmip_status_t fail(kmip_status_t s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+kmip_status_t ok() {
+    g_last_error.clear();
+    return KMIP_OK;
+}
+
+kmip_status_t hip_fail(hipError_t e, const char* what) {
+    return fail(KMIP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Sizes shared by all entry points.
+kmip_status_t check_sizes(int64_t N, int32_t H, int32_t d, int32_t k) {
+    if (N < 0 || N >= (int64_t(1) << 31)) return fail(KMIP_ERR_INVALID_ARG, "N=%lld out of range", (long long)N);
+    if (H < 1) return fail(KMIP_ERR_INVALID_ARG, "H=%d must be >= 1", H);
+    if (k < 1) return fail(KMIP_ERR_INVALID_ARG, "k=%d must be >= 1", k);
+    if (d != 16 && d != 32 && d != 64) return fail(KMIP_ERR_UNSUPPORTED, "d=%d not in {16, 32, 64}", d);
+    if (k > KMIP_MAX_K) return fail(KMIP_ERR_UNSUPPORTED, "k=%d exceeds %d", k, KMIP_MAX_K);
+    const int64_t wide = N * (int64_t)H * std::max<int64_t>(d, k);
+    if (wide >= (int64_t(1) << 31)) return fail(KMIP_ERR_INVALID_ARG, "N*H*max(d,k) >= 2^31");
+    return KMIP_OK;
+}
+
+kmip_status_t check_scale(float scale) {
+    if (!std::isfinite(scale) || !(scale > 0.0f)) return fail(KMIP_ERR_INVALID_ARG, "scale must be finite and > 0");
+    return KMIP_OK;
+}
+
+kmip_status_t check_offsets(const int32_t* off, int32_t G, int64_t N) {
+    if (off == nullptr) return KMIP_OK;
+    if (G < 1) return fail(KMIP_ERR_INVALID_ARG, "num_graphs=%d must be >= 1 with offsets", G);
+    if (off[0] != 0) return fail(KMIP_ERR_INVALID_ARG, "graph_offsets[0]=%d must be 0", off[0]);
+    for (int32_t g = 0; g < G; ++g)
+        if (off[g + 1] < off[g]) return fail(KMIP_ERR_INVALID_ARG, "graph_offsets decrease at %d", g);
+    if (off[G] != N) return fail(KMIP_ERR_INVALID_ARG, "graph_offsets[G]=%d != N=%lld", off[G], (long long)N);
+    return KMIP_OK;
+}
+
+int32_t num_tiles(int64_t N) { return (int32_t)((N + 31) / 32); }
+
+size_t packed_k_bytes(int64_t N, int32_t H, int32_t d) {
+    return (size_t)H * (size_t)num_tiles(N) * 32 * (size_t)d * 2;
+}
+
+// Upper bound on the work-list length for any query-block size.
+size_t max_tasks(int64_t N, int32_t G) { return (size_t)(N / 32 + G + 1); }
+
+// Query blocks of 32 per wave: two when k is small and there are enough
+// items to fill the chip, one otherwise (bounded by LDS per workgroup).
+int32_t choose_qb(int64_t N, int32_t H, int32_t k, int32_t G) {
+    if (k > 32) return 1;
+    const int64_t items = (N + 63) / 64 * H;
+    return (items >= 8192 && G == 1) ? 2 : 1;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* kmip_status_string(kmip_status_t s) {
+    switch (s) {
+        case KMIP_OK: return "ok";
+        case KMIP_ERR_INVALID_ARG: return "invalid argument";
+        case KMIP_ERR_UNSUPPORTED: return "unsupported size";
+        case KMIP_ERR_WORKSPACE: return "workspace missing or too small";
+        case KMIP_ERR_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+const char* kmip_last_error(void) { return g_last_error.c_str(); }
+
+size_t kmip_topk_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t num_graphs) {
+    if (check_sizes(N, H, d, k) != KMIP_OK) return 0;
+    const int32_t G = num_graphs < 1 ? 1 : num_graphs;
+    size_t bytes = align_up(packed_k_bytes(N, H, d));
+    if (G > 1) bytes += align_up(max_tasks(N, G) * sizeof(kmip::Task));
+    return bytes;
+}
+
+size_t kmip_fwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t num_graphs) {
+    return kmip_topk_workspace_size(N, H, d, k, num_graphs);
+}
+
+kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offsets,
+                        int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
+                        int32_t* topk_idx, void* workspace, size_t workspace_bytes,
+                        void* stream_) {
+    kmip_status_t s = check_sizes(N, H, d, k);
+    if (s != KMIP_OK) return s;
+    if ((s = check_offsets(graph_offsets, num_graphs, N)) != KMIP_OK) return s;
+    if (N == 0) return ok();
+    if (!Q || !K || !topk_idx) return fail(KMIP_ERR_INVALID_ARG, "null Q, K or topk_idx");
+    if (!aligned16(Q) || !aligned16(K)) return fail(KMIP_ERR_INVALID_ARG, "Q and K must be 16-byte aligned");
+    const int32_t G = graph_offsets ? num_graphs : 1;
+    const size_t need = kmip_topk_workspace_size(N, H, d, k, G);
+    if (workspace == nullptr || workspace_bytes < need)
+        return fail(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
+    if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0)
+        return fail(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+
+    const int32_t n32 = (int32_t)N;
+    const int32_t ntiles = num_tiles(N);
+    char* ws = reinterpret_cast<char*>(workspace);
+    void* kp = ws;
+    const int32_t qb = choose_qb(N, H, k, G);
+
+    const kmip::Task* dtasks = nullptr;
+    int32_t ntasks = 0;
+    if (G > 1) {
+        // Block-diagonal batch: one task per run of 32*qb queries of a graph,
+        // heaviest first (cost ~ queries x keys) to balance the tail.
+        std::vector<kmip::Task> tasks;
+        tasks.reserve(max_tasks(N, G));
+        const int32_t step = 32 * qb;
+        for (int32_t g = 0; g < G; ++g) {
+            const int32_t lo = graph_offsets[g], hi = graph_offsets[g + 1];
+            for (int32_t q0 = lo; q0 < hi; q0 += step)
+                tasks.push_back(kmip::Task{q0, std::min(step, hi - q0), lo, hi});
+        }
+        std::stable_sort(tasks.begin(), tasks.end(), [](const kmip::Task& a, const kmip::Task& b) {
+            return (int64_t)a.q_count * (a.key_hi - a.key_lo) > (int64_t)b.q_count * (b.key_hi - b.key_lo);
+        });
+        ntasks = (int32_t)tasks.size();
+        void* dst = ws + align_up(packed_k_bytes(N, H, d));
+        hipError_t e = hipMemcpyAsync(dst, tasks.data(), tasks.size() * sizeof(kmip::Task),
+                                      hipMemcpyHostToDevice, stream);
+        if (e != hipSuccess) return hip_fail(e, "work list upload");
+        dtasks = reinterpret_cast<const kmip::Task*>(dst);
+    } else {
+        ntasks = (int32_t)((N + 32 * qb - 1) / (32 * qb));
+    }
+
+    hipError_t e = kmip::launch_pack_k(K, kp, n32, H, d, ntiles, stream);
+    if (e != hipSuccess) return hip_fail(e, "pack_k launch");
+    e = kmip::launch_select(kp, Q, dtasks, ntasks, n32, H, d, k, ntiles, qb, topk_idx, stream);
+    if (e != hipSuccess) return hip_fail(e, "select launch");
+    return ok();
+}
+
+kmip_status_t kmip_attend(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
+                          int32_t d, int32_t k, float scale, const int32_t* topk_idx, float* out,
+                          float* lse, void* stream_) {
+    kmip_status_t s = check_sizes(N, H, d, k);
+    if (s != KMIP_OK) return s;
+    if ((s = check_scale(scale)) != KMIP_OK) return s;
+    if (N == 0) return ok();
+    if (!Q || !K || !V || !topk_idx || !out || !lse)
+        return fail(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_attend");
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V))
+        return fail(KMIP_ERR_INVALID_ARG, "Q, K and V must be 16-byte aligned");
+    hipError_t e = kmip::launch_attend(Q, K, V, topk_idx, (int32_t)N, H, d, k, scale, out, lse,
+                                       reinterpret_cast<hipStream_t>(stream_));
+    if (e != hipSuccess) return hip_fail(e, "attend launch");
+    return ok();
+}
+
+kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
+                       int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
+                       float scale, float* out, int32_t* topk_idx, float* lse, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+    kmip_status_t s = check_sizes(N, H, d, k);
+    if (s != KMIP_OK) return s;
+    if ((s = check_scale(scale)) != KMIP_OK) return s;
+    if (N > 0 && (!V || !out || !lse)) return fail(KMIP_ERR_INVALID_ARG, "null V, out or lse");
+    if (N > 0 && !aligned16(V)) return fail(KMIP_ERR_INVALID_ARG, "V must be 16-byte aligned");
+    s = kmip_topk(Q, K, graph_offsets, num_graphs, N, H, d, k, topk_idx, workspace,
+                  workspace_bytes, stream);
+    if (s != KMIP_OK) return s;
+    return kmip_attend(Q, K, V, N, H, d, k, scale, topk_idx, out, lse, stream);
+}
+
+size_t kmip_bwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t variant) {
+    (void)N;
+    (void)H;
+    (void)d;
+    (void)k;
+    (void)variant;
+    return 0;
+}
+
+kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* dOut,
+                       const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
+                       int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
+                       int32_t variant, void* workspace, size_t workspace_bytes, void* stream_) {
+    (void)workspace;
+    (void)workspace_bytes;
+    kmip_status_t s = check_sizes(N, H, d, k);
+    if (s != KMIP_OK) return s;
+    if ((s = check_scale(scale)) != KMIP_OK) return s;
+    if (variant != 0 && variant != 1) return fail(KMIP_ERR_UNSUPPORTED, "backward variant %d", variant);
+    if (N == 0) return ok();
+    if (!Q || !K || !V || !dOut || !topk_idx || !lse || !dQ || !dK || !dV)
+        return fail(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_bwd");
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(dOut))
+        return fail(KMIP_ERR_INVALID_ARG, "Q, K, V and dOut must be 16-byte aligned");
+    if (!aligned16(dK) || !aligned16(dV)) return fail(KMIP_ERR_INVALID_ARG, "dK and dV must be 16-byte aligned");
+    hipError_t e = kmip::launch_bwd_atomic(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale,
+                                           dQ, dK, dV, reinterpret_cast<hipStream_t>(stream_));
+    if (e != hipSuccess) return hip_fail(e, "backward launch");
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,90 @@
+// Device-side helpers shared by the kmip kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kmip {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) {
+    return __uint_as_float(bits16 << 16);
+}
+
+// Order-preserving map of a float32 score to uint32 (larger score, larger
+// code).  -0 is folded onto +0 first so that equal scores compare equal.
+__device__ __forceinline__ uint32_t score_code(float s) {
+    uint32_t b = __float_as_uint(s + 0.0f);
+    return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
+}
+
+__device__ __forceinline__ float score_from_code(uint32_t u) {
+    uint32_t b = (u & 0x80000000u) ? (u ^ 0x80000000u) : ~u;
+    return __uint_as_float(b);
+}
+
+// 64-bit selection key: score code in the high word, bitwise-not of the key
+// index in the low word.  Larger key = better (higher score, then lower index).
+// Key 0 is a sentinel below every real key and decodes to index -1.
+__device__ __forceinline__ uint64_t make_key(float s, int32_t j) {
+    return ((uint64_t)score_code(s) << 32) | (uint32_t)(~j);
+}
+
+__device__ __forceinline__ int32_t key_index(uint64_t key) {
+    return ~(int32_t)(uint32_t)key;
+}
+
+__device__ __forceinline__ float key_score(uint64_t key) {
+    return score_from_code((uint32_t)(key >> 32));
+}
+
+// Dot product of a float32 query row held in registers with a bf16 row in
+// global memory, accumulated in float32 in dimension order t = 0..D-1.  Both
+// the aggregate and the backward kernels call this one function, so they see
+// bit-identical scores.
+template <int D>
+__device__ __forceinline__ float dot_row_bf16(const float (&q)[D], const uint16_t* __restrict__ row) {
+    float s = 0.0f;
+#pragma unroll
+    for (int c = 0; c < D / 8; ++c) {
+        uint4 u = *reinterpret_cast<const uint4*>(row + 8 * c);
+        uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            s = fmaf(q[8 * c + 2 * e], bf16_bits_to_f32(w[e] & 0xFFFFu), s);
+            s = fmaf(q[8 * c + 2 * e + 1], bf16_bits_to_f32(w[e] >> 16), s);
+        }
+    }
+    return s;
+}
+
+template <int D>
+__device__ __forceinline__ void load_row_f32(float (&q)[D], const uint16_t* __restrict__ row) {
+#pragma unroll
+    for (int c = 0; c < D / 8; ++c) {
+        uint4 u = *reinterpret_cast<const uint4*>(row + 8 * c);
+        uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            q[8 * c + 2 * e] = bf16_bits_to_f32(w[e] & 0xFFFFu);
+            q[8 * c + 2 * e + 1] = bf16_bits_to_f32(w[e] >> 16);
+        }
+    }
+}
+
+// Reductions over aligned groups of 16 lanes.
+__device__ __forceinline__ float group16_max(float v) {
+#pragma unroll
+    for (int m = 8; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 16));
+    return v;
+}
+
+__device__ __forceinline__ float group16_sum(float v) {
+#pragma unroll
+    for (int m = 8; m >= 1; m >>= 1) v += __shfl_xor(v, m, 16);
+    return v;
+}
+
+}  // namespace kmip

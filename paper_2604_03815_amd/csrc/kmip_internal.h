@@ -1,0 +1,51 @@
+// Internal declarations shared by the kmip HIP sources (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kmip {
+
+// Candidate-buffer slots per lane and per query block in the select kernel.
+constexpr int kCandSlots = 32;
+
+// Number of XCDs of MI355X; workgroups are dispatched to them round-robin.
+constexpr int kNumXcd = 8;
+
+// One unit of score+select work: a run of up to 32*QB queries of one graph
+// and the key range of that graph.
+struct Task {
+    int32_t q_begin;
+    int32_t q_count;
+    int32_t key_lo;
+    int32_t key_hi;
+};
+
+// ---- launchers (host side); each returns hipSuccess or the launch error ----
+
+// Tiles K [N,H,d] bf16 into the matrix-core operand order: for head h and key
+// tile t (32 keys), chunk c of 16 dims, lane l holds 8 bf16 of key 32t + l%32,
+// dims 16c + 8(l/32) .. +8.  Keys >= N are zero.
+hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t d, int32_t ntiles,
+                         hipStream_t stream);
+
+// Score + select.  qb = query blocks (of 32) per wave, 1 or 2.
+hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, int32_t ntasks,
+                         int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles, int32_t qb,
+                         int32_t* topk_idx, hipStream_t stream);
+
+// Bytes of LDS one select workgroup uses.
+size_t select_lds_bytes(int32_t k, int32_t qb);
+
+hipError_t launch_attend(const void* Q, const void* K, const void* V, const int32_t* idx,
+                         int32_t N, int32_t H, int32_t d, int32_t k, float scale, float* out,
+                         float* lse, hipStream_t stream);
+
+hipError_t launch_bwd_atomic(const void* Q, const void* K, const void* V, const void* dO,
+                             const int32_t* idx, const float* lse, int32_t N, int32_t H,
+                             int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
+                             hipStream_t stream);
+
+hipError_t launch_fill_zero(float* p, size_t n, hipStream_t stream);
+
+}  // namespace kmip

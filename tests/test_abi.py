@@ -1,0 +1,113 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every symbol include/kmip.h declares, sizes its workspace, and rejects bad
+arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+kmip = pytest.importorskip("paper_2604_03815_amd")
+from paper_2604_03815_amd import _lib  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2604_03815_amd import build
+        build.build()
+    return _lib.load()
+
+
+def _declared_symbols():
+    with open(os.path.join(ROOT, "include", "kmip.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kmip_[a-z_]+)\s*\(", text)))
+
+
+def test_header_matches_binding():
+    assert sorted(_lib.EXPORTS) == _declared_symbols()
+
+
+def test_all_declared_symbols_exported(lib):
+    for name in _declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for s in range(5):
+        assert lib.kmip_status_string(s)
+    assert lib.kmip_status_string(99) == b"unknown status"
+
+
+def test_workspace_size(lib):
+    # tiled copy of K, padded to whole 32-key tiles, 256-byte aligned
+    n = lib.kmip_topk_workspace_size(500_000, 4, 16, 32, 1)
+    assert n == 4 * 15625 * 32 * 16 * 2
+    assert lib.kmip_topk_workspace_size(33, 1, 16, 4, 1) == 2 * 32 * 16 * 2
+    multi = lib.kmip_topk_workspace_size(1000, 2, 32, 16, 7)
+    assert multi > lib.kmip_topk_workspace_size(1000, 2, 32, 16, 1)
+    assert lib.kmip_topk_workspace_size(100, 1, 24, 4, 1) == 0   # unsupported d
+    assert lib.kmip_topk_workspace_size(-1, 1, 16, 4, 1) == 0
+    assert lib.kmip_fwd_workspace_size(1000, 2, 32, 16, 1) == lib.kmip_topk_workspace_size(1000, 2, 32, 16, 1)
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == 0
+
+
+P = ctypes.c_void_p
+FAKE = P(256)  # never dereferenced: every call below fails validation first
+
+
+def _topk(lib, N=64, H=1, d=16, k=4, offsets=None, G=1, ws=FAKE, ws_bytes=1 << 20, q=FAKE):
+    optr = None if offsets is None else np.ascontiguousarray(offsets, np.int32).ctypes.data_as(P)
+    return lib.kmip_topk(q, FAKE, optr, G, N, H, d, k, FAKE, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(N=-1), 1), (dict(H=0), 1), (dict(k=0), 1), (dict(d=24), 2), (dict(k=129), 2),
+    (dict(N=1 << 31), 1), (dict(N=1 << 28, H=8, d=16), 1),
+    (dict(offsets=[1, 64], G=1), 1), (dict(offsets=[0, 40, 30, 64], G=3), 1),
+    (dict(offsets=[0, 32, 63], G=2), 1), (dict(offsets=[0, 64], G=0), 1),
+    (dict(ws=None), 3), (dict(ws_bytes=10), 3), (dict(ws=P(256 + 16)), 3),
+    (dict(q=None), 1), (dict(q=P(258)), 1),
+])
+def test_topk_rejects(lib, kw, status):
+    assert _topk(lib, **kw) == status
+    assert lib.kmip_last_error()
+
+
+def test_zero_nodes_is_a_no_op(lib):
+    assert lib.kmip_topk(None, None, None, 1, 0, 1, 16, 4, None, None, 0, None) == 0
+    assert lib.kmip_attend(None, None, None, 0, 1, 16, 4, ctypes.c_float(1.0), None, None, None, None) == 0
+
+
+def test_attend_rejects(lib):
+    f = ctypes.c_float
+    assert lib.kmip_attend(FAKE, FAKE, FAKE, 64, 1, 16, 4, f(0.0), FAKE, FAKE, FAKE, None) == 1
+    assert lib.kmip_attend(FAKE, FAKE, FAKE, 64, 1, 16, 4, f(float("nan")), FAKE, FAKE, FAKE, None) == 1
+    assert lib.kmip_attend(FAKE, FAKE, FAKE, 64, 1, 16, 4, f(float("inf")), FAKE, FAKE, FAKE, None) == 1
+    assert lib.kmip_attend(FAKE, FAKE, None, 64, 1, 16, 4, f(1.0), FAKE, FAKE, FAKE, None) == 1
+    assert lib.kmip_attend(FAKE, FAKE, FAKE, 64, 1, 48, 4, f(1.0), FAKE, FAKE, FAKE, None) == 2
+
+
+def test_bwd_rejects(lib):
+    f = ctypes.c_float
+    args = [FAKE] * 6 + [64, 1, 16, 4, f(1.0), FAKE, FAKE, FAKE]
+    assert lib.kmip_bwd(*args, 7, None, 0, None) == 2            # unknown variant
+    bad = list(args)
+    bad[3] = None                                                 # dOut
+    assert lib.kmip_bwd(*bad, 0, None, 0, None) == 1
+    bad = list(args)
+    bad[10] = f(-2.0)
+    assert lib.kmip_bwd(*bad, 0, None, 0, None) == 1
+
+
+def test_fwd_validates_before_launch(lib):
+    f = ctypes.c_float
+    assert lib.kmip_fwd(FAKE, FAKE, None, None, 1, 64, 1, 16, 4, f(1.0), FAKE, FAKE, FAKE,
+                        FAKE, 1 << 20, None) == 1
+    assert lib.kmip_fwd(FAKE, FAKE, FAKE, None, 1, 64, 1, 16, 4, f(-1.0), FAKE, FAKE, FAKE,
+                        FAKE, 1 << 20, None) == 1

@@ -1,0 +1,203 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle.
+
+Small and medium cases are checked on every query-head; the full-size
+workloads (N = 100k, 500k, 262k) on a seeded sample of query-heads for the
+index sets, and on every query-head for structure, out/lse and gradients
+(evaluated by the oracle on the GPU's own index sets).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from parity import (allclose_report, check_sets, check_structure, sample_rows)
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2604_03815_amd as kmip  # noqa: E402
+
+DEV = torch.device("cuda:0")
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(DEV)
+
+
+def _f64(w):
+    return tuple(oracle.from_bf16(getattr(w, n)) if getattr(w, n) is not None else None
+                 for n in ("q", "kk", "v", "dout"))
+
+
+def _run(w, backward=True):
+    q, k, v = _dev(w.q), _dev(w.kk), _dev(w.v)
+    print(f"[case] {w.name} N={w.N} H={w.H} d={w.d} k={w.k} graphs={w.num_graphs}", flush=True)
+    out, idx, lse = kmip.fwd(q, k, v, w.k, w.scale, graph_offsets=w.offsets)
+    grads = None
+    if backward and w.dout is not None:
+        grads = kmip.bwd(q, k, v, _dev(w.dout), idx, lse, w.scale)
+    torch.cuda.synchronize()
+    res = {"out": out.cpu().numpy(), "idx": idx.cpu().numpy(), "lse": lse.cpu().numpy()}
+    if grads is not None:
+        res.update(dq=grads[0].cpu().numpy(), dk=grads[1].cpu().numpy(), dv=grads[2].cpu().numpy())
+    return res
+
+
+def _check_all(w, res, sample=None):
+    Qd, Kd, Vd, dOd = _f64(w)
+    check_structure(res["idx"], w.offsets, w.N, w.H, w.k)
+    sel = None if sample is None else sample_rows(w.N, w.H, sample, seed=123)
+    strict, loose = check_sets(w, Qd, Kd, res["idx"], sel=sel)
+    ref_out, ref_lse = oracle.attend(Qd, Kd, Vd, res["idx"], w.scale)
+    allclose_report("out", res["out"].reshape(-1, w.d), ref_out)
+    allclose_report("lse", res["lse"].reshape(-1), ref_lse)
+    if "dq" in res:
+        rq, rk, rv = oracle.backward(Qd, Kd, Vd, dOd, res["idx"], w.scale)
+        allclose_report("dQ", res["dq"], rq)
+        allclose_report("dK", res["dk"], rk)
+        allclose_report("dV", res["dv"], rv)
+    return strict, loose
+
+
+SMALL = [
+    # (N, H, d, k, sizes)
+    (1, 1, 16, 1, None),
+    (33, 1, 16, 4, None),
+    (1000, 2, 16, 32, None),
+    (777, 3, 32, 16, [1, 31, 33, 0, 100, 612]),
+    (2049, 1, 64, 128, None),
+    (300, 2, 32, 128, [50, 250]),
+    (5000, 1, 16, 100, None),
+    (4097, 2, 64, 1, None),
+    (3000, 1, 32, 64, [3000]),
+    (130, 4, 16, 8, [0, 65, 0, 65, 0]),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: "N%d_H%d_d%d_k%d" % c[:4])
+def test_small_cases_full(case):
+    N, H, d, k, sizes = case
+    w = workloads.iid(N, H, d, k, seed=N + 7 * k + d, sizes=sizes)
+    _check_all(w, _run(w))
+
+
+def test_config1_full():
+    w = workloads.make(1)
+    strict, loose = _check_all(w, _run(w, backward=False))
+    print(f"c1: {strict} well-separated, {loose} near-tied query-heads")
+
+
+def test_config2_full_fwd_bwd():
+    w = workloads.make(2)
+    strict, loose = _check_all(w, _run(w))
+    print(f"c2: {strict} well-separated, {loose} near-tied query-heads")
+
+
+@pytest.mark.parametrize("d", [16, 32, 64])
+def test_exact_ties_integer_inputs(d):
+    # Integer inputs make every fp32 score exact, so the GPU must reproduce
+    # the tie rule (score desc, index asc) bit for bit, order included.
+    rng = np.random.default_rng(d)
+    N, H, k = 700, 2, 24
+    q = rng.integers(-1, 2, size=(N, H, d)).astype(np.float32)
+    kk = rng.integers(-1, 2, size=(N, H, d)).astype(np.float32)
+    v = rng.standard_normal((N, H, d)).astype(np.float32)
+    w = workloads.Workload("ties", N, H, d, k, 0.5, np.array([0, 13, 13, 400, 700], np.int32),
+                           workloads.bf16_round(q), workloads.bf16_round(kk),
+                           workloads.bf16_round(v), None, False)
+    res = _run(w, backward=False)
+    Qd, Kd, Vd, _ = _f64(w)
+    _, o_idx, _ = oracle.forward(Qd, Kd, Vd, k, w.scale, offsets=w.offsets)
+    np.testing.assert_array_equal(res["idx"], o_idx)
+
+
+def test_all_scores_tied():
+    # Q = 0: every score is 0, so each query keeps the k lowest indices of its graph.
+    N, H, d, k = 200, 1, 32, 16
+    rng = np.random.default_rng(0)
+    w = workloads.Workload("zeroq", N, H, d, k, 0.25, np.array([0, 10, 200], np.int32),
+                           workloads.bf16_round(np.zeros((N, H, d), np.float32)),
+                           workloads.bf16_round(rng.standard_normal((N, H, d)).astype(np.float32)),
+                           workloads.bf16_round(rng.standard_normal((N, H, d)).astype(np.float32)),
+                           None, False)
+    res = _run(w, backward=False)
+    idx = res["idx"][:, 0, :]
+    np.testing.assert_array_equal(idx[:10, :10], np.tile(np.arange(10), (10, 1)))
+    assert (idx[:10, 10:] == -1).all()
+    np.testing.assert_array_equal(idx[10:], np.tile(np.arange(10, 26), (190, 1)))
+    V = oracle.from_bf16(w.v)[:, 0, :]
+    allclose_report("out", res["out"][10:, 0, :], np.tile(V[10:26].mean(axis=0), (190, 1)))
+
+
+def test_deterministic_and_overwrites():
+    w = workloads.iid(3000, 2, 32, 16, seed=5, sizes=[1000, 2000])
+    q, k, v, g = _dev(w.q), _dev(w.kk), _dev(w.v), _dev(w.dout)
+    a = kmip.fwd(q, k, v, w.k, w.scale, graph_offsets=w.offsets)
+    idx = torch.full_like(a[1], 12345)
+    out = torch.full_like(a[0], float("nan"))
+    lse = torch.full_like(a[2], -7.0)
+    kmip.topk(q, k, w.k, graph_offsets=w.offsets, idx=idx)
+    kmip.attend(q, k, v, idx, w.scale, out=out, lse=lse)
+    torch.cuda.synchronize()
+    assert torch.equal(a[1], idx)
+    assert torch.equal(a[0], out)
+    assert torch.equal(a[2], lse)
+    dq = torch.full_like(a[0], 3.0)
+    dk = torch.full_like(a[0], 3.0)
+    dv = torch.full_like(a[0], 3.0)
+    g1 = kmip.bwd(q, k, v, g, idx, lse, w.scale)
+    kmip.bwd(q, k, v, g, idx, lse, w.scale, dq=dq, dk=dk, dv=dv)
+    torch.cuda.synchronize()
+    assert torch.equal(g1[0], dq)
+    # dK/dV are atomic scatters: equal up to summation order
+    allclose_report("dK rerun", dk.cpu().numpy(), g1[1].cpu().numpy(), atol=1e-6, rtol=1e-5)
+    allclose_report("dV rerun", dv.cpu().numpy(), g1[2].cpu().numpy(), atol=1e-6, rtol=1e-5)
+
+
+def test_guard_canaries():
+    # Outputs live inside larger buffers; the guard regions must stay untouched.
+    w = workloads.iid(515, 3, 16, 20, seed=9, sizes=[515])
+    q, k, v, g = _dev(w.q), _dev(w.kk), _dev(w.v), _dev(w.dout)
+    N, H, d, kk = w.N, w.H, w.d, w.k
+    pad = 4096
+    ibuf = torch.full((N * H * kk + 2 * pad,), -77, dtype=torch.int32, device=DEV)
+    obuf = torch.full((N * H * d + 2 * pad,), 5.5, dtype=torch.float32, device=DEV)
+    lbuf = torch.full((N * H + 2 * pad,), 6.5, dtype=torch.float32, device=DEV)
+    gbufs = [torch.full((N * H * d + 2 * pad,), 7.5, dtype=torch.float32, device=DEV) for _ in range(3)]
+    idx = ibuf[pad:pad + N * H * kk].view(N, H, kk)
+    out = obuf[pad:pad + N * H * d].view(N, H, d)
+    lse = lbuf[pad:pad + N * H].view(N, H)
+    kmip.topk(q, k, kk, idx=idx)
+    kmip.attend(q, k, v, idx, w.scale, out=out, lse=lse)
+    views = [b[pad:pad + N * H * d].view(N, H, d) for b in gbufs]
+    kmip.bwd(q, k, v, g, idx, lse, w.scale, dq=views[0], dk=views[1], dv=views[2])
+    torch.cuda.synchronize()
+    for b, fill in [(ibuf, -77), (obuf, 5.5), (lbuf, 6.5)] + [(x, 7.5) for x in gbufs]:
+        assert (b[:pad] == fill).all() and (b[-pad:] == fill).all()
+    assert (idx >= 0).all()
+
+
+def test_invalid_arguments_leave_outputs_untouched():
+    w = workloads.iid(64, 1, 16, 4, seed=3)
+    q, k, v = _dev(w.q), _dev(w.kk), _dev(w.v)
+    idx = torch.full((64, 1, 4), -9, dtype=torch.int32, device=DEV)
+    with pytest.raises(kmip.KmipError) as e:
+        kmip.topk(q, k, 4, graph_offsets=[0, 30, 20, 64], idx=idx)
+    assert e.value.status == 1
+    with pytest.raises(kmip.KmipError) as e:
+        kmip.topk(q, k, 129, idx=torch.empty((64, 1, 129), dtype=torch.int32, device=DEV))
+    assert e.value.status == 2
+    with pytest.raises(kmip.KmipError):
+        kmip.attend(q, k, v, idx, -1.0)
+    torch.cuda.synchronize()
+    assert (idx == -9).all()
+
+
+@pytest.mark.parametrize("cfg,sample", [(3, 384), (4, 256), (5, 256)])
+def test_full_size_sampled(cfg, sample):
+    w = workloads.make(cfg)
+    strict, loose = _check_all(w, _run(w), sample=sample)
+    print(f"c{cfg}: sampled {strict} well-separated, {loose} near-tied query-heads")
