@@ -7,7 +7,7 @@
 namespace kmip {
 
 // Candidate-buffer slots per lane and per query block in the select kernel.
-constexpr int kCandSlots = 32;
+constexpr int kCandSlots = 8;
 
 // Number of XCDs of MI355X; workgroups are dispatched to them round-robin.
 constexpr int kNumXcd = 8;

@@ -8,30 +8,61 @@
 // (fp32 accumulation) and keeps a running top-k per query in LDS.
 //
 // Work decomposition: one wave per workgroup handles QB blocks of 32 queries
-// of one graph and one head, and streams all 32-key tiles of that graph.
-// MFMA operand roles: A = 32 keys x 16 dims, B = 16 dims x 32 queries, so
-// lane l ends up holding 16 scores of query (l % 32) against keys
+// of one graph and one head, and streams every 32-key tile that overlaps the
+// graph.  MFMA operand roles: A = 32 keys x 16 dims, B = 16 dims x 32
+// queries, so lane l ends up holding 16 scores of query (l % 32) against keys
 //   row(r, l) = 8 * (r / 4) + 4 * (l / 32) + (r % 4),  r = 0..15
 // of the tile.  Lanes l and l + 32 share a query.
 //
 // Selection per query: a min-heap of the k best 64-bit keys (score code,
-// ~index) in LDS whose root gives a threshold theta.  Each lane reduces its
-// 16 scores with max3 and compares once with theta; only when some lane
-// beats theta does the wave look at individual scores and append the
-// winners to a per-lane candidate buffer in LDS.  When a buffer may overflow
-// on the next tile, the wave folds the buffers into the heaps (first the
-// lanes of the lower half-wave, then the upper one, since they share heaps)
-// and refreshes theta.  Keys are streamed in increasing index order, so a
-// key whose score equals theta loses the tie to the heap entries and a
-// strict comparison is exact; the heap itself orders by the full key.
+// ~index) in LDS; its root's score is a threshold theta kept in a register.
+// Per tile and block each lane reduces its 16 scores with a max3 tree and
+// compares once with theta.  Only when some lane's maximum beats theta does
+// the wave pick out the scores above theta, append them (with their key
+// index) to a per-lane candidate buffer in LDS, and fold the buffers into the
+// heaps (refreshing theta) whenever one fills up.
+//
+// Exactness of the strict filter: when block b's scores of a tile are
+// compared with theta, its heap holds only keys of earlier tiles, whose
+// indices are all lower; a score equal to theta therefore loses the tie and
+// may be skipped.  Candidates are compared again, by full key, when they are
+// folded into the heap.  Keys of a tile that lie outside the query's graph
+// are not masked in the streaming loop; they can only send a tile down the
+// rare path, which drops them by index.
 #include "kmip_device.h"
 #include "kmip_internal.h"
 
 namespace kmip {
 namespace {
 
+constexpr int kSlots = kCandSlots;
+
 __device__ __forceinline__ int tile_row(int r, int half) {
     return 8 * (r >> 2) + 4 * half + (r & 3);
+}
+
+// Key tiles are streamed with loads issued from inline assembly, in a fixed
+// order, and waited for with explicit vmcnt counts: the compiler may reorder
+// ordinary loads of the prefetch ring, and its wait analysis then falls back
+// to draining every load before each tile.  vmcnt(n) waits until at most n
+// vector-memory operations are outstanding; loads complete in issue order,
+// so with n = the number of ring loads issued after the one needed, that load
+// has arrived (any other outstanding operation only makes the wait longer).
+// The tile address lives in SGPRs, the lane offset in a VGPR.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+template <int OFF>
+__device__ __forceinline__ i32x4 ring_load(const void* tile_base, uint32_t lane_off) {
+    i32x4 v;
+    asm volatile("global_load_dwordx4 %0, %1, %2 offset:%3"
+                 : "=v"(v)
+                 : "v"(lane_off), "s"(tile_base), "n"(OFF));
+    return v;
+}
+
+template <int N>
+__device__ __forceinline__ void ring_wait(i32x4& v) {
+    asm volatile("s_waitcnt vmcnt(%1)" : "+v"(v) : "n"(N));
 }
 
 // Min-heap in LDS, column `col` of a [size][32] array of keys.  Places x at
@@ -63,6 +94,7 @@ __global__ __launch_bounds__(64) void select_kernel(
     int32_t ntasks, int32_t N, int32_t H, int32_t k, int32_t ntiles,
     int32_t* __restrict__ topk_idx) {
     constexpr int NC = D / 16;
+    constexpr int TILE_BYTES = NC * 64 * 16;
     extern __shared__ uint64_t lds[];
 
     // XCD-aware order: the workgroups that land on one XCD take a contiguous
@@ -91,8 +123,9 @@ __global__ __launch_bounds__(64) void select_kernel(
     const int col = lane & 31;
     const int half = lane >> 5;
 
-    uint64_t* heaps = lds;                       // [QB][k][32]
-    uint64_t* cand = lds + (size_t)QB * k * 32;  // [QB][kCandSlots][64]
+    uint64_t* heaps = lds;                          // [QB][k][32]
+    uint64_t* cand = lds + (size_t)QB * k * 32;     // [QB][kSlots][64]
+    float* stash = reinterpret_cast<float*>(cand + (size_t)QB * kSlots * 64);  // [16][64]
 
     bf16x8 bq[QB][NC];
     float theta[QB];
@@ -111,45 +144,96 @@ __global__ __launch_bounds__(64) void select_kernel(
         cnt[b] = 0;
     }
     for (int e = lane; e < QB * k * 32; e += 64) heaps[e] = 0ull;
-    __syncthreads();
 
-    auto merge = [&](int b) {
-        uint64_t* hp = heaps + (size_t)b * k * 32;
-        const uint64_t* cb = cand + (size_t)b * kCandSlots * 64;
+    // Fold every lane's candidates into the heaps and refresh theta.  With
+    // two blocks, each phase has the lower half-wave on one block's heaps and
+    // the upper half-wave on the other's, so all lanes work on disjoint heaps.
+    auto merge_all = [&]() {
 #pragma unroll
         for (int ph = 0; ph < 2; ++ph) {
-            if (half == ph) {
-                const int n = cnt[b];
+            const int b = QB == 2 ? (half ^ ph) : 0;
+            if (QB == 2 || half == ph) {
+                uint64_t* hp = heaps + (size_t)b * k * 32;
+                const uint64_t* cb = cand + (size_t)b * kSlots * 64;
+                const int n = b == 0 ? cnt[0] : cnt[QB - 1];
                 for (int e = 0; e < n; ++e) {
                     uint64_t c = cb[e * 64 + lane];
                     if (c > hp[col]) heap_sift_down(hp, col, k, c);
                 }
             }
-            __syncthreads();
+            // One wave per workgroup: its LDS instructions execute in program
+            // order, so the next phase sees this phase's heap writes.  Only
+            // compiler reordering has to be fenced off.
+            __builtin_amdgcn_wave_barrier();
         }
-        if (theta[b] != INFINITY) {
-            uint64_t root = hp[col];
-            theta[b] = root == 0ull ? -INFINITY : key_score(root);
+#pragma unroll
+        for (int b = 0; b < QB; ++b) {
+            if (theta[b] != INFINITY) {
+                const uint64_t root = heaps[(size_t)b * k * 32 + col];
+                theta[b] = root == 0ull ? -INFINITY : key_score(root);
+            }
+            cnt[b] = 0;
         }
-        cnt[b] = 0;
+    };
+
+    // Rare path for block b of the tile starting at key tbase.  Each lane
+    // builds a 16-bit mask of its scores above theta (theta still reflects
+    // earlier tiles only, so the strict test is exact), parks the scores in
+    // LDS, and the wave then walks the set bits: as many rounds as the
+    // largest per-lane count, usually one or two.  A buffer that fills up is
+    // folded between two rounds.
+    auto rare_path = [&](const f32x16& acc, int b, int tbase) {
+        uint64_t* cb = cand + (size_t)b * kSlots * 64;
+        uint32_t mask = 0;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mask |= (acc[r] > theta[b] ? 1u : 0u) << r;
+        if (tbase < key_lo || tbase + 32 > key_hi) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int j = tbase + tile_row(r, half);
+                if (j < key_lo || j >= key_hi) mask &= ~(1u << r);
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) stash[r * 64 + lane] = acc[r];
+        while (__builtin_amdgcn_ballot_w64(mask != 0u) != 0ull) {
+            if (mask != 0u) {
+                const int r = __builtin_ctz(mask);
+                mask &= mask - 1u;
+                cb[cnt[b] * 64 + lane] = make_key(stash[r * 64 + lane], tbase + tile_row(r, half));
+                cnt[b] += 1;
+            }
+            if (__builtin_amdgcn_ballot_w64(cnt[b] == kSlots) != 0ull) merge_all();
+        }
+        __builtin_amdgcn_wave_barrier();
     };
 
     const int t0 = key_lo >> 5;
     const int t1 = (key_hi + 31) >> 5;
-    const uint4* kbase = kp + (size_t)head * ntiles * NC * 64 + lane;
+    const char* kbase = reinterpret_cast<const char*>(kp) + (size_t)head * ntiles * TILE_BYTES;
+    const uint32_t lane_off = (uint32_t)lane * 16u;
 
-    // Prefetch ring of key tiles in registers; loads past the last tile are
-    // clamped to it (harmless repeats, never out of bounds).
+    // Prefetch ring: slot (T - t0) % PF holds tile T; it is refilled with
+    // tile T + PF as soon as tile T's MFMAs are issued.  Loads past the last
+    // tile are clamped to it (harmless repeats, never out of bounds).
     constexpr int PF = 8 / NC;
-    uint4 ring[PF][NC];
+    i32x4 ring[PF][NC];
+    auto refill = [&](i32x4 (&slot)[NC], int tt) {
+        const char* base = kbase + (size_t)min(tt, t1 - 1) * TILE_BYTES;
+        slot[0] = ring_load<0>(base, lane_off);
+        if constexpr (NC >= 2) slot[1] = ring_load<1024>(base, lane_off);
+        if constexpr (NC >= 4) {
+            slot[2] = ring_load<2048>(base, lane_off);
+            slot[3] = ring_load<3072>(base, lane_off);
+        }
+    };
 #pragma unroll
-    for (int u = 0; u < PF; ++u) {
-        const int tt = min(t0 + u, t1 - 1);
-#pragma unroll
-        for (int c = 0; c < NC; ++c) ring[u][c] = kbase[((size_t)tt * NC + c) * 64];
-    }
+    for (int u = 0; u < PF; ++u) refill(ring[u], t0 + u);
 
-    auto scores = [&](const uint4 (&a)[NC], f32x16 (&acc)[QB]) {
+    // Scores of the tile in ring slot `a`; PF - 1 later tiles are in flight.
+    auto scores = [&](i32x4 (&a)[NC], f32x16 (&acc)[QB]) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) ring_wait<(PF - 1) * NC>(a[c]);
 #pragma unroll
         for (int b = 0; b < QB; ++b) {
             acc[b] = f32x16{};
@@ -160,74 +244,58 @@ __global__ __launch_bounds__(64) void select_kernel(
         }
     };
 
-    auto filter = [&](f32x16 (&acc)[QB], int t) {
-        const int tbase = t << 5;
-        if (tbase < key_lo || tbase + 32 > key_hi) {
-            // Tile straddles the graph boundary: keys outside never qualify.
+    // Largest of a lane's 16 scores: a max3 tree of depth 3 (8 instructions)
+    // rather than a chain, so the two blocks' reductions interleave.
+    auto max16 = [](const f32x16& a) {
+        const float l0 = fmaxf(fmaxf(a[0], a[1]), a[2]);
+        const float l1 = fmaxf(fmaxf(a[3], a[4]), a[5]);
+        const float l2 = fmaxf(fmaxf(a[6], a[7]), a[8]);
+        const float l3 = fmaxf(fmaxf(a[9], a[10]), a[11]);
+        const float l4 = fmaxf(fmaxf(a[12], a[13]), a[14]);
+        return fmaxf(fmaxf(fmaxf(l0, l1), l2), fmaxf(fmaxf(l3, l4), a[15]));
+    };
+
+    auto filter = [&](const f32x16 (&acc)[QB], int t) {
+        float m[QB];
+        bool pass = false;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int j = tbase + tile_row(r, half);
-                if (j < key_lo || j >= key_hi) {
+        for (int b = 0; b < QB; ++b) m[b] = max16(acc[b]);
 #pragma unroll
-                    for (int b = 0; b < QB; ++b) acc[b][r] = -INFINITY;
-                }
-            }
-        }
+        for (int b = 0; b < QB; ++b) pass = pass || m[b] > theta[b];
+        if (__builtin_amdgcn_ballot_w64(pass) != 0ull) {
 #pragma unroll
-        for (int b = 0; b < QB; ++b) {
-            float m = fmaxf(fmaxf(acc[b][0], acc[b][1]), acc[b][2]);
-#pragma unroll
-            for (int r = 3; r < 15; r += 2) m = fmaxf(fmaxf(m, acc[b][r]), acc[b][r + 1]);
-            m = fmaxf(m, acc[b][15]);
-            if (__builtin_amdgcn_ballot_w64(m > theta[b]) != 0ull) {
-                uint64_t* cb = cand + (size_t)b * kCandSlots * 64;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const bool hit = acc[b][r] > theta[b];
-                    if (__builtin_amdgcn_ballot_w64(hit) != 0ull) {
-                        if (hit) {
-                            cb[cnt[b] * 64 + lane] = make_key(acc[b][r], tbase + tile_row(r, half));
-                            cnt[b] += 1;
-                        }
-                    }
-                }
-                if (__builtin_amdgcn_ballot_w64(cnt[b] > kCandSlots - 16) != 0ull) merge(b);
-            }
+            for (int b = 0; b < QB; ++b)
+                if (__builtin_amdgcn_ballot_w64(m[b] > theta[b]) != 0ull) rare_path(acc[b], b, t << 5);
         }
     };
 
-    // Software pipeline: the MFMAs of tile t+1 are issued before tile t is
-    // filtered, so the matrix cores and the filter overlap.
-    f32x16 acc_next[QB];
-    scores(ring[0], acc_next);
-    {
-        const int tt = min(t0 + PF, t1 - 1);
+    // Software pipeline with two accumulator sets: the MFMAs of tile t+1 are
+    // issued before tile t is filtered, so matrix cores and filter overlap.
+    f32x16 acc_a[QB], acc_b[QB];
+    scores(ring[0], acc_a);
+    refill(ring[0], t0 + PF);
+    for (int t = t0;; t += PF) {
 #pragma unroll
-        for (int c = 0; c < NC; ++c) ring[0][c] = kbase[((size_t)tt * NC + c) * 64];
-    }
-    for (int t = t0; t < t1; t += PF) {
-#pragma unroll
-        for (int u = 0; u < PF; ++u) {
-            const int tc = t + u;
-            if (tc >= t1) break;
-            f32x16 acc[QB];
-#pragma unroll
-            for (int b = 0; b < QB; ++b) acc[b] = acc_next[b];
-            const int un = (u + 1) % PF;
+        for (int u = 0; u < PF; u += 2) {
+            const int tc = t + u;  // acc_a holds tile tc
+            if (tc >= t1) goto stream_done;
             if (tc + 1 < t1) {
-                scores(ring[un], acc_next);
-                const int tt = min(tc + 1 + PF, t1 - 1);
-#pragma unroll
-                for (int c = 0; c < NC; ++c) ring[un][c] = kbase[((size_t)tt * NC + c) * 64];
+                scores(ring[u + 1], acc_b);
+                refill(ring[u + 1], tc + 1 + PF);
             }
-            filter(acc, tc);
+            filter(acc_a, tc);
+            if (tc + 1 >= t1) goto stream_done;
+            if (tc + 2 < t1) {
+                scores(ring[(u + 2) % PF], acc_a);
+                refill(ring[(u + 2) % PF], tc + 2 + PF);
+            }
+            filter(acc_b, tc + 1);
         }
     }
-
-#pragma unroll
-    for (int b = 0; b < QB; ++b) {
-        if (__builtin_amdgcn_ballot_w64(cnt[b] > 0) != 0ull) merge(b);
-    }
+stream_done:
+    // Drain the ring so no load is still writing registers at exit.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    merge_all();
 
     // Drain each heap in increasing order into slots k-1 .. 0, which leaves
     // the row sorted by (score desc, index asc); sentinels become -1.
@@ -282,7 +350,8 @@ hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, int
 }  // namespace
 
 size_t select_lds_bytes(int32_t k, int32_t qb) {
-    return (size_t)qb * ((size_t)k * 32 + (size_t)kCandSlots * 64) * sizeof(uint64_t);
+    return (size_t)qb * ((size_t)k * 32 + (size_t)kSlots * 64) * sizeof(uint64_t) +
+           (size_t)16 * 64 * sizeof(float);
 }
 
 hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t d, int32_t ntiles,
