@@ -69,7 +69,7 @@ kmip_status_t check_offsets(const int32_t* off, int32_t G, int64_t N) {
 int32_t num_tiles(int64_t N) { return (int32_t)((N + 31) / 32); }
 
 size_t packed_k_bytes(int64_t N, int32_t H, int32_t d) {
-    return (size_t)H * (size_t)num_tiles(N) * 32 * (size_t)d * 2;
+    return (size_t)H * (size_t)(num_tiles(N) + kmip::kPadTiles) * 32 * (size_t)d * 2;
 }
 
 // Upper bound on the work-list length for any query-block size.

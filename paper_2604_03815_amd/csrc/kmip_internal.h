@@ -9,6 +9,11 @@ namespace kmip {
 // Candidate-buffer slots per lane and per query block in the select kernel.
 constexpr int kCandSlots = 8;
 
+// Zero tiles appended to each head of the tiled key buffer, so that key
+// prefetches running past a head's last tile stay in bounds (at least the
+// prefetch depth plus one).
+constexpr int kPadTiles = 16;
+
 // Number of XCDs of MI355X; workgroups are dispatched to them round-robin.
 constexpr int kNumXcd = 8;
 
@@ -25,7 +30,8 @@ struct Task {
 
 // Tiles K [N,H,d] bf16 into the matrix-core operand order: for head h and key
 // tile t (32 keys), chunk c of 16 dims, lane l holds 8 bf16 of key 32t + l%32,
-// dims 16c + 8(l/32) .. +8.  Keys >= N are zero.
+// dims 16c + 8(l/32) .. +8.  Keys >= N are zero; each head has ntiles +
+// kPadTiles tiles.
 hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t d, int32_t ntiles,
                          hipStream_t stream);
 

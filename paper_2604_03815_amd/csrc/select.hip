@@ -7,9 +7,9 @@
 // streams key tiles, forms 32x32 score tiles with one bf16 MFMA per 16 dims
 // (fp32 accumulation) and keeps a running top-k per query in LDS.
 //
-// Work decomposition: one wave per workgroup handles QB blocks of 32 queries
-// of one graph and one head, and streams every 32-key tile that overlaps the
-// graph.  MFMA operand roles: A = 32 keys x 16 dims, B = 16 dims x 32
+// Work decomposition: an item is QB blocks of 32 queries of one graph and
+// one head; its wave streams every 32-key tile that overlaps the graph.  One
+// wave per workgroup; workgroups are persistent and loop over items.  MFMA operand roles: A = 32 keys x 16 dims, B = 16 dims x 32
 // queries, so lane l ends up holding 16 scores of query (l % 32) against keys
 //   row(r, l) = 8 * (r / 4) + 4 * (l / 32) + (r % 4),  r = 0..15
 // of the tile.  Lanes l and l + 32 share a query.
@@ -29,6 +29,8 @@
 // folded into the heap.  Keys of a tile that lie outside the query's graph
 // are not masked in the streaming loop; they can only send a tile down the
 // rare path, which drops them by index.
+#include <algorithm>
+
 #include "kmip_device.h"
 #include "kmip_internal.h"
 
@@ -49,6 +51,9 @@ __device__ __forceinline__ int tile_row(int r, int half) {
 // so with n = the number of ring loads issued after the one needed, that load
 // has arrived (any other outstanding operation only makes the wait longer).
 // The tile address lives in SGPRs, the lane offset in a VGPR.
+// The compiler believes an asm load writes its registers at once, so a
+// ring register must stay live (be an operand of a later wait) until its
+// load has landed; the stream's final drain lists every ring register.
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 template <int OFF>
@@ -97,13 +102,20 @@ __global__ __launch_bounds__(64) void select_kernel(
     constexpr int TILE_BYTES = NC * 64 * 16;
     extern __shared__ uint64_t lds[];
 
-    // XCD-aware order: the workgroups that land on one XCD take a contiguous
-    // range of (head, task) items, so each XCD's L2 streams few heads.
-    const int per_xcd = gridDim.x / kNumXcd;
-    const int vid = (blockIdx.x % kNumXcd) * per_xcd + blockIdx.x / kNumXcd;
-    if (vid >= ntasks * H) return;
-    const int head = vid / ntasks;
-    const int task = vid - head * ntasks;
+    // Persistent, XCD-aware schedule.  Workgroups are dispatched to the XCDs
+    // round-robin; the ones on XCD x walk a contiguous range of (head, task)
+    // items in lock-step rounds.  All workgroups start together and items
+    // stream the same key tiles in the same order, so the waves of one XCD
+    // read each tile at nearly the same time and share it in that XCD's L2.
+    const int items = ntasks * H;
+    const int xcd = blockIdx.x % kNumXcd;
+    const int wgs_per_xcd = gridDim.x / kNumXcd;
+    const int items_per_xcd = (items + kNumXcd - 1) / kNumXcd;
+    const int item_end = min(items, (xcd + 1) * items_per_xcd);
+    for (int item = xcd * items_per_xcd + blockIdx.x / kNumXcd; item < item_end;
+         item += wgs_per_xcd) {
+    const int head = item / ntasks;
+    const int task = item - head * ntasks;
 
     int q_begin, q_count, key_lo, key_hi;
     if (tasks != nullptr) {
@@ -184,21 +196,24 @@ __global__ __launch_bounds__(64) void select_kernel(
     // folded between two rounds.
     auto rare_path = [&](const f32x16& acc, int b, int tbase) {
         uint64_t* cb = cand + (size_t)b * kSlots * 64;
+        // Bit 15 - r of mask is set when score r beats theta: theta - s is
+        // negative exactly then, and alignbit shifts its sign bit in.
         uint32_t mask = 0;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mask |= (acc[r] > theta[b] ? 1u : 0u) << r;
+        for (int r = 0; r < 16; ++r)
+            mask = __builtin_amdgcn_alignbit(mask, __float_as_uint(theta[b] - acc[r]), 31);
         if (tbase < key_lo || tbase + 32 > key_hi) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int j = tbase + tile_row(r, half);
-                if (j < key_lo || j >= key_hi) mask &= ~(1u << r);
+                if (j < key_lo || j >= key_hi) mask &= ~(1u << (15 - r));
             }
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) stash[r * 64 + lane] = acc[r];
         while (__builtin_amdgcn_ballot_w64(mask != 0u) != 0ull) {
             if (mask != 0u) {
-                const int r = __builtin_ctz(mask);
+                const int r = 15 - __builtin_ctz(mask);
                 mask &= mask - 1u;
                 cb[cnt[b] * 64 + lane] = make_key(stash[r * 64 + lane], tbase + tile_row(r, half));
                 cnt[b] += 1;
@@ -210,25 +225,28 @@ __global__ __launch_bounds__(64) void select_kernel(
 
     const int t0 = key_lo >> 5;
     const int t1 = (key_hi + 31) >> 5;
-    const char* kbase = reinterpret_cast<const char*>(kp) + (size_t)head * ntiles * TILE_BYTES;
     const uint32_t lane_off = (uint32_t)lane * 16u;
 
     // Prefetch ring: slot (T - t0) % PF holds tile T; it is refilled with
-    // tile T + PF as soon as tile T's MFMAs are issued.  Loads past the last
-    // tile are clamped to it (harmless repeats, never out of bounds).
+    // tile T + PF as soon as tile T's MFMAs are issued.  `next` walks the
+    // tiled key buffer one tile per refill; the buffer carries kPadTiles
+    // zero tiles per head past the last one, so prefetches beyond the
+    // graph's last tile stay in bounds and need no clamping.
     constexpr int PF = 8 / NC;
+    const char* next = reinterpret_cast<const char*>(kp) +
+                       ((size_t)head * (ntiles + kPadTiles) + t0) * TILE_BYTES;
     i32x4 ring[PF][NC];
-    auto refill = [&](i32x4 (&slot)[NC], int tt) {
-        const char* base = kbase + (size_t)min(tt, t1 - 1) * TILE_BYTES;
-        slot[0] = ring_load<0>(base, lane_off);
-        if constexpr (NC >= 2) slot[1] = ring_load<1024>(base, lane_off);
+    auto refill = [&](i32x4 (&slot)[NC]) {
+        slot[0] = ring_load<0>(next, lane_off);
+        if constexpr (NC >= 2) slot[1] = ring_load<1024>(next, lane_off);
         if constexpr (NC >= 4) {
-            slot[2] = ring_load<2048>(base, lane_off);
-            slot[3] = ring_load<3072>(base, lane_off);
+            slot[2] = ring_load<2048>(next, lane_off);
+            slot[3] = ring_load<3072>(next, lane_off);
         }
+        next += TILE_BYTES;
     };
 #pragma unroll
-    for (int u = 0; u < PF; ++u) refill(ring[u], t0 + u);
+    for (int u = 0; u < PF; ++u) refill(ring[u]);
 
     // Scores of the tile in ring slot `a`; PF - 1 later tiles are in flight.
     auto scores = [&](i32x4 (&a)[NC], f32x16 (&acc)[QB]) {
@@ -245,7 +263,7 @@ __global__ __launch_bounds__(64) void select_kernel(
     };
 
     // Largest of a lane's 16 scores: a max3 tree of depth 3 (8 instructions)
-    // rather than a chain, so the two blocks' reductions interleave.
+    // rather than a chain, so the blocks' reductions interleave.
     auto max16 = [](const f32x16& a) {
         const float l0 = fmaxf(fmaxf(a[0], a[1]), a[2]);
         const float l1 = fmaxf(fmaxf(a[3], a[4]), a[5]);
@@ -257,12 +275,12 @@ __global__ __launch_bounds__(64) void select_kernel(
 
     auto filter = [&](const f32x16 (&acc)[QB], int t) {
         float m[QB];
-        bool pass = false;
 #pragma unroll
         for (int b = 0; b < QB; ++b) m[b] = max16(acc[b]);
+        uint64_t any = 0;
 #pragma unroll
-        for (int b = 0; b < QB; ++b) pass = pass || m[b] > theta[b];
-        if (__builtin_amdgcn_ballot_w64(pass) != 0ull) {
+        for (int b = 0; b < QB; ++b) any |= __builtin_amdgcn_ballot_w64(m[b] > theta[b]);
+        if (any != 0ull) {
 #pragma unroll
             for (int b = 0; b < QB; ++b)
                 if (__builtin_amdgcn_ballot_w64(m[b] > theta[b]) != 0ull) rare_path(acc[b], b, t << 5);
@@ -271,30 +289,45 @@ __global__ __launch_bounds__(64) void select_kernel(
 
     // Software pipeline with two accumulator sets: the MFMAs of tile t+1 are
     // issued before tile t is filtered, so matrix cores and filter overlap.
+    // Scores of tiles past t1 (padding or a following graph) may be formed
+    // but are never filtered.  The main loop runs whole groups of PF tiles
+    // without checks; the tail group checks each tile.
     f32x16 acc_a[QB], acc_b[QB];
     scores(ring[0], acc_a);
-    refill(ring[0], t0 + PF);
-    for (int t = t0;; t += PF) {
+    refill(ring[0]);
+    int t = t0;
+    for (const int t_full = t0 + (t1 - t0) / PF * PF; t < t_full; t += PF) {
 #pragma unroll
         for (int u = 0; u < PF; u += 2) {
-            const int tc = t + u;  // acc_a holds tile tc
-            if (tc >= t1) goto stream_done;
-            if (tc + 1 < t1) {
-                scores(ring[u + 1], acc_b);
-                refill(ring[u + 1], tc + 1 + PF);
-            }
-            filter(acc_a, tc);
-            if (tc + 1 >= t1) goto stream_done;
-            if (tc + 2 < t1) {
-                scores(ring[(u + 2) % PF], acc_a);
-                refill(ring[(u + 2) % PF], tc + 2 + PF);
-            }
-            filter(acc_b, tc + 1);
+            scores(ring[u + 1], acc_b);
+            refill(ring[u + 1]);
+            filter(acc_a, t + u);
+            scores(ring[(u + 2) % PF], acc_a);
+            refill(ring[(u + 2) % PF]);
+            filter(acc_b, t + u + 1);
         }
     }
+#pragma unroll
+    for (int u = 0; u < PF; u += 2) {
+        if (t + u >= t1) goto stream_done;
+        scores(ring[u + 1], acc_b);
+        refill(ring[u + 1]);
+        filter(acc_a, t + u);
+        if (t + u + 1 >= t1) goto stream_done;
+        scores(ring[(u + 2) % PF], acc_a);
+        refill(ring[(u + 2) % PF]);
+        filter(acc_b, t + u + 1);
+    }
 stream_done:
-    // Drain the ring so no load is still writing registers at exit.
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // Drain the ring.  Every ring register is an operand of the wait: a
+    // prefetch whose tile is never used is dead to the compiler, which could
+    // otherwise hand its registers to other values while the load is still
+    // in flight and would land on top of them.
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) ring_wait<0>(ring[u][c]);
+    }
     merge_all();
 
     // Drain each heap in increasing order into slots k-1 .. 0, which leaves
@@ -311,20 +344,25 @@ stream_done:
             }
         }
     }
+    // The next item reinitialises the heaps this wave just drained.
+    __builtin_amdgcn_wave_barrier();
+    }  // item loop
 }
 
+// Tiles t >= ntiles of each head (the kPadTiles padding) are written as zeros.
 __global__ __launch_bounds__(256) void pack_k_kernel(const uint16_t* __restrict__ K,
                                                      uint4* __restrict__ kp, int32_t N, int32_t H,
                                                      int32_t nchunk, int32_t ntiles) {
-    const size_t total = (size_t)H * ntiles * nchunk * 64;
+    const int32_t ntiles_all = ntiles + kPadTiles;
+    const size_t total = (size_t)H * ntiles_all * nchunk * 64;
     const size_t u = (size_t)blockIdx.x * 256 + threadIdx.x;
     if (u >= total) return;
     const int lane = (int)(u & 63);
     size_t r = u >> 6;
     const int c = (int)(r % nchunk);
     r /= nchunk;
-    const int t = (int)(r % ntiles);
-    const int h = (int)(r / ntiles);
+    const int t = (int)(r % ntiles_all);
+    const int h = (int)(r / ntiles_all);
     const int key = t * 32 + (lane & 31);
     uint4 v = make_uint4(0, 0, 0, 0);
     if (key < N) {
@@ -339,8 +377,18 @@ hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, int
                            int32_t N, int32_t H, int32_t k, int32_t ntiles, int32_t* topk_idx,
                            hipStream_t stream) {
     const int64_t items = (int64_t)ntasks * H;
-    const int64_t grid = (items + kNumXcd - 1) / kNumXcd * kNumXcd;
     const size_t lds = select_lds_bytes(k, QB);
+    // One resident wave per workgroup slot of the chip, a multiple of the XCD
+    // count, never more workgroups than items.
+    int dev = 0, cus = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_kernel<D, QB>, 64, lds);
+    if (e != hipSuccess) return e;
+    const int64_t slots = (int64_t)std::max(cus, 1) * std::max(per_cu, 1);
+    const int64_t want = std::min<int64_t>(slots, (items + kNumXcd - 1) / kNumXcd * kNumXcd);
+    const int64_t grid = std::max<int64_t>(kNumXcd, want / kNumXcd * kNumXcd);
     hipLaunchKernelGGL((select_kernel<D, QB>), dim3((unsigned)grid), dim3(64), lds, stream,
                        reinterpret_cast<const uint4*>(kp), reinterpret_cast<const uint16_t*>(Q),
                        tasks, ntasks, N, H, k, ntiles, topk_idx);
@@ -357,7 +405,7 @@ size_t select_lds_bytes(int32_t k, int32_t qb) {
 hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t d, int32_t ntiles,
                          hipStream_t stream) {
     const int nchunk = d / 16;
-    const size_t total = (size_t)H * ntiles * nchunk * 64;
+    const size_t total = (size_t)H * (ntiles + kPadTiles) * nchunk * 64;
     if (total == 0) return hipSuccess;
     const unsigned blocks = (unsigned)((total + 255) / 256);
     hipLaunchKernelGGL(pack_k_kernel, dim3(blocks), dim3(256), 0, stream,

@@ -47,8 +47,8 @@ def test_status_strings(lib):
 def test_workspace_size(lib):
     # tiled copy of K, padded to whole 32-key tiles, 256-byte aligned
     n = lib.kmip_topk_workspace_size(500_000, 4, 16, 32, 1)
-    assert n == 4 * 15625 * 32 * 16 * 2
-    assert lib.kmip_topk_workspace_size(33, 1, 16, 4, 1) == 2 * 32 * 16 * 2
+    assert n == 4 * (15625 + 16) * 32 * 16 * 2
+    assert lib.kmip_topk_workspace_size(33, 1, 16, 4, 1) == (2 + 16) * 32 * 16 * 2
     multi = lib.kmip_topk_workspace_size(1000, 2, 32, 16, 7)
     assert multi > lib.kmip_topk_workspace_size(1000, 2, 32, 16, 1)
     assert lib.kmip_topk_workspace_size(100, 1, 24, 4, 1) == 0   # unsupported d
