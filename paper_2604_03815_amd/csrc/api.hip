@@ -77,11 +77,18 @@ size_t max_tasks(int64_t N, int32_t G) { return (size_t)(N / 32 + G + 1); }
 
 // Query blocks of 32 per wave: two when k is small and there are enough
 // items to fill the chip, one otherwise (bounded by LDS per workgroup).
-int32_t choose_qb(int64_t N, int32_t H, int32_t k, int32_t G) {
-    if (k > 32) return 1;
+// Candidate slots per lane: few, since LDS bounds the resident waves per CU
+// and occupancy pays more than the extra merges cost (4 with two blocks, 8
+// with one, measured on the 100k/500k/262k-node workloads).
+kmip::SelectShape choose_shape(int64_t N, int32_t H, int32_t k, int32_t G) {
     const int64_t items = (N + 63) / 64 * H;
-    return (items >= 8192 && G == 1) ? 2 : 1;
+    if (k <= 32 && items >= 8192 && G == 1) return kmip::SelectShape{2, 4};
+    return kmip::SelectShape{1, 8};
 }
+
+// Queries are grouped by direction (group.hip) for a single graph large
+// enough for the pre-pass to pay off.
+bool use_grouping(int64_t N, int32_t G) { return G == 1 && N >= 8192; }
 
 }  // namespace
 
@@ -105,6 +112,7 @@ size_t kmip_topk_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int3
     const int32_t G = num_graphs < 1 ? 1 : num_graphs;
     size_t bytes = align_up(packed_k_bytes(N, H, d));
     if (G > 1) bytes += align_up(max_tasks(N, G) * sizeof(kmip::Task));
+    if (use_grouping(N, G)) bytes += align_up(kmip::group_workspace_bytes((int32_t)N, H, d));
     return bytes;
 }
 
@@ -134,7 +142,8 @@ kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offse
     const int32_t ntiles = num_tiles(N);
     char* ws = reinterpret_cast<char*>(workspace);
     void* kp = ws;
-    const int32_t qb = choose_qb(N, H, k, G);
+    const kmip::SelectShape shape = choose_shape(N, H, k, G);
+    const int32_t qb = shape.qb;
 
     const kmip::Task* dtasks = nullptr;
     int32_t ntasks = 0;
@@ -162,9 +171,16 @@ kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offse
         ntasks = (int32_t)((N + 32 * qb - 1) / (32 * qb));
     }
 
+    int32_t* qperm = nullptr;
+    if (use_grouping(N, G)) {
+        void* gws = ws + align_up(packed_k_bytes(N, H, d));
+        hipError_t e = kmip::launch_group_queries(Q, n32, H, d, gws, &qperm, stream);
+        if (e != hipSuccess) return hip_fail(e, "query grouping launch");
+    }
     hipError_t e = kmip::launch_pack_k(K, kp, n32, H, d, ntiles, stream);
     if (e != hipSuccess) return hip_fail(e, "pack_k launch");
-    e = kmip::launch_select(kp, Q, dtasks, ntasks, n32, H, d, k, ntiles, qb, topk_idx, stream);
+    e = kmip::launch_select(kp, Q, dtasks, qperm, ntasks, n32, H, d, k, ntiles, shape, topk_idx,
+                            stream);
     if (e != hipSuccess) return hip_fail(e, "select launch");
     return ok();
 }

@@ -1,0 +1,165 @@
+// Query grouping for the score+select kernel.
+//
+// Which keys win the top-k of a query depends only on the query's direction
+// (scaling q by a positive factor scales every score alike).  Queries that
+// point the same way therefore share most of their top-k keys, and a wave
+// that holds such queries sees its running thresholds rise together and sends
+// far fewer key tiles down the selection path.  Per head, every query is
+// labelled with the nearest (largest cosine) of kGroupCenters reference
+// directions, taken from an evenly strided sample of the queries, and the
+// queries are stably bucketed by label.  The result is a permutation of the
+// query positions per head; the select kernel reads query perm[h][p] for
+// position p and writes that query's own output row, so the results do not
+// depend on the grouping at all, only the speed does.
+#include "kmip_device.h"
+#include "kmip_internal.h"
+
+namespace kmip {
+namespace {
+
+constexpr int C = kGroupCenters;
+
+// centers[h][c][:] = unit vector of query row floor((2c+1) N / 2C) of head h
+// (zero if that row is zero).
+__global__ __launch_bounds__(256) void group_centers_kernel(const uint16_t* __restrict__ Q,
+                                                            int32_t N, int32_t H, int32_t d,
+                                                            float* __restrict__ centers) {
+    const int c = threadIdx.x;
+    const int h = blockIdx.x;
+    const int64_t row = ((int64_t)(2 * c + 1) * N) / (2 * C);
+    const uint16_t* q = Q + ((size_t)row * H + h) * d;
+    float ss = 0.0f;
+    for (int t = 0; t < d; ++t) {
+        const float x = bf16_bits_to_f32(q[t]);
+        ss = fmaf(x, x, ss);
+    }
+    const float inv = ss > 0.0f ? rsqrtf(ss) : 0.0f;
+    float* dst = centers + ((size_t)h * C + c) * d;
+    for (int t = 0; t < d; ++t) dst[t] = bf16_bits_to_f32(q[t]) * inv;
+}
+
+// label[h][i] = argmax_c <q_i, center_c> (lowest c on ties); hist[h][c] counts
+// the labels.  One block of 256 queries of one head; the head's centres pass
+// through LDS in chunks of at most 32 KB, and every thread reads the same
+// centre at a time (broadcast).
+template <int D>
+__global__ __launch_bounds__(256) void group_label_kernel(const uint16_t* __restrict__ Q,
+                                                          const float* __restrict__ centers,
+                                                          int32_t N, int32_t H,
+                                                          uint16_t* __restrict__ label,
+                                                          int32_t* __restrict__ hist) {
+    constexpr int CH = (8192 / D) < C ? (8192 / D) : C;
+    __shared__ float cs[CH * D];
+    __shared__ int32_t lh[C];
+    const int h = blockIdx.y;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const bool valid = i < N;
+    float q[D];
+    const uint16_t* row = Q + ((size_t)(valid ? i : 0) * H + h) * D;
+#pragma unroll
+    for (int c8 = 0; c8 < D / 8; ++c8) {
+        const uint4 u = *reinterpret_cast<const uint4*>(row + 8 * c8);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            q[8 * c8 + 2 * e] = bf16_bits_to_f32(w[e] & 0xFFFFu);
+            q[8 * c8 + 2 * e + 1] = bf16_bits_to_f32(w[e] >> 16);
+        }
+    }
+    lh[threadIdx.x] = 0;
+    float best = -INFINITY;
+    int arg = 0;
+    for (int c0 = 0; c0 < C; c0 += CH) {
+        __syncthreads();
+        for (int e = threadIdx.x; e < CH * D; e += 256) cs[e] = centers[((size_t)h * C + c0) * D + e];
+        __syncthreads();
+        for (int c = 0; c < CH; ++c) {
+            float s = 0.0f;
+#pragma unroll
+            for (int t = 0; t < D; ++t) s = fmaf(q[t], cs[c * D + t], s);
+            if (s > best) {
+                best = s;
+                arg = c0 + c;
+            }
+        }
+    }
+    if (valid) {
+        label[(size_t)h * N + i] = (uint16_t)arg;
+        atomicAdd(&lh[arg], 1);
+    }
+    __syncthreads();
+    if (lh[threadIdx.x] != 0) atomicAdd(&hist[(size_t)h * C + threadIdx.x], lh[threadIdx.x]);
+}
+
+// Exclusive prefix sum of each head's histogram, in place (one block per head).
+__global__ __launch_bounds__(256) void group_scan_kernel(int32_t* __restrict__ hist) {
+    __shared__ int32_t s[C];
+    int32_t* hh = hist + (size_t)blockIdx.x * C;
+    const int t = threadIdx.x;
+    const int32_t own = hh[t];
+    s[t] = own;
+    __syncthreads();
+    for (int off = 1; off < C; off <<= 1) {
+        const int32_t add = t >= off ? s[t - off] : 0;
+        __syncthreads();
+        s[t] += add;
+        __syncthreads();
+    }
+    hh[t] = s[t] - own;
+}
+
+// perm[h][cursor[h][label]++] = i.  The order inside one bucket follows the
+// atomics and is not fixed; any order is a valid grouping.
+__global__ __launch_bounds__(256) void group_scatter_kernel(const uint16_t* __restrict__ label,
+                                                            int32_t* __restrict__ cursor,
+                                                            int32_t N, int32_t H,
+                                                            int32_t* __restrict__ perm) {
+    const int h = blockIdx.y;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= N) return;
+    const int lab = label[(size_t)h * N + i];
+    const int32_t pos = atomicAdd(&cursor[(size_t)h * C + lab], 1);
+    perm[(size_t)h * N + pos] = (int32_t)i;
+}
+
+}  // namespace
+
+size_t group_workspace_bytes(int32_t N, int32_t H, int32_t d) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    return al((size_t)H * C * d * sizeof(float)) + al((size_t)H * N * sizeof(uint16_t)) +
+           al((size_t)H * C * sizeof(int32_t)) + al((size_t)H * N * sizeof(int32_t));
+}
+
+hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, void* ws,
+                                int32_t** perm_out, hipStream_t stream) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    char* p = reinterpret_cast<char*>(ws);
+    float* centers = reinterpret_cast<float*>(p);
+    p += al((size_t)H * C * d * sizeof(float));
+    uint16_t* label = reinterpret_cast<uint16_t*>(p);
+    p += al((size_t)H * N * sizeof(uint16_t));
+    int32_t* hist = reinterpret_cast<int32_t*>(p);
+    p += al((size_t)H * C * sizeof(int32_t));
+    int32_t* perm = reinterpret_cast<int32_t*>(p);
+    *perm_out = perm;
+
+    const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
+    hipError_t e = launch_fill_zero(reinterpret_cast<float*>(hist), (size_t)H * C, stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(group_centers_kernel, dim3(H), dim3(C), 0, stream, q, N, H, d, centers);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const dim3 grid((unsigned)((N + 255) / 256), (unsigned)H);
+    if (d == 16)
+        hipLaunchKernelGGL(group_label_kernel<16>, grid, dim3(256), 0, stream, q, centers, N, H, label, hist);
+    else if (d == 32)
+        hipLaunchKernelGGL(group_label_kernel<32>, grid, dim3(256), 0, stream, q, centers, N, H, label, hist);
+    else
+        hipLaunchKernelGGL(group_label_kernel<64>, grid, dim3(256), 0, stream, q, centers, N, H, label, hist);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(group_scan_kernel, dim3(H), dim3(C), 0, stream, hist);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(group_scatter_kernel, grid, dim3(256), 0, stream, label, hist, N, H, perm);
+    return hipGetLastError();
+}
+
+}  // namespace kmip

@@ -6,9 +6,6 @@
 
 namespace kmip {
 
-// Candidate-buffer slots per lane and per query block in the select kernel.
-constexpr int kCandSlots = 8;
-
 // Zero tiles appended to each head of the tiled key buffer, so that key
 // prefetches running past a head's last tile stay in bounds (at least the
 // prefetch depth plus one).
@@ -35,13 +32,33 @@ struct Task {
 hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t d, int32_t ntiles,
                          hipStream_t stream);
 
-// Score + select.  qb = query blocks (of 32) per wave, 1 or 2.
-hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, int32_t ntasks,
-                         int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles, int32_t qb,
-                         int32_t* topk_idx, hipStream_t stream);
+// Shape of one select wave: query blocks of 32 (1 or 2) and candidate-buffer
+// slots per lane and block (4, 8 or 16; 4 and 8 with two blocks, 8 and 16
+// with one).
+struct SelectShape {
+    int32_t qb;
+    int32_t slots;
+};
+
+// Score + select.  qperm: NULL, or per head a permutation [H][N] of the query
+// positions (query qperm[h][p] is processed at position p).
+hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
+                         int32_t ntasks, int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles,
+                         SelectShape shape, int32_t* topk_idx, hipStream_t stream);
 
 // Bytes of LDS one select workgroup uses.
-size_t select_lds_bytes(int32_t k, int32_t qb);
+size_t select_lds_bytes(int32_t k, SelectShape shape);
+
+// Query grouping by direction (group.hip): reference directions per head.
+constexpr int kGroupCenters = 256;
+
+// Workspace bytes launch_group_queries needs.
+size_t group_workspace_bytes(int32_t N, int32_t H, int32_t d);
+
+// Writes into ws a per-head permutation [H][N] of the queries that places
+// queries of similar direction next to each other; *perm_out points to it.
+hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, void* ws,
+                                int32_t** perm_out, hipStream_t stream);
 
 hipError_t launch_attend(const void* Q, const void* K, const void* V, const int32_t* idx,
                          int32_t N, int32_t H, int32_t d, int32_t k, float scale, float* out,

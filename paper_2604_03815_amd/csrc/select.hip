@@ -7,15 +7,18 @@
 // streams key tiles, forms 32x32 score tiles with one bf16 MFMA per 16 dims
 // (fp32 accumulation) and keeps a running top-k per query in LDS.
 //
-// Work decomposition: an item is QB blocks of 32 queries of one graph and
-// one head; its wave streams every 32-key tile that overlaps the graph.  One
+// Work decomposition: an item is QB blocks of 32 query positions of one graph
+// and one head; its wave streams every 32-key tile that overlaps the graph.
+// Positions map to queries through an optional per-head permutation that
+// puts queries of similar direction side by side (group.hip).  One
 // wave per workgroup; workgroups are persistent and loop over items.  MFMA operand roles: A = 32 keys x 16 dims, B = 16 dims x 32
 // queries, so lane l ends up holding 16 scores of query (l % 32) against keys
 //   row(r, l) = 8 * (r / 4) + 4 * (l / 32) + (r % 4),  r = 0..15
 // of the tile.  Lanes l and l + 32 share a query.
 //
-// Selection per query: a min-heap of the k best 64-bit keys (score code,
-// ~index) in LDS; its root's score is a threshold theta kept in a register.
+// Selection per query: a 4-ary min-heap of the k best 64-bit keys (score
+// code, ~index) in LDS; its root's score is a threshold theta kept in a
+// register.
 // Per tile and block each lane reduces its 16 scores with a max3 tree and
 // compares once with theta.  Only when some lane's maximum beats theta does
 // the wave pick out the scores above theta, append them (with their key
@@ -36,8 +39,6 @@
 
 namespace kmip {
 namespace {
-
-constexpr int kSlots = kCandSlots;
 
 __device__ __forceinline__ int tile_row(int r, int half) {
     return 8 * (r >> 2) + 4 * half + (r & 3);
@@ -70,34 +71,41 @@ __device__ __forceinline__ void ring_wait(i32x4& v) {
     asm volatile("s_waitcnt vmcnt(%1)" : "+v"(v) : "n"(N));
 }
 
-// Min-heap in LDS, column `col` of a [size][32] array of keys.  Places x at
-// the root and sifts it down.
-__device__ __forceinline__ void heap_sift_down(uint64_t* hp, int col, int size, uint64_t x) {
+// 4-ary min-heap in LDS: column `col` of a [k + kHeapPad][32] array of keys,
+// node p with children 4p+1 .. 4p+4.  Rows k .. k+2 hold kHeapTop, above any
+// real key, so that the last parent's missing children never win and no
+// child needs a bounds check; a drained row is set to kHeapTop too.  Four
+// children per level (read together, one LDS round trip) halve the depth of
+// a binary heap: 3 levels below the root for k = 32, 4 for k = 128.
+constexpr int kHeapPad = 3;
+constexpr uint64_t kHeapTop = ~0ull;
+
+__device__ __forceinline__ uint64_t min_u64(uint64_t a, uint64_t b) { return b < a ? b : a; }
+
+// Places x at the root and sifts it down.
+__device__ __forceinline__ void heap_sift_down(uint64_t* hp, int col, int k, uint64_t x) {
     int pos = 0;
     for (;;) {
-        int l = 2 * pos + 1;
-        if (l >= size) break;
-        uint64_t cm = hp[l * 32 + col];
-        int m = l;
-        if (l + 1 < size) {
-            uint64_t cr = hp[(l + 1) * 32 + col];
-            if (cr < cm) {
-                cm = cr;
-                m = l + 1;
-            }
-        }
-        if (x <= cm) break;
-        hp[pos * 32 + col] = cm;
-        pos = m;
+        const int c = 4 * pos + 1;
+        if (c >= k) break;
+        const uint64_t m0 = hp[c * 32 + col], m1 = hp[(c + 1) * 32 + col];
+        const uint64_t m2 = hp[(c + 2) * 32 + col], m3 = hp[(c + 3) * 32 + col];
+        const int j01 = m1 < m0 ? 1 : 0, j23 = m3 < m2 ? 3 : 2;
+        const uint64_t v01 = min_u64(m0, m1), v23 = min_u64(m2, m3);
+        const int j = v23 < v01 ? j23 : j01;
+        const uint64_t m = min_u64(v01, v23);
+        if (x <= m) break;
+        hp[pos * 32 + col] = m;
+        pos = c + j;
     }
     hp[pos * 32 + col] = x;
 }
 
-template <int D, int QB>
+template <int D, int QB, int SLOTS>
 __global__ __launch_bounds__(64) void select_kernel(
     const uint4* __restrict__ kp, const uint16_t* __restrict__ Q, const Task* __restrict__ tasks,
-    int32_t ntasks, int32_t N, int32_t H, int32_t k, int32_t ntiles,
-    int32_t* __restrict__ topk_idx) {
+    const int32_t* __restrict__ qperm, int32_t ntasks, int32_t N, int32_t H, int32_t k,
+    int32_t ntiles, int32_t* __restrict__ topk_idx) {
     constexpr int NC = D / 16;
     constexpr int TILE_BYTES = NC * 64 * 16;
     extern __shared__ uint64_t lds[];
@@ -135,18 +143,22 @@ __global__ __launch_bounds__(64) void select_kernel(
     const int col = lane & 31;
     const int half = lane >> 5;
 
-    uint64_t* heaps = lds;                          // [QB][k][32]
-    uint64_t* cand = lds + (size_t)QB * k * 32;     // [QB][kSlots][64]
-    float* stash = reinterpret_cast<float*>(cand + (size_t)QB * kSlots * 64);  // [16][64]
+    const int hrows = k + kHeapPad;
+    uint64_t* heaps = lds;                              // [QB][k + kHeapPad][32]
+    uint64_t* cand = lds + (size_t)QB * hrows * 32;     // [QB][SLOTS][64]
+    float* stash = reinterpret_cast<float*>(cand + (size_t)QB * SLOTS * 64);  // [16][64]
 
     bf16x8 bq[QB][NC];
     float theta[QB];
     int cnt[QB];
+    int32_t qid[QB];
+    const int32_t* hperm = qperm != nullptr ? qperm + (size_t)head * N : nullptr;
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
         const int qi = 32 * b + col;
         const bool valid = qi < q_count;
-        const uint16_t* qrow = Q + ((size_t)(q_begin + qi) * H + head) * D + 8 * half;
+        qid[b] = valid ? (hperm != nullptr ? hperm[q_begin + qi] : q_begin + qi) : 0;
+        const uint16_t* qrow = Q + ((size_t)qid[b] * H + head) * D + 8 * half;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             uint4 u = valid ? *reinterpret_cast<const uint4*>(qrow + 16 * c) : make_uint4(0, 0, 0, 0);
@@ -155,7 +167,7 @@ __global__ __launch_bounds__(64) void select_kernel(
         theta[b] = valid ? -INFINITY : INFINITY;
         cnt[b] = 0;
     }
-    for (int e = lane; e < QB * k * 32; e += 64) heaps[e] = 0ull;
+    for (int e = lane; e < QB * hrows * 32; e += 64) heaps[e] = (e / 32) % hrows < k ? 0ull : kHeapTop;
 
     // Fold every lane's candidates into the heaps and refresh theta.  With
     // two blocks, each phase has the lower half-wave on one block's heaps and
@@ -165,8 +177,8 @@ __global__ __launch_bounds__(64) void select_kernel(
         for (int ph = 0; ph < 2; ++ph) {
             const int b = QB == 2 ? (half ^ ph) : 0;
             if (QB == 2 || half == ph) {
-                uint64_t* hp = heaps + (size_t)b * k * 32;
-                const uint64_t* cb = cand + (size_t)b * kSlots * 64;
+                uint64_t* hp = heaps + (size_t)b * hrows * 32;
+                const uint64_t* cb = cand + (size_t)b * SLOTS * 64;
                 const int n = b == 0 ? cnt[0] : cnt[QB - 1];
                 for (int e = 0; e < n; ++e) {
                     uint64_t c = cb[e * 64 + lane];
@@ -181,7 +193,7 @@ __global__ __launch_bounds__(64) void select_kernel(
 #pragma unroll
         for (int b = 0; b < QB; ++b) {
             if (theta[b] != INFINITY) {
-                const uint64_t root = heaps[(size_t)b * k * 32 + col];
+                const uint64_t root = heaps[(size_t)b * hrows * 32 + col];
                 theta[b] = root == 0ull ? -INFINITY : key_score(root);
             }
             cnt[b] = 0;
@@ -195,7 +207,7 @@ __global__ __launch_bounds__(64) void select_kernel(
     // largest per-lane count, usually one or two.  A buffer that fills up is
     // folded between two rounds.
     auto rare_path = [&](const f32x16& acc, int b, int tbase) {
-        uint64_t* cb = cand + (size_t)b * kSlots * 64;
+        uint64_t* cb = cand + (size_t)b * SLOTS * 64;
         // Bit 15 - r of mask is set when score r beats theta: theta - s is
         // negative exactly then, and alignbit shifts its sign bit in.
         uint32_t mask = 0;
@@ -218,7 +230,7 @@ __global__ __launch_bounds__(64) void select_kernel(
                 cb[cnt[b] * 64 + lane] = make_key(stash[r * 64 + lane], tbase + tile_row(r, half));
                 cnt[b] += 1;
             }
-            if (__builtin_amdgcn_ballot_w64(cnt[b] == kSlots) != 0ull) merge_all();
+            if (__builtin_amdgcn_ballot_w64(cnt[b] == SLOTS) != 0ull) merge_all();
         }
         __builtin_amdgcn_wave_barrier();
     };
@@ -331,16 +343,21 @@ stream_done:
     merge_all();
 
     // Drain each heap in increasing order into slots k-1 .. 0, which leaves
-    // the row sorted by (score desc, index asc); sentinels become -1.
+    // the row sorted by (score desc, index asc); sentinels become -1.  The
+    // vacated last row takes kHeapTop, so the heap shrinks without bounds.
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
         const int qi = 32 * b + col;
         if (half == 0 && qi < q_count) {
-            uint64_t* hp = heaps + (size_t)b * k * 32;
-            int32_t* dst = topk_idx + ((size_t)(q_begin + qi) * H + head) * k;
+            uint64_t* hp = heaps + (size_t)b * hrows * 32;
+            int32_t* dst = topk_idx + ((size_t)qid[b] * H + head) * k;
             for (int p = k - 1; p >= 0; --p) {
                 dst[p] = key_index(hp[col]);
-                if (p > 0) heap_sift_down(hp, col, p, hp[p * 32 + col]);
+                if (p > 0) {
+                    const uint64_t last = hp[p * 32 + col];
+                    hp[p * 32 + col] = kHeapTop;
+                    heap_sift_down(hp, col, k, last);
+                }
             }
         }
     }
@@ -372,33 +389,33 @@ __global__ __launch_bounds__(256) void pack_k_kernel(const uint16_t* __restrict_
     kp[u] = v;
 }
 
-template <int D, int QB>
-hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, int32_t ntasks,
-                           int32_t N, int32_t H, int32_t k, int32_t ntiles, int32_t* topk_idx,
-                           hipStream_t stream) {
+template <int D, int QB, int SLOTS>
+hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
+                           int32_t ntasks, int32_t N, int32_t H, int32_t k, int32_t ntiles,
+                           int32_t* topk_idx, hipStream_t stream) {
     const int64_t items = (int64_t)ntasks * H;
-    const size_t lds = select_lds_bytes(k, QB);
+    const size_t lds = select_lds_bytes(k, SelectShape{QB, SLOTS});
     // One resident wave per workgroup slot of the chip, a multiple of the XCD
     // count, never more workgroups than items.
     int dev = 0, cus = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_kernel<D, QB>, 64, lds);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_kernel<D, QB, SLOTS>, 64, lds);
     if (e != hipSuccess) return e;
     const int64_t slots = (int64_t)std::max(cus, 1) * std::max(per_cu, 1);
     const int64_t want = std::min<int64_t>(slots, (items + kNumXcd - 1) / kNumXcd * kNumXcd);
     const int64_t grid = std::max<int64_t>(kNumXcd, want / kNumXcd * kNumXcd);
-    hipLaunchKernelGGL((select_kernel<D, QB>), dim3((unsigned)grid), dim3(64), lds, stream,
+    hipLaunchKernelGGL((select_kernel<D, QB, SLOTS>), dim3((unsigned)grid), dim3(64), lds, stream,
                        reinterpret_cast<const uint4*>(kp), reinterpret_cast<const uint16_t*>(Q),
-                       tasks, ntasks, N, H, k, ntiles, topk_idx);
+                       tasks, qperm, ntasks, N, H, k, ntiles, topk_idx);
     return hipGetLastError();
 }
 
 }  // namespace
 
-size_t select_lds_bytes(int32_t k, int32_t qb) {
-    return (size_t)qb * ((size_t)k * 32 + (size_t)kSlots * 64) * sizeof(uint64_t) +
+size_t select_lds_bytes(int32_t k, SelectShape shape) {
+    return (size_t)shape.qb * ((size_t)(k + kHeapPad) * 32 + (size_t)shape.slots * 64) * sizeof(uint64_t) +
            (size_t)16 * 64 * sizeof(float);
 }
 
@@ -414,19 +431,23 @@ hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t 
     return hipGetLastError();
 }
 
-hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, int32_t ntasks,
-                         int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles, int32_t qb,
-                         int32_t* topk_idx, hipStream_t stream) {
+hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
+                         int32_t ntasks, int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles,
+                         SelectShape shape, int32_t* topk_idx, hipStream_t stream) {
     if (ntasks <= 0) return hipSuccess;
-#define KMIP_SELECT_CASE(DD, QQ)                                                                 \
-    if (d == DD && qb == QQ)                                                                     \
-        return launch_select_t<DD, QQ>(kp, Q, tasks, ntasks, N, H, k, ntiles, topk_idx, stream);
-    KMIP_SELECT_CASE(16, 1)
-    KMIP_SELECT_CASE(16, 2)
-    KMIP_SELECT_CASE(32, 1)
-    KMIP_SELECT_CASE(32, 2)
-    KMIP_SELECT_CASE(64, 1)
-    KMIP_SELECT_CASE(64, 2)
+#define KMIP_SELECT_CASE(DD, QQ, SS)                                                             \
+    if (d == DD && shape.qb == QQ && shape.slots == SS)                                          \
+        return launch_select_t<DD, QQ, SS>(kp, Q, tasks, qperm, ntasks, N, H, k, ntiles,         \
+                                           topk_idx, stream);
+#define KMIP_SELECT_D(DD)         \
+    KMIP_SELECT_CASE(DD, 2, 4)    \
+    KMIP_SELECT_CASE(DD, 2, 8)    \
+    KMIP_SELECT_CASE(DD, 1, 8)    \
+    KMIP_SELECT_CASE(DD, 1, 16)
+    KMIP_SELECT_D(16)
+    KMIP_SELECT_D(32)
+    KMIP_SELECT_D(64)
+#undef KMIP_SELECT_D
 #undef KMIP_SELECT_CASE
     return hipErrorInvalidValue;
 }
