@@ -72,6 +72,9 @@ size_t packed_k_bytes(int64_t N, int32_t H, int32_t d) {
     return (size_t)H * (size_t)(num_tiles(N) + kmip::kPadTiles) * 32 * (size_t)d * 2;
 }
 
+// The select kernel's per-XCD work counters, right after the tiled keys.
+constexpr size_t kCounterBytes = kAlign;
+
 // Upper bound on the work-list length for any query-block size.
 size_t max_tasks(int64_t N, int32_t G) { return (size_t)(N / 32 + G + 1); }
 
@@ -110,7 +113,7 @@ const char* kmip_last_error(void) { return g_last_error.c_str(); }
 size_t kmip_topk_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t num_graphs) {
     if (check_sizes(N, H, d, k) != KMIP_OK) return 0;
     const int32_t G = num_graphs < 1 ? 1 : num_graphs;
-    size_t bytes = align_up(packed_k_bytes(N, H, d));
+    size_t bytes = align_up(packed_k_bytes(N, H, d)) + kCounterBytes;
     if (G > 1) bytes += align_up(max_tasks(N, G) * sizeof(kmip::Task));
     if (use_grouping(N, G)) bytes += align_up(kmip::group_workspace_bytes((int32_t)N, H, d));
     return bytes;
@@ -162,7 +165,7 @@ kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offse
             return (int64_t)a.q_count * (a.key_hi - a.key_lo) > (int64_t)b.q_count * (b.key_hi - b.key_lo);
         });
         ntasks = (int32_t)tasks.size();
-        void* dst = ws + align_up(packed_k_bytes(N, H, d));
+        void* dst = ws + align_up(packed_k_bytes(N, H, d)) + kCounterBytes;
         hipError_t e = hipMemcpyAsync(dst, tasks.data(), tasks.size() * sizeof(kmip::Task),
                                       hipMemcpyHostToDevice, stream);
         if (e != hipSuccess) return hip_fail(e, "work list upload");
@@ -173,14 +176,15 @@ kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offse
 
     int32_t* qperm = nullptr;
     if (use_grouping(N, G)) {
-        void* gws = ws + align_up(packed_k_bytes(N, H, d));
+        void* gws = ws + align_up(packed_k_bytes(N, H, d)) + kCounterBytes;
         hipError_t e = kmip::launch_group_queries(Q, n32, H, d, gws, &qperm, stream);
         if (e != hipSuccess) return hip_fail(e, "query grouping launch");
     }
     hipError_t e = kmip::launch_pack_k(K, kp, n32, H, d, ntiles, stream);
     if (e != hipSuccess) return hip_fail(e, "pack_k launch");
-    e = kmip::launch_select(kp, Q, dtasks, qperm, ntasks, n32, H, d, k, ntiles, shape, topk_idx,
-                            stream);
+    int32_t* work_ctr = reinterpret_cast<int32_t*>(ws + align_up(packed_k_bytes(N, H, d)));
+    e = kmip::launch_select(kp, Q, dtasks, qperm, ntasks, n32, H, d, k, ntiles, shape, work_ctr,
+                            topk_idx, stream);
     if (e != hipSuccess) return hip_fail(e, "select launch");
     return ok();
 }

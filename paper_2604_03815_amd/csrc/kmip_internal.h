@@ -41,10 +41,12 @@ struct SelectShape {
 };
 
 // Score + select.  qperm: NULL, or per head a permutation [H][N] of the query
-// positions (query qperm[h][p] is processed at position p).
+// positions (query qperm[h][p] is processed at position p).  work_ctr:
+// kNumXcd device ints of scratch (the per-XCD item counters, zeroed here).
 hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
                          int32_t ntasks, int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles,
-                         SelectShape shape, int32_t* topk_idx, hipStream_t stream);
+                         SelectShape shape, int32_t* work_ctr, int32_t* topk_idx,
+                         hipStream_t stream);
 
 // Bytes of LDS one select workgroup uses.
 size_t select_lds_bytes(int32_t k, SelectShape shape);

@@ -71,6 +71,30 @@ __device__ __forceinline__ void ring_wait(i32x4& v) {
     asm volatile("s_waitcnt vmcnt(%1)" : "+v"(v) : "n"(N));
 }
 
+// acc[r] for a lane-varying r in 0..15, without indexed register access: a
+// 4-level tree of bitwise selects (one v_bfi per node) keyed on the bits of
+// r.  Written with masks rather than conditionals so that the compiler does
+// not turn the tree back into a dynamic vector index.
+__device__ __forceinline__ uint32_t bit_mask(int r, int bit) {
+    return 0u - (((uint32_t)r >> bit) & 1u);
+}
+
+__device__ __forceinline__ uint32_t bsel(uint32_t m, uint32_t x, uint32_t y) {
+    return (x & m) | (y & ~m);
+}
+
+__device__ __forceinline__ float pick16(const f32x16& a, int r) {
+    const uint32_t m3 = bit_mask(r, 3), m2 = bit_mask(r, 2), m1 = bit_mask(r, 1), m0 = bit_mask(r, 0);
+    uint32_t v8[8], v4[4], v2[2];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v8[i] = bsel(m3, __float_as_uint(a[i + 8]), __float_as_uint(a[i]));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v4[i] = bsel(m2, v8[i + 4], v8[i]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) v2[i] = bsel(m1, v4[i + 2], v4[i]);
+    return __uint_as_float(bsel(m0, v2[1], v2[0]));
+}
+
 // 4-ary min-heap in LDS: column `col` of a [k + kHeapPad][32] array of keys,
 // node p with children 4p+1 .. 4p+4.  Rows k .. k+2 hold kHeapTop, above any
 // real key, so that the last parent's missing children never win and no
@@ -105,23 +129,29 @@ template <int D, int QB, int SLOTS>
 __global__ __launch_bounds__(64) void select_kernel(
     const uint4* __restrict__ kp, const uint16_t* __restrict__ Q, const Task* __restrict__ tasks,
     const int32_t* __restrict__ qperm, int32_t ntasks, int32_t N, int32_t H, int32_t k,
-    int32_t ntiles, int32_t* __restrict__ topk_idx) {
+    int32_t ntiles, int32_t* __restrict__ work_ctr, int32_t* __restrict__ topk_idx) {
     constexpr int NC = D / 16;
     constexpr int TILE_BYTES = NC * 64 * 16;
     extern __shared__ uint64_t lds[];
 
     // Persistent, XCD-aware schedule.  Workgroups are dispatched to the XCDs
-    // round-robin; the ones on XCD x walk a contiguous range of (head, task)
-    // items in lock-step rounds.  All workgroups start together and items
-    // stream the same key tiles in the same order, so the waves of one XCD
-    // read each tile at nearly the same time and share it in that XCD's L2.
+    // round-robin; the ones on XCD x take items of a contiguous range of
+    // (head, task) items, in order, from that XCD's counter.  Items stream
+    // the same key tiles in the same order, so the waves of one XCD read each
+    // tile at nearly the same time and share it in that XCD's L2.  Taking
+    // items from a counter balances items of unequal cost and keeps a
+    // workgroup that only becomes resident late (when the grid exceeds what
+    // fits) from delaying the items it would otherwise own.
     const int items = ntasks * H;
     const int xcd = blockIdx.x % kNumXcd;
-    const int wgs_per_xcd = gridDim.x / kNumXcd;
     const int items_per_xcd = (items + kNumXcd - 1) / kNumXcd;
-    const int item_end = min(items, (xcd + 1) * items_per_xcd);
-    for (int item = xcd * items_per_xcd + blockIdx.x / kNumXcd; item < item_end;
-         item += wgs_per_xcd) {
+    const int item_lo = xcd * items_per_xcd;
+    const int item_end = min(items, item_lo + items_per_xcd);
+    for (;;) {
+    int claim = 0;
+    if (threadIdx.x == 0) claim = atomicAdd(&work_ctr[xcd], 1);
+    const int item = item_lo + __builtin_amdgcn_readfirstlane(claim);
+    if (item >= item_end) break;
     const int head = item / ntasks;
     const int task = item - head * ntasks;
 
@@ -146,7 +176,6 @@ __global__ __launch_bounds__(64) void select_kernel(
     const int hrows = k + kHeapPad;
     uint64_t* heaps = lds;                              // [QB][k + kHeapPad][32]
     uint64_t* cand = lds + (size_t)QB * hrows * 32;     // [QB][SLOTS][64]
-    float* stash = reinterpret_cast<float*>(cand + (size_t)QB * SLOTS * 64);  // [16][64]
 
     bf16x8 bq[QB][NC];
     float theta[QB];
@@ -202,10 +231,11 @@ __global__ __launch_bounds__(64) void select_kernel(
 
     // Rare path for block b of the tile starting at key tbase.  Each lane
     // builds a 16-bit mask of its scores above theta (theta still reflects
-    // earlier tiles only, so the strict test is exact), parks the scores in
-    // LDS, and the wave then walks the set bits: as many rounds as the
-    // largest per-lane count, usually one or two.  A buffer that fills up is
-    // folded between two rounds.
+    // earlier tiles only, so the strict test is exact), and the wave then
+    // walks the set bits: as many rounds as the largest per-lane count,
+    // usually one or two.  A lane picks the score of its bit out of its 16
+    // registers with a 4-level select on the bits of the register number.  A
+    // buffer that fills up is folded between two rounds.
     auto rare_path = [&](const f32x16& acc, int b, int tbase) {
         uint64_t* cb = cand + (size_t)b * SLOTS * 64;
         // Bit 15 - r of mask is set when score r beats theta: theta - s is
@@ -221,13 +251,11 @@ __global__ __launch_bounds__(64) void select_kernel(
                 if (j < key_lo || j >= key_hi) mask &= ~(1u << (15 - r));
             }
         }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) stash[r * 64 + lane] = acc[r];
         while (__builtin_amdgcn_ballot_w64(mask != 0u) != 0ull) {
             if (mask != 0u) {
                 const int r = 15 - __builtin_ctz(mask);
                 mask &= mask - 1u;
-                cb[cnt[b] * 64 + lane] = make_key(stash[r * 64 + lane], tbase + tile_row(r, half));
+                cb[cnt[b] * 64 + lane] = make_key(pick16(acc, r), tbase + tile_row(r, half));
                 cnt[b] += 1;
             }
             if (__builtin_amdgcn_ballot_w64(cnt[b] == SLOTS) != 0ull) merge_all();
@@ -392,7 +420,7 @@ __global__ __launch_bounds__(256) void pack_k_kernel(const uint16_t* __restrict_
 template <int D, int QB, int SLOTS>
 hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
                            int32_t ntasks, int32_t N, int32_t H, int32_t k, int32_t ntiles,
-                           int32_t* topk_idx, hipStream_t stream) {
+                           int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream) {
     const int64_t items = (int64_t)ntasks * H;
     const size_t lds = select_lds_bytes(k, SelectShape{QB, SLOTS});
     // One resident wave per workgroup slot of the chip, a multiple of the XCD
@@ -403,20 +431,20 @@ hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, con
     if (e == hipSuccess)
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_kernel<D, QB, SLOTS>, 64, lds);
     if (e != hipSuccess) return e;
+    if ((e = launch_fill_zero(reinterpret_cast<float*>(work_ctr), kNumXcd, stream)) != hipSuccess) return e;
     const int64_t slots = (int64_t)std::max(cus, 1) * std::max(per_cu, 1);
     const int64_t want = std::min<int64_t>(slots, (items + kNumXcd - 1) / kNumXcd * kNumXcd);
     const int64_t grid = std::max<int64_t>(kNumXcd, want / kNumXcd * kNumXcd);
     hipLaunchKernelGGL((select_kernel<D, QB, SLOTS>), dim3((unsigned)grid), dim3(64), lds, stream,
                        reinterpret_cast<const uint4*>(kp), reinterpret_cast<const uint16_t*>(Q),
-                       tasks, qperm, ntasks, N, H, k, ntiles, topk_idx);
+                       tasks, qperm, ntasks, N, H, k, ntiles, work_ctr, topk_idx);
     return hipGetLastError();
 }
 
 }  // namespace
 
 size_t select_lds_bytes(int32_t k, SelectShape shape) {
-    return (size_t)shape.qb * ((size_t)(k + kHeapPad) * 32 + (size_t)shape.slots * 64) * sizeof(uint64_t) +
-           (size_t)16 * 64 * sizeof(float);
+    return (size_t)shape.qb * ((size_t)(k + kHeapPad) * 32 + (size_t)shape.slots * 64) * sizeof(uint64_t);
 }
 
 hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t d, int32_t ntiles,
@@ -433,12 +461,13 @@ hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t 
 
 hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
                          int32_t ntasks, int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles,
-                         SelectShape shape, int32_t* topk_idx, hipStream_t stream) {
+                         SelectShape shape, int32_t* work_ctr, int32_t* topk_idx,
+                         hipStream_t stream) {
     if (ntasks <= 0) return hipSuccess;
 #define KMIP_SELECT_CASE(DD, QQ, SS)                                                             \
     if (d == DD && shape.qb == QQ && shape.slots == SS)                                          \
         return launch_select_t<DD, QQ, SS>(kp, Q, tasks, qperm, ntasks, N, H, k, ntiles,         \
-                                           topk_idx, stream);
+                                           work_ctr, topk_idx, stream);
 #define KMIP_SELECT_D(DD)         \
     KMIP_SELECT_CASE(DD, 2, 4)    \
     KMIP_SELECT_CASE(DD, 2, 8)    \
