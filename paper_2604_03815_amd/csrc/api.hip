@@ -72,8 +72,8 @@ size_t packed_k_bytes(int64_t N, int32_t H, int32_t d) {
     return (size_t)H * (size_t)(num_tiles(N) + kmip::kPadTiles) * 32 * (size_t)d * 2;
 }
 
-// The select kernel's per-XCD work counters, right after the tiled keys.
-constexpr size_t kCounterBytes = kAlign;
+// The select kernel's per-XCD work counters and pacers, after the tiled keys.
+constexpr size_t kCounterBytes = kmip::kSelectCounterBytes;
 
 // Upper bound on the work-list length for any query-block size.
 size_t max_tasks(int64_t N, int32_t G) { return (size_t)(N / 32 + G + 1); }

@@ -14,6 +14,9 @@ constexpr int kPadTiles = 16;
 // Number of XCDs of MI355X; workgroups are dispatched to them round-robin.
 constexpr int kNumXcd = 8;
 
+// Device scratch the select kernel needs for its work counters and pacers.
+constexpr size_t kSelectCounterBytes = 512;
+
 // One unit of score+select work: a run of up to 32*QB queries of one graph
 // and the key range of that graph.
 struct Task {
@@ -33,8 +36,7 @@ hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t 
                          hipStream_t stream);
 
 // Shape of one select wave: query blocks of 32 (1 or 2) and candidate-buffer
-// slots per lane and block (4, 8 or 16; 4 and 8 with two blocks, 8 and 16
-// with one).
+// slots per lane and block (4 or 8 with two blocks, 8 or 16 with one).
 struct SelectShape {
     int32_t qb;
     int32_t slots;
@@ -42,7 +44,8 @@ struct SelectShape {
 
 // Score + select.  qperm: NULL, or per head a permutation [H][N] of the query
 // positions (query qperm[h][p] is processed at position p).  work_ctr:
-// kNumXcd device ints of scratch (the per-XCD item counters, zeroed here).
+// kSelectCounterBytes of device scratch, 8-byte aligned (per-XCD item
+// counters and stream pacers, zeroed here).
 hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
                          int32_t ntasks, int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles,
                          SelectShape shape, int32_t* work_ctr, int32_t* topk_idx,

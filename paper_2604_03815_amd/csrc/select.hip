@@ -25,14 +25,18 @@
 // index) to a per-lane candidate buffer in LDS, and fold the buffers into the
 // heaps (refreshing theta) whenever one fills up.
 //
-// Exactness of the strict filter: when block b's scores of a tile are
-// compared with theta, its heap holds only keys of earlier tiles, whose
-// indices are all lower; a score equal to theta therefore loses the tie and
-// may be skipped.  Candidates are compared again, by full key, when they are
-// folded into the heap.  Keys of a tile that lie outside the query's graph
-// are not masked in the streaming loop; they can only send a tile down the
-// rare path, which drops them by index.
+// Exactness of the filter: theta is the largest float below the k-th best
+// score in the heap, so s > theta holds exactly for s >= that score; every
+// key that could displace a heap entry, ties included, reaches the rare
+// path, and the heap compares full keys (score, then lower index).  The
+// result therefore does not depend on the order keys are streamed in, and
+// the scan of a graph's tiles may start anywhere and wrap around (used to
+// keep the waves of an XCD on the same tiles, see the pacer below).  Keys of
+// a tile that lie outside the query's graph are not masked in the streaming
+// loop; they can only send a tile down the rare path, which drops them by
+// index.
 #include <algorithm>
+#include <cfloat>
 
 #include "kmip_device.h"
 #include "kmip_internal.h"
@@ -104,6 +108,61 @@ __device__ __forceinline__ float pick16(const f32x16& a, int r) {
 constexpr int kHeapPad = 3;
 constexpr uint64_t kHeapTop = ~0ull;
 
+// The largest float below x, for a finite heap score x; a zero or denormal
+// x gives -FLT_MIN instead, so that the threshold is never a denormal (a
+// looser threshold only admits a few more candidates).
+__device__ __forceinline__ float float_below(float x) {
+    const uint32_t b = __float_as_uint(x);
+    if ((b & 0x7F800000u) == 0u) return -FLT_MIN;
+    return __uint_as_float((int32_t)b >= 0 ? b - 1u : b + 1u);
+}
+
+// Pacer of one XCD: a virtual position in a graph's key stream that moves at
+// the average speed of that XCD's waves, P(t) = pos + (t - t_ref) * rate
+// (tiles per tick of the 100 MHz wall clock).  A wave starts each item's
+// scan at P(now), so that waves which start items at different times still
+// read the same tiles at about the same time and share them in the XCD's
+// L2.  Each finished item folds its own speed into rate (moving average)
+// and re-anchors (pos, t_ref).  The fields are read and written without
+// synchronisation; a torn read only yields a worse start tile, never a
+// wrong result.
+struct Pacer {
+    double pos;
+    double rate;
+    int64_t t_ref;
+    int64_t pad;
+};
+
+static_assert(kNumXcd * (sizeof(int32_t) + sizeof(Pacer)) <= kSelectCounterBytes,
+              "work counters and pacers must fit their scratch");
+
+// Scan start for a graph of nt tiles (0 .. nt-1, relative to its first tile).
+__device__ __forceinline__ int pacer_start(const Pacer* p, int64_t now, int nt) {
+    const double rate = __hip_atomic_load(&p->rate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!(rate > 0.0)) return 0;
+    const double pos = __hip_atomic_load(&p->pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int64_t t_ref = __hip_atomic_load(&p->t_ref, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const double v = pos + (double)(now - t_ref) * rate;
+    if (!(v >= 0.0) || v > 1e15) return 0;
+    const int64_t w = (int64_t)v % nt;
+    return (int)w;
+}
+
+// Folds the speed of an item that scanned nt tiles in `ticks` into the pacer.
+__device__ __forceinline__ void pacer_update(Pacer* p, int64_t now, int nt, int64_t ticks) {
+    if (ticks <= 0) return;
+    const double own = (double)nt / (double)ticks;
+    const double rate = __hip_atomic_load(&p->rate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const double pos = __hip_atomic_load(&p->pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int64_t t_ref = __hip_atomic_load(&p->t_ref, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    double v = rate > 0.0 ? pos + (double)(now - t_ref) * rate : 0.0;
+    if (!(v >= 0.0) || v > 1e15) v = 0.0;
+    const double next_rate = rate > 0.0 ? 0.875 * rate + 0.125 * own : own;
+    __hip_atomic_store(&p->pos, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&p->t_ref, now, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&p->rate, next_rate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ uint64_t min_u64(uint64_t a, uint64_t b) { return b < a ? b : a; }
 
 // Places x at the root and sifts it down.
@@ -125,23 +184,26 @@ __device__ __forceinline__ void heap_sift_down(uint64_t* hp, int col, int k, uin
     hp[pos * 32 + col] = x;
 }
 
+// At least one wave per SIMD: the kernel may use the whole register file
+// rather than have the compiler trade registers for occupancy by spilling.
 template <int D, int QB, int SLOTS>
-__global__ __launch_bounds__(64) void select_kernel(
+__global__ __launch_bounds__(64, 1) void select_kernel(
     const uint4* __restrict__ kp, const uint16_t* __restrict__ Q, const Task* __restrict__ tasks,
     const int32_t* __restrict__ qperm, int32_t ntasks, int32_t N, int32_t H, int32_t k,
-    int32_t ntiles, int32_t* __restrict__ work_ctr, int32_t* __restrict__ topk_idx) {
+    int32_t ntiles, int32_t* __restrict__ work_ctr, Pacer* __restrict__ pacers,
+    int32_t* __restrict__ topk_idx) {
     constexpr int NC = D / 16;
     constexpr int TILE_BYTES = NC * 64 * 16;
     extern __shared__ uint64_t lds[];
+    const int hrows = k + kHeapPad;
 
     // Persistent, XCD-aware schedule.  Workgroups are dispatched to the XCDs
     // round-robin; the ones on XCD x take items of a contiguous range of
-    // (head, task) items, in order, from that XCD's counter.  Items stream
-    // the same key tiles in the same order, so the waves of one XCD read each
-    // tile at nearly the same time and share it in that XCD's L2.  Taking
-    // items from a counter balances items of unequal cost and keeps a
-    // workgroup that only becomes resident late (when the grid exceeds what
-    // fits) from delaying the items it would otherwise own.
+    // (head, task) items, in order, from that XCD's counter, so an XCD works
+    // on one head's keys at a time, and its pacer keeps its waves on the
+    // same tiles.  Taking items from a counter balances items of unequal
+    // cost and keeps a workgroup that only becomes resident late (when the
+    // grid exceeds what fits) from delaying the items it would otherwise own.
     const int items = ntasks * H;
     const int xcd = blockIdx.x % kNumXcd;
     const int items_per_xcd = (items + kNumXcd - 1) / kNumXcd;
@@ -173,7 +235,6 @@ __global__ __launch_bounds__(64) void select_kernel(
     const int col = lane & 31;
     const int half = lane >> 5;
 
-    const int hrows = k + kHeapPad;
     uint64_t* heaps = lds;                              // [QB][k + kHeapPad][32]
     uint64_t* cand = lds + (size_t)QB * hrows * 32;     // [QB][SLOTS][64]
 
@@ -214,24 +275,23 @@ __global__ __launch_bounds__(64) void select_kernel(
                     if (c > hp[col]) heap_sift_down(hp, col, k, c);
                 }
             }
-            // One wave per workgroup: its LDS instructions execute in program
-            // order, so the next phase sees this phase's heap writes.  Only
-            // compiler reordering has to be fenced off.
+            // The heaps are private to this wave, whose LDS instructions
+            // execute in program order, so the next phase sees this phase's
+            // heap writes.  Only compiler reordering has to be fenced off.
             __builtin_amdgcn_wave_barrier();
         }
 #pragma unroll
         for (int b = 0; b < QB; ++b) {
             if (theta[b] != INFINITY) {
                 const uint64_t root = heaps[(size_t)b * hrows * 32 + col];
-                theta[b] = root == 0ull ? -INFINITY : key_score(root);
+                theta[b] = root == 0ull ? -INFINITY : float_below(key_score(root));
             }
             cnt[b] = 0;
         }
     };
 
     // Rare path for block b of the tile starting at key tbase.  Each lane
-    // builds a 16-bit mask of its scores above theta (theta still reflects
-    // earlier tiles only, so the strict test is exact), and the wave then
+    // builds a 16-bit mask of its scores above theta, and the wave then
     // walks the set bits: as many rounds as the largest per-lane count,
     // usually one or two.  A lane picks the score of its bit out of its 16
     // registers with a 4-level select on the bits of the register number.  A
@@ -263,18 +323,33 @@ __global__ __launch_bounds__(64) void select_kernel(
         __builtin_amdgcn_wave_barrier();
     };
 
+    // The graph's tiles t0 .. t1-1 are scanned in the order ts .. t1-1,
+    // t0 .. ts-1; with one graph, ts comes from the XCD's pacer.
     const int t0 = key_lo >> 5;
     const int t1 = (key_hi + 31) >> 5;
+    const int nt = t1 - t0;
+    int64_t item_start = 0;
+    int ts = t0;
+    if (tasks == nullptr) {
+        int rel = 0;
+        if (lane == 0) {
+            item_start = wall_clock64();
+            rel = pacer_start(&pacers[xcd], item_start, nt);
+        }
+        ts = t0 + __builtin_amdgcn_readfirstlane(rel);
+    }
+    auto tile_at = [&](int i) { return ts + i >= t1 ? ts + i - nt : ts + i; };
     const uint32_t lane_off = (uint32_t)lane * 16u;
 
-    // Prefetch ring: slot (T - t0) % PF holds tile T; it is refilled with
-    // tile T + PF as soon as tile T's MFMAs are issued.  `next` walks the
-    // tiled key buffer one tile per refill; the buffer carries kPadTiles
-    // zero tiles per head past the last one, so prefetches beyond the
-    // graph's last tile stay in bounds and need no clamping.
+    // Prefetch ring: scan position i sits in slot i % PF; the slot is
+    // refilled with position i + PF as soon as position i's MFMAs are
+    // issued.  `next` walks the graph's tiles one per refill and wraps from
+    // t1 back to t0, so it never leaves the graph's tiles.
     constexpr int PF = 8 / NC;
-    const char* next = reinterpret_cast<const char*>(kp) +
-                       ((size_t)head * (ntiles + kPadTiles) + t0) * TILE_BYTES;
+    const char* head_tiles = reinterpret_cast<const char*>(kp) + (size_t)head * (ntiles + kPadTiles) * TILE_BYTES;
+    const char* wrap_lo = head_tiles + (size_t)t0 * TILE_BYTES;
+    const char* wrap_hi = head_tiles + (size_t)t1 * TILE_BYTES;
+    const char* next = head_tiles + (size_t)ts * TILE_BYTES;
     i32x4 ring[PF][NC];
     auto refill = [&](i32x4 (&slot)[NC]) {
         slot[0] = ring_load<0>(next, lane_off);
@@ -284,6 +359,7 @@ __global__ __launch_bounds__(64) void select_kernel(
             slot[3] = ring_load<3072>(next, lane_off);
         }
         next += TILE_BYTES;
+        if (next == wrap_hi) next = wrap_lo;
     };
 #pragma unroll
     for (int u = 0; u < PF; ++u) refill(ring[u]);
@@ -313,7 +389,8 @@ __global__ __launch_bounds__(64) void select_kernel(
         return fmaxf(fmaxf(fmaxf(l0, l1), l2), fmaxf(fmaxf(l3, l4), a[15]));
     };
 
-    auto filter = [&](const f32x16 (&acc)[QB], int t) {
+    // Filter the scores of scan position i.
+    auto filter = [&](const f32x16 (&acc)[QB], int i) {
         float m[QB];
 #pragma unroll
         for (int b = 0; b < QB; ++b) m[b] = max16(acc[b]);
@@ -321,42 +398,43 @@ __global__ __launch_bounds__(64) void select_kernel(
 #pragma unroll
         for (int b = 0; b < QB; ++b) any |= __builtin_amdgcn_ballot_w64(m[b] > theta[b]);
         if (any != 0ull) {
+            const int tile = tile_at(i);
 #pragma unroll
             for (int b = 0; b < QB; ++b)
-                if (__builtin_amdgcn_ballot_w64(m[b] > theta[b]) != 0ull) rare_path(acc[b], b, t << 5);
+                if (__builtin_amdgcn_ballot_w64(m[b] > theta[b]) != 0ull) rare_path(acc[b], b, tile << 5);
         }
     };
 
-    // Software pipeline with two accumulator sets: the MFMAs of tile t+1 are
-    // issued before tile t is filtered, so matrix cores and filter overlap.
-    // Scores of tiles past t1 (padding or a following graph) may be formed
-    // but are never filtered.  The main loop runs whole groups of PF tiles
-    // without checks; the tail group checks each tile.
+    // Software pipeline with two accumulator sets: the MFMAs of position
+    // i+1 are issued before position i is filtered, so matrix cores and
+    // filter overlap.  Scores of positions past nt may be formed but are
+    // never filtered.  The main loop runs whole groups of PF positions
+    // without checks; the tail group checks each position.
     f32x16 acc_a[QB], acc_b[QB];
     scores(ring[0], acc_a);
     refill(ring[0]);
-    int t = t0;
-    for (const int t_full = t0 + (t1 - t0) / PF * PF; t < t_full; t += PF) {
+    int i = 0;
+    for (const int i_full = nt / PF * PF; i < i_full; i += PF) {
 #pragma unroll
         for (int u = 0; u < PF; u += 2) {
             scores(ring[u + 1], acc_b);
             refill(ring[u + 1]);
-            filter(acc_a, t + u);
+            filter(acc_a, i + u);
             scores(ring[(u + 2) % PF], acc_a);
             refill(ring[(u + 2) % PF]);
-            filter(acc_b, t + u + 1);
+            filter(acc_b, i + u + 1);
         }
     }
 #pragma unroll
     for (int u = 0; u < PF; u += 2) {
-        if (t + u >= t1) goto stream_done;
+        if (i + u >= nt) goto stream_done;
         scores(ring[u + 1], acc_b);
         refill(ring[u + 1]);
-        filter(acc_a, t + u);
-        if (t + u + 1 >= t1) goto stream_done;
+        filter(acc_a, i + u);
+        if (i + u + 1 >= nt) goto stream_done;
         scores(ring[(u + 2) % PF], acc_a);
         refill(ring[(u + 2) % PF]);
-        filter(acc_b, t + u + 1);
+        filter(acc_b, i + u + 1);
     }
 stream_done:
     // Drain the ring.  Every ring register is an operand of the wait: a
@@ -369,6 +447,10 @@ stream_done:
         for (int c = 0; c < NC; ++c) ring_wait<0>(ring[u][c]);
     }
     merge_all();
+    if (tasks == nullptr && lane == 0) {
+        const int64_t now = wall_clock64();
+        pacer_update(&pacers[xcd], now, nt, now - item_start);
+    }
 
     // Drain each heap in increasing order into slots k-1 .. 0, which leaves
     // the row sorted by (score desc, index asc); sentinels become -1.  The
@@ -425,19 +507,29 @@ hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, con
     const size_t lds = select_lds_bytes(k, SelectShape{QB, SLOTS});
     // One resident wave per workgroup slot of the chip, a multiple of the XCD
     // count, never more workgroups than items.
+    // The key-tile loads are asynchronous register writes the compiler does
+    // not know about: a spill of a prefetch register would save it before its
+    // load lands.  Refuse to run a build in which the kernel uses scratch.
+    hipFuncAttributes fa;
+    hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(select_kernel<D, QB, SLOTS>));
+    if (e != hipSuccess) return e;
+    if (fa.localSizeBytes != 0) return hipErrorInvalidDeviceFunction;
     int dev = 0, cus = 0, per_cu = 0;
-    hipError_t e = hipGetDevice(&dev);
+    e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_kernel<D, QB, SLOTS>, 64, lds);
     if (e != hipSuccess) return e;
-    if ((e = launch_fill_zero(reinterpret_cast<float*>(work_ctr), kNumXcd, stream)) != hipSuccess) return e;
+    // work_ctr: kNumXcd item counters, then kNumXcd pacers (all fields 0).
+    Pacer* pacers = reinterpret_cast<Pacer*>(work_ctr + kNumXcd);
+    const size_t words = (kNumXcd * sizeof(int32_t) + kNumXcd * sizeof(Pacer)) / sizeof(float);
+    if ((e = launch_fill_zero(reinterpret_cast<float*>(work_ctr), words, stream)) != hipSuccess) return e;
     const int64_t slots = (int64_t)std::max(cus, 1) * std::max(per_cu, 1);
     const int64_t want = std::min<int64_t>(slots, (items + kNumXcd - 1) / kNumXcd * kNumXcd);
     const int64_t grid = std::max<int64_t>(kNumXcd, want / kNumXcd * kNumXcd);
     hipLaunchKernelGGL((select_kernel<D, QB, SLOTS>), dim3((unsigned)grid), dim3(64), lds, stream,
                        reinterpret_cast<const uint4*>(kp), reinterpret_cast<const uint16_t*>(Q),
-                       tasks, qperm, ntasks, N, H, k, ntiles, work_ctr, topk_idx);
+                       tasks, qperm, ntasks, N, H, k, ntiles, work_ctr, pacers, topk_idx);
     return hipGetLastError();
 }
 

@@ -47,14 +47,14 @@ def test_status_strings(lib):
 def test_workspace_size(lib):
     # tiled copy of K, padded to whole 32-key tiles, 256-byte aligned
     n = lib.kmip_topk_workspace_size(500_000, 4, 16, 32, 1)
-    packed = 4 * (15625 + 16) * 32 * 16 * 2 + 256   # tiled K, then 256 B of work counters
+    packed = 4 * (15625 + 16) * 32 * 16 * 2 + 512   # tiled K, then 512 B of work counters
     # one graph of >= 8192 nodes: query grouping adds reference directions
     # [H][256][d] f32, labels [H][N] u16, a histogram [H][256] and the
     # permutation [H][N] i32, each 256-byte aligned
     grouping = 4 * 256 * 16 * 4 + 4 * 500_000 * 2 + 4 * 256 * 4 + 4 * 500_000 * 4
     assert n == packed + grouping
-    assert lib.kmip_topk_workspace_size(8191, 1, 16, 4, 1) == (256 + 16) * 32 * 16 * 2 + 256
-    assert lib.kmip_topk_workspace_size(33, 1, 16, 4, 1) == (2 + 16) * 32 * 16 * 2 + 256
+    assert lib.kmip_topk_workspace_size(8191, 1, 16, 4, 1) == (256 + 16) * 32 * 16 * 2 + 512
+    assert lib.kmip_topk_workspace_size(33, 1, 16, 4, 1) == (2 + 16) * 32 * 16 * 2 + 512
     multi = lib.kmip_topk_workspace_size(1000, 2, 32, 16, 7)
     assert multi > lib.kmip_topk_workspace_size(1000, 2, 32, 16, 1)
     assert lib.kmip_topk_workspace_size(100, 1, 24, 4, 1) == 0   # unsupported d
