@@ -174,17 +174,18 @@ kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offse
         ntasks = (int32_t)((N + 32 * qb - 1) / (32 * qb));
     }
 
-    int32_t* qperm = nullptr;
-    if (use_grouping(N, G)) {
+    kmip::QueryGroups groups{};
+    const bool grouped = use_grouping(N, G);
+    if (grouped) {
         void* gws = ws + align_up(packed_k_bytes(N, H, d)) + kCounterBytes;
-        hipError_t e = kmip::launch_group_queries(Q, n32, H, d, gws, &qperm, stream);
+        hipError_t e = kmip::launch_group_queries(Q, n32, H, d, gws, &groups, stream);
         if (e != hipSuccess) return hip_fail(e, "query grouping launch");
     }
     hipError_t e = kmip::launch_pack_k(K, kp, n32, H, d, ntiles, stream);
     if (e != hipSuccess) return hip_fail(e, "pack_k launch");
     int32_t* work_ctr = reinterpret_cast<int32_t*>(ws + align_up(packed_k_bytes(N, H, d)));
-    e = kmip::launch_select(kp, Q, dtasks, qperm, ntasks, n32, H, d, k, ntiles, shape, work_ctr,
-                            topk_idx, stream);
+    e = kmip::launch_select(kp, Q, dtasks, grouped ? &groups : nullptr, ntasks, n32, H, d, k, ntiles,
+                            shape, work_ctr, topk_idx, stream);
     if (e != hipSuccess) return hip_fail(e, "select launch");
     return ok();
 }

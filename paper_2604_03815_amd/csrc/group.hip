@@ -127,24 +127,27 @@ __global__ __launch_bounds__(256) void group_scatter_kernel(const uint16_t* __re
 size_t group_workspace_bytes(int32_t N, int32_t H, int32_t d) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };
     return al((size_t)H * C * d * sizeof(float)) + al((size_t)H * N * sizeof(uint16_t)) +
-           al((size_t)H * C * sizeof(int32_t)) + al((size_t)H * N * sizeof(int32_t));
+           al((size_t)2 * H * C * sizeof(int32_t)) + al((size_t)H * N * sizeof(int32_t));
 }
 
 hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, void* ws,
-                                int32_t** perm_out, hipStream_t stream) {
+                                QueryGroups* out, hipStream_t stream) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };
     char* p = reinterpret_cast<char*>(ws);
     float* centers = reinterpret_cast<float*>(p);
     p += al((size_t)H * C * d * sizeof(float));
     uint16_t* label = reinterpret_cast<uint16_t*>(p);
     p += al((size_t)H * N * sizeof(uint16_t));
-    int32_t* hist = reinterpret_cast<int32_t*>(p);
-    p += al((size_t)H * C * sizeof(int32_t));
+    int32_t* hist = reinterpret_cast<int32_t*>(p);          // [H][C], then seed_ref [H][C]
+    int32_t* seed_ref = hist + (size_t)H * C;
+    p += al((size_t)2 * H * C * sizeof(int32_t));
     int32_t* perm = reinterpret_cast<int32_t*>(p);
-    *perm_out = perm;
+    out->perm = perm;
+    out->label = label;
+    out->seed_ref = seed_ref;
 
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
-    hipError_t e = launch_fill_zero(reinterpret_cast<float*>(hist), (size_t)H * C, stream);
+    hipError_t e = launch_fill_zero(reinterpret_cast<float*>(hist), (size_t)2 * H * C, stream);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(group_centers_kernel, dim3(H), dim3(C), 0, stream, q, N, H, d, centers);
     if ((e = hipGetLastError()) != hipSuccess) return e;

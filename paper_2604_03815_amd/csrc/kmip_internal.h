@@ -42,11 +42,23 @@ struct SelectShape {
     int32_t slots;
 };
 
-// Score + select.  qperm: NULL, or per head a permutation [H][N] of the query
-// positions (query qperm[h][p] is processed at position p).  work_ctr:
+// Queries grouped by direction (group.hip), all arrays in device memory:
+//   perm     [H][N]  query processed at position p of head h;
+//   label    [H][N]  reference direction nearest to query i of head h;
+//   seed_ref [H][kGroupCenters]  0, or 1 + a query id of that label whose
+//            finished top-k row other queries of the label may seed from
+//            (zero before the select launch).
+struct QueryGroups {
+    const int32_t* perm;
+    const uint16_t* label;
+    int32_t* seed_ref;
+};
+
+// Score + select.  groups: NULL (identity order, no seeding; always so for a
+// block-diagonal batch), or the grouping of the queries.  work_ctr:
 // kSelectCounterBytes of device scratch, 8-byte aligned (per-XCD item
 // counters and stream pacers, zeroed here).
-hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
+hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const QueryGroups* groups,
                          int32_t ntasks, int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles,
                          SelectShape shape, int32_t* work_ctr, int32_t* topk_idx,
                          hipStream_t stream);
@@ -60,10 +72,10 @@ constexpr int kGroupCenters = 256;
 // Workspace bytes launch_group_queries needs.
 size_t group_workspace_bytes(int32_t N, int32_t H, int32_t d);
 
-// Writes into ws a per-head permutation [H][N] of the queries that places
-// queries of similar direction next to each other; *perm_out points to it.
+// Groups the queries of each head by direction into ws and describes the
+// result in *out.
 hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, void* ws,
-                                int32_t** perm_out, hipStream_t stream);
+                                QueryGroups* out, hipStream_t stream);
 
 hipError_t launch_attend(const void* Q, const void* K, const void* V, const int32_t* idx,
                          int32_t N, int32_t H, int32_t d, int32_t k, float scale, float* out,

@@ -189,7 +189,8 @@ __device__ __forceinline__ void heap_sift_down(uint64_t* hp, int col, int k, uin
 template <int D, int QB, int SLOTS>
 __global__ __launch_bounds__(64, 1) void select_kernel(
     const uint4* __restrict__ kp, const uint16_t* __restrict__ Q, const Task* __restrict__ tasks,
-    const int32_t* __restrict__ qperm, int32_t ntasks, int32_t N, int32_t H, int32_t k,
+    const int32_t* __restrict__ qperm, const uint16_t* __restrict__ qlabel,
+    int32_t* __restrict__ seed_ref, int32_t ntasks, int32_t N, int32_t H, int32_t k,
     int32_t ntiles, int32_t* __restrict__ work_ctr, Pacer* __restrict__ pacers,
     int32_t* __restrict__ topk_idx) {
     constexpr int NC = D / 16;
@@ -198,22 +199,39 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     const int hrows = k + kHeapPad;
 
     // Persistent, XCD-aware schedule.  Workgroups are dispatched to the XCDs
-    // round-robin; the ones on XCD x take items of a contiguous range of
-    // (head, task) items, in order, from that XCD's counter, so an XCD works
-    // on one head's keys at a time, and its pacer keeps its waves on the
-    // same tiles.  Taking items from a counter balances items of unequal
-    // cost and keeps a workgroup that only becomes resident late (when the
-    // grid exceeds what fits) from delaying the items it would otherwise own.
+    // round-robin; the ones on XCD x take the items of a contiguous range of
+    // (head, task) items from that XCD's counter, so an XCD works on one
+    // head's keys at a time, and its pacer keeps its waves on the same
+    // tiles.  Taking items from a counter balances items of unequal cost and
+    // keeps a workgroup that only becomes resident late (when the grid
+    // exceeds what fits) from delaying the items it would otherwise own.
+    // With grouped queries the counter walks the range with a stride
+    // coprime to its length, so that the first items to run cover all
+    // direction groups and can seed the items that follow (see below).
     const int items = ntasks * H;
     const int xcd = blockIdx.x % kNumXcd;
     const int items_per_xcd = (items + kNumXcd - 1) / kNumXcd;
     const int item_lo = xcd * items_per_xcd;
-    const int item_end = min(items, item_lo + items_per_xcd);
+    const int range = min(items, item_lo + items_per_xcd) - item_lo;
+    int stride = 1;
+    if (qlabel != nullptr && range > 1) {
+        stride = max(1, range / max(1, (int)gridDim.x / kNumXcd));
+        for (;; ++stride) {
+            int a = stride, b = range;
+            while (b != 0) {
+                const int r = a % b;
+                a = b;
+                b = r;
+            }
+            if (a == 1) break;
+        }
+    }
     for (;;) {
     int claim = 0;
     if (threadIdx.x == 0) claim = atomicAdd(&work_ctr[xcd], 1);
-    const int item = item_lo + __builtin_amdgcn_readfirstlane(claim);
-    if (item >= item_end) break;
+    claim = __builtin_amdgcn_readfirstlane(claim);
+    if (claim >= range) break;
+    const int item = item_lo + (int)(((int64_t)claim * stride) % range);
     const int head = item / ntasks;
     const int task = item - head * ntasks;
 
@@ -259,6 +277,52 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     }
     for (int e = lane; e < QB * hrows * 32; e += 64) heaps[e] = (e / 32) % hrows < k ? 0ull : kHeapTop;
 
+    // Seeded thresholds.  Queries of one direction label share most of their
+    // top-k keys.  When some query of the label of a block's first query has
+    // published its finished top-k row, the block scores its queries against
+    // those k keys (one MFMA tile per 32 keys, gathered from the tiled keys)
+    // and starts from theta = the float below each query's lowest such
+    // score: k distinct keys of the graph score at least that much, so the
+    // query's k-th best does too, and every key that can enter its top-k
+    // still passes the filter.  Scores come from the same MFMA on the same
+    // operands as in the stream, hence are the same values.  The heap starts
+    // empty and fills with keys that pass; theta only ever rises.
+    if (qlabel != nullptr) {
+        const uint4* head_tiles = kp + (size_t)head * (ntiles + kPadTiles) * NC * 64;
+#pragma unroll
+        for (int b = 0; b < QB; ++b) {
+            if (32 * b >= q_count) continue;
+            int ref = 0;
+            if (lane == 0) {
+                const int lab = qlabel[(size_t)head * N + qid[b]];
+                ref = __hip_atomic_load(&seed_ref[(size_t)head * kGroupCenters + lab], __ATOMIC_ACQUIRE,
+                                        __HIP_MEMORY_SCOPE_AGENT);
+            }
+            ref = __builtin_amdgcn_readfirstlane(ref);
+            if (ref <= 0 || ref > N) continue;
+            const int32_t* srow = topk_idx + ((size_t)(ref - 1) * H + head) * k;
+            float low = INFINITY;
+            bool ok = true;
+            for (int s0 = 0; s0 < k; s0 += 32) {
+                const int j = srow[s0 + col < k ? s0 + col : s0];
+                ok = ok && j >= 0 && j < N;
+                const int jj = (j >= 0 && j < N) ? j : 0;
+                const uint4* src = head_tiles + (size_t)(jj >> 5) * NC * 64 + (jj & 31) + 32 * half;
+                f32x16 sacc = f32x16{};
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, src[c * 64]), bq[b][c], sacc, 0, 0, 0);
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    if (s0 + tile_row(r, half) < k) low = fminf(low, sacc[r]);
+            }
+            low = fminf(low, __shfl_xor(low, 32));
+            if (__builtin_amdgcn_ballot_w64(!ok) != 0ull) continue;
+            if (theta[b] != INFINITY) theta[b] = float_below(low);
+        }
+    }
+
     // Fold every lane's candidates into the heaps and refresh theta.  With
     // two blocks, each phase has the lower half-wave on one block's heaps and
     // the upper half-wave on the other's, so all lanes work on disjoint heaps.
@@ -284,7 +348,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         for (int b = 0; b < QB; ++b) {
             if (theta[b] != INFINITY) {
                 const uint64_t root = heaps[(size_t)b * hrows * 32 + col];
-                theta[b] = root == 0ull ? -INFINITY : float_below(key_score(root));
+                theta[b] = fmaxf(theta[b], root == 0ull ? -INFINITY : float_below(key_score(root)));
             }
             cnt[b] = 0;
         }
@@ -471,6 +535,13 @@ stream_done:
             }
         }
     }
+    // Publish the row of the item's first query (drained by lane 0 above) as
+    // the seed of its label, unless one is published already.
+    if (qlabel != nullptr && lane == 0) {
+        __threadfence();
+        const int lab = qlabel[(size_t)head * N + qid[0]];
+        atomicCAS(&seed_ref[(size_t)head * kGroupCenters + lab], 0, qid[0] + 1);
+    }
     // The next item reinitialises the heaps this wave just drained.
     __builtin_amdgcn_wave_barrier();
     }  // item loop
@@ -500,7 +571,7 @@ __global__ __launch_bounds__(256) void pack_k_kernel(const uint16_t* __restrict_
 }
 
 template <int D, int QB, int SLOTS>
-hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
+hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, const QueryGroups* groups,
                            int32_t ntasks, int32_t N, int32_t H, int32_t k, int32_t ntiles,
                            int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream) {
     const int64_t items = (int64_t)ntasks * H;
@@ -529,7 +600,9 @@ hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, con
     const int64_t grid = std::max<int64_t>(kNumXcd, want / kNumXcd * kNumXcd);
     hipLaunchKernelGGL((select_kernel<D, QB, SLOTS>), dim3((unsigned)grid), dim3(64), lds, stream,
                        reinterpret_cast<const uint4*>(kp), reinterpret_cast<const uint16_t*>(Q),
-                       tasks, qperm, ntasks, N, H, k, ntiles, work_ctr, pacers, topk_idx);
+                       tasks, groups ? groups->perm : nullptr, groups ? groups->label : nullptr,
+                       groups ? groups->seed_ref : nullptr, ntasks, N, H, k, ntiles, work_ctr, pacers,
+                       topk_idx);
     return hipGetLastError();
 }
 
@@ -551,14 +624,14 @@ hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t 
     return hipGetLastError();
 }
 
-hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const int32_t* qperm,
+hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const QueryGroups* groups,
                          int32_t ntasks, int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles,
                          SelectShape shape, int32_t* work_ctr, int32_t* topk_idx,
                          hipStream_t stream) {
     if (ntasks <= 0) return hipSuccess;
 #define KMIP_SELECT_CASE(DD, QQ, SS)                                                             \
     if (d == DD && shape.qb == QQ && shape.slots == SS)                                          \
-        return launch_select_t<DD, QQ, SS>(kp, Q, tasks, qperm, ntasks, N, H, k, ntiles,         \
+        return launch_select_t<DD, QQ, SS>(kp, Q, tasks, groups, ntasks, N, H, k, ntiles,        \
                                            work_ctr, topk_idx, stream);
 #define KMIP_SELECT_D(DD)         \
     KMIP_SELECT_CASE(DD, 2, 4)    \

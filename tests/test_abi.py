@@ -49,9 +49,9 @@ def test_workspace_size(lib):
     n = lib.kmip_topk_workspace_size(500_000, 4, 16, 32, 1)
     packed = 4 * (15625 + 16) * 32 * 16 * 2 + 512   # tiled K, then 512 B of work counters
     # one graph of >= 8192 nodes: query grouping adds reference directions
-    # [H][256][d] f32, labels [H][N] u16, a histogram [H][256] and the
-    # permutation [H][N] i32, each 256-byte aligned
-    grouping = 4 * 256 * 16 * 4 + 4 * 500_000 * 2 + 4 * 256 * 4 + 4 * 500_000 * 4
+    # [H][256][d] f32, labels [H][N] u16, a histogram and the seed references
+    # [2][H][256] i32 and the permutation [H][N] i32, each 256-byte aligned
+    grouping = 4 * 256 * 16 * 4 + 4 * 500_000 * 2 + 2 * 4 * 256 * 4 + 4 * 500_000 * 4
     assert n == packed + grouping
     assert lib.kmip_topk_workspace_size(8191, 1, 16, 4, 1) == (256 + 16) * 32 * 16 * 2 + 512
     assert lib.kmip_topk_workspace_size(33, 1, 16, 4, 1) == (2 + 16) * 32 * 16 * 2 + 512

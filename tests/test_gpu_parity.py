@@ -132,6 +132,45 @@ def test_all_scores_tied():
     allclose_report("out", res["out"][10:, 0, :], np.tile(V[10:26].mean(axis=0), (190, 1)))
 
 
+# One graph of 100k nodes and two heads: enough items that the grouped path
+# runs with seeded thresholds and scans that start mid-graph and wrap.
+GROUPED_N, GROUPED_H = 100_000, 2
+
+
+@pytest.mark.parametrize("d,k", [(16, 32), (32, 16), (64, 128)])
+def test_exact_ties_grouped_seeded(d, k):
+    # Scores in a small integer range tie everywhere: the set, its order and
+    # the tie rule must match the oracle exactly on a sample of query-heads,
+    # however the keys were streamed and whatever threshold seeded them.
+    rng = np.random.default_rng(100 + d + k)
+    N, H = GROUPED_N, GROUPED_H
+    q = rng.integers(-2, 3, size=(N, H, d)).astype(np.float32)
+    kk = rng.integers(-1, 2, size=(N, H, d)).astype(np.float32)
+    v = rng.standard_normal((N, H, d)).astype(np.float32)
+    w = workloads.Workload("ties_grouped", N, H, d, k, 0.25, None, workloads.bf16_round(q),
+                           workloads.bf16_round(kk), workloads.bf16_round(v), None, False)
+    res = _run(w, backward=False)
+    check_structure(res["idx"], None, N, H, k)
+    sel = sample_rows(N, H, 512, seed=5)
+    Qd, Kd, _, _ = _f64(w)
+    o_idx, _, _ = oracle.topk(Qd, Kd, k, sel=sel)
+    np.testing.assert_array_equal(res["idx"].reshape(N * H, k)[sel], o_idx)
+
+
+def test_all_scores_tied_grouped():
+    # Q = 0 on a large graph: every score is 0, so every query keeps keys
+    # 0 .. k-1, in that order, even though scans start mid-graph.
+    N, H, d, k = GROUPED_N, GROUPED_H, 16, 32
+    rng = np.random.default_rng(1)
+    w = workloads.Workload("zeroq_grouped", N, H, d, k, 0.25, None,
+                           workloads.bf16_round(np.zeros((N, H, d), np.float32)),
+                           workloads.bf16_round(rng.standard_normal((N, H, d)).astype(np.float32)),
+                           workloads.bf16_round(rng.standard_normal((N, H, d)).astype(np.float32)),
+                           None, False)
+    res = _run(w, backward=False)
+    assert (res["idx"] == np.arange(k, dtype=np.int32)).all()
+
+
 def test_deterministic_and_overwrites():
     w = workloads.iid(3000, 2, 32, 16, seed=5, sizes=[1000, 2000])
     q, k, v, g = _dev(w.q), _dev(w.kk), _dev(w.v), _dev(w.dout)
