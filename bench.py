@@ -44,6 +44,7 @@ def parse():
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-sample", type=int, default=2048, help="query-heads in the oracle sample")
+    p.add_argument("--bwd-variant", type=int, default=0, help="backward: 0 library choice, 1 per-pair atomics, 2 key-aggregated, 3 key-sorted segmented")
     return p.parse_args()
 
 
@@ -110,9 +111,11 @@ def main():
     out = torch.empty((N, H, d), dtype=torch.float32, device=dev)
     lse = torch.empty((N, H), dtype=torch.float32, device=dev)
     dq, dk, dv = (torch.empty((N, H, d), dtype=torch.float32, device=dev) for _ in range(3))
-    ws = kmip.Workspace(dev)
-    ws.get(kmip.topk_workspace_size(N, H, d, kk, w.num_graphs))
     backward = w.backward and g is not None
+    # one workspace, sized for the larger of the two uses, allocated up front
+    ws = kmip.Workspace(dev)
+    ws.get(max(kmip.topk_workspace_size(N, H, d, kk, w.num_graphs),
+               kmip.bwd_workspace_size(N, H, d, kk, args.bwd_variant) if backward else 0))
 
     def step(ev=None):
         if ev is not None:
@@ -124,7 +127,8 @@ def main():
         if ev is not None:
             ev[2].record()
         if backward:
-            kmip.bwd(q, k, v, g, idx, lse, w.scale, dq=dq, dk=dk, dv=dv)
+            kmip.bwd(q, k, v, g, idx, lse, w.scale, variant=args.bwd_variant, dq=dq, dk=dk, dv=dv,
+                     workspace=ws)
         if ev is not None:
             ev[3].record()
 

@@ -111,9 +111,21 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
  *   in:  dOut bf16 [N, H, d]; topk_idx [N, H, k] and lse [N, H] as written
  *        by the forward.
  *   out: dQ, dK, dV float32 [N, H, d], overwritten.
- *   variant: 0 = library's choice, 1 = scatter with fp32 atomics
- *            (summation order not fixed), others reserved (UNSUPPORTED).
- *   workspace: kmip_bwd_workspace_size() bytes (currently 0; may be NULL).
+ *   variant: how dK and dV are summed over the queries that selected a
+ *            key (all use fp32 atomics somewhere, so the summation order is
+ *            not fixed and results may differ in the last bits from call to
+ *            call):
+ *            1 = every selected pair adds its rows with atomics;
+ *            2 = key-aggregated: queries are grouped by direction, each
+ *                workgroup of 256 queries sums its pairs per key in LDS and
+ *                adds each key's sums once;
+ *            3 = key-sorted segmented reduction: the pairs are counting-
+ *                sorted by key and each key's run is summed in registers,
+ *                one atomic per run piece of 256 pairs;
+ *            0 = library's choice (currently 3); others UNSUPPORTED.
+ *   workspace: kmip_bwd_workspace_size(variant) bytes, 256-byte aligned
+ *              (0 for variant 1, which accepts NULL); too small or
+ *              misaligned -> KMIP_ERR_WORKSPACE.
  */
 size_t kmip_bwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t variant);
 kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* dOut,

@@ -222,12 +222,14 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
     return kmip_attend(Q, K, V, N, H, d, k, scale, topk_idx, out, lse, stream);
 }
 
+// Backward variant the library picks (variant 0).
+constexpr int32_t kDefaultBwdVariant = 3;
+
 size_t kmip_bwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t variant) {
-    (void)N;
-    (void)H;
-    (void)d;
-    (void)k;
-    (void)variant;
+    if (check_sizes(N, H, d, k) != KMIP_OK) return 0;
+    const int32_t v = variant == 0 ? kDefaultBwdVariant : variant;
+    if (v == 2) return align_up(kmip::bwd_agg_workspace_bytes((int32_t)N, H, d));
+    if (v == 3) return align_up(kmip::bwd_csr_workspace_bytes((int32_t)N, H, k));
     return 0;
 }
 
@@ -235,20 +237,36 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
                        const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
                        int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
                        int32_t variant, void* workspace, size_t workspace_bytes, void* stream_) {
-    (void)workspace;
-    (void)workspace_bytes;
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
-    if (variant != 0 && variant != 1) return fail(KMIP_ERR_UNSUPPORTED, "backward variant %d", variant);
+    if (variant < 0 || variant > 3) return fail(KMIP_ERR_UNSUPPORTED, "backward variant %d", variant);
     if (N == 0) return ok();
     if (!Q || !K || !V || !dOut || !topk_idx || !lse || !dQ || !dK || !dV)
         return fail(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_bwd");
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(dOut))
         return fail(KMIP_ERR_INVALID_ARG, "Q, K, V and dOut must be 16-byte aligned");
     if (!aligned16(dK) || !aligned16(dV)) return fail(KMIP_ERR_INVALID_ARG, "dK and dV must be 16-byte aligned");
-    hipError_t e = kmip::launch_bwd_atomic(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale,
-                                           dQ, dK, dV, reinterpret_cast<hipStream_t>(stream_));
+    const int32_t v = variant == 0 ? kDefaultBwdVariant : variant;
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    hipError_t e;
+    if (v != 1) {
+        const size_t need = kmip_bwd_workspace_size(N, H, d, k, v);
+        if (workspace == nullptr || workspace_bytes < need)
+            return fail(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
+        if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0)
+            return fail(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    }
+    if (v == 2) {
+        e = kmip::launch_bwd_agg(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
+                                 dV, workspace, stream);
+    } else if (v == 3) {
+        e = kmip::launch_bwd_csr(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
+                                 dV, workspace, stream);
+    } else {
+        e = kmip::launch_bwd_atomic(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ,
+                                    dK, dV, stream);
+    }
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     return ok();
 }

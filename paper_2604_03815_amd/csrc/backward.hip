@@ -6,12 +6,20 @@
 // fp32 exactly as the forward aggregate does, p_j = exp(z_j - lse_i):
 //   dp_j = dO_i . v_j,  D_i = sum_j p_j dp_j,  g_j = p_j (dp_j - D_i)
 //   dQ_i = scale sum_j g_j k_j      (row-local, plain store)
-//   dK_j += scale g_j q_i,  dV_j += p_j dO_i   (scatter with fp32 atomics)
+//   dK_j += scale g_j q_i,  dV_j += p_j dO_i   (scatter)
 //
 // Mapping: a team of 16 lanes per (query, head) as in the aggregate kernel:
 // slots on lanes for the per-pair scalars, dimensions on lanes for the
-// row-vector updates, so each atomic instruction of a team covers one
-// contiguous 64-byte run of a dK or dV row.
+// row-vector updates.  Two ways to scatter:
+//   * per pair: each pair adds its dK and dV rows with fp32 atomics, one
+//     64-byte run per instruction;
+//   * key-aggregated: the queries are grouped by direction (group.hip), so
+//     the 256 queries of a workgroup share most of their keys; the
+//     workgroup sums its pairs per key in an LDS hash table and adds each
+//     key's sums to dK and dV with one atomic per dimension.  Pairs whose
+//     key finds no table slot add directly.  When a few keys are selected
+//     by most queries, per-pair atomics serialise on those keys' rows; the
+//     table removes nearly all of them.
 #include "kmip_device.h"
 #include "kmip_internal.h"
 
@@ -20,17 +28,59 @@ namespace {
 
 constexpr int kMaxSlotsPerLane = (128 + 15) / 16;
 
+// Key-aggregated scatter: a workgroup of 16 teams takes kAggQueries
+// consecutive positions of one head in the grouped query order, and sums
+// per key in a table of kSlots keys (32 KB of sums).
+constexpr int kAggQueries = 256;
+
 template <int D>
-__global__ __launch_bounds__(256) void bwd_atomic_kernel(
+struct AggTable {
+    static constexpr int kSlots = D == 16 ? 256 : D == 32 ? 128 : 64;
+    static constexpr int kProbes = 8;
+};
+
+// LDS table of one workgroup: key row index and the 2D sums (dK, then dV).
+template <int D>
+struct AggLds {
+    int32_t key[AggTable<D>::kSlots];
+    float acc[AggTable<D>::kSlots][2 * D];
+};
+
+// Finds or claims the table slot of key row js; -1 when all probes are taken
+// by other keys.  A plain read finds a key that is in the table already (the
+// common case, and a broadcast when many lanes ask for the same key); only an
+// empty slot is claimed with a compare-and-swap.  Every lane of a team runs
+// the same probes, and a claim by one of them reads back as the key itself
+// for the others.
+template <int D>
+__device__ __forceinline__ int agg_slot(AggLds<D>* t, int32_t js) {
+    constexpr int C = AggTable<D>::kSlots;
+    const uint32_t hsh = ((uint32_t)js * 0x9E3779B1u) >> (32 - __builtin_ctz(C));
+    for (int p = 0; p < AggTable<D>::kProbes; ++p) {
+        const int ts = (int)((hsh + p) & (C - 1));
+        const int32_t cur = __hip_atomic_load(&t->key[ts], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (cur == js) return ts;
+        if (cur == -1) {
+            const int32_t old = atomicCAS(&t->key[ts], -1, js);
+            if (old == -1 || old == js) return ts;
+        }
+    }
+    return -1;
+}
+
+// Backward of one (query, head) qh by a team of 16 lanes (tl = lane in team).
+// Pair scalars live with the slots on lanes; for the scatter, each round of
+// 16 slots is broadcast to the team, which then works with dimensions on
+// lanes.  All 16 pairs' key elements for dQ are loaded before any is used.
+// With tab != nullptr the dK/dV sums go to the workgroup's table when the
+// key has a slot there.
+template <int D>
+__device__ __forceinline__ void bwd_query(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
-    int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float* __restrict__ dK,
-    float* __restrict__ dV) {
-    const int tl = threadIdx.x & 15;
-    const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
-    if (qh >= (int64_t)N * H) return;  // whole team exits together
-    const int h = (int)(qh % H);
-
+    int64_t qh, int h, int tl, int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ,
+    float* __restrict__ dK, float* __restrict__ dV, AggLds<D>* tab) {
+    constexpr int U = D / 16;
     float q[D], g[D];
     load_row_f32<D>(q, Q + (size_t)qh * D);
     load_row_f32<D>(g, dO + (size_t)qh * D);
@@ -59,7 +109,6 @@ __global__ __launch_bounds__(256) void bwd_atomic_kernel(
     }
     dsum = group16_sum(dsum);
 
-    constexpr int U = D / 16;
     float qd[U], gd[U], dq[U];
     {
         // this lane's dimensions of q_i and dO_i, read straight from memory so
@@ -77,25 +126,94 @@ __global__ __launch_bounds__(256) void bwd_atomic_kernel(
     for (int s = 0; s < kMaxSlotsPerLane; ++s) {
         if (s < ns) {
             const float gs_own = p[s] * (dp[s] - dsum);
+            int32_t js[16];
+            float gsv[16], ps[16], kel[16][U];
+#pragma unroll
             for (int src = 0; src < 16; ++src) {
-                const int32_t js = __shfl(jj[s], src, 16);
-                const float gsv = __shfl(gs_own, src, 16);
-                const float ps = __shfl(p[s], src, 16);
-                if (js >= 0) {
-                    const size_t base = ((size_t)js * H + h) * D + tl;
-                    const uint16_t* krow = K + base;
+                js[src] = __shfl(jj[s], src, 16);
+                gsv[src] = __shfl(gs_own, src, 16);
+                ps[src] = __shfl(p[s], src, 16);
+            }
+#pragma unroll
+            for (int src = 0; src < 16; ++src) {
+                const uint16_t* krow = K + ((size_t)(js[src] < 0 ? 0 : js[src]) * H + h) * D + tl;
+#pragma unroll
+                for (int u = 0; u < U; ++u) kel[src][u] = js[src] < 0 ? 0.0f : bf16_bits_to_f32(krow[16 * u]);
+            }
+#pragma unroll
+            for (int src = 0; src < 16; ++src) {
+                if (js[src] < 0) continue;
+                const int ts = tab != nullptr ? agg_slot<D>(tab, js[src]) : -1;
+                if (ts >= 0) {
 #pragma unroll
                     for (int u = 0; u < U; ++u) {
-                        dq[u] = fmaf(gsv, bf16_bits_to_f32(krow[16 * u]), dq[u]);
-                        atomicAdd(dK + base + 16 * u, scale * gsv * qd[u]);
-                        atomicAdd(dV + base + 16 * u, ps * gd[u]);
+                        atomicAdd(&tab->acc[ts][16 * u + tl], scale * gsv[src] * qd[u]);
+                        atomicAdd(&tab->acc[ts][D + 16 * u + tl], ps[src] * gd[u]);
+                    }
+                } else {
+                    const size_t base = ((size_t)js[src] * H + h) * D + tl;
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        atomicAdd(dK + base + 16 * u, scale * gsv[src] * qd[u]);
+                        atomicAdd(dV + base + 16 * u, ps[src] * gd[u]);
                     }
                 }
             }
+#pragma unroll
+            for (int src = 0; src < 16; ++src)
+#pragma unroll
+                for (int u = 0; u < U; ++u) dq[u] = fmaf(gsv[src], kel[src][u], dq[u]);
         }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) dQ[(size_t)qh * D + tl + 16 * u] = scale * dq[u];
+}
+
+// Per-pair scatter: one team per (query, head), 16 per workgroup.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_atomic_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
+    const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
+    int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float* __restrict__ dK,
+    float* __restrict__ dV) {
+    const int tl = threadIdx.x & 15;
+    const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+    if (qh >= (int64_t)N * H) return;  // whole team exits together
+    bwd_query<D>(Q, K, V, dO, idx, lse, qh, (int)(qh % H), tl, N, H, k, scale, dQ, dK, dV, nullptr);
+}
+
+// Key-aggregated scatter: one workgroup per kAggQueries positions of head
+// blockIdx.y in the grouped order.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_agg_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
+    const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
+    const int32_t* __restrict__ perm, int32_t N, int32_t H, int32_t k, float scale,
+    float* __restrict__ dQ, float* __restrict__ dK, float* __restrict__ dV) {
+    constexpr int C = AggTable<D>::kSlots;
+    __shared__ AggLds<D> tab;
+    const int tl = threadIdx.x & 15;
+    const int team = threadIdx.x >> 4;
+    const int h = blockIdx.y;
+    for (int e = threadIdx.x; e < C; e += 256) tab.key[e] = -1;
+    for (int e = threadIdx.x; e < C * 2 * D; e += 256) (&tab.acc[0][0])[e] = 0.0f;
+    __syncthreads();
+    for (int round = 0; round < kAggQueries / 16; ++round) {
+        const int64_t pos = (int64_t)blockIdx.x * kAggQueries + round * 16 + team;
+        if (pos >= N) break;  // positions grow with round: the team is done
+        const int64_t qh = (int64_t)perm[(size_t)h * N + pos] * H + h;
+        bwd_query<D>(Q, K, V, dO, idx, lse, qh, h, tl, N, H, k, scale, dQ, dK, dV, &tab);
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < C * 2 * D; e += 256) {
+        const int s = e / (2 * D), c = e - s * 2 * D;
+        const int32_t j = tab.key[s];
+        const float v = (&tab.acc[0][0])[e];
+        if (j >= 0 && v != 0.0f) {
+            float* dst = c < D ? dK : dV;
+            atomicAdd(dst + ((size_t)j * H + h) * D + (c < D ? c : c - D), v);
+        }
+    }
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(float4* __restrict__ p, size_t n4) {
@@ -141,6 +259,47 @@ hipError_t launch_bwd_atomic(const void* Q, const void* K, const void* V, const 
         case 64:
             hipLaunchKernelGGL(bwd_atomic_kernel<64>, dim3(blocks), dim3(256), 0, stream, q, kk, v,
                                g, idx, lse, N, H, k, scale, dQ, dK, dV);
+            break;
+        default:
+            return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace kmip
+
+namespace kmip {
+
+size_t bwd_agg_workspace_bytes(int32_t N, int32_t H, int32_t d) { return group_workspace_bytes(N, H, d); }
+
+hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const void* dO,
+                          const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
+                          int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
+                          hipStream_t stream) {
+    const int64_t nqh = (int64_t)N * H;
+    if (nqh == 0) return hipSuccess;
+    QueryGroups groups{};
+    hipError_t e = launch_group_queries(Q, N, H, d, ws, &groups, stream);
+    if (e != hipSuccess) return e;
+    if ((e = launch_fill_zero(dK, (size_t)nqh * d, stream)) != hipSuccess) return e;
+    if ((e = launch_fill_zero(dV, (size_t)nqh * d, stream)) != hipSuccess) return e;
+    const dim3 grid((unsigned)((N + kAggQueries - 1) / kAggQueries), (unsigned)H);
+    const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
+    const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
+    const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
+    const uint16_t* g = reinterpret_cast<const uint16_t*>(dO);
+    switch (d) {
+        case 16:
+            hipLaunchKernelGGL(bwd_agg_kernel<16>, grid, dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                               groups.perm, N, H, k, scale, dQ, dK, dV);
+            break;
+        case 32:
+            hipLaunchKernelGGL(bwd_agg_kernel<32>, grid, dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                               groups.perm, N, H, k, scale, dQ, dK, dV);
+            break;
+        case 64:
+            hipLaunchKernelGGL(bwd_agg_kernel<64>, grid, dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                               groups.perm, N, H, k, scale, dQ, dK, dV);
             break;
         default:
             return hipErrorInvalidValue;

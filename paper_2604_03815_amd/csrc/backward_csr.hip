@@ -1,0 +1,398 @@
+// Backward of k-MIP attention with a key-sorted segmented reduction.
+//
+// Same gradients as backward.hip (index set held fixed; Section 3.1, last
+// paragraph, and Appendix E, last paragraph, of arXiv 2604.03815):
+//   dQ_i = scale sum_j g_ij k_j,  dK_j = sum_i a_ij q_i,  dV_j = sum_i p_ij dO_i
+// with a_ij = scale g_ij.  Instead of scattering every pair's rows with
+// atomics, the pairs are sorted by key (a counting sort on the key row
+// j*H + h), and each key's rows are summed in registers over its run:
+//   1. coef:   per (query, head): p, dp, D, g; dQ_i; coefficients (a, p) of
+//              each selected pair, stored in pair order;
+//   2. count:  pairs per key row;
+//   3. scan:   exclusive prefix sum of the counts (three small kernels);
+//   4. place:  the pairs' records (key row, query, coefficients) in key
+//              order (the scanned counts serve as cursors);
+//   5. reduce: fixed chunks of the sorted pairs; a team of 16 lanes walks a
+//              contiguous stretch, dimensions on lanes, keeps the running
+//              sums of the current key in registers and adds them to dK and
+//              dV with one atomic per dimension where the key changes or
+//              the stretch ends.
+// Counting and placing aggregate equal key rows within a workgroup of 256
+// queries first, so a key that most queries select costs one global atomic
+// per workgroup, not one per pair.
+#include "kmip_device.h"
+#include "kmip_internal.h"
+
+namespace kmip {
+namespace {
+
+constexpr int kSlotsPerLane = (128 + 15) / 16;
+constexpr int kScanBlock = 1024;     // counts per block of the scan
+constexpr int kChunk = 1024;         // sorted pairs per wave in the reduction
+
+// 1. Per (query, head), a team of 16 lanes with the slots on lanes.
+template <int D>
+__global__ __launch_bounds__(256) void csr_coef_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
+    const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
+    int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float2* __restrict__ coef) {
+    const int tl = threadIdx.x & 15;
+    const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+    if (qh >= (int64_t)N * H) return;  // whole team exits together
+    const int h = (int)(qh % H);
+    float q[D], g[D];
+    load_row_f32<D>(q, Q + (size_t)qh * D);
+    load_row_f32<D>(g, dO + (size_t)qh * D);
+    const float l = lse[qh];
+    const int ns = (k + 15) >> 4;
+    float p[kSlotsPerLane], dp[kSlotsPerLane];
+    int32_t jj[kSlotsPerLane];
+    float dsum = 0.0f;
+#pragma unroll
+    for (int s = 0; s < kSlotsPerLane; ++s) {
+        p[s] = 0.0f;
+        dp[s] = 0.0f;
+        jj[s] = -1;
+        const int slot = tl + 16 * s;
+        if (s < ns && slot < k && l != -INFINITY) {
+            const int32_t j = idx[(size_t)qh * k + slot];
+            if (j >= 0 && j < N) {
+                jj[s] = j;
+                const float z = scale * dot_row_bf16<D>(q, K + ((size_t)j * H + h) * D);
+                p[s] = __expf(z - l);
+                dp[s] = dot_row_bf16<D>(g, V + ((size_t)j * H + h) * D);
+            }
+        }
+        dsum = fmaf(p[s], dp[s], dsum);
+    }
+    dsum = group16_sum(dsum);
+    // dQ: each slot lane adds g_s k_j over its own slots (the key row is read
+    // again, from cache), then the team reduces the D-vector so that lane tl
+    // ends up with dimensions tl, tl+16, ...
+    float acc[D];
+#pragma unroll
+    for (int t = 0; t < D; ++t) acc[t] = 0.0f;
+#pragma unroll
+    for (int s = 0; s < kSlotsPerLane; ++s) {
+        const int slot = tl + 16 * s;
+        if (s < ns && slot < k) {
+            const float gs = p[s] * (dp[s] - dsum);
+            coef[(size_t)qh * k + slot] = make_float2(scale * gs, p[s]);
+            if (jj[s] >= 0) {
+                float kr[D];
+                load_row_f32<D>(kr, K + ((size_t)jj[s] * H + h) * D);
+#pragma unroll
+                for (int t = 0; t < D; ++t) acc[t] = fmaf(gs, kr[t], acc[t]);
+            }
+        }
+    }
+    float out[D / 16];
+#pragma unroll
+    for (int u = 0; u < D / 16; ++u) {
+        float v = 0.0f;
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+            // lane tl keeps the team sum of dimension 16u + tl
+            const float tsum = group16_sum(acc[16 * u + t]);
+            if (t == tl) v = tsum;
+        }
+        out[u] = v;
+    }
+#pragma unroll
+    for (int u = 0; u < D / 16; ++u) dQ[(size_t)qh * D + 16 * u + tl] = scale * out[u];
+}
+
+// Key row of slot s of query-head qh, or -1 (padding).
+__device__ __forceinline__ int32_t pair_row(const int32_t* __restrict__ idx, int64_t qh, int s,
+                                            int32_t k, int32_t N, int32_t H) {
+    const int32_t j = idx[(size_t)qh * k + s];
+    return (j >= 0 && j < N) ? j * H + (int32_t)(qh % H) : -1;
+}
+
+// 2 and 4.  A workgroup takes 256 query-heads (a thread each, walking its
+// k slots) and first counts its pairs per key row in an LDS table, so that
+// a key row most queries select costs one global atomic per workgroup.
+// Rows that find no table slot count with their own global atomic.  The
+// count pass adds the table's counts to cnt.  The place pass reserves a range
+// of positions per table row with one atomic on the cursors (the scanned
+// counts), then gives each pair the next position of its row's range and
+// writes the pair's record there.
+constexpr int kTab = 2048;      // table rows per workgroup
+constexpr int kTabProbes = 8;
+
+struct PairRecord {
+    int32_t row;    // key row j*H + h
+    int32_t qh;     // query-head i*H + h
+    float a;        // scale * g_ij
+    float p;        // p_ij
+};
+
+struct CountTable {
+    int32_t key[kTab];
+    int32_t n[kTab];
+    int32_t base[kTab];
+};
+
+// Slot of key row r in the table (claimed if absent), or -1 if every probe
+// is taken by other rows.  With `claim` false, only looks up.
+__device__ __forceinline__ int tab_slot(CountTable* t, int32_t r, bool claim) {
+    const uint32_t hsh = ((uint32_t)r * 0x9E3779B1u) >> (32 - 11);
+    for (int p = 0; p < kTabProbes; ++p) {
+        const int ts = (int)((hsh + p) & (kTab - 1));
+        const int32_t cur = __hip_atomic_load(&t->key[ts], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (cur == r) return ts;
+        if (cur == -1) {
+            if (!claim) return -1;
+            const int32_t old = atomicCAS(&t->key[ts], -1, r);
+            if (old == -1 || old == r) return ts;
+        }
+    }
+    return -1;
+}
+
+template <bool kPlace>
+__global__ __launch_bounds__(256) void csr_count_kernel(const int32_t* __restrict__ idx,
+                                                        const float2* __restrict__ coef, int32_t N,
+                                                        int32_t H, int32_t k,
+                                                        int32_t* __restrict__ cnt,
+                                                        PairRecord* __restrict__ rec) {
+    static_assert(kTab == 1 << 11, "hash width");
+    __shared__ CountTable tab;
+    for (int e = threadIdx.x; e < kTab; e += 256) {
+        tab.key[e] = -1;
+        tab.n[e] = 0;
+    }
+    __syncthreads();
+    const int64_t qh = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const bool live = qh < (int64_t)N * H;
+    for (int s = 0; live && s < k; ++s) {
+        const int32_t r = pair_row(idx, qh, s, k, N, H);
+        if (r < 0) continue;
+        const int ts = tab_slot(&tab, r, true);
+        if (ts >= 0) {
+            atomicAdd(&tab.n[ts], 1);
+        } else if (kPlace) {
+            const float2 c = coef[(size_t)qh * k + s];
+            rec[atomicAdd(&cnt[r], 1)] = PairRecord{r, (int32_t)qh, c.x, c.y};
+        } else {
+            atomicAdd(&cnt[r], 1);
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < kTab; e += 256) {
+        const int32_t r = tab.key[e];
+        if (r < 0 || tab.n[e] == 0) continue;
+        const int32_t b = atomicAdd(&cnt[r], tab.n[e]);
+        if (kPlace) tab.base[e] = b;
+    }
+    if constexpr (kPlace) {
+        __syncthreads();
+        for (int e = threadIdx.x; e < kTab; e += 256) tab.n[e] = 0;
+        __syncthreads();
+        for (int s = 0; live && s < k; ++s) {
+            const int32_t r = pair_row(idx, qh, s, k, N, H);
+            if (r < 0) continue;
+            const int ts = tab_slot(&tab, r, false);
+            if (ts < 0) continue;  // placed above
+            const float2 c = coef[(size_t)qh * k + s];
+            rec[tab.base[ts] + atomicAdd(&tab.n[ts], 1)] = PairRecord{r, (int32_t)qh, c.x, c.y};
+        }
+    }
+}
+
+// 3.  Exclusive scan of n counts in place: block sums, a scan of the block
+// sums (one block), then each block's own scan plus its offset.
+__device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, int32_t* sh, int32_t* total) {
+    const int t = threadIdx.x;
+    sh[t] = v;
+    __syncthreads();
+    for (int off = 1; off < kScanBlock; off <<= 1) {
+        const int32_t add = t >= off ? sh[t - off] : 0;
+        __syncthreads();
+        sh[t] += add;
+        __syncthreads();
+    }
+    const int32_t incl = sh[t];
+    if (total != nullptr && t == kScanBlock - 1) *total = incl;
+    __syncthreads();
+    return incl - v;
+}
+
+__global__ __launch_bounds__(kScanBlock) void scan_blocks_kernel(const int32_t* __restrict__ cnt,
+                                                                 int64_t n, int32_t* __restrict__ sums) {
+    __shared__ int32_t sh[kScanBlock];
+    const int64_t i = (int64_t)blockIdx.x * kScanBlock + threadIdx.x;
+    block_exclusive_scan(i < n ? cnt[i] : 0, sh, &sums[blockIdx.x]);
+}
+
+// Scans the nb block sums in place, kScanBlock at a time with a running
+// carry; sums[nb] receives the grand total.
+__global__ __launch_bounds__(kScanBlock) void scan_sums_kernel(int32_t* __restrict__ sums, int32_t nb) {
+    __shared__ int32_t sh[kScanBlock];
+    __shared__ int32_t total;
+    const int t = threadIdx.x;
+    int32_t carry = 0;
+    for (int32_t base = 0; base < nb; base += kScanBlock) {
+        const int32_t v = base + t < nb ? sums[base + t] : 0;
+        const int32_t ex = block_exclusive_scan(v, sh, &total);
+        if (base + t < nb) sums[base + t] = ex + carry;
+        carry += total;
+        __syncthreads();  // every thread has read total before it is rewritten
+    }
+    if (t == 0) sums[nb] = carry;
+}
+
+__global__ __launch_bounds__(kScanBlock) void scan_apply_kernel(int32_t* __restrict__ cnt, int64_t n,
+                                                                const int32_t* __restrict__ sums) {
+    __shared__ int32_t sh[kScanBlock];
+    const int64_t i = (int64_t)blockIdx.x * kScanBlock + threadIdx.x;
+    const int32_t ex = block_exclusive_scan(i < n ? cnt[i] : 0, sh, nullptr);
+    if (i < n) cnt[i] = ex + sums[blockIdx.x];
+}
+
+// 5.  A wave per chunk of kChunk sorted pairs, four teams per wave, each team
+// a contiguous quarter of the chunk.  `total` = number of sorted pairs.
+template <int D>
+__global__ __launch_bounds__(256) void csr_reduce_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ dO,
+    const PairRecord* __restrict__ rec, const int32_t* __restrict__ total,
+    float* __restrict__ dK, float* __restrict__ dV) {
+    constexpr int U = D / 16;
+    constexpr int kTeamSpan = kChunk / 4;
+    const int tl = threadIdx.x & 15;
+    const int team = (int)(blockIdx.x * 16 + (threadIdx.x >> 4));
+    const int64_t e0 = (int64_t)team * kTeamSpan;
+    const int64_t e1 = min((int64_t)*total, e0 + kTeamSpan);
+    int32_t cur = -1;
+    float ak[U], av[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ak[u] = av[u] = 0.0f;
+    auto flush = [&]() {
+        if (cur >= 0) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                atomicAdd(dK + (size_t)cur * D + 16 * u + tl, ak[u]);
+                atomicAdd(dV + (size_t)cur * D + 16 * u + tl, av[u]);
+                ak[u] = av[u] = 0.0f;
+            }
+        }
+    };
+    for (int64_t b = e0; b < e1; b += 16) {
+        // Sixteen records at a time: lane t fetches record b + t, then the
+        // team walks them in order with each record broadcast.
+        const int64_t e = b + tl;
+        PairRecord r{-1, 0, 0.0f, 0.0f};
+        if (e < e1) r = rec[e];
+        const int n = (int)min((int64_t)16, e1 - b);
+        for (int t = 0; t < n; ++t) {
+            const int32_t rt = __shfl(r.row, t, 16);
+            const int32_t qt = __shfl(r.qh, t, 16);
+            const float at = __shfl(r.a, t, 16);
+            const float pt = __shfl(r.p, t, 16);
+            if (rt != cur) {
+                flush();
+                cur = rt;
+            }
+            const size_t qrow = (size_t)qt * D + tl;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                ak[u] = fmaf(at, bf16_bits_to_f32(Q[qrow + 16 * u]), ak[u]);
+                av[u] = fmaf(pt, bf16_bits_to_f32(dO[qrow + 16 * u]), av[u]);
+            }
+        }
+    }
+    flush();
+}
+
+}  // namespace
+
+size_t bwd_csr_workspace_bytes(int32_t N, int32_t H, int32_t k) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    const size_t nh = (size_t)N * H, pairs = nh * k;
+    const size_t nb = (nh + kScanBlock - 1) / kScanBlock;
+    return al(pairs * sizeof(float2)) + al(pairs * sizeof(PairRecord)) + al(nh * sizeof(int32_t)) +
+           al((nb + 1) * sizeof(int32_t));
+}
+
+hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const void* dO,
+                          const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
+                          int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
+                          hipStream_t stream) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    const int64_t nh = (int64_t)N * H;
+    if (nh == 0) return hipSuccess;
+    const size_t pairs = (size_t)nh * k;
+    const int32_t nb = (int32_t)((nh + kScanBlock - 1) / kScanBlock);
+    char* p = reinterpret_cast<char*>(ws);
+    float2* coef = reinterpret_cast<float2*>(p);
+    p += al(pairs * sizeof(float2));
+    PairRecord* rec = reinterpret_cast<PairRecord*>(p);
+    p += al(pairs * sizeof(PairRecord));
+    int32_t* cnt = reinterpret_cast<int32_t*>(p);
+    p += al((size_t)nh * sizeof(int32_t));
+    int32_t* sums = reinterpret_cast<int32_t*>(p);
+
+    const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
+    const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
+    const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
+    const uint16_t* g = reinterpret_cast<const uint16_t*>(dO);
+    hipError_t e;
+    // counts are zeroed with the float fill (same bits); n padded to 4
+    if ((e = launch_fill_zero(reinterpret_cast<float*>(cnt), ((size_t)nh + 3) / 4 * 4, stream)) != hipSuccess) return e;
+    if ((e = launch_fill_zero(dK, (size_t)nh * d, stream)) != hipSuccess) return e;
+    if ((e = launch_fill_zero(dV, (size_t)nh * d, stream)) != hipSuccess) return e;
+    const unsigned team_blocks = (unsigned)((nh + 15) / 16);
+    switch (d) {
+        case 16:
+            hipLaunchKernelGGL(csr_coef_kernel<16>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
+                               idx, lse, N, H, k, scale, dQ, coef);
+            break;
+        case 32:
+            hipLaunchKernelGGL(csr_coef_kernel<32>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
+                               idx, lse, N, H, k, scale, dQ, coef);
+            break;
+        case 64:
+            hipLaunchKernelGGL(csr_coef_kernel<64>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
+                               idx, lse, N, H, k, scale, dQ, coef);
+            break;
+        default:
+            return hipErrorInvalidValue;
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const unsigned qh_blocks = (unsigned)((nh + 255) / 256);
+    hipLaunchKernelGGL(csr_count_kernel<false>, dim3(qh_blocks), dim3(256), 0, stream, idx, coef, N, H,
+                       k, cnt, rec);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_blocks_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, stream, cnt,
+                       (int64_t)nh, sums);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(kScanBlock), 0, stream, sums, nb);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_apply_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, stream, cnt,
+                       (int64_t)nh, sums);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(csr_count_kernel<true>, dim3(qh_blocks), dim3(256), 0, stream, idx, coef, N, H,
+                       k, cnt, rec);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // one team per kChunk/4 sorted pairs, 16 teams per block; the grid covers
+    // every pair slot, teams past the total exit at once
+    const unsigned red_blocks = (unsigned)((pairs + kChunk * 4 - 1) / (kChunk * 4));
+    const int32_t* total = sums + nb;
+    switch (d) {
+        case 16:
+            hipLaunchKernelGGL(csr_reduce_kernel<16>, dim3(red_blocks), dim3(256), 0, stream, q, g, rec,
+                               total, dK, dV);
+            break;
+        case 32:
+            hipLaunchKernelGGL(csr_reduce_kernel<32>, dim3(red_blocks), dim3(256), 0, stream, q, g, rec,
+                               total, dK, dV);
+            break;
+        default:
+            hipLaunchKernelGGL(csr_reduce_kernel<64>, dim3(red_blocks), dim3(256), 0, stream, q, g, rec,
+                               total, dK, dV);
+            break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace kmip

@@ -86,6 +86,21 @@ hipError_t launch_bwd_atomic(const void* Q, const void* K, const void* V, const 
                              int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
                              hipStream_t stream);
 
+// Backward with key-aggregated scatter; ws holds bwd_agg_workspace_bytes().
+size_t bwd_agg_workspace_bytes(int32_t N, int32_t H, int32_t d);
+hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const void* dO,
+                          const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
+                          int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
+                          hipStream_t stream);
+
+// Backward with a key-sorted segmented reduction (backward_csr.hip); ws
+// holds bwd_csr_workspace_bytes().
+size_t bwd_csr_workspace_bytes(int32_t N, int32_t H, int32_t k);
+hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const void* dO,
+                          const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
+                          int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
+                          hipStream_t stream);
+
 hipError_t launch_fill_zero(float* p, size_t n, hipStream_t stream);
 
 }  // namespace kmip

@@ -60,7 +60,18 @@ def test_workspace_size(lib):
     assert lib.kmip_topk_workspace_size(100, 1, 24, 4, 1) == 0   # unsupported d
     assert lib.kmip_topk_workspace_size(-1, 1, 16, 4, 1) == 0
     assert lib.kmip_fwd_workspace_size(1000, 2, 32, 16, 1) == lib.kmip_topk_workspace_size(1000, 2, 32, 16, 1)
-    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == 0
+    # backward: per-pair atomics need none; key aggregation groups the queries
+    # (reference directions, labels, histogram + seed slots, permutation)
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 1) == 0
+    agg = 2 * 256 * 32 * 4 + 4096 + 2 * 2 * 256 * 4 + 8192
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 2) == agg
+    # the segmented reduction: pair coefficients (2 f32), the key-sorted pair
+    # records (16 B), per-key counts and the scan's block sums, each 256-byte
+    # aligned
+    csr = 32000 * 8 + 32000 * 16 + 8192 + 256
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 3) == csr
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == csr
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 4) == 0
 
 
 P = ctypes.c_void_p
@@ -103,6 +114,9 @@ def test_bwd_rejects(lib):
     f = ctypes.c_float
     args = [FAKE] * 6 + [64, 1, 16, 4, f(1.0), FAKE, FAKE, FAKE]
     assert lib.kmip_bwd(*args, 7, None, 0, None) == 2            # unknown variant
+    assert lib.kmip_bwd(*args, 3, None, 0, None) == 3            # segmented needs workspace
+    assert lib.kmip_bwd(*args, 2, None, 0, None) == 3            # aggregated needs workspace
+    assert lib.kmip_bwd(*args, 0, FAKE, 16, None) == 3           # workspace too small
     bad = list(args)
     bad[3] = None                                                 # dOut
     assert lib.kmip_bwd(*bad, 0, None, 0, None) == 1

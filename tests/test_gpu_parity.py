@@ -32,13 +32,14 @@ def _f64(w):
                  for n in ("q", "kk", "v", "dout"))
 
 
-def _run(w, backward=True):
+def _run(w, backward=True, variant=0):
     q, k, v = _dev(w.q), _dev(w.kk), _dev(w.v)
-    print(f"[case] {w.name} N={w.N} H={w.H} d={w.d} k={w.k} graphs={w.num_graphs}", flush=True)
+    print(f"[case] {w.name} N={w.N} H={w.H} d={w.d} k={w.k} graphs={w.num_graphs} bwd variant {variant}",
+          flush=True)
     out, idx, lse = kmip.fwd(q, k, v, w.k, w.scale, graph_offsets=w.offsets)
     grads = None
     if backward and w.dout is not None:
-        grads = kmip.bwd(q, k, v, _dev(w.dout), idx, lse, w.scale)
+        grads = kmip.bwd(q, k, v, _dev(w.dout), idx, lse, w.scale, variant=variant)
     torch.cuda.synchronize()
     res = {"out": out.cpu().numpy(), "idx": idx.cpu().numpy(), "lse": lse.cpu().numpy()}
     if grads is not None:
@@ -90,10 +91,35 @@ def test_config1_full():
     print(f"c1: {strict} well-separated, {loose} near-tied query-heads")
 
 
-def test_config2_full_fwd_bwd():
+@pytest.mark.parametrize("variant", [1, 2, 3])
+def test_config2_full_fwd_bwd(variant):
     w = workloads.make(2)
-    strict, loose = _check_all(w, _run(w))
+    strict, loose = _check_all(w, _run(w, variant=variant))
     print(f"c2: {strict} well-separated, {loose} near-tied query-heads")
+
+
+@pytest.mark.parametrize("d,k", [(16, 32), (32, 16), (64, 128)])
+def test_backward_hub_keys(d, k):
+    # Queries that all point the same way select the same few keys: the
+    # key-aggregated scatter then sums nearly all pairs in LDS.  Both
+    # backward variants must match the oracle on the GPU's own index sets.
+    rng = np.random.default_rng(d + k)
+    N, H = 20_000, 2
+    base = rng.standard_normal((1, H, d)).astype(np.float32)
+    q = base + 0.1 * rng.standard_normal((N, H, d)).astype(np.float32)
+    kk = rng.standard_normal((N, H, d)).astype(np.float32)
+    w = workloads.Workload("hubs", N, H, d, k, 1.0 / np.sqrt(d), None, workloads.bf16_round(q),
+                           workloads.bf16_round(kk),
+                           workloads.bf16_round(rng.standard_normal((N, H, d)).astype(np.float32)),
+                           workloads.bf16_round(rng.standard_normal((N, H, d)).astype(np.float32)),
+                           True)
+    Qd, Kd, Vd, dOd = _f64(w)
+    for variant in (1, 2, 3):
+        res = _run(w, variant=variant)
+        rq, rk, rv = oracle.backward(Qd, Kd, Vd, dOd, res["idx"], w.scale)
+        allclose_report("dQ", res["dq"], rq)
+        allclose_report("dK", res["dk"], rk)
+        allclose_report("dV", res["dv"], rv)
 
 
 @pytest.mark.parametrize("d", [16, 32, 64])
