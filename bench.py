@@ -45,7 +45,22 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-sample", type=int, default=2048, help="query-heads in the oracle sample")
     p.add_argument("--bwd-variant", type=int, default=0, help="backward: 0 library choice, 1 per-pair atomics, 2 key-aggregated, 3 key-sorted segmented")
+    p.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
+                   help="before the warm-up, run one plain copy kernel that reads and writes MIB MiB "
+                        "(the reference for the FETCH_SIZE/WRITE_SIZE counter runs)")
     return p.parse_args()
+
+
+def measured_traffic():
+    """Bytes per launch of the score+select kernel from profiles/select_traffic.json,
+    or None when there is none or the select sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "select_traffic.json")
+    if not os.path.exists(path):
+        return None
+    import rocprof_summary
+    with open(path) as f:
+        rec = json.load(f)
+    return rec["bytes_per_launch"] if rec.get("sources_sha256") == rocprof_summary.sources_hash() else None
 
 
 def cpu_baseline(w, sample):
@@ -132,6 +147,13 @@ def main():
         if ev is not None:
             ev[3].record()
 
+    if args.calib_copy > 0:
+        n = args.calib_copy * 2**20 // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats(dev)
     for _ in range(args.warmup):
@@ -192,8 +214,9 @@ def main():
         "peak_mem_bytes": peak_mem,
         "roofline": {
             "bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": tflops / PEAK_BF16_TFLOPS, "traffic": None,
-            "kernel": "select_kernel (score+select), incl. the K tiling pass in the timed call",
+            "frac": tflops / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),
+            "kernel": ("select_kernel (score+select); timed as the whole kmip_topk call, which also "
+                       "runs the query-grouping and key-tiling pre-passes"),
             "algorithmic": f"2*H*sum(n_g^2)*d = {flops:.4g} FLOP per launch",
         },
         "cpu_baseline": cpu,

@@ -1,0 +1,124 @@
+"""Summaries of rocprofv3 output for profiles/ and bench.py.
+
+  python rocprof_summary.py stats <results.db> <title> <command> > profiles/<name>.md
+      per-kernel durations (count, avg/min/max ms, share of GPU time) from a
+      --kernel-trace run.
+
+  python rocprof_summary.py traffic <fetch.db> <write.db> <copy_bytes> <command...>
+      HBM traffic of the score+select kernel from a FETCH_SIZE run and a
+      WRITE_SIZE run (both in KiB per dispatch), each scaled by what the same
+      counter reads for the calibration copy kernel (bench.py --calib-copy),
+      which reads and writes copy_bytes.  Writes profiles/select_traffic.json
+      (with a hash of the sources the counters were taken on; bench.py only
+      reports the figure while the sources are unchanged) and prints a
+      markdown summary.
+
+Reads the SQLite databases rocprofv3 writes by default.
+"""
+from __future__ import annotations
+
+import hashlib
+import json
+import os
+import sqlite3
+import sys
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "select_traffic.json")
+# sources whose change invalidates a measured traffic figure
+SELECT_SOURCES = ["paper_2604_03815_amd/csrc/select.hip", "paper_2604_03815_amd/csrc/group.hip",
+                  "paper_2604_03815_amd/csrc/api.hip", "paper_2604_03815_amd/csrc/kmip_device.h",
+                  "paper_2604_03815_amd/csrc/kmip_internal.h"]
+
+
+def sources_hash() -> str:
+    h = hashlib.sha256()
+    for rel in SELECT_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(rel.encode() + b"\0" + f.read() + b"\0")
+    return h.hexdigest()
+
+
+def short(name: str) -> str:
+    name = name.replace("kmip::(anonymous namespace)::", "")
+    if name.startswith("void "):
+        name = name[5:]
+    depth, out = 0, []
+    for ch in name:
+        if ch == "(" and depth == 0:
+            break
+        depth += ch == "<"
+        depth -= ch == ">"
+        out.append(ch)
+    return "".join(out).strip()
+
+
+def stats(db: str, title: str, command: str) -> None:
+    c = sqlite3.connect(db)
+    rows = c.execute("select name, count(*), avg(end-start), min(end-start), max(end-start), "
+                     "sum(end-start) from kernels group by name order by sum(end-start) desc").fetchall()
+    total = sum(r[5] for r in rows)
+    print(f"# Kernel durations: {title}\n")
+    print("Command (one MI355X, from the repository root; rocprofv3 writes its database to a "
+          "scratch directory):\n")
+    print(f"```\n{command}\n```\n")
+    print("| kernel | calls | avg ms | min ms | max ms | % of GPU time |")
+    print("|---|---|---|---|---|---|")
+    for name, n, avg, mn, mx, tot in rows:
+        print(f"| `{short(name)}` | {n} | {avg / 1e6:.3f} | {mn / 1e6:.3f} | {mx / 1e6:.3f} | "
+              f"{100 * tot / total:.2f} |")
+
+
+def counter_per_dispatch(db: str, counter: str):
+    """{short kernel name: mean over dispatches of the counter summed over its dimensions}."""
+    c = sqlite3.connect(db)
+    q = ("select kernel_name, dispatch_id, sum(value) from counters_collection "
+         "where counter_name = ? group by kernel_name, dispatch_id")
+    acc = {}
+    for kn, _, v in c.execute(q, (counter,)):
+        acc.setdefault(short(kn), []).append(v)
+    return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def traffic(fetch_db: str, write_db: str, copy_bytes: int, command: str) -> None:
+    fetch = counter_per_dispatch(fetch_db, "FETCH_SIZE")
+    write = counter_per_dispatch(write_db, "WRITE_SIZE")
+    copy = [k for k in fetch if "elementwise" in k.lower()]
+    sel = [k for k in fetch if k.startswith("select_kernel")]
+    if not copy or not sel:
+        raise SystemExit(f"need the calibration copy and select_kernel in the runs, got {sorted(fetch)}")
+    ck, sk = copy[0], sel[0]
+    f_scale = copy_bytes / (fetch[ck] * 1024.0)
+    w_scale = copy_bytes / (write[ck] * 1024.0)
+    fetch_b = fetch[sk] * 1024.0 * f_scale
+    write_b = write[sk] * 1024.0 * w_scale
+    res = {
+        "kernel": sk, "sources_sha256": sources_hash(), "fetch_bytes": fetch_b, "write_bytes": write_b,
+        "bytes_per_launch": fetch_b + write_b, "fetch_kib_raw": fetch[sk], "write_kib_raw": write[sk],
+        "copy_kernel": ck, "copy_bytes": copy_bytes, "copy_fetch_kib": fetch[ck],
+        "copy_write_kib": write[ck], "fetch_scale": f_scale, "write_scale": w_scale,
+        "command": command,
+    }
+    with open(TRAFFIC_JSON, "w") as f:
+        json.dump(res, f, indent=1)
+        f.write("\n")
+    print(f"# HBM traffic of `{sk}`\n")
+    print(f"Commands: `{command}`, once with `--pmc FETCH_SIZE` and once with `--pmc WRITE_SIZE`.\n")
+    print("| counter | select_kernel KiB/dispatch | copy kernel KiB | copy bytes | scale | select bytes |")
+    print("|---|---|---|---|---|---|")
+    print(f"| FETCH_SIZE | {fetch[sk]:.4g} | {fetch[ck]:.4g} | {copy_bytes} | {f_scale:.4f} | {fetch_b:.4g} |")
+    print(f"| WRITE_SIZE | {write[sk]:.4g} | {write[ck]:.4g} | {copy_bytes} | {w_scale:.4f} | {write_b:.4g} |")
+    print(f"\nTotal {fetch_b + write_b:.4g} bytes per launch.")
+
+
+def main(argv):
+    if len(argv) >= 4 and argv[1] == "stats":
+        stats(argv[2], argv[3], " ".join(argv[4:]))
+    elif len(argv) >= 5 and argv[1] == "traffic":
+        traffic(argv[2], argv[3], int(argv[4]), " ".join(argv[5:]))
+    else:
+        raise SystemExit(__doc__)
+
+
+if __name__ == "__main__":
+    main(sys.argv)
