@@ -30,8 +30,8 @@
 // key that could displace a heap entry, ties included, reaches the rare
 // path, and the heap compares full keys (score, then lower index).  The
 // result therefore does not depend on the order keys are streamed in, and
-// the scan of a graph's tiles may start anywhere and wrap around (used to
-// keep the waves of an XCD on the same tiles, see the pacer below).  Keys of
+// the scan may visit a graph's tiles in any order (used to keep the waves of
+// an XCD on the same tiles, see the pacer below).  Keys of
 // a tile that lie outside the query's graph are not masked in the streaming
 // loop; they can only send a tile down the rare path, which drops them by
 // index.
@@ -119,10 +119,10 @@ __device__ __forceinline__ float float_below(float x) {
 
 // Pacer of one XCD: a virtual position in a graph's key stream that moves at
 // the average speed of that XCD's waves, P(t) = pos + (t - t_ref) * rate
-// (tiles per tick of the 100 MHz wall clock).  A wave starts each item's
-// scan at P(now), so that waves which start items at different times still
-// read the same tiles at about the same time and share them in the XCD's
-// L2.  Each finished item folds its own speed into rate (moving average)
+// (tiles per tick of the 100 MHz wall clock).  A wave scans each item's
+// tiles chunk by chunk, taking the chunk at P(now) next, so that waves
+// which started items at different times still read the same tiles at
+// about the same time and share them in the XCD's L2.  Each finished item folds its own speed into rate (moving average)
 // and re-anchors (pos, t_ref).  The fields are read and written without
 // synchronisation; a torn read only yields a worse start tile, never a
 // wrong result.
@@ -135,18 +135,6 @@ struct Pacer {
 
 static_assert(kNumXcd * (sizeof(int32_t) + sizeof(Pacer)) <= kSelectCounterBytes,
               "work counters and pacers must fit their scratch");
-
-// Scan start for a graph of nt tiles (0 .. nt-1, relative to its first tile).
-__device__ __forceinline__ int pacer_start(const Pacer* p, int64_t now, int nt) {
-    const double rate = __hip_atomic_load(&p->rate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (!(rate > 0.0)) return 0;
-    const double pos = __hip_atomic_load(&p->pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int64_t t_ref = __hip_atomic_load(&p->t_ref, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const double v = pos + (double)(now - t_ref) * rate;
-    if (!(v >= 0.0) || v > 1e15) return 0;
-    const int64_t w = (int64_t)v % nt;
-    return (int)w;
-}
 
 // Folds the speed of an item that scanned nt tiles in `ticks` into the pacer.
 __device__ __forceinline__ void pacer_update(Pacer* p, int64_t now, int nt, int64_t ticks) {
@@ -387,35 +375,66 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         __builtin_amdgcn_wave_barrier();
     };
 
-    // The graph's tiles t0 .. t1-1 are scanned in the order ts .. t1-1,
-    // t0 .. ts-1; with one graph, ts comes from the XCD's pacer.
+    // The graph's tiles t0 .. t1-1 are scanned in nch <= 64 chunks of cs
+    // tiles.  After each chunk the wave goes on with the first chunk not yet
+    // scanned at or after its XCD's virtual position (cyclically), evaluated
+    // from the pacer state read at the item's start and the wall clock; with
+    // several graphs, or before the pacer knows a speed, chunks go in order.
+    // A wave that falls behind or runs ahead of the others thus rejoins them
+    // at every chunk, not just at the next item.
     const int t0 = key_lo >> 5;
     const int t1 = (key_hi + 31) >> 5;
     const int nt = t1 - t0;
+    const int cs = (nt + 63) / 64;
+    const int nch = (nt + cs - 1) / cs;
+    const uint64_t all_chunks = nch == 64 ? ~0ull : ((1ull << nch) - 1ull);
+    // The virtual position relative to t0 at the item's start (pace_v0, in
+    // [0, nt)) and its speed (tiles per tick; 0 when unknown).
+    float pace_v0 = 0.0f, pace_rate = 0.0f;
     int64_t item_start = 0;
-    int ts = t0;
     if (tasks == nullptr) {
-        int rel = 0;
-        if (lane == 0) {
-            item_start = wall_clock64();
-            rel = pacer_start(&pacers[xcd], item_start, nt);
+        const Pacer* pc = &pacers[xcd];
+        const double rate = __hip_atomic_load(&pc->rate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const double pos = __hip_atomic_load(&pc->pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int64_t ref = __hip_atomic_load(&pc->t_ref, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        item_start = wall_clock64();
+        const double v = pos + (double)(item_start - ref) * rate;
+        if (rate > 0.0 && v >= 0.0 && v < 1e15) {
+            pace_v0 = (float)((int64_t)v % nt);
+            pace_rate = (float)rate;
         }
-        ts = t0 + __builtin_amdgcn_readfirstlane(rel);
     }
-    auto tile_at = [&](int i) { return ts + i >= t1 ? ts + i - nt : ts + i; };
+    const float inv_cs = 1.0f / (float)cs;
+    // Next chunk: the first one not in `done` at or after the virtual
+    // position's chunk, else `fallback`'s.
+    auto choose = [&](uint64_t done, int fallback) {
+        int vc = fallback;
+        if (pace_rate > 0.0f) {
+            float v = pace_v0 + (float)(wall_clock64() - item_start) * pace_rate;
+            v -= (float)nt * floorf(v / (float)nt);
+            vc = min(nch - 1, max(0, (int)(v * inv_cs)));
+        }
+        vc = __builtin_amdgcn_readfirstlane(vc);
+        const uint64_t avail = all_chunks & ~done;
+        const uint64_t ahead = avail & (~0ull << vc);
+        return ahead != 0ull ? (int)__builtin_ctzll(ahead) : (int)__builtin_ctzll(avail);
+    };
     const uint32_t lane_off = (uint32_t)lane * 16u;
 
-    // Prefetch ring: scan position i sits in slot i % PF; the slot is
-    // refilled with position i + PF as soon as position i's MFMAs are
-    // issued.  `next` walks the graph's tiles one per refill and wraps from
-    // t1 back to t0, so it never leaves the graph's tiles.
+    // Prefetch ring: each slot holds one tile, and slot_tile[] remembers
+    // which; a slot is refilled with the next tile of the scan as soon as its
+    // MFMAs are issued.  Once every chunk has been issued the refills keep
+    // reading valid tiles of the graph that are never filtered.
     constexpr int PF = 8 / NC;
     const char* head_tiles = reinterpret_cast<const char*>(kp) + (size_t)head * (ntiles + kPadTiles) * TILE_BYTES;
-    const char* wrap_lo = head_tiles + (size_t)t0 * TILE_BYTES;
-    const char* wrap_hi = head_tiles + (size_t)t1 * TILE_BYTES;
-    const char* next = head_tiles + (size_t)ts * TILE_BYTES;
+    int cur = choose(0ull, 0);
+    uint64_t done = 1ull << cur;
+    int rel = cur * cs, rel_end = min(nt, rel + cs);
+    const char* next = head_tiles + (size_t)(t0 + rel) * TILE_BYTES;
     i32x4 ring[PF][NC];
-    auto refill = [&](i32x4 (&slot)[NC]) {
+    int slot_tile[PF];
+    auto refill = [&](i32x4 (&slot)[NC], int& stile) {
+        stile = t0 + rel;
         slot[0] = ring_load<0>(next, lane_off);
         if constexpr (NC >= 2) slot[1] = ring_load<1024>(next, lane_off);
         if constexpr (NC >= 4) {
@@ -423,10 +442,21 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
             slot[3] = ring_load<3072>(next, lane_off);
         }
         next += TILE_BYTES;
-        if (next == wrap_hi) next = wrap_lo;
+        if (++rel == rel_end) {
+            if (done != all_chunks) {
+                cur = choose(done, cur + 1 < nch ? cur + 1 : 0);
+                done |= 1ull << cur;
+                rel = cur * cs;
+                rel_end = min(nt, rel + cs);
+            } else {
+                rel = 0;
+                rel_end = nt;
+            }
+            next = head_tiles + (size_t)(t0 + rel) * TILE_BYTES;
+        }
     };
 #pragma unroll
-    for (int u = 0; u < PF; ++u) refill(ring[u]);
+    for (int u = 0; u < PF; ++u) refill(ring[u], slot_tile[u]);
 
     // Scores of the tile in ring slot `a`; PF - 1 later tiles are in flight.
     auto scores = [&](i32x4 (&a)[NC], f32x16 (&acc)[QB]) {
@@ -453,8 +483,8 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         return fmaxf(fmaxf(fmaxf(l0, l1), l2), fmaxf(fmaxf(l3, l4), a[15]));
     };
 
-    // Filter the scores of scan position i.
-    auto filter = [&](const f32x16 (&acc)[QB], int i) {
+    // Filter the scores of key tile `tile`.
+    auto filter = [&](const f32x16 (&acc)[QB], int tile) {
         float m[QB];
 #pragma unroll
         for (int b = 0; b < QB; ++b) m[b] = max16(acc[b]);
@@ -462,43 +492,47 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
 #pragma unroll
         for (int b = 0; b < QB; ++b) any |= __builtin_amdgcn_ballot_w64(m[b] > theta[b]);
         if (any != 0ull) {
-            const int tile = tile_at(i);
 #pragma unroll
             for (int b = 0; b < QB; ++b)
                 if (__builtin_amdgcn_ballot_w64(m[b] > theta[b]) != 0ull) rare_path(acc[b], b, tile << 5);
         }
     };
 
-    // Software pipeline with two accumulator sets: the MFMAs of position
-    // i+1 are issued before position i is filtered, so matrix cores and
-    // filter overlap.  Scores of positions past nt may be formed but are
-    // never filtered.  The main loop runs whole groups of PF positions
-    // without checks; the tail group checks each position.
+    // Software pipeline with two accumulator sets: the MFMAs of scan
+    // position i+1 are issued before position i is filtered, so matrix cores
+    // and filter overlap.  Scores past the nt positions of the scan may be
+    // formed but are never filtered.  The main loop runs whole groups of PF
+    // positions without checks; the tail group checks each position.
     f32x16 acc_a[QB], acc_b[QB];
+    int tile_a = slot_tile[0], tile_b = 0;
     scores(ring[0], acc_a);
-    refill(ring[0]);
+    refill(ring[0], slot_tile[0]);
     int i = 0;
     for (const int i_full = nt / PF * PF; i < i_full; i += PF) {
 #pragma unroll
         for (int u = 0; u < PF; u += 2) {
+            tile_b = slot_tile[u + 1];
             scores(ring[u + 1], acc_b);
-            refill(ring[u + 1]);
-            filter(acc_a, i + u);
+            refill(ring[u + 1], slot_tile[u + 1]);
+            filter(acc_a, tile_a);
+            tile_a = slot_tile[(u + 2) % PF];
             scores(ring[(u + 2) % PF], acc_a);
-            refill(ring[(u + 2) % PF]);
-            filter(acc_b, i + u + 1);
+            refill(ring[(u + 2) % PF], slot_tile[(u + 2) % PF]);
+            filter(acc_b, tile_b);
         }
     }
 #pragma unroll
     for (int u = 0; u < PF; u += 2) {
         if (i + u >= nt) goto stream_done;
+        tile_b = slot_tile[u + 1];
         scores(ring[u + 1], acc_b);
-        refill(ring[u + 1]);
-        filter(acc_a, i + u);
+        refill(ring[u + 1], slot_tile[u + 1]);
+        filter(acc_a, tile_a);
         if (i + u + 1 >= nt) goto stream_done;
+        tile_a = slot_tile[(u + 2) % PF];
         scores(ring[(u + 2) % PF], acc_a);
-        refill(ring[(u + 2) % PF]);
-        filter(acc_b, i + u + 1);
+        refill(ring[(u + 2) % PF], slot_tile[(u + 2) % PF]);
+        filter(acc_b, tile_b);
     }
 stream_done:
     // Drain the ring.  Every ring register is an operand of the wait: a
