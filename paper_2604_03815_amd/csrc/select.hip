@@ -99,13 +99,12 @@ __device__ __forceinline__ float pick16(const f32x16& a, int r) {
     return __uint_as_float(bsel(m0, v2[1], v2[0]));
 }
 
-// 4-ary min-heap in LDS: column `col` of a [k + kHeapPad][32] array of keys,
-// node p with children 4p+1 .. 4p+4.  Rows k .. k+2 hold kHeapTop, above any
-// real key, so that the last parent's missing children never win and no
-// child needs a bounds check; a drained row is set to kHeapTop too.  Four
-// children per level (read together, one LDS round trip) halve the depth of
-// a binary heap: 3 levels below the root for k = 32, 4 for k = 128.
-constexpr int kHeapPad = 3;
+// 4-ary min-heap in LDS: column `col` of a [k][32] array of keys, node p
+// with children 4p+1 .. 4p+4.  A missing child (past row k-1) reads as
+// kHeapTop, above any real key, so it never wins; a drained row is set to
+// kHeapTop too.  Four children per level (read together, one LDS round
+// trip) halve the depth of a binary heap: 3 levels below the root for
+// k = 32, 4 for k = 128.
 constexpr uint64_t kHeapTop = ~0ull;
 
 // The largest float below x, for a finite heap score x; a zero or denormal
@@ -159,8 +158,14 @@ __device__ __forceinline__ void heap_sift_down(uint64_t* hp, int col, int k, uin
     for (;;) {
         const int c = 4 * pos + 1;
         if (c >= k) break;
-        const uint64_t m0 = hp[c * 32 + col], m1 = hp[(c + 1) * 32 + col];
-        const uint64_t m2 = hp[(c + 2) * 32 + col], m3 = hp[(c + 3) * 32 + col];
+        // rows past k - 1 are clamped for the read and replaced by kHeapTop
+        const uint64_t m0 = hp[c * 32 + col];
+        const uint64_t r1 = hp[min(c + 1, k - 1) * 32 + col];
+        const uint64_t r2 = hp[min(c + 2, k - 1) * 32 + col];
+        const uint64_t r3 = hp[min(c + 3, k - 1) * 32 + col];
+        const uint64_t m1 = c + 1 < k ? r1 : kHeapTop;
+        const uint64_t m2 = c + 2 < k ? r2 : kHeapTop;
+        const uint64_t m3 = c + 3 < k ? r3 : kHeapTop;
         const int j01 = m1 < m0 ? 1 : 0, j23 = m3 < m2 ? 3 : 2;
         const uint64_t v01 = min_u64(m0, m1), v23 = min_u64(m2, m3);
         const int j = v23 < v01 ? j23 : j01;
@@ -184,7 +189,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     constexpr int NC = D / 16;
     constexpr int TILE_BYTES = NC * 64 * 16;
     extern __shared__ uint64_t lds[];
-    const int hrows = k + kHeapPad;
+    const int hrows = k;
 
     // Persistent, XCD-aware schedule.  Workgroups are dispatched to the XCDs
     // round-robin; the ones on XCD x take the items of a contiguous range of
@@ -241,7 +246,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     const int col = lane & 31;
     const int half = lane >> 5;
 
-    uint64_t* heaps = lds;                              // [QB][k + kHeapPad][32]
+    uint64_t* heaps = lds;                              // [QB][k][32]
     uint64_t* cand = lds + (size_t)QB * hrows * 32;     // [QB][SLOTS][64]
 
     bf16x8 bq[QB][NC];
@@ -263,7 +268,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         theta[b] = valid ? -INFINITY : INFINITY;
         cnt[b] = 0;
     }
-    for (int e = lane; e < QB * hrows * 32; e += 64) heaps[e] = (e / 32) % hrows < k ? 0ull : kHeapTop;
+    for (int e = lane; e < QB * hrows * 32; e += 64) heaps[e] = 0ull;
 
     // Seeded thresholds.  Queries of one direction label share most of their
     // top-k keys.  When some query of the label of a block's first query has
@@ -552,7 +557,7 @@ stream_done:
 
     // Drain each heap in increasing order into slots k-1 .. 0, which leaves
     // the row sorted by (score desc, index asc); sentinels become -1.  The
-    // vacated last row takes kHeapTop, so the heap shrinks without bounds.
+    // vacated last row takes kHeapTop, so the heap shrinks without a size.
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
         const int qi = 32 * b + col;
@@ -643,7 +648,7 @@ hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, con
 }  // namespace
 
 size_t select_lds_bytes(int32_t k, SelectShape shape) {
-    return (size_t)shape.qb * ((size_t)(k + kHeapPad) * 32 + (size_t)shape.slots * 64) * sizeof(uint64_t);
+    return (size_t)shape.qb * ((size_t)k * 32 + (size_t)shape.slots * 64) * sizeof(uint64_t);
 }
 
 hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t d, int32_t ntiles,
