@@ -63,7 +63,9 @@ typedef enum {
 /*
  * Bytes of device workspace kmip_topk / kmip_fwd need for these sizes
  * (0 if the sizes are invalid).  Holds a tiled copy of K and, for more than
- * one graph, the work list.
+ * one graph, the work list; for a single graph of at least 8192 nodes, the
+ * grouping of the queries by direction and the stored order of the keys
+ * with the bounds the kernel uses to skip key blocks (linear in N).
  */
 size_t kmip_topk_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t num_graphs);
 

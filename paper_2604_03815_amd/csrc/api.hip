@@ -72,6 +72,9 @@ size_t packed_k_bytes(int64_t N, int32_t H, int32_t d) {
     return (size_t)H * (size_t)(num_tiles(N) + kmip::kPadTiles) * 32 * (size_t)d * 2;
 }
 
+// The tiled keys, before the counters.
+size_t tiled_bytes(int64_t N, int32_t H, int32_t d) { return align_up(packed_k_bytes(N, H, d)); }
+
 // The select kernel's per-XCD work counters and pacers, after the tiled keys.
 constexpr size_t kCounterBytes = kmip::kSelectCounterBytes;
 
@@ -113,9 +116,11 @@ const char* kmip_last_error(void) { return g_last_error.c_str(); }
 size_t kmip_topk_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t num_graphs) {
     if (check_sizes(N, H, d, k) != KMIP_OK) return 0;
     const int32_t G = num_graphs < 1 ? 1 : num_graphs;
-    size_t bytes = align_up(packed_k_bytes(N, H, d)) + kCounterBytes;
+    size_t bytes = tiled_bytes(N, H, d) + kCounterBytes;
     if (G > 1) bytes += align_up(max_tasks(N, G) * sizeof(kmip::Task));
-    if (use_grouping(N, G)) bytes += align_up(kmip::group_workspace_bytes((int32_t)N, H, d));
+    if (use_grouping(N, G))
+        bytes += align_up(kmip::group_workspace_bytes((int32_t)N, H, d)) +
+                 align_up(kmip::key_order_workspace_bytes((int32_t)N, H, d));
     return bytes;
 }
 
@@ -165,7 +170,7 @@ kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offse
             return (int64_t)a.q_count * (a.key_hi - a.key_lo) > (int64_t)b.q_count * (b.key_hi - b.key_lo);
         });
         ntasks = (int32_t)tasks.size();
-        void* dst = ws + align_up(packed_k_bytes(N, H, d)) + kCounterBytes;
+        void* dst = ws + tiled_bytes(N, H, d) + kCounterBytes;
         hipError_t e = hipMemcpyAsync(dst, tasks.data(), tasks.size() * sizeof(kmip::Task),
                                       hipMemcpyHostToDevice, stream);
         if (e != hipSuccess) return hip_fail(e, "work list upload");
@@ -174,18 +179,24 @@ kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offse
         ntasks = (int32_t)((N + 32 * qb - 1) / (32 * qb));
     }
 
+    // A single large graph: queries grouped by direction, keys stored in
+    // superblock order with bounds.
     kmip::QueryGroups groups{};
+    kmip::KeyOrder keys{};
     const bool grouped = use_grouping(N, G);
     if (grouped) {
-        void* gws = ws + align_up(packed_k_bytes(N, H, d)) + kCounterBytes;
+        char* gws = ws + tiled_bytes(N, H, d) + kCounterBytes;
         hipError_t e = kmip::launch_group_queries(Q, n32, H, d, gws, &groups, stream);
         if (e != hipSuccess) return hip_fail(e, "query grouping launch");
+        char* kws = gws + align_up(kmip::group_workspace_bytes(n32, H, d));
+        e = kmip::launch_key_order(K, n32, H, d, ntiles, kws, &keys, stream);
+        if (e != hipSuccess) return hip_fail(e, "key order launch");
     }
-    hipError_t e = kmip::launch_pack_k(K, kp, n32, H, d, ntiles, stream);
+    hipError_t e = kmip::launch_pack_k(K, grouped ? keys.perm : nullptr, kp, n32, H, d, ntiles, stream);
     if (e != hipSuccess) return hip_fail(e, "pack_k launch");
-    int32_t* work_ctr = reinterpret_cast<int32_t*>(ws + align_up(packed_k_bytes(N, H, d)));
-    e = kmip::launch_select(kp, Q, dtasks, grouped ? &groups : nullptr, ntasks, n32, H, d, k, ntiles,
-                            shape, work_ctr, topk_idx, stream);
+    int32_t* work_ctr = reinterpret_cast<int32_t*>(ws + tiled_bytes(N, H, d));
+    e = kmip::launch_select(kp, Q, K, dtasks, grouped ? &groups : nullptr, grouped ? &keys : nullptr,
+                            ntasks, n32, H, d, k, ntiles, shape, work_ctr, topk_idx, stream);
     if (e != hipSuccess) return hip_fail(e, "select launch");
     return ok();
 }

@@ -1,0 +1,611 @@
+// Key order and superblock bounds for the score+select kernel.
+//
+// Every key the select kernel skips must provably score no more than the
+// query's threshold.  Keys are grouped into superblocks of 256 (kSuperTiles
+// tiles), each with a ball that contains all of its keys: a center c (the
+// mean, rounded to bf16) and a radius R >= |k - c| with margins that cover
+// the rounding of the scores (see sb_bounds_kernel).  For a query q every
+// key of the superblock then scores at most q.c + |q| R, and a superblock
+// whose bound does not beat any of a wave's thresholds is skipped.
+//
+// The bounds are tight when each superblock is small in every direction.
+// The keys are therefore stored, per head, in the leaf order of a balanced
+// binary space-partitioning tree: each node splits its keys at the median of
+// their projections on the node's principal axis (estimated by power
+// iteration on an evenly spaced sample of the node), with the left part
+// rounded up to a whole number of superblocks, down to nodes of at most 256
+// keys.  Every leaf is then exactly one superblock.  The tree is built level
+// by level; a level's split is an exact selection of the left part by a
+// two-pass radix select on a 16-bit quantisation of the projections (keys
+// with the split value are assigned to the two sides by ticket).  The order
+// only decides which tiles the select kernel visits together: it records
+// each candidate by its original key index, so the result does not depend
+// on it.
+#include "kmip_device.h"
+#include "kmip_internal.h"
+
+namespace kmip {
+namespace {
+
+constexpr int SBK = kSuperTiles * 32;  // keys per superblock
+static_assert(SBK == 256, "one thread per key of a superblock");
+constexpr int kSample = 256;           // keys sampled per node for its axis
+constexpr int kPowerIters = 8;
+
+// Per-node working data of one level, [H][width]:
+//   f: mean[d], axis[d], lo, inv_step (projection p maps to
+//      clamp((p - lo) * inv_step) in 0 .. 65535)
+//   h: hist1[256], hist2[256], then left, right, tie counters
+constexpr int kNodeInts = 512 + 4;
+
+// Size of the left part of a node of n > SBK keys: half, rounded up to whole
+// superblocks, and at least one key on the right.
+__host__ __device__ __forceinline__ int split_left(int n) {
+    const int half = (n + 1) / 2;
+    const int nl = (half + SBK - 1) / SBK * SBK;
+    return nl < n - 1 ? nl : n - 1;
+}
+
+// Node of level lev (root: 0) that holds position p: its first position lo,
+// size n and index among the level's nodes.  False when p lies in a leaf of
+// an earlier level (no longer split).
+__device__ __forceinline__ bool node_of(int p, int N, int lev, int& lo, int& n, int& idx) {
+    lo = 0;
+    n = N;
+    idx = 0;
+    for (int l = 0; l < lev; ++l) {
+        if (n <= SBK) return false;
+        const int nl = split_left(n);
+        if (p < lo + nl) {
+            n = nl;
+            idx = 2 * idx;
+        } else {
+            lo += nl;
+            n -= nl;
+            idx = 2 * idx + 1;
+        }
+    }
+    return n > SBK;
+}
+
+// Node idx of level lev by its path (bit lev-1-l of idx picks the side at
+// level l).  False when the path ends in a leaf before level lev.
+__device__ __forceinline__ bool node_by_index(int idx, int N, int lev, int& lo, int& n) {
+    lo = 0;
+    n = N;
+    for (int l = 0; l < lev; ++l) {
+        if (n <= SBK) return false;
+        const int nl = split_left(n);
+        if (((idx >> (lev - 1 - l)) & 1) == 0) {
+            n = nl;
+        } else {
+            lo += nl;
+            n -= nl;
+        }
+    }
+    return n > SBK;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+    return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
+    return v;
+}
+
+__device__ __forceinline__ float wave_min(float v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v = fminf(v, __shfl_xor(v, m));
+    return v;
+}
+
+// Sum over the 256 threads of a block of each of D values; every thread
+// gets the sums in out[].  red: LDS [4][D].
+template <int D>
+__device__ __forceinline__ void block_sum(const float (&v)[D], float (&out)[D], float (*red)[D]) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+        const float s = wave_sum(v[i]);
+        if ((t & 63) == 0) red[t >> 6][i] = s;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < D; ++i) out[i] = (red[0][i] + red[1][i]) + (red[2][i] + red[3][i]);
+    __syncthreads();
+}
+
+// Level lev, one block per node: the node's mean and principal axis from an
+// evenly spaced sample of its keys, the quantisation range of the sample's
+// projections, and zeroed histograms and counters.
+template <int D>
+__global__ __launch_bounds__(256) void tree_axis_kernel(const uint16_t* __restrict__ K,
+                                                        const int32_t* __restrict__ perm, int32_t N,
+                                                        int32_t H, int32_t lev, int32_t width,
+                                                        float* __restrict__ nodef,
+                                                        int32_t* __restrict__ nodeh) {
+    __shared__ float red[4][D];
+    __shared__ float rmax[4];
+    __shared__ int rarg[4];
+    const int idx = blockIdx.x;
+    const int h = blockIdx.y;
+    const int t = threadIdx.x;
+    int lo, n;
+    if (!node_by_index(idx, N, lev, lo, n)) return;
+    int32_t* nh = nodeh + ((size_t)h * width + idx) * kNodeInts;
+    for (int e = t; e < kNodeInts; e += 256) nh[e] = 0;
+    const int S = n < kSample ? n : kSample;
+    const bool act = t < S;
+    float x[D];
+    if (act) {
+        const int p = lo + (int)(((int64_t)(2 * t + 1) * n) / (2 * S));
+        load_row_f32<D>(x, K + ((size_t)perm[(size_t)h * N + p] * H + h) * D);
+    } else {
+#pragma unroll
+        for (int i = 0; i < D; ++i) x[i] = 0.0f;
+    }
+    float mu[D];
+    block_sum<D>(x, mu, red);
+    const float inv_s = 1.0f / (float)S;
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+        mu[i] *= inv_s;
+        x[i] = act ? x[i] - mu[i] : 0.0f;
+    }
+    // start from the sample farthest from the mean
+    float dd = 0.0f;
+#pragma unroll
+    for (int i = 0; i < D; ++i) dd = fmaf(x[i], x[i], dd);
+    float m = wave_max(dd);
+    const uint64_t hit = __builtin_amdgcn_ballot_w64(dd == m);
+    if ((t & 63) == 0) {
+        rmax[t >> 6] = m;
+        rarg[t >> 6] = (t & ~63) + (int)__builtin_ctzll(hit);
+    }
+    __syncthreads();
+    int far = rarg[0];
+    float fm = rmax[0];
+    for (int wv = 1; wv < 4; ++wv)
+        if (rmax[wv] > fm) {
+            fm = rmax[wv];
+            far = rarg[wv];
+        }
+    float axis[D];
+#pragma unroll
+    for (int i = 0; i < D; ++i) axis[i] = t == far ? x[i] : 0.0f;
+    block_sum<D>(axis, axis, red);
+    // power iteration: axis <- sum_s (x_s . axis) x_s, normalised
+    for (int it = 0; it < kPowerIters; ++it) {
+        float nn = 0.0f;
+#pragma unroll
+        for (int i = 0; i < D; ++i) nn = fmaf(axis[i], axis[i], nn);
+        const float inv = nn > 0.0f ? rsqrtf(nn) : 0.0f;
+        float pr = 0.0f;
+#pragma unroll
+        for (int i = 0; i < D; ++i) pr = fmaf(x[i], axis[i] * inv, pr);
+        float c[D];
+#pragma unroll
+        for (int i = 0; i < D; ++i) c[i] = pr * x[i];
+        block_sum<D>(c, axis, red);
+    }
+    float nn = 0.0f;
+#pragma unroll
+    for (int i = 0; i < D; ++i) nn = fmaf(axis[i], axis[i], nn);
+    if (nn > 0.0f) {
+        const float inv = rsqrtf(nn);
+#pragma unroll
+        for (int i = 0; i < D; ++i) axis[i] *= inv;
+    } else {
+#pragma unroll
+        for (int i = 0; i < D; ++i) axis[i] = i == 0 ? 1.0f : 0.0f;
+    }
+    float pr = 0.0f;
+#pragma unroll
+    for (int i = 0; i < D; ++i) pr = fmaf(x[i], axis[i], pr);
+    float pmin = wave_min(act ? pr : INFINITY), pmax = wave_max(act ? pr : -INFINITY);
+    if ((t & 63) == 0) {
+        red[t >> 6][0] = pmin;
+        red[t >> 6][1] = pmax;
+    }
+    __syncthreads();
+    pmin = fminf(fminf(red[0][0], red[1][0]), fminf(red[2][0], red[3][0]));
+    pmax = fmaxf(fmaxf(red[0][1], red[1][1]), fmaxf(red[2][1], red[3][1]));
+    float* nf = nodef + ((size_t)h * width + idx) * (2 * D + 2);
+    if (t < D) {
+        nf[t] = mu[t];
+        nf[D + t] = axis[t];
+    }
+    if (t == 0) {
+        // the mean-centred projection of the sample, widened a little so that
+        // most keys fall inside the quantised range
+        const float span = pmax - pmin;
+        nf[2 * D] = pmin - 0.0625f * span;
+        nf[2 * D + 1] = span > 0.0f ? 65535.0f / (1.125f * span) : 0.0f;
+    }
+}
+
+template <int D>
+__device__ __forceinline__ uint32_t quantise(const float* __restrict__ nf, const float (&x)[D]) {
+    float pr = 0.0f;
+#pragma unroll
+    for (int i = 0; i < D; ++i) pr = fmaf(x[i] - nf[i], nf[D + i], pr);
+    const float u = (pr - nf[2 * D]) * nf[2 * D + 1];
+    return (uint32_t)fminf(fmaxf(u, 0.0f), 65535.0f);
+}
+
+// Level lev, one thread per position: the 16-bit projection code of the key
+// at that position, and the histogram of its high byte per node.
+template <int D>
+__global__ __launch_bounds__(256) void tree_project_kernel(const uint16_t* __restrict__ K,
+                                                           const int32_t* __restrict__ perm, int32_t N,
+                                                           int32_t H, int32_t lev, int32_t width,
+                                                           const float* __restrict__ nodef,
+                                                           int32_t* __restrict__ nodeh,
+                                                           uint16_t* __restrict__ code) {
+    const int h = blockIdx.y;
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    int lo, n, idx;
+    if (p >= N || !node_of(p, N, lev, lo, n, idx)) return;
+    float x[D];
+    load_row_f32<D>(x, K + ((size_t)perm[(size_t)h * N + p] * H + h) * D);
+    const uint32_t q = quantise<D>(nodef + ((size_t)h * width + idx) * (2 * D + 2), x);
+    code[(size_t)h * N + p] = (uint16_t)q;
+    atomicAdd(&nodeh[((size_t)h * width + idx) * kNodeInts + (q >> 8)], 1);
+}
+
+// The bin of a 256-bin histogram in which the target-th element (0-based, in
+// increasing order) falls, and the count below that bin.  Run by every
+// thread of the block over the same LDS array after a barrier.
+__device__ __forceinline__ void find_bin(const int32_t* hs, int target, int& bin, int& below) {
+    int acc = 0;
+    bin = 255;
+    below = 0;
+    for (int b = 0; b < 256; ++b) {
+        const int c = hs[b];
+        if (acc + c > target) {
+            bin = b;
+            below = acc;
+            return;
+        }
+        acc += c;
+    }
+    below = acc;
+}
+
+// A block covers 256 consecutive positions, hence at most two nodes that are
+// still split (each has more than 256 positions).  Loads the histograms of
+// those nodes into LDS.
+struct BlockNodes {
+    int idx[2];
+    int lo[2];
+    int n[2];
+    int count;
+};
+
+__device__ __forceinline__ void block_nodes(int N, int lev, BlockNodes& bn) {
+    bn.count = 0;
+    const int p0 = blockIdx.x * 256;
+    const int p1 = min(N, p0 + 256) - 1;
+    int lo, n, idx;
+    if (node_of(p0, N, lev, lo, n, idx)) {
+        bn.idx[bn.count] = idx;
+        bn.lo[bn.count] = lo;
+        bn.n[bn.count] = n;
+        ++bn.count;
+    }
+    if (node_of(p1, N, lev, lo, n, idx) && (bn.count == 0 || idx != bn.idx[0])) {
+        bn.idx[bn.count] = idx;
+        bn.lo[bn.count] = lo;
+        bn.n[bn.count] = n;
+        ++bn.count;
+    }
+}
+
+// Level lev: histogram of the low byte of the codes whose high byte is the
+// split bin of their node.
+__global__ __launch_bounds__(256) void tree_hist2_kernel(int32_t N, int32_t lev, int32_t width,
+                                                         int32_t* __restrict__ nodeh,
+                                                         const uint16_t* __restrict__ code) {
+    __shared__ int32_t hs[2][256];
+    const int h = blockIdx.y;
+    const int t = threadIdx.x;
+    BlockNodes bn;
+    block_nodes(N, lev, bn);
+    if (bn.count == 0) return;
+    for (int s = 0; s < bn.count; ++s) hs[s][t] = nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + t];
+    __syncthreads();
+    int b1[2] = {0, 0};
+    for (int s = 0; s < bn.count; ++s) {
+        int below;
+        find_bin(hs[s], split_left(bn.n[s]), b1[s], below);
+    }
+    const int p = blockIdx.x * 256 + t;
+    if (p >= N) return;
+    const int s = (bn.count == 2 && p >= bn.lo[1]) ? 1 : 0;
+    if (p < bn.lo[s] || p >= bn.lo[s] + bn.n[s]) return;
+    const uint32_t q = code[(size_t)h * N + p];
+    if ((int)(q >> 8) == b1[s])
+        atomicAdd(&nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + 256 + (q & 255u)], 1);
+}
+
+// Level lev: every position of a node that is split moves to its side.  The
+// left side takes the keys whose code is below the split value and, by
+// ticket, as many keys with the split value as the left size still needs.
+// Positions in leaves keep their key.
+__global__ __launch_bounds__(256) void tree_scatter_kernel(int32_t N, int32_t lev, int32_t width,
+                                                           int32_t* __restrict__ nodeh,
+                                                           const uint16_t* __restrict__ code,
+                                                           const int32_t* __restrict__ perm_in,
+                                                           int32_t* __restrict__ perm_out) {
+    __shared__ int32_t hs[2][256];
+    __shared__ int32_t cnt[2][2];
+    __shared__ int32_t base[2][2];
+    const int h = blockIdx.y;
+    const int t = threadIdx.x;
+    const int p = blockIdx.x * 256 + t;
+    BlockNodes bn;
+    block_nodes(N, lev, bn);
+    const int32_t key = p < N ? perm_in[(size_t)h * N + p] : 0;
+    if (bn.count == 0) {
+        if (p < N) perm_out[(size_t)h * N + p] = key;
+        return;
+    }
+    int split[2] = {0, 0}, ties_left[2] = {0, 0};
+    for (int s = 0; s < bn.count; ++s) {
+        hs[s][t] = nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + t];
+        if (t < 2) cnt[s][t] = 0;
+    }
+    __syncthreads();
+    for (int s = 0; s < bn.count; ++s) {
+        const int nl = split_left(bn.n[s]);
+        int b1, below1;
+        find_bin(hs[s], nl, b1, below1);
+        split[s] = b1 << 8;
+        ties_left[s] = nl - below1;
+    }
+    __syncthreads();
+    for (int s = 0; s < bn.count; ++s) hs[s][t] = nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + 256 + t];
+    __syncthreads();
+    for (int s = 0; s < bn.count; ++s) {
+        int b2, below2;
+        find_bin(hs[s], ties_left[s], b2, below2);
+        split[s] |= b2;
+        ties_left[s] -= below2;
+    }
+    int s = -1, side = 0, rank = 0;
+    if (p < N) {
+        s = (bn.count == 2 && p >= bn.lo[1]) ? 1 : 0;
+        if (p < bn.lo[s] || p >= bn.lo[s] + bn.n[s]) s = -1;
+    }
+    if (s >= 0) {
+        const int q = code[(size_t)h * N + p];
+        if (q < split[s]) {
+            side = 0;
+        } else if (q > split[s]) {
+            side = 1;
+        } else {
+            const int tk = atomicAdd(&nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + 514], 1);
+            side = tk < ties_left[s] ? 0 : 1;
+        }
+        rank = atomicAdd(&cnt[s][side], 1);
+    }
+    __syncthreads();
+    if (t < 2 * bn.count) {
+        const int ss = t >> 1, sd = t & 1;
+        base[ss][sd] = cnt[ss][sd] > 0
+                           ? atomicAdd(&nodeh[((size_t)h * width + bn.idx[ss]) * kNodeInts + 512 + sd],
+                                       cnt[ss][sd])
+                           : 0;
+    }
+    __syncthreads();
+    if (p >= N) return;
+    if (s < 0) {
+        perm_out[(size_t)h * N + p] = key;
+        return;
+    }
+    const int nl = split_left(bn.n[s]);
+    const int dst = bn.lo[s] + (side == 0 ? 0 : nl) + base[s][side] + rank;
+    perm_out[(size_t)h * N + dst] = key;
+}
+
+__global__ __launch_bounds__(256) void iota_kernel(int32_t N, int32_t* __restrict__ perm) {
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    if (p < N) perm[(size_t)blockIdx.y * N + p] = p;
+}
+
+// bf16 bits of x rounded to nearest even (finite x).
+__device__ __forceinline__ uint16_t bf16_rne(float x) {
+    const uint32_t b = __float_as_uint(x);
+    return (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+
+// bf16 bits of the smallest bf16 >= x, for finite x >= 0.
+__device__ __forceinline__ uint16_t bf16_up(float x) {
+    const uint32_t b = __float_as_uint(x);
+    return (uint16_t)((b >> 16) + ((b & 0xFFFFu) != 0u ? 1u : 0u));
+}
+
+// One block per superblock s of head h (its 256 keys are positions 256 s ..
+// of the order; positions >= N are absent).  Writes the superblock's row of
+// the bound tiles: tile s / 32, row s % 32, in the key-tile operand layout
+// with NC + 1 chunks of 16 dims.  Chunks 0 .. NC-1 hold c, the mean of the
+// keys rounded to bf16; chunk NC holds R_up in its first dim and zeros
+// elsewhere.  A query's bound tile row q is then (q, |q|_up, 0 ..) . (c,
+// R_up, 0 ..), formed by the same MFMA as the scores.
+//
+// Why the bound holds for the MFMA scores: every key k of the superblock
+// has q.k = q.c + q.(k - c) <= q.c + |q| r with r = max |k - c|.  The radius
+// r is computed in fp32 from bf16 data (relative error below (D/2 + 2)
+// 2^-24), the MFMA's fp32 sums of D + 16 products err by less than about
+// (D + 16) 2^-24 (|q||c| + |q||k| + |q| R) on both the score and the bound,
+// and |k| <= |c| + r.  R = r (1 + 2^-12) + |c| 2^-12 exceeds r by far more
+// than all of these together for D <= 64, and rounding R and |q| up to bf16
+// only raises the bound further.  An empty superblock gets c = 0, R = 0;
+// the select kernel never scans superblocks past the last one anyway.
+template <int D>
+__global__ __launch_bounds__(256) void sb_bounds_kernel(const uint16_t* __restrict__ K,
+                                                        const int32_t* __restrict__ perm, int32_t N,
+                                                        int32_t H, int32_t ctiles,
+                                                        uint16_t* __restrict__ bounds) {
+    constexpr int NC = D / 16;
+    __shared__ float part[4][D];
+    __shared__ float cen[D];
+    __shared__ float rpart[4];
+    const int s = blockIdx.x;
+    const int h = blockIdx.y;
+    const int t = threadIdx.x;
+    const int wave = t >> 6;
+    const int64_t pos = (int64_t)s * SBK + t;
+    const bool valid = pos < N;
+    float x[D];
+    if (valid) {
+        load_row_f32<D>(x, K + ((size_t)perm[(size_t)h * N + pos] * H + h) * D);
+    } else {
+#pragma unroll
+        for (int i = 0; i < D; ++i) x[i] = 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+        const float v = wave_sum(x[i]);
+        if ((t & 63) == 0) part[wave][i] = v;
+    }
+    __syncthreads();
+    const int64_t left = (int64_t)N - (int64_t)s * SBK;
+    const int count = left <= 0 ? 0 : (left >= SBK ? SBK : (int)left);
+    const int row = s & 31;
+    uint16_t* tile = bounds + (((size_t)h * ctiles + (s >> 5)) * (NC + 1)) * 64 * 8;
+    if (t < D) {
+        const float sum = (part[0][t] + part[1][t]) + (part[2][t] + part[3][t]);
+        const uint16_t cb = count > 0 ? bf16_rne(sum / (float)count) : (uint16_t)0;
+        cen[t] = bf16_bits_to_f32(cb);
+        tile[((t >> 4) * 64 + row + 32 * ((t >> 3) & 1)) * 8 + (t & 7)] = cb;
+    }
+    __syncthreads();
+    float d2 = 0.0f;
+    if (valid) {
+#pragma unroll
+        for (int i = 0; i < D; ++i) {
+            const float e = x[i] - cen[i];
+            d2 = fmaf(e, e, d2);
+        }
+    }
+    const float m = wave_max(d2);
+    if ((t & 63) == 0) rpart[wave] = m;
+    __syncthreads();
+    if (t >= D && t < D + 16) {
+        const int j = t - D;
+        uint16_t v = 0;
+        if (j == 0 && count > 0) {
+            float cn2 = 0.0f;
+            for (int i = 0; i < D; ++i) cn2 = fmaf(cen[i], cen[i], cn2);
+            const float r = sqrtf(fmaxf(fmaxf(rpart[0], rpart[1]), fmaxf(rpart[2], rpart[3])));
+            const float R = fmaf(r, 1.0f + 0x1p-12f, sqrtf(cn2) * 0x1p-12f);
+            v = bf16_up(R);
+        }
+        tile[(NC * 64 + row + 32 * (j >> 3)) * 8 + (j & 7)] = v;
+    }
+}
+
+// Levels of splitting for N keys: nodes of level l are split while l <
+// levels (the deepest split level has at most width nodes).
+void tree_shape(int32_t N, int32_t& levels, int32_t& width) {
+    const int32_t nsb = (N + SBK - 1) / SBK;
+    levels = 0;
+    while ((1 << levels) < nsb) ++levels;
+    width = levels > 0 ? (1 << (levels - 1)) : 1;
+}
+
+}  // namespace
+
+int32_t key_order_ctiles(int32_t ntiles) {
+    const int32_t nsb = (ntiles + kSuperTiles - 1) / kSuperTiles;
+    return (nsb + 63) / 64 * 2;
+}
+
+size_t key_order_workspace_bytes(int32_t N, int32_t H, int32_t d) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    const int32_t ntiles = (N + 31) / 32;
+    const size_t ctiles = (size_t)key_order_ctiles(ntiles);
+    int32_t levels, width;
+    tree_shape(N, levels, width);
+    return 2 * al((size_t)H * N * sizeof(int32_t)) + al((size_t)H * N * sizeof(uint16_t)) +
+           al((size_t)H * width * (2 * d + 2) * sizeof(float)) +
+           al((size_t)H * width * kNodeInts * sizeof(int32_t)) + al((size_t)H * sizeof(int32_t)) +
+           al((size_t)H * ctiles * (d / 16 + 1) * 64 * 16);
+}
+
+hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int32_t ntiles, void* ws,
+                            KeyOrder* out, hipStream_t stream) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    const int32_t ctiles = key_order_ctiles(ntiles);
+    int32_t levels, width;
+    tree_shape(N, levels, width);
+    char* p = reinterpret_cast<char*>(ws);
+    int32_t* perm_a = reinterpret_cast<int32_t*>(p);
+    p += al((size_t)H * N * sizeof(int32_t));
+    int32_t* perm_b = reinterpret_cast<int32_t*>(p);
+    p += al((size_t)H * N * sizeof(int32_t));
+    uint16_t* code = reinterpret_cast<uint16_t*>(p);
+    p += al((size_t)H * N * sizeof(uint16_t));
+    float* nodef = reinterpret_cast<float*>(p);
+    p += al((size_t)H * width * (2 * d + 2) * sizeof(float));
+    int32_t* nodeh = reinterpret_cast<int32_t*>(p);
+    p += al((size_t)H * width * kNodeInts * sizeof(int32_t));
+    int32_t* votes = reinterpret_cast<int32_t*>(p);
+    p += al((size_t)H * sizeof(int32_t));
+    uint16_t* bounds = reinterpret_cast<uint16_t*>(p);
+
+    const uint16_t* k = reinterpret_cast<const uint16_t*>(K);
+    hipError_t e = launch_fill_zero(reinterpret_cast<float*>(votes), (size_t)H, stream);
+    if (e != hipSuccess) return e;
+    const dim3 grid((unsigned)((N + 255) / 256), (unsigned)H);
+    hipLaunchKernelGGL(iota_kernel, grid, dim3(256), 0, stream, N, perm_a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    int32_t* cur = perm_a;
+    int32_t* nxt = perm_b;
+    for (int lev = 0; lev < levels; ++lev) {
+        const dim3 ngrid((unsigned)(1 << lev), (unsigned)H);
+#define KMIP_TREE_LEVEL(DD)                                                                          \
+    hipLaunchKernelGGL(tree_axis_kernel<DD>, ngrid, dim3(256), 0, stream, k, cur, N, H, lev, width,  \
+                       nodef, nodeh);                                                                \
+    if ((e = hipGetLastError()) != hipSuccess) return e;                                             \
+    hipLaunchKernelGGL(tree_project_kernel<DD>, grid, dim3(256), 0, stream, k, cur, N, H, lev, width, \
+                       nodef, nodeh, code);
+        if (d == 16) {
+            KMIP_TREE_LEVEL(16)
+        } else if (d == 32) {
+            KMIP_TREE_LEVEL(32)
+        } else {
+            KMIP_TREE_LEVEL(64)
+        }
+#undef KMIP_TREE_LEVEL
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(tree_hist2_kernel, grid, dim3(256), 0, stream, N, lev, width, nodeh, code);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(tree_scatter_kernel, grid, dim3(256), 0, stream, N, lev, width, nodeh, code, cur,
+                           nxt);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        int32_t* tmp = cur;
+        cur = nxt;
+        nxt = tmp;
+    }
+    out->perm = cur;
+    out->bounds = reinterpret_cast<const uint4*>(bounds);
+    out->votes = votes;
+    out->ctiles = ctiles;
+    const dim3 sgrid((unsigned)(ctiles * 32), (unsigned)H);
+    if (d == 16)
+        hipLaunchKernelGGL(sb_bounds_kernel<16>, sgrid, dim3(256), 0, stream, k, cur, N, H, ctiles, bounds);
+    else if (d == 32)
+        hipLaunchKernelGGL(sb_bounds_kernel<32>, sgrid, dim3(256), 0, stream, k, cur, N, H, ctiles, bounds);
+    else
+        hipLaunchKernelGGL(sb_bounds_kernel<64>, sgrid, dim3(256), 0, stream, k, cur, N, H, ctiles, bounds);
+    return hipGetLastError();
+}
+
+}  // namespace kmip

@@ -29,14 +29,43 @@ struct Task {
 // ---- launchers (host side); each returns hipSuccess or the launch error ----
 
 // Tiles K [N,H,d] bf16 into the matrix-core operand order: for head h and key
-// tile t (32 keys), chunk c of 16 dims, lane l holds 8 bf16 of key 32t + l%32,
-// dims 16c + 8(l/32) .. +8.  Keys >= N are zero; each head has ntiles +
-// kPadTiles tiles.
-hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t d, int32_t ntiles,
-                         hipStream_t stream);
+// tile t (32 positions), chunk c of 16 dims, lane l holds 8 bf16 of the key at
+// position p = 32t + l%32, dims 16c + 8(l/32) .. +8.  Position p holds key
+// perm[h][p] (key p when perm is NULL); positions >= N are zero; each head has
+// ntiles + kPadTiles tiles.
+hipError_t launch_pack_k(const void* K, const int32_t* perm, void* kp, int32_t N, int32_t H, int32_t d,
+                         int32_t ntiles, hipStream_t stream);
 
-// Shape of one select wave: query blocks of 32 (1 or 2) and candidate-buffer
-// slots per lane and block (4 or 8 with two blocks, 8 or 16 with one).
+// Stored key order with superblock bounds (keyorder.hip): the leaf order of
+// a balanced space-partitioning tree whose leaves are superblocks of
+// kSuperTiles tiles, each with a ball bound.
+constexpr int kSuperTiles = 8;
+// Net votes (items finding most superblocks needed, minus the others) at
+// which a head's select items stop forming masks and scan every superblock.
+constexpr int kDenseVotes = 16;
+
+// Device arrays of a key order:
+//   perm   [H][N]  key stored at each position;
+//   bounds [H][ctiles][d/16 + 1][64] uint4: bound tiles, superblock s in
+//          tile s / 32, row s % 32, in the key-tile operand layout: chunks
+//          0 .. d/16-1 the bf16 center, chunk d/16 the radius R (bf16, rounded
+//          up) in dim 0;
+//   votes  [H]  dense-mode votes (zero before the select launch).
+struct KeyOrder {
+    const int32_t* perm;
+    const uint4* bounds;
+    int32_t* votes;
+    int32_t ctiles;
+};
+
+// Bound tiles per head for ntiles key tiles: two per 64 superblocks.
+int32_t key_order_ctiles(int32_t ntiles);
+size_t key_order_workspace_bytes(int32_t N, int32_t H, int32_t d);
+hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int32_t ntiles, void* ws,
+                            KeyOrder* out, hipStream_t stream);
+
+// Shape of one select wave: query blocks of 32 and candidate-buffer slots
+// per lane and block, {2, 4} or {1, 8}.
 struct SelectShape {
     int32_t qb;
     int32_t slots;
@@ -54,14 +83,16 @@ struct QueryGroups {
     int32_t* seed_ref;
 };
 
-// Score + select.  groups: NULL (identity order, no seeding; always so for a
-// block-diagonal batch), or the grouping of the queries.  work_ctr:
-// kSelectCounterBytes of device scratch, 8-byte aligned (per-XCD item
-// counters and stream pacers, zeroed here).
-hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const QueryGroups* groups,
-                         int32_t ntasks, int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles,
-                         SelectShape shape, int32_t* work_ctr, int32_t* topk_idx,
-                         hipStream_t stream);
+// Score + select.  kp: the tiled keys (launch_pack_k).  groups: NULL
+// (identity order, no seeding; always so for a block-diagonal batch), or the
+// grouping of the queries.  keys: NULL (every tile scanned), or the stored
+// key order kp was packed in, with its bounds.  K: the keys in their own
+// layout (seed rows are gathered from it).  work_ctr: kSelectCounterBytes of device scratch, 8-byte aligned
+// (per-XCD item counters and stream pacers, zeroed here).
+hipError_t launch_select(const void* kp, const void* Q, const void* K, const Task* tasks,
+                         const QueryGroups* groups, const KeyOrder* keys, int32_t ntasks, int32_t N,
+                         int32_t H, int32_t d, int32_t k, int32_t ntiles, SelectShape shape,
+                         int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream);
 
 // Bytes of LDS one select workgroup uses.
 size_t select_lds_bytes(int32_t k, SelectShape shape);

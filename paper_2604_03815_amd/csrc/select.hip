@@ -181,13 +181,15 @@ __device__ __forceinline__ void heap_sift_down(uint64_t* hp, int col, int k, uin
 // rather than have the compiler trade registers for occupancy by spilling.
 template <int D, int QB, int SLOTS>
 __global__ __launch_bounds__(64, 1) void select_kernel(
-    const uint4* __restrict__ kp, const uint16_t* __restrict__ Q, const Task* __restrict__ tasks,
-    const int32_t* __restrict__ qperm, const uint16_t* __restrict__ qlabel,
-    int32_t* __restrict__ seed_ref, int32_t ntasks, int32_t N, int32_t H, int32_t k,
-    int32_t ntiles, int32_t* __restrict__ work_ctr, Pacer* __restrict__ pacers,
-    int32_t* __restrict__ topk_idx) {
+    const uint4* __restrict__ kp, const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+    const Task* __restrict__ tasks, const int32_t* __restrict__ qperm,
+    const uint16_t* __restrict__ qlabel, int32_t* __restrict__ seed_ref, const int32_t* __restrict__ kperm,
+    const uint4* __restrict__ bounds, int32_t* __restrict__ votes, int32_t ctiles, int32_t ntasks,
+    int32_t N, int32_t H, int32_t k, int32_t ntiles, int32_t* __restrict__ work_ctr,
+    Pacer* __restrict__ pacers, int32_t* __restrict__ topk_idx) {
     constexpr int NC = D / 16;
     constexpr int TILE_BYTES = NC * 64 * 16;
+    constexpr int SBT = kSuperTiles;
     extern __shared__ uint64_t lds[];
     const int hrows = k;
 
@@ -253,6 +255,8 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     float theta[QB];
     int cnt[QB];
     int32_t qid[QB];
+    // |q| rounded up to bf16 (bits), the query's entry of the bound operand
+    uint32_t qn_up[QB];
     const int32_t* hperm = qperm != nullptr ? qperm + (size_t)head * N : nullptr;
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
@@ -260,11 +264,23 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         const bool valid = qi < q_count;
         qid[b] = valid ? (hperm != nullptr ? hperm[q_begin + qi] : q_begin + qi) : 0;
         const uint16_t* qrow = Q + ((size_t)qid[b] * H + head) * D + 8 * half;
+        float ss = 0.0f;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             uint4 u = valid ? *reinterpret_cast<const uint4*>(qrow + 16 * c) : make_uint4(0, 0, 0, 0);
             bq[b][c] = __builtin_bit_cast(bf16x8, u);
+            const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float lo = bf16_bits_to_f32(w4[e] & 0xFFFFu), hi = bf16_bits_to_f32(w4[e] >> 16);
+                ss = fmaf(lo, lo, ss);
+                ss = fmaf(hi, hi, ss);
+            }
         }
+        ss += __shfl_xor(ss, 32);
+        // sqrt in fp32 errs by far less than the 2^-12 added before rounding up
+        const uint32_t nb = __float_as_uint(sqrtf(ss) * (1.0f + 0x1p-12f));
+        qn_up[b] = (nb >> 16) + ((nb & 0xFFFFu) != 0u ? 1u : 0u);
         theta[b] = valid ? -INFINITY : INFINITY;
         cnt[b] = 0;
     }
@@ -273,15 +289,14 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     // Seeded thresholds.  Queries of one direction label share most of their
     // top-k keys.  When some query of the label of a block's first query has
     // published its finished top-k row, the block scores its queries against
-    // those k keys (one MFMA tile per 32 keys, gathered from the tiled keys)
-    // and starts from theta = the float below each query's lowest such
-    // score: k distinct keys of the graph score at least that much, so the
-    // query's k-th best does too, and every key that can enter its top-k
-    // still passes the filter.  Scores come from the same MFMA on the same
+    // those k keys (one MFMA tile per 32 keys, gathered from K) and starts
+    // from theta = the float below each query's lowest such score: k
+    // distinct keys of the graph score at least that much, so the query's
+    // k-th best does too, and every key that can enter its top-k still
+    // passes the filter.  Scores come from the same MFMA on the same
     // operands as in the stream, hence are the same values.  The heap starts
     // empty and fills with keys that pass; theta only ever rises.
     if (qlabel != nullptr) {
-        const uint4* head_tiles = kp + (size_t)head * (ntiles + kPadTiles) * NC * 64;
 #pragma unroll
         for (int b = 0; b < QB; ++b) {
             if (32 * b >= q_count) continue;
@@ -300,12 +315,12 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
                 const int j = srow[s0 + col < k ? s0 + col : s0];
                 ok = ok && j >= 0 && j < N;
                 const int jj = (j >= 0 && j < N) ? j : 0;
-                const uint4* src = head_tiles + (size_t)(jj >> 5) * NC * 64 + (jj & 31) + 32 * half;
+                const uint4* src = reinterpret_cast<const uint4*>(K + ((size_t)jj * H + head) * D + 8 * half);
                 f32x16 sacc = f32x16{};
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
                     sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, src[c * 64]), bq[b][c], sacc, 0, 0, 0);
+                        __builtin_bit_cast(bf16x8, src[2 * c]), bq[b][c], sacc, 0, 0, 0);
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     if (s0 + tile_row(r, half) < k) low = fminf(low, sacc[r]);
@@ -319,7 +334,31 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     // Fold every lane's candidates into the heaps and refresh theta.  With
     // two blocks, each phase has the lower half-wave on one block's heaps and
     // the upper half-wave on the other's, so all lanes work on disjoint heaps.
+    const int32_t* kperm_h = kperm != nullptr ? kperm + (size_t)head * N : nullptr;
     auto merge_all = [&]() {
+        if (kperm_h != nullptr) {
+            // With a stored key order, candidates carry the key's position in
+            // that order; swap in the key's own index before the heap applies
+            // its tie rule.  Every slot is looked up (unused ones at position
+            // 0) so that all of a lane's loads are in flight together.
+            int32_t orig[QB][SLOTS];
+#pragma unroll
+            for (int b = 0; b < QB; ++b) {
+#pragma unroll
+                for (int e = 0; e < SLOTS; ++e) {
+                    const int pos = e < cnt[b] ? key_index(cand[((size_t)b * SLOTS + e) * 64 + lane]) : 0;
+                    orig[b][e] = kperm_h[pos];
+                }
+            }
+#pragma unroll
+            for (int b = 0; b < QB; ++b) {
+#pragma unroll
+                for (int e = 0; e < SLOTS; ++e) {
+                    uint64_t* c = &cand[((size_t)b * SLOTS + e) * 64 + lane];
+                    if (e < cnt[b]) *c = (*c & 0xFFFFFFFF00000000ull) | (uint32_t)~orig[b][e];
+                }
+            }
+        }
 #pragma unroll
         for (int ph = 0; ph < 2; ++ph) {
             const int b = QB == 2 ? (half ^ ph) : 0;
@@ -347,9 +386,9 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         }
     };
 
-    // Rare path for block b of the tile starting at key tbase.  Each lane
-    // builds a 16-bit mask of its scores above theta, and the wave then
-    // walks the set bits: as many rounds as the largest per-lane count,
+    // Rare path for block b of the tile starting at key position tbase.
+    // Each lane builds a 16-bit mask of its scores above theta, and the wave
+    // then walks the set bits: as many rounds as the largest per-lane count,
     // usually one or two.  A lane picks the score of its bit out of its 16
     // registers with a 4-level select on the bits of the register number.  A
     // buffer that fills up is folded between two rounds.
@@ -380,90 +419,248 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         __builtin_amdgcn_wave_barrier();
     };
 
-    // The graph's tiles t0 .. t1-1 are scanned in nch <= 64 chunks of cs
-    // tiles.  After each chunk the wave goes on with the first chunk not yet
-    // scanned at or after its XCD's virtual position (cyclically), evaluated
-    // from the pacer state read at the item's start and the wall clock; with
-    // several graphs, or before the pacer knows a speed, chunks go in order.
-    // A wave that falls behind or runs ahead of the others thus rejoins them
-    // at every chunk, not just at the next item.
+    // ---- Key stream ----
+    // The graph's tiles t0 .. t1-1 form nsb superblocks of SBT tiles, and
+    // every 64 superblocks form a window.  Superblocks are scanned whole (the
+    // last one may run into the next graph's or the padding tiles: such
+    // keys only reach the rare path, which drops them by position), window
+    // by window, each window's in increasing order, skipping the ones not in
+    // the window's mask.
+    //
+    // Dense mode: every superblock, starting from the one at the XCD's
+    // virtual position (single graph) and wrapping around.  Pruned mode
+    // (keys stored in superblock order with bounds): a superblock is in the
+    // mask when its bound beats the theta of at least one valid query of
+    // the wave; theta only rises, so a superblock left out can never hold a
+    // key that passes the filter.  Masks of up to 64 windows (a batch) are
+    // formed at once, lane w holding window w's.  A head turns to dense
+    // mode once seeded items keep finding most superblocks needed (votes).
     const int t0 = key_lo >> 5;
     const int t1 = (key_hi + 31) >> 5;
     const int nt = t1 - t0;
-    const int cs = (nt + 63) / 64;
-    const int nch = (nt + cs - 1) / cs;
-    const uint64_t all_chunks = nch == 64 ? ~0ull : ((1ull << nch) - 1ull);
-    // The virtual position relative to t0 at the item's start (pace_v0, in
-    // [0, nt)) and its speed (tiles per tick; 0 when unknown).
-    float pace_v0 = 0.0f, pace_rate = 0.0f;
-    int64_t item_start = 0;
-    if (tasks == nullptr) {
-        const Pacer* pc = &pacers[xcd];
-        const double rate = __hip_atomic_load(&pc->rate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const double pos = __hip_atomic_load(&pc->pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const int64_t ref = __hip_atomic_load(&pc->t_ref, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        item_start = wall_clock64();
-        const double v = pos + (double)(item_start - ref) * rate;
-        if (rate > 0.0 && v >= 0.0 && v < 1e15) {
-            pace_v0 = (float)((int64_t)v % nt);
-            pace_rate = (float)rate;
-        }
+    const int nsb = (nt + SBT - 1) / SBT;
+    const int nwin = (nsb + 63) / 64;
+    bool pruned = false;
+    if (bounds != nullptr) {
+        int v = 0;
+        if (lane == 0) v = __hip_atomic_load(&votes[head], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        pruned = __builtin_amdgcn_readfirstlane(v) < kDenseVotes;
     }
-    const float inv_cs = 1.0f / (float)cs;
-    // Next chunk: the first one not in `done` at or after the virtual
-    // position's chunk, else `fallback`'s.
-    auto choose = [&](uint64_t done, int fallback) {
-        int vc = fallback;
-        if (pace_rate > 0.0f) {
-            float v = pace_v0 + (float)(wall_clock64() - item_start) * pace_rate;
-            v -= (float)nt * floorf(v / (float)nt);
-            vc = min(nch - 1, max(0, (int)(v * inv_cs)));
-        }
-        vc = __builtin_amdgcn_readfirstlane(vc);
-        const uint64_t avail = all_chunks & ~done;
-        const uint64_t ahead = avail & (~0ull << vc);
-        return ahead != 0ull ? (int)__builtin_ctzll(ahead) : (int)__builtin_ctzll(avail);
-    };
-    const uint32_t lane_off = (uint32_t)lane * 16u;
-
-    // Prefetch ring: each slot holds one tile, and slot_tile[] remembers
-    // which; a slot is refilled with the next tile of the scan as soon as its
-    // MFMAs are issued.  Once every chunk has been issued the refills keep
-    // reading valid tiles of the graph that are never filtered.
-    constexpr int PF = 8 / NC;
-    const char* head_tiles = reinterpret_cast<const char*>(kp) + (size_t)head * (ntiles + kPadTiles) * TILE_BYTES;
-    int cur = choose(0ull, 0);
-    uint64_t done = 1ull << cur;
-    int rel = cur * cs, rel_end = min(nt, rel + cs);
-    const char* next = head_tiles + (size_t)(t0 + rel) * TILE_BYTES;
-    i32x4 ring[PF][NC];
-    int slot_tile[PF];
-    auto refill = [&](i32x4 (&slot)[NC], int& stile) {
-        stile = t0 + rel;
-        slot[0] = ring_load<0>(next, lane_off);
-        if constexpr (NC >= 2) slot[1] = ring_load<1024>(next, lane_off);
-        if constexpr (NC >= 4) {
-            slot[2] = ring_load<2048>(next, lane_off);
-            slot[3] = ring_load<3072>(next, lane_off);
-        }
-        next += TILE_BYTES;
-        if (++rel == rel_end) {
-            if (done != all_chunks) {
-                cur = choose(done, cur + 1 < nch ? cur + 1 : 0);
-                done |= 1ull << cur;
-                rel = cur * cs;
-                rel_end = min(nt, rel + cs);
-            } else {
-                rel = 0;
-                rel_end = nt;
-            }
-            next = head_tiles + (size_t)(t0 + rel) * TILE_BYTES;
-        }
-    };
+    const uint4* btiles = bounds != nullptr ? bounds + (size_t)head * ctiles * (NC + 1) * 64 : nullptr;
+    uint32_t mask_lo = 0, mask_hi = 0;
+    int mask_batch = -1;
+    // Superblocks of batch 0 already scanned by a warm-up (see below), as
+    // window masks held like mask_lo / mask_hi; left out of every mask.
+    uint32_t warm_lo = 0, warm_hi = 0;
+    // Masks of windows 64 bt .. 64 bt + 63; returns how many superblocks
+    // they keep.  Bound tile g holds superblocks 32 g .. 32 g + 31, scored
+    // like key tiles with the query's |q| bound entry as one more chunk; a
+    // window's two tiles are loaded while the previous window is scored.
+    // With track, each lane also notes, per query block, the superblock of
+    // largest bound among its rows (best_sb, -1 for an invalid query).
+    int best_sb[QB];
+    auto compute_batch = [&](int bt, bool track) {
+        const int wlo = bt * 64;
+        const int whi = min(nwin, wlo + 64);
+        uint64_t mv = 0;
+        int needed = 0;
+        bf16x8 qa[QB];
+        float best_v[QB];
 #pragma unroll
-    for (int u = 0; u < PF; ++u) refill(ring[u], slot_tile[u]);
+        for (int b = 0; b < QB; ++b) {
+            qa[b] = __builtin_bit_cast(bf16x8, make_uint4(half == 0 ? qn_up[b] : 0u, 0u, 0u, 0u));
+            best_v[b] = -INFINITY;
+            best_sb[b] = -1;
+        }
+        uint4 cn[2][NC + 1];
+        auto fetch = [&](int w) {
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                const uint4* src = btiles + (size_t)(2 * w + ct) * (NC + 1) * 64 + lane;
+#pragma unroll
+                for (int c = 0; c <= NC; ++c) cn[ct][c] = src[c * 64];
+            }
+        };
+        fetch(wlo);
+        for (int w = wlo; w < whi; ++w) {
+            uint4 cc[2][NC + 1];
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+                for (int c = 0; c <= NC; ++c) cc[ct][c] = cn[ct][c];
+            if (w + 1 < whi) fetch(w + 1);
+            uint64_t m = 0;
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                uint32_t bits = 0;
+                f32x16 bacc[QB];
+#pragma unroll
+                for (int b = 0; b < QB; ++b) {
+                    bacc[b] = f32x16{};
+#pragma unroll
+                    for (int c = 0; c < NC; ++c)
+                        bacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, cc[ct][c]),
+                                                                          bq[b][c], bacc[b], 0, 0, 0);
+                    bacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, cc[ct][NC]),
+                                                                      qa[b], bacc[b], 0, 0, 0);
+                }
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    bool need = false;
+#pragma unroll
+                    for (int b = 0; b < QB; ++b) need = need || bacc[b][r] > theta[b];
+                    const uint64_t bal = __builtin_amdgcn_ballot_w64(need);
+                    bits |= ((uint32_t)bal != 0u ? 1u : 0u) << tile_row(r, 0);
+                    bits |= ((uint32_t)(bal >> 32) != 0u ? 1u : 0u) << tile_row(r, 1);
+                }
+                if (track) {
+                    const int sb0 = 64 * w + 32 * ct;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int sb = sb0 + tile_row(r, half);
+#pragma unroll
+                        for (int b = 0; b < QB; ++b) {
+                            const bool better = sb < nsb && theta[b] != INFINITY && bacc[b][r] > best_v[b];
+                            best_v[b] = better ? bacc[b][r] : best_v[b];
+                            best_sb[b] = better ? sb : best_sb[b];
+                        }
+                    }
+                }
+                m |= (uint64_t)bits << (32 * ct);
+            }
+            const int nv = nsb - 64 * w;
+            if (nv < 64) m &= (1ull << nv) - 1ull;
+            if (lane == w - wlo) {
+                mv = m;
+                if (bt == 0) mv &= ~((uint64_t)warm_lo | ((uint64_t)warm_hi << 32));
+            }
+            needed += __builtin_popcountll(m);
+        }
+        mask_lo = (uint32_t)mv;
+        mask_hi = (uint32_t)(mv >> 32);
+        mask_batch = bt;
+        return needed;
+    };
+    auto read_mask = [&](int w) {
+        const int l = w - 64 * mask_batch;
+        return (uint64_t)(uint32_t)__builtin_amdgcn_readlane(mask_lo, l) |
+               ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(mask_hi, l) << 32);
+    };
+    auto valid_bits = [&](int w) {
+        const int nv = nsb - 64 * w;
+        return nv >= 64 ? ~0ull : (1ull << nv) - 1ull;
+    };
+
+    // Window walk: w is the current window, wm its superblocks not yet
+    // taken, wv the number of windows entered after the first.  Dense mode
+    // walks a scattered order of the superblocks (virtual superblock v is
+    // superblock v * stride_sb mod nsb, stride_sb coprime to nsb), so that
+    // the first ones scanned come from all over the stored key order and the
+    // thresholds rise early; it starts at virtual superblock s0 and visits
+    // window w0 = s0 / 64 once more at the end for its superblocks below s0.
+    int w = 0, wv = 0, b0 = 0;
+    uint64_t wm = 0;
+    int scanned = 0;
+    // With unseeded queries, masks are formed again after 16, 64, 256, ...
+    // superblocks, as the thresholds rise.
+    int stop_at = 0x7FFFFFFF;
+    // Warm-up of an item with unseeded queries (one batch of windows): the
+    // walk first takes, for every query, the superblock of largest bound,
+    // then folds its candidates and forms the masks with the thresholds that
+    // gives, leaving out the superblocks already scanned.
+    bool warm_pending = false;
+    int64_t item_start = 0;
+    int stride_sb = 1;
+    if (pruned) {
+        bool seeded = true;
+#pragma unroll
+        for (int b = 0; b < QB; ++b) seeded = seeded && __builtin_amdgcn_ballot_w64(theta[b] == -INFINITY) == 0ull;
+        const bool warm = !seeded && nwin <= 64;
+        const int needed = compute_batch(0, warm);
+        if (warm) {
+            // Masks of the union of the best superblocks, one window per lane.
+            uint64_t mv = 0;
+#pragma unroll
+            for (int b = 0; b < QB; ++b) {
+                for (;;) {
+                    const uint64_t pend = __builtin_amdgcn_ballot_w64(best_sb[b] >= 0);
+                    if (pend == 0ull) break;
+                    const int sb = __builtin_amdgcn_readlane(best_sb[b], (int)__builtin_ctzll(pend));
+                    if (lane == (sb >> 6)) mv |= 1ull << (sb & 63);
+#pragma unroll
+                    for (int b2 = 0; b2 < QB; ++b2) best_sb[b2] = best_sb[b2] == sb ? -1 : best_sb[b2];
+                }
+            }
+            mask_lo = warm_lo = (uint32_t)mv;
+            mask_hi = warm_hi = (uint32_t)(mv >> 32);
+            warm_pending = true;
+        } else if (!seeded) {
+            stop_at = 16;
+        } else if (lane == 0) {
+            atomicAdd(&votes[head], needed * 4 > min(nsb, 64 * 64) * 3 ? 1 : -1);
+        }
+        wm = read_mask(0);
+    } else {
+        stride_sb = max(1, (int)((float)nsb * 0.381966f));
+        for (;; ++stride_sb) {
+            int a = stride_sb, b = nsb;
+            while (b != 0) {
+                const int r = a % b;
+                a = b;
+                b = r;
+            }
+            if (a == 1) break;
+        }
+        int s0 = 0;
+        if (tasks == nullptr) {
+            const Pacer* pc = &pacers[xcd];
+            const double rate = __hip_atomic_load(&pc->rate, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const double pos = __hip_atomic_load(&pc->pos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const int64_t ref = __hip_atomic_load(&pc->t_ref, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            item_start = wall_clock64();
+            const double v = pos + (double)(item_start - ref) * rate;
+            if (rate > 0.0 && v >= 0.0 && v < 1e15) s0 = (int)(((int64_t)v / SBT) % nsb);
+            s0 = __builtin_amdgcn_readfirstlane(s0);
+        }
+        w = s0 >> 6;
+        b0 = s0 & 63;
+        wm = valid_bits(w) & (~0ull << b0);
+    }
+    const int nvisits = b0 == 0 ? nwin : nwin + 1;
+    bool finished = false;
+
+    // Next superblock to scan, into ls.  False when the walk is over
+    // (finished) or the masks have to be formed first (a new batch, or
+    // stop_at reached); the state is left as is, so a repeated call returns
+    // false again until the masks are redone.
+    auto next_sb = [&](int& ls) {
+        if (scanned >= stop_at) return false;
+        while (wm == 0ull) {
+            if (wv + 1 >= nvisits) {
+                finished = true;
+                return false;
+            }
+            const int wn = w + 1 == nwin ? 0 : w + 1;
+            if (pruned && (wn >> 6) != mask_batch) return false;
+            ++wv;
+            w = wn;
+            wm = pruned ? read_mask(w) : valid_bits(w);
+            if (wv == nwin) wm &= (1ull << b0) - 1ull;
+        }
+        ls = 64 * w + (int)__builtin_ctzll(wm);
+        if (!pruned) ls = (int)(((int64_t)ls * stride_sb) % nsb);
+        wm &= wm - 1ull;
+        ++scanned;
+        return true;
+    };
+
+    const uint32_t lane_off = (uint32_t)lane * 16u;
+    const char* head_tiles = reinterpret_cast<const char*>(kp) + (size_t)head * (ntiles + kPadTiles) * TILE_BYTES;
+    const char* graph_tiles = head_tiles + (size_t)t0 * TILE_BYTES;
 
     // Scores of the tile in ring slot `a`; PF - 1 later tiles are in flight.
+    constexpr int PF = 8 / NC;
+    static_assert(SBT % PF == 0, "ring slots must line up with superblocks");
     auto scores = [&](i32x4 (&a)[NC], f32x16 (&acc)[QB]) {
 #pragma unroll
         for (int c = 0; c < NC; ++c) ring_wait<(PF - 1) * NC>(a[c]);
@@ -503,54 +700,91 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         }
     };
 
-    // Software pipeline with two accumulator sets: the MFMAs of scan
-    // position i+1 are issued before position i is filtered, so matrix cores
-    // and filter overlap.  Scores past the nt positions of the scan may be
-    // formed but are never filtered.  The main loop runs whole groups of PF
-    // positions without checks; the tail group checks each position.
-    f32x16 acc_a[QB], acc_b[QB];
-    int tile_a = slot_tile[0], tile_b = 0;
-    scores(ring[0], acc_a);
-    refill(ring[0], slot_tile[0]);
-    int i = 0;
-    for (const int i_full = nt / PF * PF; i < i_full; i += PF) {
+    // Phases: each streams superblocks until next_sb stops, then drains the
+    // ring; between phases the masks are formed again.
+    for (;;) {
+        int ls = 0;
+        if (!next_sb(ls)) {
+            if (finished && !warm_pending) break;
+            // Fold pending candidates so that theta is current, then redo the
+            // masks of the batch holding the next window to scan.
+            merge_all();
+            if (finished) {
+                // End of the warm-up: walk every window again with masks
+                // that leave out the superblocks it scanned.
+                warm_pending = false;
+                finished = false;
+                stop_at = scanned + 16;
+                compute_batch(0, false);
+                w = 0;
+                wv = 0;
+                wm = read_mask(0);
+                continue;
+            }
+            if (scanned >= stop_at) stop_at = 4 * scanned;
+            const int bt = wm != 0ull ? (w >> 6) : ((w + 1 == nwin ? 0 : w + 1) >> 6);
+            compute_batch(bt, false);
+            if ((w >> 6) == bt) wm &= read_mask(w);
+            continue;
+        }
+
+        // Prefetch ring: each slot holds one tile, and slot_tile[] remembers
+        // which (-1 past the phase's last superblock, whose slots are loaded
+        // with the graph's first tile and never filtered).  A slot is
+        // refilled with the tile PF positions later as soon as its MFMAs
+        // are issued; the load cursor takes the next superblock when it
+        // passes the last tile of one (pos is known at each call site).
+        bool lex = false;
+        i32x4 ring[PF][NC];
+        int slot_tile[PF];
+        auto refill = [&](i32x4 (&slot)[NC], int& stile, int pos) {
+            const int rt = lex ? 0 : ls * SBT + pos;
+            stile = lex ? -1 : t0 + rt;
+            const char* src = graph_tiles + (size_t)rt * TILE_BYTES;
+            slot[0] = ring_load<0>(src, lane_off);
+            if constexpr (NC >= 2) slot[1] = ring_load<1024>(src, lane_off);
+            if constexpr (NC >= 4) {
+                slot[2] = ring_load<2048>(src, lane_off);
+                slot[3] = ring_load<3072>(src, lane_off);
+            }
+            if (pos == SBT - 1 && !lex) lex = !next_sb(ls);
+        };
 #pragma unroll
-        for (int u = 0; u < PF; u += 2) {
-            tile_b = slot_tile[u + 1];
-            scores(ring[u + 1], acc_b);
-            refill(ring[u + 1], slot_tile[u + 1]);
-            filter(acc_a, tile_a);
-            tile_a = slot_tile[(u + 2) % PF];
-            scores(ring[(u + 2) % PF], acc_a);
-            refill(ring[(u + 2) % PF], slot_tile[(u + 2) % PF]);
-            filter(acc_b, tile_b);
+        for (int u = 0; u < PF; ++u) refill(ring[u], slot_tile[u], u);
+
+        // Software pipeline with two accumulator sets: the MFMAs of position
+        // p+1 are issued before position p is filtered, so matrix cores and
+        // filter overlap.  One pass of the loop body takes one superblock.
+        f32x16 acc_a[QB], acc_b[QB];
+        int tile_a = slot_tile[0], tile_b = 0;
+        scores(ring[0], acc_a);
+        refill(ring[0], slot_tile[0], PF % SBT);
+        while (tile_a >= 0) {
+#pragma unroll
+            for (int p = 0; p < SBT; p += 2) {
+                const int u1 = (p + 1) % PF, u2 = (p + 2) % PF;
+                tile_b = slot_tile[u1];
+                scores(ring[u1], acc_b);
+                refill(ring[u1], slot_tile[u1], (p + 1 + PF) % SBT);
+                filter(acc_a, tile_a);
+                tile_a = slot_tile[u2];
+                scores(ring[u2], acc_a);
+                refill(ring[u2], slot_tile[u2], (p + 2 + PF) % SBT);
+                filter(acc_b, tile_b);
+            }
+        }
+        // Drain the ring.  Every ring register is an operand of the wait: a
+        // prefetch whose tile is never used is dead to the compiler, which
+        // could otherwise hand its registers to other values while the load
+        // is still in flight and would land on top of them.
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+#pragma unroll
+            for (int c = 0; c < NC; ++c) ring_wait<0>(ring[u][c]);
         }
     }
-#pragma unroll
-    for (int u = 0; u < PF; u += 2) {
-        if (i + u >= nt) goto stream_done;
-        tile_b = slot_tile[u + 1];
-        scores(ring[u + 1], acc_b);
-        refill(ring[u + 1], slot_tile[u + 1]);
-        filter(acc_a, tile_a);
-        if (i + u + 1 >= nt) goto stream_done;
-        tile_a = slot_tile[(u + 2) % PF];
-        scores(ring[(u + 2) % PF], acc_a);
-        refill(ring[(u + 2) % PF], slot_tile[(u + 2) % PF]);
-        filter(acc_b, tile_b);
-    }
-stream_done:
-    // Drain the ring.  Every ring register is an operand of the wait: a
-    // prefetch whose tile is never used is dead to the compiler, which could
-    // otherwise hand its registers to other values while the load is still
-    // in flight and would land on top of them.
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-#pragma unroll
-        for (int c = 0; c < NC; ++c) ring_wait<0>(ring[u][c]);
-    }
     merge_all();
-    if (tasks == nullptr && lane == 0) {
+    if (!pruned && tasks == nullptr && lane == 0) {
         const int64_t now = wall_clock64();
         pacer_update(&pacers[xcd], now, nt, now - item_start);
     }
@@ -587,7 +821,9 @@ stream_done:
 }
 
 // Tiles t >= ntiles of each head (the kPadTiles padding) are written as zeros.
+// Position p of head h holds key perm[h][p] (key p without perm).
 __global__ __launch_bounds__(256) void pack_k_kernel(const uint16_t* __restrict__ K,
+                                                     const int32_t* __restrict__ perm,
                                                      uint4* __restrict__ kp, int32_t N, int32_t H,
                                                      int32_t nchunk, int32_t ntiles) {
     const int32_t ntiles_all = ntiles + kPadTiles;
@@ -600,19 +836,21 @@ __global__ __launch_bounds__(256) void pack_k_kernel(const uint16_t* __restrict_
     r /= nchunk;
     const int t = (int)(r % ntiles_all);
     const int h = (int)(r / ntiles_all);
-    const int key = t * 32 + (lane & 31);
+    const int pos = t * 32 + (lane & 31);
     uint4 v = make_uint4(0, 0, 0, 0);
-    if (key < N) {
+    if (pos < N) {
         const int d = nchunk * 16;
+        const int key = perm != nullptr ? perm[(size_t)h * N + pos] : pos;
         v = *reinterpret_cast<const uint4*>(K + ((size_t)key * H + h) * d + 16 * c + 8 * (lane >> 5));
     }
     kp[u] = v;
 }
 
 template <int D, int QB, int SLOTS>
-hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, const QueryGroups* groups,
-                           int32_t ntasks, int32_t N, int32_t H, int32_t k, int32_t ntiles,
-                           int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream) {
+hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const Task* tasks,
+                           const QueryGroups* groups, const KeyOrder* keys, int32_t ntasks, int32_t N,
+                           int32_t H, int32_t k, int32_t ntiles, int32_t* work_ctr, int32_t* topk_idx,
+                           hipStream_t stream) {
     const int64_t items = (int64_t)ntasks * H;
     const size_t lds = select_lds_bytes(k, SelectShape{QB, SLOTS});
     // One resident wave per workgroup slot of the chip, a multiple of the XCD
@@ -639,9 +877,11 @@ hipError_t launch_select_t(const void* kp, const void* Q, const Task* tasks, con
     const int64_t grid = std::max<int64_t>(kNumXcd, want / kNumXcd * kNumXcd);
     hipLaunchKernelGGL((select_kernel<D, QB, SLOTS>), dim3((unsigned)grid), dim3(64), lds, stream,
                        reinterpret_cast<const uint4*>(kp), reinterpret_cast<const uint16_t*>(Q),
-                       tasks, groups ? groups->perm : nullptr, groups ? groups->label : nullptr,
-                       groups ? groups->seed_ref : nullptr, ntasks, N, H, k, ntiles, work_ctr, pacers,
-                       topk_idx);
+                       reinterpret_cast<const uint16_t*>(K), tasks, groups ? groups->perm : nullptr,
+                       groups ? groups->label : nullptr, groups ? groups->seed_ref : nullptr,
+                       keys ? keys->perm : nullptr, keys ? keys->bounds : nullptr,
+                       keys ? keys->votes : nullptr, keys ? keys->ctiles : 0, ntasks, N, H, k, ntiles,
+                       work_ctr, pacers, topk_idx);
     return hipGetLastError();
 }
 
@@ -651,32 +891,30 @@ size_t select_lds_bytes(int32_t k, SelectShape shape) {
     return (size_t)shape.qb * ((size_t)k * 32 + (size_t)shape.slots * 64) * sizeof(uint64_t);
 }
 
-hipError_t launch_pack_k(const void* K, void* kp, int32_t N, int32_t H, int32_t d, int32_t ntiles,
-                         hipStream_t stream) {
+hipError_t launch_pack_k(const void* K, const int32_t* perm, void* kp, int32_t N, int32_t H, int32_t d,
+                         int32_t ntiles, hipStream_t stream) {
     const int nchunk = d / 16;
     const size_t total = (size_t)H * (ntiles + kPadTiles) * nchunk * 64;
     if (total == 0) return hipSuccess;
     const unsigned blocks = (unsigned)((total + 255) / 256);
     hipLaunchKernelGGL(pack_k_kernel, dim3(blocks), dim3(256), 0, stream,
-                       reinterpret_cast<const uint16_t*>(K), reinterpret_cast<uint4*>(kp), N, H,
+                       reinterpret_cast<const uint16_t*>(K), perm, reinterpret_cast<uint4*>(kp), N, H,
                        nchunk, ntiles);
     return hipGetLastError();
 }
 
-hipError_t launch_select(const void* kp, const void* Q, const Task* tasks, const QueryGroups* groups,
-                         int32_t ntasks, int32_t N, int32_t H, int32_t d, int32_t k, int32_t ntiles,
-                         SelectShape shape, int32_t* work_ctr, int32_t* topk_idx,
-                         hipStream_t stream) {
+hipError_t launch_select(const void* kp, const void* Q, const void* K, const Task* tasks,
+                         const QueryGroups* groups, const KeyOrder* keys, int32_t ntasks, int32_t N,
+                         int32_t H, int32_t d, int32_t k, int32_t ntiles, SelectShape shape,
+                         int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream) {
     if (ntasks <= 0) return hipSuccess;
 #define KMIP_SELECT_CASE(DD, QQ, SS)                                                             \
     if (d == DD && shape.qb == QQ && shape.slots == SS)                                          \
-        return launch_select_t<DD, QQ, SS>(kp, Q, tasks, groups, ntasks, N, H, k, ntiles,        \
+        return launch_select_t<DD, QQ, SS>(kp, Q, K, tasks, groups, keys, ntasks, N, H, k, ntiles, \
                                            work_ctr, topk_idx, stream);
 #define KMIP_SELECT_D(DD)         \
     KMIP_SELECT_CASE(DD, 2, 4)    \
-    KMIP_SELECT_CASE(DD, 2, 8)    \
-    KMIP_SELECT_CASE(DD, 1, 8)    \
-    KMIP_SELECT_CASE(DD, 1, 16)
+    KMIP_SELECT_CASE(DD, 1, 8)
     KMIP_SELECT_D(16)
     KMIP_SELECT_D(32)
     KMIP_SELECT_D(64)

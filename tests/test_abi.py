@@ -52,7 +52,15 @@ def test_workspace_size(lib):
     # [H][256][d] f32, labels [H][N] u16, a histogram and the seed references
     # [2][H][256] i32 and the permutation [H][N] i32, each 256-byte aligned
     grouping = 4 * 256 * 16 * 4 + 4 * 500_000 * 2 + 2 * 4 * 256 * 4 + 4 * 500_000 * 4
-    assert n == packed + grouping
+    # ... and the stored key order: two position buffers [H][N] i32, projection
+    # codes [H][N] u16, per-node data of the widest tree level (1954
+    # superblocks -> 11 levels, 1024 nodes) [H][1024][2d + 2] f32 and
+    # [H][1024][516] i32, votes [H] i32 (padded to 256 B), and the bound tiles:
+    # 1954 superblocks of 256 keys -> 31 windows of 64 -> 62 tiles per head of
+    # (d/16 + 1) chunks of 64 x 16 B
+    key_order = (2 * 4 * 500_000 * 4 + 4 * 500_000 * 2 + 4 * 1024 * 34 * 4 + 4 * 1024 * 516 * 4
+                 + 256 + 4 * 62 * 2 * 64 * 16)
+    assert n == packed + grouping + key_order
     assert lib.kmip_topk_workspace_size(8191, 1, 16, 4, 1) == (256 + 16) * 32 * 16 * 2 + 512
     assert lib.kmip_topk_workspace_size(33, 1, 16, 4, 1) == (2 + 16) * 32 * 16 * 2 + 512
     multi = lib.kmip_topk_workspace_size(1000, 2, 32, 16, 7)
