@@ -108,18 +108,39 @@ __global__ __launch_bounds__(256) void group_scan_kernel(int32_t* __restrict__ h
     hh[t] = s[t] - own;
 }
 
-// perm[h][cursor[h][label]++] = i.  The order inside one bucket follows the
-// atomics and is not fixed; any order is a valid grouping.
+// perm[h][cursor[h][label]++] = i, for the kScatterPer * 256 queries of a
+// block: each query takes its rank among the block's queries of its label
+// from an LDS counter, and the block reserves its places with one global
+// atomic per label.  The order inside one bucket follows the atomics and is
+// not fixed; any order is a valid grouping.
+constexpr int kScatterPer = 8;
+
 __global__ __launch_bounds__(256) void group_scatter_kernel(const uint16_t* __restrict__ label,
                                                             int32_t* __restrict__ cursor,
                                                             int32_t N, int32_t H,
                                                             int32_t* __restrict__ perm) {
+    __shared__ int32_t cnt[C];
     const int h = blockIdx.y;
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= N) return;
-    const int lab = label[(size_t)h * N + i];
-    const int32_t pos = atomicAdd(&cursor[(size_t)h * C + lab], 1);
-    perm[(size_t)h * N + pos] = (int32_t)i;
+    const int t = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * 256 * kScatterPer;
+    cnt[t] = 0;
+    __syncthreads();
+    int lab[kScatterPer], rank[kScatterPer];
+#pragma unroll
+    for (int r = 0; r < kScatterPer; ++r) {
+        const int64_t i = base + r * 256 + t;
+        lab[r] = i < N ? label[(size_t)h * N + i] : -1;
+        rank[r] = lab[r] >= 0 ? atomicAdd(&cnt[lab[r]], 1) : 0;
+    }
+    __syncthreads();
+    const int c = cnt[t];
+    if (c != 0) cnt[t] = atomicAdd(&cursor[(size_t)h * C + t], c);
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kScatterPer; ++r) {
+        const int64_t i = base + r * 256 + t;
+        if (lab[r] >= 0) perm[(size_t)h * N + cnt[lab[r]] + rank[r]] = (int32_t)i;
+    }
 }
 
 }  // namespace
@@ -161,7 +182,8 @@ hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, 
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(group_scan_kernel, dim3(H), dim3(C), 0, stream, hist);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(group_scatter_kernel, grid, dim3(256), 0, stream, label, hist, N, H, perm);
+    const dim3 sgrid((unsigned)((N + 256 * kScatterPer - 1) / (256 * kScatterPer)), (unsigned)H);
+    hipLaunchKernelGGL(group_scatter_kernel, sgrid, dim3(256), 0, stream, label, hist, N, H, perm);
     return hipGetLastError();
 }
 

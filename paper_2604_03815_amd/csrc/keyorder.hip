@@ -29,14 +29,19 @@ namespace {
 
 constexpr int SBK = kSuperTiles * 32;  // keys per superblock
 static_assert(SBK == 256, "one thread per key of a superblock");
-constexpr int kSample = 256;           // keys sampled per node for its axis
-constexpr int kPowerIters = 8;
+constexpr int kSample = 64;            // keys sampled per node for its axis
+constexpr int kPowerIters = 5;
 
 // Per-node working data of one level, [H][width]:
 //   f: mean[d], axis[d], lo, inv_step (projection p maps to
 //      clamp((p - lo) * inv_step) in 0 .. 65535)
-//   h: hist1[256], hist2[256], then left, right, tie counters
-constexpr int kNodeInts = 512 + 4;
+//   h: hist1[256], hist2[256], then the counters and split search results
+constexpr int kLeftCursor = 512;  // and kLeftCursor + 1: the right side's
+constexpr int kTieTicket = 514;
+constexpr int kHighByte = 515;
+constexpr int kSplitValue = 516;
+constexpr int kTiesLeft = 517;
+constexpr int kNodeInts = 520;
 
 // Size of the left part of a node of n > SBK keys: half, rounded up to whole
 // superblocks, and at least one key on the right.
@@ -104,41 +109,23 @@ __device__ __forceinline__ float wave_min(float v) {
     return v;
 }
 
-// Sum over the 256 threads of a block of each of D values; every thread
-// gets the sums in out[].  red: LDS [4][D].
+// Level lev, one wave per node: the node's mean and principal axis from an
+// evenly spaced sample of its keys (power iteration from the sample farthest
+// from the mean), the quantisation range of the sample's projections, and
+// zeroed histograms and counters.
 template <int D>
-__device__ __forceinline__ void block_sum(const float (&v)[D], float (&out)[D], float (*red)[D]) {
-    const int t = threadIdx.x;
-#pragma unroll
-    for (int i = 0; i < D; ++i) {
-        const float s = wave_sum(v[i]);
-        if ((t & 63) == 0) red[t >> 6][i] = s;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < D; ++i) out[i] = (red[0][i] + red[1][i]) + (red[2][i] + red[3][i]);
-    __syncthreads();
-}
-
-// Level lev, one block per node: the node's mean and principal axis from an
-// evenly spaced sample of its keys, the quantisation range of the sample's
-// projections, and zeroed histograms and counters.
-template <int D>
-__global__ __launch_bounds__(256) void tree_axis_kernel(const uint16_t* __restrict__ K,
-                                                        const int32_t* __restrict__ perm, int32_t N,
-                                                        int32_t H, int32_t lev, int32_t width,
-                                                        float* __restrict__ nodef,
-                                                        int32_t* __restrict__ nodeh) {
-    __shared__ float red[4][D];
-    __shared__ float rmax[4];
-    __shared__ int rarg[4];
+__global__ __launch_bounds__(64) void tree_axis_kernel(const uint16_t* __restrict__ K,
+                                                       const int32_t* __restrict__ perm, int32_t N,
+                                                       int32_t H, int32_t lev, int32_t width,
+                                                       float* __restrict__ nodef,
+                                                       int32_t* __restrict__ nodeh) {
     const int idx = blockIdx.x;
     const int h = blockIdx.y;
     const int t = threadIdx.x;
     int lo, n;
     if (!node_by_index(idx, N, lev, lo, n)) return;
     int32_t* nh = nodeh + ((size_t)h * width + idx) * kNodeInts;
-    for (int e = t; e < kNodeInts; e += 256) nh[e] = 0;
+    for (int e = t; e < kNodeInts; e += 64) nh[e] = 0;
     const int S = n < kSample ? n : kSample;
     const bool act = t < S;
     float x[D];
@@ -150,35 +137,20 @@ __global__ __launch_bounds__(256) void tree_axis_kernel(const uint16_t* __restri
         for (int i = 0; i < D; ++i) x[i] = 0.0f;
     }
     float mu[D];
-    block_sum<D>(x, mu, red);
     const float inv_s = 1.0f / (float)S;
 #pragma unroll
     for (int i = 0; i < D; ++i) {
-        mu[i] *= inv_s;
+        mu[i] = wave_sum(x[i]) * inv_s;
         x[i] = act ? x[i] - mu[i] : 0.0f;
     }
-    // start from the sample farthest from the mean
     float dd = 0.0f;
 #pragma unroll
     for (int i = 0; i < D; ++i) dd = fmaf(x[i], x[i], dd);
-    float m = wave_max(dd);
-    const uint64_t hit = __builtin_amdgcn_ballot_w64(dd == m);
-    if ((t & 63) == 0) {
-        rmax[t >> 6] = m;
-        rarg[t >> 6] = (t & ~63) + (int)__builtin_ctzll(hit);
-    }
-    __syncthreads();
-    int far = rarg[0];
-    float fm = rmax[0];
-    for (int wv = 1; wv < 4; ++wv)
-        if (rmax[wv] > fm) {
-            fm = rmax[wv];
-            far = rarg[wv];
-        }
+    const float m = wave_max(dd);
+    const int far = (int)__builtin_ctzll(__builtin_amdgcn_ballot_w64(dd == m));
     float axis[D];
 #pragma unroll
-    for (int i = 0; i < D; ++i) axis[i] = t == far ? x[i] : 0.0f;
-    block_sum<D>(axis, axis, red);
+    for (int i = 0; i < D; ++i) axis[i] = __shfl(x[i], far);
     // power iteration: axis <- sum_s (x_s . axis) x_s, normalised
     for (int it = 0; it < kPowerIters; ++it) {
         float nn = 0.0f;
@@ -188,10 +160,8 @@ __global__ __launch_bounds__(256) void tree_axis_kernel(const uint16_t* __restri
         float pr = 0.0f;
 #pragma unroll
         for (int i = 0; i < D; ++i) pr = fmaf(x[i], axis[i] * inv, pr);
-        float c[D];
 #pragma unroll
-        for (int i = 0; i < D; ++i) c[i] = pr * x[i];
-        block_sum<D>(c, axis, red);
+        for (int i = 0; i < D; ++i) axis[i] = wave_sum(pr * x[i]);
     }
     float nn = 0.0f;
 #pragma unroll
@@ -207,20 +177,15 @@ __global__ __launch_bounds__(256) void tree_axis_kernel(const uint16_t* __restri
     float pr = 0.0f;
 #pragma unroll
     for (int i = 0; i < D; ++i) pr = fmaf(x[i], axis[i], pr);
-    float pmin = wave_min(act ? pr : INFINITY), pmax = wave_max(act ? pr : -INFINITY);
-    if ((t & 63) == 0) {
-        red[t >> 6][0] = pmin;
-        red[t >> 6][1] = pmax;
-    }
-    __syncthreads();
-    pmin = fminf(fminf(red[0][0], red[1][0]), fminf(red[2][0], red[3][0]));
-    pmax = fmaxf(fmaxf(red[0][1], red[1][1]), fmaxf(red[2][1], red[3][1]));
-    float* nf = nodef + ((size_t)h * width + idx) * (2 * D + 2);
-    if (t < D) {
-        nf[t] = mu[t];
-        nf[D + t] = axis[t];
-    }
+    const float pmin = wave_min(act ? pr : INFINITY), pmax = wave_max(act ? pr : -INFINITY);
     if (t == 0) {
+        float* nf = nodef + ((size_t)h * width + idx) * (2 * D + 2);
+        // static indices keep the arrays in registers
+#pragma unroll
+        for (int i = 0; i < D; ++i) {
+            nf[i] = mu[i];
+            nf[D + i] = axis[i];
+        }
         // the mean-centred projection of the sample, widened a little so that
         // most keys fall inside the quantised range
         const float span = pmax - pmin;
@@ -238,8 +203,41 @@ __device__ __forceinline__ uint32_t quantise(const float* __restrict__ nf, const
     return (uint32_t)fminf(fmaxf(u, 0.0f), 65535.0f);
 }
 
-// Level lev, one thread per position: the 16-bit projection code of the key
-// at that position, and the histogram of its high byte per node.
+// The per-position level kernels give each block kBlockPos consecutive
+// positions, kPerThread per thread in rounds of 256 (so that the lanes of a
+// wave take consecutive positions, mostly of one node).  A block adds the
+// histogram counts of the node that holds its first position in LDS and
+// flushes them once: at the top levels, where all positions fall into few
+// nodes, that keeps the global atomics on one node's 256 bins few.
+constexpr int kPerThread = 8;
+constexpr int kBlockPos = 256 * kPerThread;
+
+// Adds 1 to *addr for every active lane and returns the lane's rank among
+// the lanes of its wave with the same address: one atomic per distinct
+// address in the wave.
+__device__ __forceinline__ int wave_ticket(int32_t* addr, bool active) {
+    const int lane = threadIdx.x & 63;
+    const uint64_t below = (1ull << lane) - 1ull;
+    int rank = 0;
+    uint64_t todo = __builtin_amdgcn_ballot_w64(active);
+    while (todo != 0ull) {
+        const int leader = (int)__builtin_ctzll(todo);
+        const uint64_t a = reinterpret_cast<uint64_t>(addr);
+        const uint64_t la = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)a, leader) |
+                            ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(a >> 32), leader) << 32);
+        const bool mine = active && a == la;
+        const uint64_t same = __builtin_amdgcn_ballot_w64(mine);
+        int base = 0;
+        if (lane == leader) base = atomicAdd(reinterpret_cast<int32_t*>(la), (int)__builtin_popcountll(same));
+        base = __builtin_amdgcn_readlane(base, leader);
+        if (mine) rank = base + (int)__builtin_popcountll(same & below);
+        todo &= ~same;
+    }
+    return rank;
+}
+
+// Level lev: the 16-bit projection code of the key at each position of a
+// split node, and the histogram of its high byte per node.
 template <int D>
 __global__ __launch_bounds__(256) void tree_project_kernel(const uint16_t* __restrict__ K,
                                                            const int32_t* __restrict__ perm, int32_t N,
@@ -247,62 +245,65 @@ __global__ __launch_bounds__(256) void tree_project_kernel(const uint16_t* __res
                                                            const float* __restrict__ nodef,
                                                            int32_t* __restrict__ nodeh,
                                                            uint16_t* __restrict__ code) {
+    __shared__ int32_t lh[256];
     const int h = blockIdx.y;
-    const int p = blockIdx.x * 256 + threadIdx.x;
-    int lo, n, idx;
-    if (p >= N || !node_of(p, N, lev, lo, n, idx)) return;
-    float x[D];
-    load_row_f32<D>(x, K + ((size_t)perm[(size_t)h * N + p] * H + h) * D);
-    const uint32_t q = quantise<D>(nodef + ((size_t)h * width + idx) * (2 * D + 2), x);
-    code[(size_t)h * N + p] = (uint16_t)q;
-    atomicAdd(&nodeh[((size_t)h * width + idx) * kNodeInts + (q >> 8)], 1);
+    const int t = threadIdx.x;
+    const int base = blockIdx.x * kBlockPos;
+    int lo0, n0, idx0;
+    const bool agg = node_of(base, N, lev, lo0, n0, idx0);
+    lh[t] = 0;
+    __syncthreads();
+    for (int i = 0; i < kPerThread; ++i) {
+        const int p = base + i * 256 + t;
+        int lo, n, idx;
+        if (p >= N || !node_of(p, N, lev, lo, n, idx)) continue;
+        float x[D];
+        load_row_f32<D>(x, K + ((size_t)perm[(size_t)h * N + p] * H + h) * D);
+        const uint32_t q = quantise<D>(nodef + ((size_t)h * width + idx) * (2 * D + 2), x);
+        code[(size_t)h * N + p] = (uint16_t)q;
+        if (agg && idx == idx0)
+            atomicAdd(&lh[q >> 8], 1);
+        else
+            atomicAdd(&nodeh[((size_t)h * width + idx) * kNodeInts + (q >> 8)], 1);
+    }
+    __syncthreads();
+    if (agg && lh[t] != 0) atomicAdd(&nodeh[((size_t)h * width + idx0) * kNodeInts + t], lh[t]);
 }
 
-// The bin of a 256-bin histogram in which the target-th element (0-based, in
-// increasing order) falls, and the count below that bin.  Run by every
-// thread of the block over the same LDS array after a barrier.
-__device__ __forceinline__ void find_bin(const int32_t* hs, int target, int& bin, int& below) {
-    int acc = 0;
-    bin = 255;
-    below = 0;
-    for (int b = 0; b < 256; ++b) {
-        const int c = hs[b];
-        if (acc + c > target) {
-            bin = b;
-            below = acc;
-            return;
+// Level lev, one block per split node: the split search on one of its
+// histograms.  Pass 0 finds the bin of the high byte that holds the
+// node's nl-th smallest code (0-based: the first position of the right
+// side); pass 1 finds the low byte within that bin.  Afterwards
+// kSplitValue holds the code v at which the node splits and kTiesLeft how
+// many keys with code v go left (the keys with a smaller code all do).
+__global__ __launch_bounds__(256) void tree_find_kernel(int32_t N, int32_t lev, int32_t width,
+                                                        int32_t pass, int32_t* __restrict__ nodeh) {
+    __shared__ int32_t sc[256];
+    const int idx = blockIdx.x;
+    const int h = blockIdx.y;
+    const int t = threadIdx.x;
+    int lo, n;
+    if (!node_by_index(idx, N, lev, lo, n)) return;
+    int32_t* nh = nodeh + ((size_t)h * width + idx) * kNodeInts;
+    const int target = pass == 0 ? split_left(n) : nh[kTiesLeft];
+    const int v = nh[pass * 256 + t];
+    sc[t] = v;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        const int add = t >= off ? sc[t - off] : 0;
+        __syncthreads();
+        sc[t] += add;
+        __syncthreads();
+    }
+    const int incl = sc[t], excl = incl - v;
+    if (target >= excl && target < incl) {
+        if (pass == 0) {
+            nh[kHighByte] = t;
+            nh[kTiesLeft] = target - excl;
+        } else {
+            nh[kSplitValue] = (nh[kHighByte] << 8) | t;
+            nh[kTiesLeft] = target - excl;
         }
-        acc += c;
-    }
-    below = acc;
-}
-
-// A block covers 256 consecutive positions, hence at most two nodes that are
-// still split (each has more than 256 positions).  Loads the histograms of
-// those nodes into LDS.
-struct BlockNodes {
-    int idx[2];
-    int lo[2];
-    int n[2];
-    int count;
-};
-
-__device__ __forceinline__ void block_nodes(int N, int lev, BlockNodes& bn) {
-    bn.count = 0;
-    const int p0 = blockIdx.x * 256;
-    const int p1 = min(N, p0 + 256) - 1;
-    int lo, n, idx;
-    if (node_of(p0, N, lev, lo, n, idx)) {
-        bn.idx[bn.count] = idx;
-        bn.lo[bn.count] = lo;
-        bn.n[bn.count] = n;
-        ++bn.count;
-    }
-    if (node_of(p1, N, lev, lo, n, idx) && (bn.count == 0 || idx != bn.idx[0])) {
-        bn.idx[bn.count] = idx;
-        bn.lo[bn.count] = lo;
-        bn.n[bn.count] = n;
-        ++bn.count;
     }
 }
 
@@ -311,106 +312,90 @@ __device__ __forceinline__ void block_nodes(int N, int lev, BlockNodes& bn) {
 __global__ __launch_bounds__(256) void tree_hist2_kernel(int32_t N, int32_t lev, int32_t width,
                                                          int32_t* __restrict__ nodeh,
                                                          const uint16_t* __restrict__ code) {
-    __shared__ int32_t hs[2][256];
+    __shared__ int32_t lh[256];
     const int h = blockIdx.y;
     const int t = threadIdx.x;
-    BlockNodes bn;
-    block_nodes(N, lev, bn);
-    if (bn.count == 0) return;
-    for (int s = 0; s < bn.count; ++s) hs[s][t] = nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + t];
+    const int base = blockIdx.x * kBlockPos;
+    int lo0, n0, idx0;
+    const bool agg = node_of(base, N, lev, lo0, n0, idx0);
+    const int b0 = agg ? nodeh[((size_t)h * width + idx0) * kNodeInts + kHighByte] : -1;
+    lh[t] = 0;
     __syncthreads();
-    int b1[2] = {0, 0};
-    for (int s = 0; s < bn.count; ++s) {
-        int below;
-        find_bin(hs[s], split_left(bn.n[s]), b1[s], below);
+    for (int i = 0; i < kPerThread; ++i) {
+        const int p = base + i * 256 + t;
+        int lo, n, idx;
+        if (p >= N || !node_of(p, N, lev, lo, n, idx)) continue;
+        const uint32_t q = code[(size_t)h * N + p];
+        int32_t* nh = nodeh + ((size_t)h * width + idx) * kNodeInts;
+        const bool own = agg && idx == idx0;
+        if ((int)(q >> 8) != (own ? b0 : nh[kHighByte])) continue;
+        if (own)
+            atomicAdd(&lh[q & 255u], 1);
+        else
+            atomicAdd(&nh[256 + (q & 255u)], 1);
     }
-    const int p = blockIdx.x * 256 + t;
-    if (p >= N) return;
-    const int s = (bn.count == 2 && p >= bn.lo[1]) ? 1 : 0;
-    if (p < bn.lo[s] || p >= bn.lo[s] + bn.n[s]) return;
-    const uint32_t q = code[(size_t)h * N + p];
-    if ((int)(q >> 8) == b1[s])
-        atomicAdd(&nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + 256 + (q & 255u)], 1);
+    __syncthreads();
+    if (agg && lh[t] != 0) atomicAdd(&nodeh[((size_t)h * width + idx0) * kNodeInts + 256 + t], lh[t]);
 }
 
-// Level lev: every position of a node that is split moves to its side.  The
-// left side takes the keys whose code is below the split value and, by
-// ticket, as many keys with the split value as the left size still needs.
-// Positions in leaves keep their key.
+// Level lev: every position of a split node moves to its side.  The left
+// side takes the keys whose code is below the split value and, by ticket,
+// as many keys with the split value as it still needs.  Positions in leaves
+// keep their key.  A block's positions take their ranks from LDS counters,
+// one per (node, side), and the block reserves its places in each node with
+// one global atomic: split nodes hold more than SBK positions, so the slot
+// (lo - base) / (SBK + 1) + 1 of a node starting inside the block (0 for the
+// one it starts in) tells its nodes apart.
+constexpr int kSlots = kBlockPos / (SBK + 1) + 2;
+
 __global__ __launch_bounds__(256) void tree_scatter_kernel(int32_t N, int32_t lev, int32_t width,
                                                            int32_t* __restrict__ nodeh,
                                                            const uint16_t* __restrict__ code,
                                                            const int32_t* __restrict__ perm_in,
                                                            int32_t* __restrict__ perm_out) {
-    __shared__ int32_t hs[2][256];
-    __shared__ int32_t cnt[2][2];
-    __shared__ int32_t base[2][2];
+    __shared__ int32_t cnt[kSlots][2];
+    __shared__ int32_t sidx[kSlots];
     const int h = blockIdx.y;
     const int t = threadIdx.x;
-    const int p = blockIdx.x * 256 + t;
-    BlockNodes bn;
-    block_nodes(N, lev, bn);
-    const int32_t key = p < N ? perm_in[(size_t)h * N + p] : 0;
-    if (bn.count == 0) {
-        if (p < N) perm_out[(size_t)h * N + p] = key;
-        return;
-    }
-    int split[2] = {0, 0}, ties_left[2] = {0, 0};
-    for (int s = 0; s < bn.count; ++s) {
-        hs[s][t] = nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + t];
-        if (t < 2) cnt[s][t] = 0;
-    }
+    const int base = blockIdx.x * kBlockPos;
+    if (t < 2 * kSlots) cnt[t >> 1][t & 1] = 0;
     __syncthreads();
-    for (int s = 0; s < bn.count; ++s) {
-        const int nl = split_left(bn.n[s]);
-        int b1, below1;
-        find_bin(hs[s], nl, b1, below1);
-        split[s] = b1 << 8;
-        ties_left[s] = nl - below1;
-    }
-    __syncthreads();
-    for (int s = 0; s < bn.count; ++s) hs[s][t] = nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + 256 + t];
-    __syncthreads();
-    for (int s = 0; s < bn.count; ++s) {
-        int b2, below2;
-        find_bin(hs[s], ties_left[s], b2, below2);
-        split[s] |= b2;
-        ties_left[s] -= below2;
-    }
-    int s = -1, side = 0, rank = 0;
-    if (p < N) {
-        s = (bn.count == 2 && p >= bn.lo[1]) ? 1 : 0;
-        if (p < bn.lo[s] || p >= bn.lo[s] + bn.n[s]) s = -1;
-    }
-    if (s >= 0) {
-        const int q = code[(size_t)h * N + p];
-        if (q < split[s]) {
-            side = 0;
-        } else if (q > split[s]) {
-            side = 1;
-        } else {
-            const int tk = atomicAdd(&nodeh[((size_t)h * width + bn.idx[s]) * kNodeInts + 514], 1);
-            side = tk < ties_left[s] ? 0 : 1;
+    int dst[kPerThread], slot[kPerThread], side[kPerThread], rank[kPerThread];
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+        const int p = base + i * 256 + t;
+        int lo = 0, n = 0, idx = 0;
+        const bool split = p < N && node_of(p, N, lev, lo, n, idx);
+        int32_t* nh = nodeh + ((size_t)h * width + (split ? idx : 0)) * kNodeInts;
+        const int q = split ? (int)code[(size_t)h * N + p] : 0;
+        const int v = split ? nh[kSplitValue] : 0;
+        const bool tie = split && q == v;
+        // every lane takes part in the ticket, active or not
+        const int ticket = wave_ticket(nh + kTieTicket, tie);
+        side[i] = q < v ? 0 : (q > v ? 1 : (ticket < nh[kTiesLeft] ? 0 : 1));
+        slot[i] = -1;
+        dst[i] = p;
+        if (split) {
+            slot[i] = lo < base ? 0 : (lo - base) / (SBK + 1) + 1;
+            sidx[slot[i]] = idx;
+            rank[i] = atomicAdd(&cnt[slot[i]][side[i]], 1);
+            dst[i] = lo + (side[i] == 0 ? 0 : split_left(n)) + rank[i];
         }
-        rank = atomicAdd(&cnt[s][side], 1);
     }
     __syncthreads();
-    if (t < 2 * bn.count) {
-        const int ss = t >> 1, sd = t & 1;
-        base[ss][sd] = cnt[ss][sd] > 0
-                           ? atomicAdd(&nodeh[((size_t)h * width + bn.idx[ss]) * kNodeInts + 512 + sd],
-                                       cnt[ss][sd])
-                           : 0;
+    if (t < 2 * kSlots) {
+        const int s = t >> 1, sd = t & 1;
+        const int c = cnt[s][sd];
+        if (c != 0) cnt[s][sd] = atomicAdd(&nodeh[((size_t)h * width + sidx[s]) * kNodeInts + kLeftCursor + sd], c);
     }
     __syncthreads();
-    if (p >= N) return;
-    if (s < 0) {
-        perm_out[(size_t)h * N + p] = key;
-        return;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+        const int p = base + i * 256 + t;
+        if (p >= N) continue;
+        const int32_t key = perm_in[(size_t)h * N + p];
+        perm_out[(size_t)h * N + dst[i] + (slot[i] >= 0 ? cnt[slot[i]][side[i]] : 0)] = key;
     }
-    const int nl = split_left(bn.n[s]);
-    const int dst = bn.lo[s] + (side == 0 ? 0 : nl) + base[s][side] + rank;
-    perm_out[(size_t)h * N + dst] = key;
 }
 
 __global__ __launch_bounds__(256) void iota_kernel(int32_t N, int32_t* __restrict__ perm) {
@@ -564,6 +549,7 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
     hipError_t e = launch_fill_zero(reinterpret_cast<float*>(votes), (size_t)H, stream);
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)((N + 255) / 256), (unsigned)H);
+    const dim3 pgrid((unsigned)((N + kBlockPos - 1) / kBlockPos), (unsigned)H);
     hipLaunchKernelGGL(iota_kernel, grid, dim3(256), 0, stream, N, perm_a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     int32_t* cur = perm_a;
@@ -571,10 +557,10 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
     for (int lev = 0; lev < levels; ++lev) {
         const dim3 ngrid((unsigned)(1 << lev), (unsigned)H);
 #define KMIP_TREE_LEVEL(DD)                                                                          \
-    hipLaunchKernelGGL(tree_axis_kernel<DD>, ngrid, dim3(256), 0, stream, k, cur, N, H, lev, width,  \
+    hipLaunchKernelGGL(tree_axis_kernel<DD>, ngrid, dim3(64), 0, stream, k, cur, N, H, lev, width,   \
                        nodef, nodeh);                                                                \
     if ((e = hipGetLastError()) != hipSuccess) return e;                                             \
-    hipLaunchKernelGGL(tree_project_kernel<DD>, grid, dim3(256), 0, stream, k, cur, N, H, lev, width, \
+    hipLaunchKernelGGL(tree_project_kernel<DD>, pgrid, dim3(256), 0, stream, k, cur, N, H, lev, width, \
                        nodef, nodeh, code);
         if (d == 16) {
             KMIP_TREE_LEVEL(16)
@@ -585,9 +571,13 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
         }
 #undef KMIP_TREE_LEVEL
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(tree_hist2_kernel, grid, dim3(256), 0, stream, N, lev, width, nodeh, code);
+        hipLaunchKernelGGL(tree_find_kernel, ngrid, dim3(256), 0, stream, N, lev, width, 0, nodeh);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(tree_scatter_kernel, grid, dim3(256), 0, stream, N, lev, width, nodeh, code, cur,
+        hipLaunchKernelGGL(tree_hist2_kernel, pgrid, dim3(256), 0, stream, N, lev, width, nodeh, code);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(tree_find_kernel, ngrid, dim3(256), 0, stream, N, lev, width, 1, nodeh);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(tree_scatter_kernel, pgrid, dim3(256), 0, stream, N, lev, width, nodeh, code, cur,
                            nxt);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         int32_t* tmp = cur;

@@ -55,10 +55,10 @@ def test_workspace_size(lib):
     # ... and the stored key order: two position buffers [H][N] i32, projection
     # codes [H][N] u16, per-node data of the widest tree level (1954
     # superblocks -> 11 levels, 1024 nodes) [H][1024][2d + 2] f32 and
-    # [H][1024][516] i32, votes [H] i32 (padded to 256 B), and the bound tiles:
+    # [H][1024][520] i32, votes [H] i32 (padded to 256 B), and the bound tiles:
     # 1954 superblocks of 256 keys -> 31 windows of 64 -> 62 tiles per head of
     # (d/16 + 1) chunks of 64 x 16 B
-    key_order = (2 * 4 * 500_000 * 4 + 4 * 500_000 * 2 + 4 * 1024 * 34 * 4 + 4 * 1024 * 516 * 4
+    key_order = (2 * 4 * 500_000 * 4 + 4 * 500_000 * 2 + 4 * 1024 * 34 * 4 + 4 * 1024 * 520 * 4
                  + 256 + 4 * 62 * 2 * 64 * 16)
     assert n == packed + grouping + key_order
     assert lib.kmip_topk_workspace_size(8191, 1, 16, 4, 1) == (256 + 16) * 32 * 16 * 2 + 512
