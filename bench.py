@@ -9,7 +9,10 @@ region starts.
 Prints ONE JSON line on stdout.  Extra detail goes to stderr.
   value        whole-job node-queries per second (N / step time; every head)
   roofline     the score+select kernel against the bf16 MFMA peak, from HIP
-               events recorded around it on its own stream
+               events the library records around that kernel's launch on
+               the stream it runs on; the work counted is every (query,
+               key) pair of each graph (a dense scan), of which the kernel
+               executes the fraction its bounds cannot rule out
   cpu_baseline the float64 CPU oracle on a bounded sample of the same
                workload (not an optimisation target)
 """
@@ -51,16 +54,17 @@ def parse():
     return p.parse_args()
 
 
-def measured_traffic():
-    """Bytes per launch of the score+select kernel from profiles/select_traffic.json,
-    or None when there is none or the select sources changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", "select_traffic.json")
+def measured_counters():
+    """Counter figures of the score+select kernel from profiles/select_counters.json
+    (HBM bytes per launch, MFMA instructions per launch), or None when there
+    are none or the select sources changed since they were taken."""
+    path = os.path.join(ROOT, "profiles", "select_counters.json")
     if not os.path.exists(path):
         return None
     import rocprof_summary
     with open(path) as f:
         rec = json.load(f)
-    return rec["bytes_per_launch"] if rec.get("sources_sha256") == rocprof_summary.sources_hash() else None
+    return rec if rec.get("sources_sha256") == rocprof_summary.sources_hash() else None
 
 
 def cpu_baseline(w, sample):
@@ -135,7 +139,8 @@ def main():
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        kmip.topk(q, k, kk, graph_offsets=w.offsets, idx=idx, workspace=ws)
+        kmip.topk(q, k, kk, graph_offsets=w.offsets, idx=idx, workspace=ws,
+                  select_events=None if ev is None else (ev[4], ev[5]))
         if ev is not None:
             ev[1].record()
         kmip.attend(q, k, v, idx, w.scale, out=out, lse=lse)
@@ -159,7 +164,11 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # per step: topk start/end, attend end, backward end, select kernel start/end
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    for e in evs:
+        for x in e[4:]:
+            x.record()   # creates the events the library records around the select kernel
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
@@ -168,7 +177,8 @@ def main():
     t_total = time.perf_counter() - t0
     peak_mem = torch.cuda.max_memory_allocated(dev)
 
-    t_sel = [e[0].elapsed_time(e[1]) for e in evs]
+    t_topk = [e[0].elapsed_time(e[1]) for e in evs]
+    t_sel = [e[4].elapsed_time(e[5]) for e in evs]
     t_att = [e[1].elapsed_time(e[2]) for e in evs]
     t_bwd = [e[2].elapsed_time(e[3]) for e in evs]
     ms_step = 1e3 * t_total / args.steps
@@ -176,8 +186,14 @@ def main():
     pairs = w.score_pairs()
     flops = 2.0 * H * pairs * d
     tflops = flops / (sel_ms * 1e-3) / 1e12
-    log(f"[bench] per step: select {sel_ms:.3f} ms, attend {sum(t_att) / len(t_att):.3f} ms, "
-        f"backward {sum(t_bwd) / len(t_bwd):.3f} ms, wall {ms_step:.3f} ms")
+    # MFMA work the kernel actually executed (32x32x16 bf16 MFMAs counted by
+    # rocprofv3 on the same sources), when a counter run is on record
+    counters = measured_counters() if args.config == 4 and args.n is None else None
+    executed = counters["mfma_flop_per_launch"] if counters else None
+    topk_ms = sum(t_topk) / len(t_topk)
+    log(f"[bench] per step: topk {topk_ms:.3f} ms (select kernel {sel_ms:.3f} ms), "
+        f"attend {sum(t_att) / len(t_att):.3f} ms, backward {sum(t_bwd) / len(t_bwd):.3f} ms, "
+        f"wall {ms_step:.3f} ms")
     log(f"[bench] score rate {tflops:.1f} TFLOP/s = {100 * tflops / PEAK_BF16_TFLOPS:.1f}% of bf16 peak; "
         f"peak memory {peak_mem / 2**20:.1f} MiB ({peak_mem / N:.0f} B/node)")
 
@@ -209,15 +225,20 @@ def main():
         },
         "score_tflops": tflops,
         "score_pct_bf16_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
-        "kernel_ms": {"select": sel_ms, "attend": sum(t_att) / len(t_att),
+        "kernel_ms": {"topk": topk_ms, "select_kernel": sel_ms, "attend": sum(t_att) / len(t_att),
                       "backward": sum(t_bwd) / len(t_bwd) if backward else 0.0},
         "peak_mem_bytes": peak_mem,
         "roofline": {
             "bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": tflops / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),
-            "kernel": ("select_kernel (score+select); timed as the whole kmip_topk call, which also "
-                       "runs the query-grouping and key-tiling pre-passes"),
-            "algorithmic": f"2*H*sum(n_g^2)*d = {flops:.4g} FLOP per launch",
+            "frac": tflops / PEAK_BF16_TFLOPS,
+            "traffic": counters["bytes_per_launch"] if counters else None,
+            "kernel": ("select_kernel (score+select) alone, between events recorded around its "
+                       "launch; the kmip_topk call also runs the query-grouping, key-tree and "
+                       "key-tiling pre-passes (kernel_ms.topk)"),
+            "algorithmic": (f"2*H*sum(n_g^2)*d = {flops:.4g} FLOP per launch: every (query, key) "
+                            "pair of each graph, the work of a dense scan"),
+            "executed_mfma_flop": executed,
+            "executed_frac": None if executed is None else executed / flops,
         },
         "cpu_baseline": cpu,
     }

@@ -84,6 +84,19 @@ kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offse
                         void* stream);
 
 /*
+ * kmip_topk, recording two events around the score+select kernel alone (not
+ * the pre-passes that group the queries and order the keys), for callers
+ * that time that kernel.
+ *   select_start, select_stop: hipEvent_t handles created by the caller, or
+ *   NULL to record nothing; recorded on `stream` right before and right after
+ *   the kernel's launch.  On an error return neither is recorded.
+ */
+kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t* graph_offsets,
+                                    int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
+                                    int32_t* topk_idx, void* workspace, size_t workspace_bytes,
+                                    void* stream, void* select_start, void* select_stop);
+
+/*
  * Gather-softmax-aggregate (Algorithm 1: GatherRows, softmax over the k kept
  * scores divided by sqrt(d_K) -- here times `scale` -- and the einsum
  * nk,nkv->nv).  Recomputes the k kept scores in fp32 from Q and the gathered

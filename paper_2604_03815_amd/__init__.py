@@ -79,8 +79,12 @@ def _shape(q):
 
 
 def topk(q, k_, kk: int, graph_offsets: Optional[Sequence[int]] = None, idx=None,
-         workspace: Optional[Workspace] = None):
-    """Score + select: returns topk_idx int32 [N, H, kk]."""
+         workspace: Optional[Workspace] = None, select_events=None):
+    """Score + select: returns topk_idx int32 [N, H, kk].
+
+    select_events: optional pair of torch.cuda.Event, recorded on the current
+    stream right before and after the score+select kernel (not the pre-passes).
+    """
     torch = _torch()
     N, H, d = _shape(q)
     if idx is None:
@@ -89,9 +93,18 @@ def topk(q, k_, kk: int, graph_offsets: Optional[Sequence[int]] = None, idx=None
     ws = workspace or Workspace(q.device)
     nbytes = topk_workspace_size(N, H, d, kk, G)
     buf = ws.get(nbytes)
-    check(load().kmip_topk(_dev(q, torch.bfloat16, "Q"), _dev(k_, torch.bfloat16, "K"), optr, G,
-                           N, H, d, kk, _dev(idx, torch.int32, "topk_idx"),
-                           ctypes.c_void_p(buf.data_ptr()), buf.numel(), _stream_ptr()))
+    args = (_dev(q, torch.bfloat16, "Q"), _dev(k_, torch.bfloat16, "K"), optr, G, N, H, d, kk,
+            _dev(idx, torch.int32, "topk_idx"), ctypes.c_void_p(buf.data_ptr()), buf.numel(),
+            _stream_ptr())
+    if select_events is None:
+        check(load().kmip_topk(*args))
+    else:
+        handles = []
+        for ev in select_events:
+            if not ev.cuda_event:
+                ev.record()   # the event object exists only once recorded
+            handles.append(ctypes.c_void_p(ev.cuda_event))
+        check(load().kmip_topk_with_events(*args, *handles))
     return idx
 
 

@@ -16,7 +16,7 @@ MAX_K = 128
 
 # Every symbol declared in include/kmip.h.
 EXPORTS = (
-    "kmip_topk_workspace_size", "kmip_topk", "kmip_attend", "kmip_fwd_workspace_size",
+    "kmip_topk_workspace_size", "kmip_topk", "kmip_topk_with_events", "kmip_attend", "kmip_fwd_workspace_size",
     "kmip_fwd", "kmip_bwd_workspace_size", "kmip_bwd", "kmip_status_string",
     "kmip_last_error",
 )
@@ -49,10 +49,11 @@ def load(path: str = LIB_PATH):
     lib.kmip_bwd_workspace_size.argtypes = [i64, i32, i32, i32, i32]
     lib.kmip_bwd_workspace_size.restype = sz
     lib.kmip_topk.argtypes = [P, P, P, i32, i64, i32, i32, i32, P, P, sz, P]
+    lib.kmip_topk_with_events.argtypes = [P, P, P, i32, i64, i32, i32, i32, P, P, sz, P, P, P]
     lib.kmip_attend.argtypes = [P, P, P, i64, i32, i32, i32, f32, P, P, P, P]
     lib.kmip_fwd.argtypes = [P, P, P, P, i32, i64, i32, i32, i32, f32, P, P, P, P, sz, P]
     lib.kmip_bwd.argtypes = [P, P, P, P, P, P, i64, i32, i32, i32, f32, P, P, P, i32, P, sz, P]
-    for f in ("kmip_topk", "kmip_attend", "kmip_fwd", "kmip_bwd"):
+    for f in ("kmip_topk", "kmip_topk_with_events", "kmip_attend", "kmip_fwd", "kmip_bwd"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kmip_status_string.argtypes = [ctypes.c_int]
     lib.kmip_status_string.restype = ctypes.c_char_p

@@ -131,7 +131,15 @@ size_t kmip_fwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32
 kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offsets,
                         int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
                         int32_t* topk_idx, void* workspace, size_t workspace_bytes,
-                        void* stream_) {
+                        void* stream) {
+    return kmip_topk_with_events(Q, K, graph_offsets, num_graphs, N, H, d, k, topk_idx, workspace,
+                                 workspace_bytes, stream, nullptr, nullptr);
+}
+
+kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t* graph_offsets,
+                                    int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
+                                    int32_t* topk_idx, void* workspace, size_t workspace_bytes,
+                                    void* stream_, void* select_start, void* select_stop) {
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
     if ((s = check_offsets(graph_offsets, num_graphs, N)) != KMIP_OK) return s;
@@ -196,7 +204,9 @@ kmip_status_t kmip_topk(const void* Q, const void* K, const int32_t* graph_offse
     if (e != hipSuccess) return hip_fail(e, "pack_k launch");
     int32_t* work_ctr = reinterpret_cast<int32_t*>(ws + tiled_bytes(N, H, d));
     e = kmip::launch_select(kp, Q, K, dtasks, grouped ? &groups : nullptr, grouped ? &keys : nullptr,
-                            ntasks, n32, H, d, k, ntiles, shape, work_ctr, topk_idx, stream);
+                            ntasks, n32, H, d, k, ntiles, shape, work_ctr, topk_idx, stream,
+                            reinterpret_cast<hipEvent_t>(select_start),
+                            reinterpret_cast<hipEvent_t>(select_stop));
     if (e != hipSuccess) return hip_fail(e, "select launch");
     return ok();
 }

@@ -88,11 +88,13 @@ struct QueryGroups {
 // grouping of the queries.  keys: NULL (every tile scanned), or the stored
 // key order kp was packed in, with its bounds.  K: the keys in their own
 // layout (seed rows are gathered from it).  work_ctr: kSelectCounterBytes of device scratch, 8-byte aligned
-// (per-XCD item counters and stream pacers, zeroed here).
+// (per-XCD item counters and stream pacers, zeroed here).  ev_start /
+// ev_stop: events recorded right before and after the kernel, or NULL.
 hipError_t launch_select(const void* kp, const void* Q, const void* K, const Task* tasks,
                          const QueryGroups* groups, const KeyOrder* keys, int32_t ntasks, int32_t N,
                          int32_t H, int32_t d, int32_t k, int32_t ntiles, SelectShape shape,
-                         int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream);
+                         int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream,
+                         hipEvent_t ev_start, hipEvent_t ev_stop);
 
 // Bytes of LDS one select workgroup uses.
 size_t select_lds_bytes(int32_t k, SelectShape shape);

@@ -850,7 +850,7 @@ template <int D, int QB, int SLOTS>
 hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const Task* tasks,
                            const QueryGroups* groups, const KeyOrder* keys, int32_t ntasks, int32_t N,
                            int32_t H, int32_t k, int32_t ntiles, int32_t* work_ctr, int32_t* topk_idx,
-                           hipStream_t stream) {
+                           hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
     const int64_t items = (int64_t)ntasks * H;
     const size_t lds = select_lds_bytes(k, SelectShape{QB, SLOTS});
     // One resident wave per workgroup slot of the chip, a multiple of the XCD
@@ -875,6 +875,7 @@ hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const T
     const int64_t slots = (int64_t)std::max(cus, 1) * std::max(per_cu, 1);
     const int64_t want = std::min<int64_t>(slots, (items + kNumXcd - 1) / kNumXcd * kNumXcd);
     const int64_t grid = std::max<int64_t>(kNumXcd, want / kNumXcd * kNumXcd);
+    if (ev_start != nullptr && (e = hipEventRecord(ev_start, stream)) != hipSuccess) return e;
     hipLaunchKernelGGL((select_kernel<D, QB, SLOTS>), dim3((unsigned)grid), dim3(64), lds, stream,
                        reinterpret_cast<const uint4*>(kp), reinterpret_cast<const uint16_t*>(Q),
                        reinterpret_cast<const uint16_t*>(K), tasks, groups ? groups->perm : nullptr,
@@ -882,7 +883,9 @@ hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const T
                        keys ? keys->perm : nullptr, keys ? keys->bounds : nullptr,
                        keys ? keys->votes : nullptr, keys ? keys->ctiles : 0, ntasks, N, H, k, ntiles,
                        work_ctr, pacers, topk_idx);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (ev_stop != nullptr) return hipEventRecord(ev_stop, stream);
+    return hipSuccess;
 }
 
 }  // namespace
@@ -906,12 +909,13 @@ hipError_t launch_pack_k(const void* K, const int32_t* perm, void* kp, int32_t N
 hipError_t launch_select(const void* kp, const void* Q, const void* K, const Task* tasks,
                          const QueryGroups* groups, const KeyOrder* keys, int32_t ntasks, int32_t N,
                          int32_t H, int32_t d, int32_t k, int32_t ntiles, SelectShape shape,
-                         int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream) {
+                         int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream,
+                         hipEvent_t ev_start, hipEvent_t ev_stop) {
     if (ntasks <= 0) return hipSuccess;
 #define KMIP_SELECT_CASE(DD, QQ, SS)                                                             \
     if (d == DD && shape.qb == QQ && shape.slots == SS)                                          \
         return launch_select_t<DD, QQ, SS>(kp, Q, K, tasks, groups, keys, ntasks, N, H, k, ntiles, \
-                                           work_ctr, topk_idx, stream);
+                                           work_ctr, topk_idx, stream, ev_start, ev_stop);
 #define KMIP_SELECT_D(DD)         \
     KMIP_SELECT_CASE(DD, 2, 4)    \
     KMIP_SELECT_CASE(DD, 1, 8)

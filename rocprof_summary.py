@@ -4,14 +4,15 @@
       per-kernel durations (count, avg/min/max ms, share of GPU time) from a
       --kernel-trace run.
 
-  python rocprof_summary.py traffic <fetch.db> <write.db> <copy_bytes> <command...>
+  python rocprof_summary.py counters <fetch.db> <write.db> <mfma.db> <copy_bytes> <command...>
       HBM traffic of the score+select kernel from a FETCH_SIZE run and a
       WRITE_SIZE run (both in KiB per dispatch), each scaled by what the same
       counter reads for the calibration copy kernel (bench.py --calib-copy),
-      which reads and writes copy_bytes.  Writes profiles/select_traffic.json
-      (with a hash of the sources the counters were taken on; bench.py only
-      reports the figure while the sources are unchanged) and prints a
-      markdown summary.
+      which reads and writes copy_bytes; and the MFMA work it executed, from
+      an SQ_INSTS_MFMA run (every MFMA of the kernel is a 32x32x16 bf16 one,
+      32768 FLOP).  Writes profiles/select_counters.json (with a hash of the
+      sources the counters were taken on; bench.py only reports the figures
+      while the sources are unchanged) and prints a markdown summary.
 
 Reads the SQLite databases rocprofv3 writes by default.
 """
@@ -24,11 +25,12 @@ import sqlite3
 import sys
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-TRAFFIC_JSON = os.path.join(ROOT, "profiles", "select_traffic.json")
-# sources whose change invalidates a measured traffic figure
+COUNTERS_JSON = os.path.join(ROOT, "profiles", "select_counters.json")
+# sources whose change invalidates a measured counter figure
 SELECT_SOURCES = ["paper_2604_03815_amd/csrc/select.hip", "paper_2604_03815_amd/csrc/group.hip",
-                  "paper_2604_03815_amd/csrc/api.hip", "paper_2604_03815_amd/csrc/kmip_device.h",
-                  "paper_2604_03815_amd/csrc/kmip_internal.h"]
+                  "paper_2604_03815_amd/csrc/keyorder.hip", "paper_2604_03815_amd/csrc/api.hip",
+                  "paper_2604_03815_amd/csrc/kmip_device.h", "paper_2604_03815_amd/csrc/kmip_internal.h"]
+MFMA_FLOP = 32 * 32 * 16 * 2
 
 
 def sources_hash() -> str:
@@ -80,9 +82,10 @@ def counter_per_dispatch(db: str, counter: str):
     return {k: sum(v) / len(v) for k, v in acc.items()}
 
 
-def traffic(fetch_db: str, write_db: str, copy_bytes: int, command: str) -> None:
+def counters(fetch_db: str, write_db: str, mfma_db: str, copy_bytes: int, command: str) -> None:
     fetch = counter_per_dispatch(fetch_db, "FETCH_SIZE")
     write = counter_per_dispatch(write_db, "WRITE_SIZE")
+    mfma = counter_per_dispatch(mfma_db, "SQ_INSTS_MFMA")
     copy = [k for k in fetch if "elementwise" in k.lower()]
     sel = [k for k in fetch if k.startswith("select_kernel")]
     if not copy or not sel:
@@ -97,25 +100,28 @@ def traffic(fetch_db: str, write_db: str, copy_bytes: int, command: str) -> None
         "bytes_per_launch": fetch_b + write_b, "fetch_kib_raw": fetch[sk], "write_kib_raw": write[sk],
         "copy_kernel": ck, "copy_bytes": copy_bytes, "copy_fetch_kib": fetch[ck],
         "copy_write_kib": write[ck], "fetch_scale": f_scale, "write_scale": w_scale,
+        "mfma_instructions_per_launch": mfma[sk], "mfma_flop_per_launch": mfma[sk] * MFMA_FLOP,
         "command": command,
     }
-    with open(TRAFFIC_JSON, "w") as f:
+    with open(COUNTERS_JSON, "w") as f:
         json.dump(res, f, indent=1)
         f.write("\n")
-    print(f"# HBM traffic of `{sk}`\n")
-    print(f"Commands: `{command}`, once with `--pmc FETCH_SIZE` and once with `--pmc WRITE_SIZE`.\n")
-    print("| counter | select_kernel KiB/dispatch | copy kernel KiB | copy bytes | scale | select bytes |")
+    print(f"# HBM traffic and MFMA work of `{sk}`\n")
+    print(f"Command: `{command}`, once each with `--pmc FETCH_SIZE`, `--pmc WRITE_SIZE` and "
+          f"`--pmc SQ_INSTS_MFMA`.\n")
+    print("| counter | select_kernel per dispatch | copy kernel | copy bytes | scale | select |")
     print("|---|---|---|---|---|---|")
-    print(f"| FETCH_SIZE | {fetch[sk]:.4g} | {fetch[ck]:.4g} | {copy_bytes} | {f_scale:.4f} | {fetch_b:.4g} |")
-    print(f"| WRITE_SIZE | {write[sk]:.4g} | {write[ck]:.4g} | {copy_bytes} | {w_scale:.4f} | {write_b:.4g} |")
-    print(f"\nTotal {fetch_b + write_b:.4g} bytes per launch.")
+    print(f"| FETCH_SIZE (KiB) | {fetch[sk]:.4g} | {fetch[ck]:.4g} | {copy_bytes} | {f_scale:.4f} | {fetch_b:.4g} B |")
+    print(f"| WRITE_SIZE (KiB) | {write[sk]:.4g} | {write[ck]:.4g} | {copy_bytes} | {w_scale:.4f} | {write_b:.4g} B |")
+    print(f"| SQ_INSTS_MFMA | {mfma[sk]:.4g} | | | {MFMA_FLOP} FLOP each | {mfma[sk] * MFMA_FLOP:.4g} FLOP |")
+    print(f"\nTotal {fetch_b + write_b:.4g} HBM bytes and {mfma[sk] * MFMA_FLOP:.4g} MFMA FLOP per launch.")
 
 
 def main(argv):
     if len(argv) >= 4 and argv[1] == "stats":
         stats(argv[2], argv[3], " ".join(argv[4:]))
-    elif len(argv) >= 5 and argv[1] == "traffic":
-        traffic(argv[2], argv[3], int(argv[4]), " ".join(argv[5:]))
+    elif len(argv) >= 6 and argv[1] == "counters":
+        counters(argv[2], argv[3], argv[4], int(argv[5]), " ".join(argv[6:]))
     else:
         raise SystemExit(__doc__)
 
