@@ -200,32 +200,46 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     // tiles.  Taking items from a counter balances items of unequal cost and
     // keeps a workgroup that only becomes resident late (when the grid
     // exceeds what fits) from delaying the items it would otherwise own.
-    // With grouped queries the counter walks the range with a stride
-    // coprime to its length, so that the first items to run cover all
-    // direction groups and can seed the items that follow (see below).
+    // A wave whose XCD's range is used up goes on with the next XCD's
+    // counter, and so on round the XCDs: ranges differ in cost (heads and
+    // direction groups prune differently), and without this the XCDs with
+    // cheap ranges would sit idle at the end.
+    // With grouped queries the counter walks a range with a stride coprime
+    // to its length, so that the first items to run cover all direction
+    // groups and can seed the items that follow (see below).
     const int items = ntasks * H;
     const int xcd = blockIdx.x % kNumXcd;
     const int items_per_xcd = (items + kNumXcd - 1) / kNumXcd;
-    const int item_lo = xcd * items_per_xcd;
-    const int range = min(items, item_lo + items_per_xcd) - item_lo;
-    int stride = 1;
-    if (qlabel != nullptr && range > 1) {
-        stride = max(1, range / max(1, (int)gridDim.x / kNumXcd));
-        for (;; ++stride) {
-            int a = stride, b = range;
-            while (b != 0) {
-                const int r = a % b;
-                a = b;
-                b = r;
+    int vx = xcd, visited = 0;
+    int item_lo = 0, range = 0, stride = 1;
+    auto xcd_range = [&](int x) {
+        item_lo = min(items, x * items_per_xcd);
+        range = min(items, item_lo + items_per_xcd) - item_lo;
+        stride = 1;
+        if (qlabel != nullptr && range > 1) {
+            stride = max(1, range / max(1, (int)gridDim.x / kNumXcd));
+            for (;; ++stride) {
+                int a = stride, b = range;
+                while (b != 0) {
+                    const int r = a % b;
+                    a = b;
+                    b = r;
+                }
+                if (a == 1) break;
             }
-            if (a == 1) break;
         }
-    }
+    };
+    xcd_range(vx);
     for (;;) {
     int claim = 0;
-    if (threadIdx.x == 0) claim = atomicAdd(&work_ctr[xcd], 1);
+    if (threadIdx.x == 0) claim = atomicAdd(&work_ctr[vx], 1);
     claim = __builtin_amdgcn_readfirstlane(claim);
-    if (claim >= range) break;
+    if (claim >= range) {
+        if (++visited == kNumXcd) break;
+        vx = vx + 1 == kNumXcd ? 0 : vx + 1;
+        xcd_range(vx);
+        continue;
+    }
     const int item = item_lo + (int)(((int64_t)claim * stride) % range);
     const int head = item / ntasks;
     const int task = item - head * ntasks;
@@ -296,16 +310,25 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     // passes the filter.  Scores come from the same MFMA on the same
     // operands as in the stream, hence are the same values.  The heap starts
     // empty and fills with keys that pass; theta only ever rises.
+    // A block tries the seeds of the labels of its first and of its last
+    // query (a block can straddle two labels) and keeps, per query, the
+    // larger threshold: each is a valid lower bound of its k-th best.
     if (qlabel != nullptr) {
 #pragma unroll
         for (int b = 0; b < QB; ++b) {
             if (32 * b >= q_count) continue;
+            const int last = min(31, q_count - 1 - 32 * b);
+            int labs[2] = {0, 0};
+            if (lane == 0) labs[0] = qlabel[(size_t)head * N + qid[b]];
+            if (lane == last) labs[1] = qlabel[(size_t)head * N + qid[b]];
+            labs[0] = __builtin_amdgcn_readfirstlane(labs[0]);
+            labs[1] = __builtin_amdgcn_readlane(labs[1], last);
+            for (int si = 0; si < 2; ++si) {
+            if (si == 1 && labs[1] == labs[0]) break;
             int ref = 0;
-            if (lane == 0) {
-                const int lab = qlabel[(size_t)head * N + qid[b]];
-                ref = __hip_atomic_load(&seed_ref[(size_t)head * kGroupCenters + lab], __ATOMIC_ACQUIRE,
+            if (lane == 0)
+                ref = __hip_atomic_load(&seed_ref[(size_t)head * kGroupCenters + labs[si]], __ATOMIC_ACQUIRE,
                                         __HIP_MEMORY_SCOPE_AGENT);
-            }
             ref = __builtin_amdgcn_readfirstlane(ref);
             if (ref <= 0 || ref > N) continue;
             const int32_t* srow = topk_idx + ((size_t)(ref - 1) * H + head) * k;
@@ -327,7 +350,8 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
             }
             low = fminf(low, __shfl_xor(low, 32));
             if (__builtin_amdgcn_ballot_w64(!ok) != 0ull) continue;
-            if (theta[b] != INFINITY) theta[b] = float_below(low);
+            if (theta[b] != INFINITY) theta[b] = fmaxf(theta[b], float_below(low));
+            }
         }
     }
 
@@ -575,8 +599,11 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         bool seeded = true;
 #pragma unroll
         for (int b = 0; b < QB; ++b) seeded = seeded && __builtin_amdgcn_ballot_w64(theta[b] == -INFINITY) == 0ull;
-        const bool warm = !seeded && nwin <= 64;
-        const int needed = compute_batch(0, warm);
+        const int needed = compute_batch(0, nwin <= 64);
+        // Seeded items whose masks still keep more than half of the
+        // superblocks warm up as well: a poorly seeded query widens the
+        // masks of its whole wave.
+        const bool warm = nwin <= 64 && (!seeded || 2 * needed > nsb);
         if (warm) {
             // Masks of the union of the best superblocks, one window per lane.
             uint64_t mv = 0;
@@ -596,9 +623,8 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
             warm_pending = true;
         } else if (!seeded) {
             stop_at = 16;
-        } else if (lane == 0) {
-            atomicAdd(&votes[head], needed * 4 > min(nsb, 64 * 64) * 3 ? 1 : -1);
         }
+        if (seeded && lane == 0) atomicAdd(&votes[head], needed * 4 > min(nsb, 64 * 64) * 3 ? 1 : -1);
         wm = read_mask(0);
     } else {
         stride_sb = max(1, (int)((float)nsb * 0.381966f));
