@@ -23,6 +23,8 @@
 #include "kmip_device.h"
 #include "kmip_internal.h"
 
+#include <algorithm>
+
 namespace kmip {
 namespace {
 
@@ -304,7 +306,379 @@ __global__ __launch_bounds__(256) void csr_reduce_kernel(
     flush();
 }
 
+// ---- Variant 4: pairs bucketed by blocks of key rows, sorted in LDS ----
+//
+// The key rows are cut into buckets of RB = 4096 / d consecutive rows, at
+// most kMaxBuckets of them.  The pairs are counting-sorted by bucket only: a
+// workgroup takes a range of consecutive pairs and counts or places them
+// with an LDS histogram over the buckets, one global atomic per bucket it
+// touches (against one per key row and workgroup for the full sort, whose
+// per-row tables overflow when pairs spread over many keys).  Each bucket's
+// records are then cut into pieces that one workgroup sorts by key row in
+// LDS and reduces like the full sort's reduction.
+constexpr int kMaxBuckets = 8192;
+
+__host__ __device__ __forceinline__ int bucket_rows(int d) { return 4096 / d; }
+__host__ __device__ __forceinline__ int bucket_shift(int d) { return d == 16 ? 8 : (d == 32 ? 7 : 6); }
+
+// Takes one slot of LDS counter ctr[bk] for each lane with bk >= 0 and
+// returns its number (kReturn) or nothing.  Lanes of a wave that share a bucket are served
+// by one atomic while the group the wave's first pending lane belongs to
+// holds at least 8 lanes (a bucket most pairs fall in: one atomic per wave
+// instead of one per lane); the rest take one atomic each.
+template <bool kReturn>
+__device__ __forceinline__ int32_t claim_slot(int32_t* ctr, int32_t bk) {
+    const int lane = threadIdx.x & 63;
+    bool pending = bk >= 0;
+    int32_t slot = 0;
+    for (int it = 0; it < 4; ++it) {
+        const uint64_t act = __ballot(pending);
+        if (act == 0) break;
+        int32_t grp = 0;
+        if (pending) {
+            const int32_t b0 = __builtin_amdgcn_readfirstlane(bk);
+            const uint64_t eq = __ballot(bk == b0);
+            grp = __popcll(eq);
+            if (grp >= 8) {
+                const int leader = __ffsll((unsigned long long)eq) - 1;
+                int32_t base0 = 0;
+                if (lane == leader) base0 = atomicAdd(&ctr[b0], grp);
+                if (kReturn) base0 = __shfl(base0, leader, 64);
+                if (bk == b0) {
+                    slot = base0 + (int32_t)__popcll(eq & ((1ull << lane) - 1ull));
+                    pending = false;
+                }
+            }
+        }
+        // this round's group size, as seen by its first lane
+        if (__builtin_amdgcn_readlane(grp, __ffsll((unsigned long long)act) - 1) < 8) break;
+    }
+    if (pending) slot = atomicAdd(&ctr[bk], 1);
+    return slot;
+}
+
+// Counting (kPlace false) and placing (true) pass over a range of `per`
+// consecutive pairs (pair e = query-head e / k, slot e % k, so that lanes
+// read idx and the coefficients contiguously): the workgroup counts its
+// pairs per bucket in LDS, adds the counts to the global ones (count) or
+// reserves a range of each bucket's positions with one atomic (place) and
+// writes each pair's record at the next position of its range.
+template <bool kPlace>
+__global__ __launch_bounds__(256) void bkt_count_kernel(const int32_t* __restrict__ idx,
+                                                        const float2* __restrict__ coef, int32_t N,
+                                                        int32_t H, int32_t k, int32_t shift, int32_t nbk,
+                                                        uint32_t per, int32_t* __restrict__ gcnt,
+                                                        PairRecord* __restrict__ rec) {
+    __shared__ int32_t hist[kMaxBuckets];
+    __shared__ int32_t base[kPlace ? kMaxBuckets : 1];
+    const int t = threadIdx.x;
+    const uint32_t P = (uint32_t)N * (uint32_t)H * (uint32_t)k;
+    const uint32_t p0 = blockIdx.x * per;
+    const uint32_t p1 = min(P, p0 + per);
+    auto row_of = [&](uint32_t e) -> int32_t {
+        if (e >= p1) return -1;
+        const int32_t j = idx[e];
+        const uint32_t qh = e / (uint32_t)k;
+        return (j >= 0 && j < N) ? j * H + (int32_t)(qh % (uint32_t)H) : -1;
+    };
+    for (int e = t; e < nbk; e += 256) hist[e] = 0;
+    __syncthreads();
+    // every lane runs the same number of rounds (wave-wide claims); four
+    // pairs' loads are issued before their claims
+    for (uint32_t pb = p0; pb < p1; pb += 1024) {
+        int32_t r[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) r[u] = row_of(pb + 256 * u + t);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) claim_slot<false>(hist, r[u] >= 0 ? r[u] >> shift : -1);
+    }
+    __syncthreads();
+    for (int e = t; e < nbk; e += 256) {
+        const int32_t c = hist[e];
+        if (c == 0) continue;
+        if (kPlace)
+            base[e] = atomicAdd(&gcnt[e], c);
+        else
+            atomicAdd(&gcnt[e], c);
+    }
+    if constexpr (kPlace) {
+        __syncthreads();
+        for (int e = t; e < nbk; e += 256) hist[e] = 0;
+        __syncthreads();
+        for (uint32_t pb = p0; pb < p1; pb += 1024) {
+            int32_t r[4];
+            float2 c[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t e = pb + 256 * u + t;
+                r[u] = row_of(e);
+                c[u] = e < p1 ? coef[e] : make_float2(0.0f, 0.0f);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t e = pb + 256 * u + t;
+                const int32_t bk = r[u] >= 0 ? r[u] >> shift : -1;
+                const int32_t slot = claim_slot<true>(hist, bk);
+                if (bk >= 0) rec[base[bk] + slot] = PairRecord{r[u], (int32_t)(e / (uint32_t)k), c[u].x, c[u].y};
+            }
+        }
+    }
+}
+
+constexpr int kPiece = 8192;   // records per reduction workgroup (fits a uint16 order)
+
+// After the scan: the start of each bucket's records (kept; the place pass
+// moves the cursors) and its number of pieces of at most kPiece records.
+__global__ __launch_bounds__(256) void bkt_pieces_kernel(const int32_t* __restrict__ start, int32_t nbk,
+                                                         int32_t* __restrict__ sstart,
+                                                         int32_t* __restrict__ npieces) {
+    const int b = blockIdx.x * 256 + threadIdx.x;
+    if (b > nbk) return;
+    sstart[b] = start[b];
+    if (b < nbk) npieces[b] = (start[b + 1] - start[b] + kPiece - 1) / kPiece;
+    else npieces[b] = 0;
+}
+
+// One workgroup per piece (a stretch of at most kPiece records of one
+// bucket, found by binary search in the scanned piece counts):
+//   1. counting sort of the piece's records by key row in LDS (claim_slot:
+//      a key most pairs share costs about one LDS atomic per wave);
+//   2. sixteen teams of 16 lanes walk contiguous stretches of the sorted
+//      order, dimensions on lanes, keep the sums of the current key row in
+//      registers and add them to dK and dV (zero at the start) with one
+//      atomic per dimension where the row changes or the stretch ends; a
+//      team loads the query rows of several pairs before adding them up.
+template <int D>
+__global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restrict__ Q,
+                                                         const uint16_t* __restrict__ dO,
+                                                         const PairRecord* __restrict__ rec,
+                                                         const int32_t* __restrict__ sstart,
+                                                         const int32_t* __restrict__ pstart, int32_t nbk,
+                                                         float* __restrict__ dK, float* __restrict__ dV) {
+    constexpr int RB = 4096 / D;
+    constexpr int U = D / 16;           // dims per lane of a team, for each of dK and dV
+    constexpr int G = 8 / U;            // pairs whose rows a team loads at once
+    __shared__ uint16_t ord[kPiece];
+    __shared__ uint8_t lrow[kPiece];
+    __shared__ int32_t cursor[RB];
+    __shared__ int32_t sh[256];
+    const int t = threadIdx.x;
+    const int w = blockIdx.x;
+    if (w >= pstart[nbk]) return;
+    // bucket b with pstart[b] <= w < pstart[b + 1]
+    int lo = 0, hi = nbk;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (pstart[mid] <= w) lo = mid; else hi = mid;
+    }
+    const int32_t e0 = sstart[lo] + (w - pstart[lo]) * kPiece;
+    const int32_t n = min(sstart[lo + 1] - e0, kPiece);
+    if (t < RB) cursor[t] = 0;
+    __syncthreads();
+
+    // 1a. records per key row; the rows (local to the bucket) are kept in LDS
+    for (int base = 0; base < n; base += 1024) {
+        int32_t row[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = base + 256 * u + t;
+            row[u] = i < n ? (rec[e0 + i].row & (RB - 1)) : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = base + 256 * u + t;
+            if (row[u] >= 0) lrow[i] = (uint8_t)row[u];
+            claim_slot<false>(cursor, row[u]);
+        }
+    }
+    __syncthreads();
+    // 1b. exclusive scan of the counts: the cursors
+    const int32_t c = t < RB ? cursor[t] : 0;
+    sh[t] = c;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        const int32_t add = t >= off ? sh[t - off] : 0;
+        __syncthreads();
+        sh[t] += add;
+        __syncthreads();
+    }
+    if (t < RB) cursor[t] = sh[t] - c;
+    __syncthreads();
+    // 1c. place the record numbers in key-row order
+    for (int base = 0; base < n; base += 256) {
+        const int i = base + t;
+        const int32_t row = i < n ? (int32_t)lrow[i] : -1;
+        const int32_t slot = claim_slot<true>(cursor, row);
+        if (row >= 0) ord[slot] = (uint16_t)i;
+    }
+    __syncthreads();
+
+    // 2. teams walk the sorted order
+    const int tl = t & 15;
+    const int team = t >> 4;
+    const int span = (n + 15) / 16;
+    const int p0 = min(n, team * span), p1 = min(n, p0 + span);
+    int32_t cur = -1;
+    float ak[U], av[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ak[u] = av[u] = 0.0f;
+    auto flush = [&]() {
+        if (cur >= 0) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                atomicAdd(dK + (size_t)cur * D + 16 * u + tl, ak[u]);
+                atomicAdd(dV + (size_t)cur * D + 16 * u + tl, av[u]);
+                ak[u] = av[u] = 0.0f;
+            }
+        }
+    };
+    PairRecord next{-1, 0, 0.0f, 0.0f};
+    if (p0 + tl < p1) next = rec[e0 + ord[p0 + tl]];
+    for (int pb = p0; pb < p1; pb += 16) {
+        const PairRecord r = next;   // this batch's records; the next batch's are fetched now
+        next = PairRecord{-1, 0, 0.0f, 0.0f};
+        if (pb + 16 + tl < p1) next = rec[e0 + ord[pb + 16 + tl]];
+        const int m = min(16, p1 - pb);
+        for (int s0 = 0; s0 < m; s0 += G) {
+            int32_t rt[G];
+            float at[G], pt[G], qv[G][U], ov[G][U];
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                rt[g] = __shfl(r.row, s0 + g, 16);
+                const int32_t qt = __shfl(r.qh, s0 + g, 16);
+                at[g] = __shfl(r.a, s0 + g, 16);
+                pt[g] = __shfl(r.p, s0 + g, 16);
+                const size_t qrow = (size_t)qt * D + tl;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    qv[g][u] = s0 + g < m ? bf16_bits_to_f32(Q[qrow + 16 * u]) : 0.0f;
+                    ov[g][u] = s0 + g < m ? bf16_bits_to_f32(dO[qrow + 16 * u]) : 0.0f;
+                }
+            }
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                if (s0 + g >= m) break;
+                if (rt[g] != cur) {
+                    flush();
+                    cur = rt[g];
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    ak[u] = fmaf(at[g], qv[g][u], ak[u]);
+                    av[u] = fmaf(pt[g], ov[g][u], av[u]);
+                }
+            }
+        }
+    }
+    flush();
+}
+
 }  // namespace
+
+bool bwd_bucket_supported(int32_t N, int32_t H, int32_t d) {
+    const int64_t nbk = ((int64_t)N * H + bucket_rows(d) - 1) / bucket_rows(d);
+    return nbk <= kMaxBuckets;
+}
+
+size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    const size_t nh = (size_t)N * H, pairs = nh * k;
+    const size_t nbk = (nh + bucket_rows(d) - 1) / bucket_rows(d);
+    const size_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
+    return al(pairs * sizeof(float2)) + al(pairs * sizeof(PairRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
+           al((nb + 1) * sizeof(int32_t));
+}
+
+hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const void* dO,
+                             const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
+                             int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
+                             hipStream_t stream) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    const int64_t nh = (int64_t)N * H;
+    if (nh == 0) return hipSuccess;
+    const size_t pairs = (size_t)nh * k;
+    const int32_t rb = bucket_rows(d);
+    const int32_t nbk = (int32_t)((nh + rb - 1) / rb);
+    if (nbk > kMaxBuckets) return hipErrorInvalidValue;
+    const int32_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
+    char* p = reinterpret_cast<char*>(ws);
+    float2* coef = reinterpret_cast<float2*>(p);
+    p += al(pairs * sizeof(float2));
+    PairRecord* rec = reinterpret_cast<PairRecord*>(p);
+    p += al(pairs * sizeof(PairRecord));
+    int32_t* gcnt = reinterpret_cast<int32_t*>(p);   // counts, then starts (nbk + 1 entries)
+    p += al(((size_t)nbk + 1) * sizeof(int32_t));
+    int32_t* sstart = reinterpret_cast<int32_t*>(p);   // kept starts
+    p += al(((size_t)nbk + 1) * sizeof(int32_t));
+    int32_t* pstart = reinterpret_cast<int32_t*>(p);   // pieces per bucket, then their starts
+    p += al(((size_t)nbk + 1) * sizeof(int32_t));
+    int32_t* sums = reinterpret_cast<int32_t*>(p);
+
+    const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
+    const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
+    const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
+    const uint16_t* g = reinterpret_cast<const uint16_t*>(dO);
+    hipError_t e;
+    if ((e = launch_fill_zero(reinterpret_cast<float*>(gcnt), ((size_t)nbk + 1 + 3) / 4 * 4, stream)) != hipSuccess)
+        return e;
+    if ((e = launch_fill_zero(dK, (size_t)nh * d, stream)) != hipSuccess) return e;
+    if ((e = launch_fill_zero(dV, (size_t)nh * d, stream)) != hipSuccess) return e;
+    const unsigned team_blocks = (unsigned)((nh + 15) / 16);
+    if (d == 16)
+        hipLaunchKernelGGL(csr_coef_kernel<16>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                           N, H, k, scale, dQ, coef);
+    else if (d == 32)
+        hipLaunchKernelGGL(csr_coef_kernel<32>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                           N, H, k, scale, dQ, coef);
+    else
+        hipLaunchKernelGGL(csr_coef_kernel<64>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                           N, H, k, scale, dQ, coef);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // pairs per counting workgroup: about 1024 workgroups, 8192 .. 65536 pairs each
+    const uint32_t per = (uint32_t)std::min<size_t>(65536, std::max<size_t>(8192, (pairs / 1024 + 255) / 256 * 256));
+    const unsigned cblocks = (unsigned)((pairs + per - 1) / per);
+    const int32_t shift = bucket_shift(d);
+    hipLaunchKernelGGL(bkt_count_kernel<false>, dim3(cblocks), dim3(256), 0, stream, idx, coef, N, H, k, shift,
+                       nbk, per, gcnt, rec);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // exclusive scan of the nbk counts; gcnt[nbk] (zero) becomes the total
+    hipLaunchKernelGGL(scan_blocks_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, stream, gcnt,
+                       (int64_t)nbk + 1, sums);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(kScanBlock), 0, stream, sums, nb);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_apply_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, stream, gcnt,
+                       (int64_t)nbk + 1, sums);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // keep the starts, count the pieces and scan them
+    hipLaunchKernelGGL(bkt_pieces_kernel, dim3((unsigned)((nbk + 1 + 255) / 256)), dim3(256), 0, stream, gcnt,
+                       nbk, sstart, pstart);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_blocks_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, stream, pstart,
+                       (int64_t)nbk + 1, sums);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(kScanBlock), 0, stream, sums, nb);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_apply_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, stream, pstart,
+                       (int64_t)nbk + 1, sums);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // the place pass advances each bucket's start to its end
+    hipLaunchKernelGGL(bkt_count_kernel<true>, dim3(cblocks), dim3(256), 0, stream, idx, coef, N, H, k, shift,
+                       nbk, per, gcnt, rec);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // at most one piece per bucket plus one per kPiece pairs; the rest exit
+    const unsigned rblocks = (unsigned)(nbk + (pairs + kPiece - 1) / kPiece);
+    if (d == 16)
+        hipLaunchKernelGGL(bkt_reduce_kernel<16>, dim3(rblocks), dim3(256), 0, stream, q, g, rec, sstart, pstart,
+                           nbk, dK, dV);
+    else if (d == 32)
+        hipLaunchKernelGGL(bkt_reduce_kernel<32>, dim3(rblocks), dim3(256), 0, stream, q, g, rec, sstart, pstart,
+                           nbk, dK, dV);
+    else
+        hipLaunchKernelGGL(bkt_reduce_kernel<64>, dim3(rblocks), dim3(256), 0, stream, q, g, rec, sstart, pstart,
+                           nbk, dK, dV);
+    return hipGetLastError();
+}
 
 size_t bwd_csr_workspace_bytes(int32_t N, int32_t H, int32_t k) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };

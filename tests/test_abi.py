@@ -78,8 +78,19 @@ def test_workspace_size(lib):
     # aligned
     csr = 32000 * 8 + 32000 * 16 + 8192 + 256
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 3) == csr
-    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == csr
-    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 4) == 0
+    # the bucketed reduction: pair coefficients, the bucket-sorted records,
+    # three arrays over the 2000 / (4096 / 32) = 16 key-row buckets (+1:
+    # counts, kept starts, pieces) and the scan's block sums
+    bucket = 32000 * 8 + 32000 * 16 + 3 * 256 + 256
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 4) == bucket
+    # the library picks the bucketed reduction where it fits
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == bucket
+    # more than 8192 buckets: unsupported, size 0; the library picks the
+    # full key sort
+    assert lib.kmip_bwd_workspace_size(1_000_000, 4, 16, 16, 4) == 0
+    assert (lib.kmip_bwd_workspace_size(1_000_000, 4, 16, 16, 0)
+            == lib.kmip_bwd_workspace_size(1_000_000, 4, 16, 16, 3) > 0)
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 5) == 0
 
 
 P = ctypes.c_void_p
@@ -124,6 +135,7 @@ def test_bwd_rejects(lib):
     assert lib.kmip_bwd(*args, 7, None, 0, None) == 2            # unknown variant
     assert lib.kmip_bwd(*args, 3, None, 0, None) == 3            # segmented needs workspace
     assert lib.kmip_bwd(*args, 2, None, 0, None) == 3            # aggregated needs workspace
+    assert lib.kmip_bwd(*args, 4, None, 0, None) == 3            # bucketed needs workspace
     assert lib.kmip_bwd(*args, 0, FAKE, 16, None) == 3           # workspace too small
     bad = list(args)
     bad[3] = None                                                 # dOut

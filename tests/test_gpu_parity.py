@@ -91,7 +91,7 @@ def test_config1_full():
     print(f"c1: {strict} well-separated, {loose} near-tied query-heads")
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4])
 def test_config2_full_fwd_bwd(variant):
     w = workloads.make(2)
     strict, loose = _check_all(w, _run(w, variant=variant))
@@ -114,7 +114,7 @@ def test_backward_hub_keys(d, k):
                            workloads.bf16_round(rng.standard_normal((N, H, d)).astype(np.float32)),
                            True)
     Qd, Kd, Vd, dOd = _f64(w)
-    for variant in (1, 2, 3):
+    for variant in (1, 2, 3, 4):
         res = _run(w, variant=variant)
         rq, rk, rv = oracle.backward(Qd, Kd, Vd, dOd, res["idx"], w.scale)
         allclose_report("dQ", res["dq"], rq)
