@@ -191,8 +191,15 @@ def main():
     counters = measured_counters() if args.config == 4 and args.n is None else None
     executed = counters["mfma_flop_per_launch"] if counters else None
     topk_ms = sum(t_topk) / len(t_topk)
+    att_ms = sum(t_att) / len(t_att)
+    bwd_ms = sum(t_bwd) / len(t_bwd) if backward else 0.0
+    # algorithmic HBM bytes per call (every operand read once per use, no
+    # reuse of gathered key/value rows assumed; bf16 inputs, fp32 outputs)
+    nh = N * H
+    att_bytes = nh * (2 * d + 4 * kk + 2 * (2 * kk * d) + 4 * d + 4)
+    bwd_bytes = nh * (2 * 2 * d + 4 * kk + 4 + 2 * (2 * kk * d) + 3 * 4 * d)
     log(f"[bench] per step: topk {topk_ms:.3f} ms (select kernel {sel_ms:.3f} ms), "
-        f"attend {sum(t_att) / len(t_att):.3f} ms, backward {sum(t_bwd) / len(t_bwd):.3f} ms, "
+        f"attend {att_ms:.3f} ms, backward {bwd_ms:.3f} ms, "
         f"wall {ms_step:.3f} ms")
     log(f"[bench] score rate {tflops:.1f} TFLOP/s = {100 * tflops / PEAK_BF16_TFLOPS:.1f}% of bf16 peak; "
         f"peak memory {peak_mem / 2**20:.1f} MiB ({peak_mem / N:.0f} B/node)")
@@ -225,8 +232,17 @@ def main():
         },
         "score_tflops": tflops,
         "score_pct_bf16_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
-        "kernel_ms": {"topk": topk_ms, "select_kernel": sel_ms, "attend": sum(t_att) / len(t_att),
-                      "backward": sum(t_bwd) / len(t_bwd) if backward else 0.0},
+        "kernel_ms": {"topk": topk_ms, "select_kernel": sel_ms, "attend": att_ms, "backward": bwd_ms},
+        "hbm": {
+            "attend": {"algorithmic_bytes": att_bytes, "gbs": att_bytes / (att_ms * 1e6),
+                       "frac": att_bytes / (att_ms * 1e6) / PEAK_HBM_GBS,
+                       "bytes": "N*H*(2d q + 4k idx + 2*2kd gathered key and value rows + 4d out + 4 lse)"},
+            "backward": None if not backward else {
+                "algorithmic_bytes": bwd_bytes, "gbs": bwd_bytes / (bwd_ms * 1e6),
+                "frac": bwd_bytes / (bwd_ms * 1e6) / PEAK_HBM_GBS,
+                "bytes": ("N*H*(2*2d q, dO + 4k idx + 4 lse + 2*2kd gathered key and value rows "
+                          "+ 3*4d dQ, dK, dV)")},
+        },
         "peak_mem_bytes": peak_mem,
         "roofline": {
             "bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",

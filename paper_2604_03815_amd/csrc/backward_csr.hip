@@ -37,11 +37,18 @@ template <int D>
 __global__ __launch_bounds__(256) void csr_coef_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
-    int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float2* __restrict__ coef) {
+    int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float2* __restrict__ coef,
+    uint16_t* __restrict__ Qt, uint16_t* __restrict__ dOt) {
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
     if (qh >= (int64_t)N * H) return;  // whole team exits together
     const int h = (int)(qh % H);
+    if (Qt != nullptr && tl < D / 8) {
+        // head-major copies [H][N][d] of the query and output-gradient rows
+        const size_t ht = ((size_t)h * N + (size_t)(qh / H)) * D;
+        reinterpret_cast<uint4*>(Qt + ht)[tl] = reinterpret_cast<const uint4*>(Q + (size_t)qh * D)[tl];
+        reinterpret_cast<uint4*>(dOt + ht)[tl] = reinterpret_cast<const uint4*>(dO + (size_t)qh * D)[tl];
+    }
     float q[D], g[D];
     load_row_f32<D>(q, Q + (size_t)qh * D);
     load_row_f32<D>(g, dO + (size_t)qh * D);
@@ -124,7 +131,7 @@ constexpr int kTabProbes = 8;
 
 struct PairRecord {
     int32_t row;    // key row j*H + h
-    int32_t qh;     // query-head i*H + h
+    int32_t qh;     // query-head i*H + h (full sort), or its head-major row h*N + i (buckets)
     float a;        // scale * g_ij
     float p;        // p_ij
 };
@@ -419,7 +426,11 @@ __global__ __launch_bounds__(256) void bkt_count_kernel(const int32_t* __restric
                 const uint32_t e = pb + 256 * u + t;
                 const int32_t bk = r[u] >= 0 ? r[u] >> shift : -1;
                 const int32_t slot = claim_slot<true>(hist, bk);
-                if (bk >= 0) rec[base[bk] + slot] = PairRecord{r[u], (int32_t)(e / (uint32_t)k), c[u].x, c[u].y};
+                if (bk >= 0) {
+                    const uint32_t qh = e / (uint32_t)k;
+                    const int32_t ht = (int32_t)((qh % (uint32_t)H) * (uint32_t)N + qh / (uint32_t)H);
+                    rec[base[bk] + slot] = PairRecord{r[u], ht, c[u].x, c[u].y};
+                }
             }
         }
     }
@@ -444,7 +455,9 @@ __global__ __launch_bounds__(256) void bkt_pieces_kernel(const int32_t* __restri
 //   1. counting sort of the piece's records by key row in LDS (claim_slot:
 //      a key most pairs share costs about one LDS atomic per wave);
 //   2. sixteen teams of 16 lanes walk contiguous stretches of the sorted
-//      order, dimensions on lanes, keep the sums of the current key row in
+//      order, dimensions on lanes, reading the query and output-gradient
+//      rows from head-major copies (a key's run of queries of one head then
+//      reads consecutive rows, not one row per 128-byte line), keep the sums of the current key row in
 //      registers and add them to dK and dV (zero at the start) with one
 //      atomic per dimension where the row changes or the stretch ends; a
 //      team loads the query rows of several pairs before adding them up.
@@ -586,7 +599,7 @@ size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k) {
     const size_t nbk = (nh + bucket_rows(d) - 1) / bucket_rows(d);
     const size_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
     return al(pairs * sizeof(float2)) + al(pairs * sizeof(PairRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
-           al((nb + 1) * sizeof(int32_t));
+           al((nb + 1) * sizeof(int32_t)) + 2 * al(nh * d * sizeof(uint16_t));
 }
 
 hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const void* dO,
@@ -613,6 +626,10 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     int32_t* pstart = reinterpret_cast<int32_t*>(p);   // pieces per bucket, then their starts
     p += al(((size_t)nbk + 1) * sizeof(int32_t));
     int32_t* sums = reinterpret_cast<int32_t*>(p);
+    p += al(((size_t)nb + 1) * sizeof(int32_t));
+    uint16_t* qt = reinterpret_cast<uint16_t*>(p);   // Q and dO head-major, [H][N][d]
+    p += al((size_t)nh * d * sizeof(uint16_t));
+    uint16_t* gt = reinterpret_cast<uint16_t*>(p);
 
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
@@ -626,13 +643,13 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     const unsigned team_blocks = (unsigned)((nh + 15) / 16);
     if (d == 16)
         hipLaunchKernelGGL(csr_coef_kernel<16>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef);
+                           N, H, k, scale, dQ, coef, qt, gt);
     else if (d == 32)
         hipLaunchKernelGGL(csr_coef_kernel<32>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef);
+                           N, H, k, scale, dQ, coef, qt, gt);
     else
         hipLaunchKernelGGL(csr_coef_kernel<64>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef);
+                           N, H, k, scale, dQ, coef, qt, gt);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // pairs per counting workgroup: about 1024 workgroups, 8192 .. 65536 pairs each
     const uint32_t per = (uint32_t)std::min<size_t>(65536, std::max<size_t>(8192, (pairs / 1024 + 255) / 256 * 256));
@@ -669,14 +686,14 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     // at most one piece per bucket plus one per kPiece pairs; the rest exit
     const unsigned rblocks = (unsigned)(nbk + (pairs + kPiece - 1) / kPiece);
     if (d == 16)
-        hipLaunchKernelGGL(bkt_reduce_kernel<16>, dim3(rblocks), dim3(256), 0, stream, q, g, rec, sstart, pstart,
-                           nbk, dK, dV);
+        hipLaunchKernelGGL(bkt_reduce_kernel<16>, dim3(rblocks), dim3(256), 0, stream, qt, gt, rec, sstart,
+                           pstart, nbk, dK, dV);
     else if (d == 32)
-        hipLaunchKernelGGL(bkt_reduce_kernel<32>, dim3(rblocks), dim3(256), 0, stream, q, g, rec, sstart, pstart,
-                           nbk, dK, dV);
+        hipLaunchKernelGGL(bkt_reduce_kernel<32>, dim3(rblocks), dim3(256), 0, stream, qt, gt, rec, sstart,
+                           pstart, nbk, dK, dV);
     else
-        hipLaunchKernelGGL(bkt_reduce_kernel<64>, dim3(rblocks), dim3(256), 0, stream, q, g, rec, sstart, pstart,
-                           nbk, dK, dV);
+        hipLaunchKernelGGL(bkt_reduce_kernel<64>, dim3(rblocks), dim3(256), 0, stream, qt, gt, rec, sstart,
+                           pstart, nbk, dK, dV);
     return hipGetLastError();
 }
 
@@ -719,15 +736,15 @@ hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const voi
     switch (d) {
         case 16:
             hipLaunchKernelGGL(csr_coef_kernel<16>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
-                               idx, lse, N, H, k, scale, dQ, coef);
+                               idx, lse, N, H, k, scale, dQ, coef, nullptr, nullptr);
             break;
         case 32:
             hipLaunchKernelGGL(csr_coef_kernel<32>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
-                               idx, lse, N, H, k, scale, dQ, coef);
+                               idx, lse, N, H, k, scale, dQ, coef, nullptr, nullptr);
             break;
         case 64:
             hipLaunchKernelGGL(csr_coef_kernel<64>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
-                               idx, lse, N, H, k, scale, dQ, coef);
+                               idx, lse, N, H, k, scale, dQ, coef, nullptr, nullptr);
             break;
         default:
             return hipErrorInvalidValue;

@@ -14,6 +14,9 @@
       sources the counters were taken on; bench.py only reports the figures
       while the sources are unchanged) and prints a markdown summary.
 
+  python rocprof_summary.py pmc <results.db> <command...>
+      per-kernel table (mean per dispatch) of every counter of one --pmc run.
+
 Reads the SQLite databases rocprofv3 writes by default.
 """
 from __future__ import annotations
@@ -115,6 +118,24 @@ def counters(fetch_db: str, write_db: str, mfma_db: str, copy_bytes: int, comman
     print(f"| WRITE_SIZE (KiB) | {write[sk]:.4g} | {write[ck]:.4g} | {copy_bytes} | {w_scale:.4f} | {write_b:.4g} B |")
     print(f"| SQ_INSTS_MFMA | {mfma[sk]:.4g} | | | {MFMA_FLOP} FLOP each | {mfma[sk] * MFMA_FLOP:.4g} FLOP |")
     print(f"\nTotal {fetch_b + write_b:.4g} HBM bytes and {mfma[sk] * MFMA_FLOP:.4g} MFMA FLOP per launch.")
+    print("\nEvery kernel of the same runs, per dispatch, scaled the same way:\n")
+    print("| kernel | fetch bytes | write bytes |")
+    print("|---|---|---|")
+    for k in sorted(fetch, key=lambda k: -fetch[k] - write.get(k, 0.0)):
+        print(f"| `{k}` | {fetch[k] * 1024.0 * f_scale:.4g} | {write.get(k, 0.0) * 1024.0 * w_scale:.4g} |")
+
+
+def pmc(db: str, command: str) -> None:
+    """Per-kernel table of every counter in one --pmc run (mean per dispatch)."""
+    c = sqlite3.connect(db)
+    names = [r[0] for r in c.execute("select distinct counter_name from counters_collection")]
+    table = {n: counter_per_dispatch(db, n) for n in names}
+    kernels = sorted({k for t in table.values() for k in t})
+    print(f"Command: `{command}`\n")
+    print("| kernel | " + " | ".join(names) + " |")
+    print("|---|" + "---|" * len(names))
+    for k in kernels:
+        print(f"| `{k}` | " + " | ".join(f"{table[n].get(k, 0.0):.4g}" for n in names) + " |")
 
 
 def main(argv):
@@ -122,6 +143,8 @@ def main(argv):
         stats(argv[2], argv[3], " ".join(argv[4:]))
     elif len(argv) >= 6 and argv[1] == "counters":
         counters(argv[2], argv[3], argv[4], int(argv[5]), " ".join(argv[6:]))
+    elif len(argv) >= 3 and argv[1] == "pmc":
+        pmc(argv[2], " ".join(argv[3:]))
     else:
         raise SystemExit(__doc__)
 

@@ -80,8 +80,9 @@ def test_workspace_size(lib):
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 3) == csr
     # the bucketed reduction: pair coefficients, the bucket-sorted records,
     # three arrays over the 2000 / (4096 / 32) = 16 key-row buckets (+1:
-    # counts, kept starts, pieces) and the scan's block sums
-    bucket = 32000 * 8 + 32000 * 16 + 3 * 256 + 256
+    # counts, kept starts, pieces), the scan's block sums and head-major
+    # copies of Q and dO (bf16)
+    bucket = 32000 * 8 + 32000 * 16 + 3 * 256 + 256 + 2 * 2000 * 32 * 2
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 4) == bucket
     # the library picks the bucketed reduction where it fits
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == bucket
