@@ -16,19 +16,19 @@
 //   row(r, l) = 8 * (r / 4) + 4 * (l / 32) + (r % 4),  r = 0..15
 // of the tile.  Lanes l and l + 32 share a query.
 //
-// Selection per query: a 4-ary min-heap of the k best 64-bit keys (score
-// code, ~index) in LDS; its root's score is a threshold theta kept in a
-// register.
+// Selection per query: a loser tree (tournament) over the k best 64-bit
+// keys (score code, ~index) in LDS, whose winner is the k-th best; its score
+// gives a threshold theta kept in a register.
 // Per tile and block each lane reduces its 16 scores with a max3 tree and
 // compares once with theta.  Only when some lane's maximum beats theta does
 // the wave pick out the scores above theta, append them (with their key
 // index) to a per-lane candidate buffer in LDS, and fold the buffers into the
-// heaps (refreshing theta) whenever one fills up.
+// trees (refreshing theta) whenever one fills up.
 //
 // Exactness of the filter: theta is the largest float below the k-th best
-// score in the heap, so s > theta holds exactly for s >= that score; every
-// key that could displace a heap entry, ties included, reaches the rare
-// path, and the heap compares full keys (score, then lower index).  The
+// score in the tree, so s > theta holds exactly for s >= that score; every
+// key that could displace a tree entry, ties included, reaches the rare
+// path, and the tree compares full keys (score, then lower index).  The
 // result therefore does not depend on the order keys are streamed in, and
 // the scan may visit a graph's tiles in any order (used to keep the waves of
 // an XCD on the same tiles, see the pacer below).  Keys of
@@ -99,15 +99,60 @@ __device__ __forceinline__ float pick16(const f32x16& a, int r) {
     return __uint_as_float(bsel(m0, v2[1], v2[0]));
 }
 
-// 4-ary min-heap in LDS: column `col` of a [k][32] array of keys, node p
-// with children 4p+1 .. 4p+4.  A missing child (past row k-1) reads as
-// kHeapTop, above any real key, so it never wins; a drained row is set to
-// kHeapTop too.  Four children per level (read together, one LDS round
-// trip) halve the depth of a binary heap: 3 levels below the root for
-// k = 32, 4 for k = 128.
+// Loser tree in LDS: column `col` of a [KP][32] array of keys, KP = k rounded
+// up to a power of two, 2^lb.  Leaves 0 .. KP-1 (not stored) hold the k best
+// keys so far, or sentinels; internal node i (rows 1 .. KP-1) has children
+// 2i and 2i+1, leaf L being node KP + L, and stores the loser (the larger
+// key) of the match between its children's winners; row 0 holds the overall
+// winner, the smallest key.  Replacing the winner by a larger key only
+// replays the matches on the winner's path to the root, whose nodes are
+// known up front: their loads go out together, one LDS round trip per
+// insertion (a 4-ary heap needs one per level).
+//
+// Tree keys carry their leaf in the low lb bits: the low word ~j of a key
+// is shifted up by lb, which drops only one-bits (the sizes accepted keep
+// j < 2^31 / max(d, k), so ~j starts with at least lb ones) and keeps the
+// order of keys of different j.  A sentinel is leaf L's key L (score word
+// 0, below every real key), and a leaf past k - 1 holds kHeapTop, above
+// every key, so it never wins.
 constexpr uint64_t kHeapTop = ~0ull;
 
-// The largest float below x, for a finite heap score x; a zero or denormal
+// A selection key in tree form at leaf bits 0.
+__device__ __forceinline__ uint64_t tree_key(uint64_t key, int lb) {
+    return (key & 0xFFFFFFFF00000000ull) | (uint64_t)((uint32_t)key << lb);
+}
+
+// Key index of a tree key; -1 for a sentinel.
+__device__ __forceinline__ int32_t tree_index(uint64_t x, int lb) {
+    if ((x >> 32) == 0ull) return -1;
+    const uint32_t top = lb > 0 ? ~0u << (32 - lb) : 0u;
+    return ~(int32_t)(((uint32_t)x >> lb) | top);
+}
+
+// Replaces the winner (at leaf `leaf`) by x, which carries that leaf in its
+// low bits, and returns the new winner.  The path is LBMAX >= lb levels long
+// so that it stays in registers without branches: levels past lb address
+// row 0 (node >> i = 0 there), which the caller sets to kHeapTop while it
+// keeps the winner in a register, so they never swap.
+template <int LBMAX>
+__device__ __forceinline__ uint64_t tree_replace(uint64_t* tp, int col, int lb, uint64_t x, int leaf) {
+    const int node = (leaf + (1 << lb)) >> 1;
+    uint64_t ls[LBMAX];
+#pragma unroll
+    for (int i = 0; i < LBMAX; ++i) ls[i] = tp[(node >> i) * 32 + col];
+#pragma unroll
+    for (int i = 0; i < LBMAX; ++i) {
+        const bool sw = ls[i] < x;
+        const uint64_t lo = sw ? ls[i] : x;
+        ls[i] = sw ? x : ls[i];
+        x = lo;
+    }
+#pragma unroll
+    for (int i = 0; i < LBMAX; ++i) tp[(node >> i) * 32 + col] = ls[i];
+    return x;
+}
+
+// The largest float below x, for a finite tree score x; a zero or denormal
 // x gives -FLT_MIN instead, so that the threshold is never a denormal (a
 // looser threshold only admits a few more candidates).
 __device__ __forceinline__ float float_below(float x) {
@@ -152,31 +197,6 @@ __device__ __forceinline__ void pacer_update(Pacer* p, int64_t now, int nt, int6
 
 __device__ __forceinline__ uint64_t min_u64(uint64_t a, uint64_t b) { return b < a ? b : a; }
 
-// Places x at the root and sifts it down.
-__device__ __forceinline__ void heap_sift_down(uint64_t* hp, int col, int k, uint64_t x) {
-    int pos = 0;
-    for (;;) {
-        const int c = 4 * pos + 1;
-        if (c >= k) break;
-        // rows past k - 1 are clamped for the read and replaced by kHeapTop
-        const uint64_t m0 = hp[c * 32 + col];
-        const uint64_t r1 = hp[min(c + 1, k - 1) * 32 + col];
-        const uint64_t r2 = hp[min(c + 2, k - 1) * 32 + col];
-        const uint64_t r3 = hp[min(c + 3, k - 1) * 32 + col];
-        const uint64_t m1 = c + 1 < k ? r1 : kHeapTop;
-        const uint64_t m2 = c + 2 < k ? r2 : kHeapTop;
-        const uint64_t m3 = c + 3 < k ? r3 : kHeapTop;
-        const int j01 = m1 < m0 ? 1 : 0, j23 = m3 < m2 ? 3 : 2;
-        const uint64_t v01 = min_u64(m0, m1), v23 = min_u64(m2, m3);
-        const int j = v23 < v01 ? j23 : j01;
-        const uint64_t m = min_u64(v01, v23);
-        if (x <= m) break;
-        hp[pos * 32 + col] = m;
-        pos = c + j;
-    }
-    hp[pos * 32 + col] = x;
-}
-
 // At least one wave per SIMD: the kernel may use the whole register file
 // rather than have the compiler trade registers for occupancy by spilling.
 template <int D, int QB, int SLOTS>
@@ -191,7 +211,11 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     constexpr int TILE_BYTES = NC * 64 * 16;
     constexpr int SBT = kSuperTiles;
     extern __shared__ uint64_t lds[];
-    const int hrows = k;
+    // loser trees of 2^lb leaves, lb <= LBMAX (k <= 32 with two blocks)
+    constexpr int LBMAX = QB == 2 ? 5 : 7;
+    const int lb = k <= 1 ? 0 : 32 - __clz(k - 1);
+    const int hrows = 1 << lb;
+    const uint64_t leaf_mask = (uint64_t)(hrows - 1);
 
     // Persistent, XCD-aware schedule.  Workgroups are dispatched to the XCDs
     // round-robin; the ones on XCD x take the items of a contiguous range of
@@ -262,7 +286,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     const int col = lane & 31;
     const int half = lane >> 5;
 
-    uint64_t* heaps = lds;                              // [QB][k][32]
+    uint64_t* trees = lds;                              // [QB][hrows][32] loser trees
     uint64_t* cand = lds + (size_t)QB * hrows * 32;     // [QB][SLOTS][64]
 
     bf16x8 bq[QB][NC];
@@ -298,7 +322,19 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         theta[b] = valid ? -INFINITY : INFINITY;
         cnt[b] = 0;
     }
-    for (int e = lane; e < QB * hrows * 32; e += 64) heaps[e] = 0ull;
+    // Empty trees: leaf L holds sentinel L (L < k) or kHeapTop; the winner
+    // is leaf 0, and node r keeps the winner of its right subtree, that
+    // subtree's leftmost leaf.
+    for (int e = lane; e < QB * hrows * 32; e += 64) {
+        const int r = (e >> 5) & (hrows - 1);
+        uint64_t v = 0ull;
+        if (r > 0) {
+            const int dep = 31 - __clz(r);
+            const int leaf = ((2 * r + 1) << (lb - dep - 1)) - hrows;
+            v = leaf < k ? (uint64_t)leaf : kHeapTop;
+        }
+        trees[e] = v;
+    }
 
     // Seeded thresholds.  Queries of one direction label share most of their
     // top-k keys.  When some query of the label of a block's first query has
@@ -308,7 +344,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     // distinct keys of the graph score at least that much, so the query's
     // k-th best does too, and every key that can enter its top-k still
     // passes the filter.  Scores come from the same MFMA on the same
-    // operands as in the stream, hence are the same values.  The heap starts
+    // operands as in the stream, hence are the same values.  The tree starts
     // empty and fills with keys that pass; theta only ever rises.
     // A block tries the seeds of the labels of its first and of its last
     // query (a block can straddle two labels) and keeps, per query, the
@@ -355,14 +391,14 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         }
     }
 
-    // Fold every lane's candidates into the heaps and refresh theta.  With
-    // two blocks, each phase has the lower half-wave on one block's heaps and
-    // the upper half-wave on the other's, so all lanes work on disjoint heaps.
+    // Fold every lane's candidates into the trees and refresh theta.  With
+    // two blocks, each phase has the lower half-wave on one block's trees and
+    // the upper half-wave on the other's, so all lanes work on disjoint trees.
     const int32_t* kperm_h = kperm != nullptr ? kperm + (size_t)head * N : nullptr;
     auto merge_all = [&]() {
         if (kperm_h != nullptr) {
             // With a stored key order, candidates carry the key's position in
-            // that order; swap in the key's own index before the heap applies
+            // that order; swap in the key's own index before the tree applies
             // its tie rule.  Every slot is looked up (unused ones at position
             // 0) so that all of a lane's loads are in flight together.
             int32_t orig[QB][SLOTS];
@@ -383,28 +419,39 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
                 }
             }
         }
-#pragma unroll
+        // (not unrolled: the merge is inlined at every filter site of the
+        // unrolled key stream, and one copy of the replay keeps that loop
+        // small enough to be unrolled, with its ring registers static)
+#pragma unroll 1
         for (int ph = 0; ph < 2; ++ph) {
             const int b = QB == 2 ? (half ^ ph) : 0;
             if (QB == 2 || half == ph) {
-                uint64_t* hp = heaps + (size_t)b * hrows * 32;
+                uint64_t* tp = trees + (size_t)b * hrows * 32;
                 const uint64_t* cb = cand + (size_t)b * SLOTS * 64;
                 const int n = b == 0 ? cnt[0] : cnt[QB - 1];
+                // the winner stays in a register; row 0 holds kHeapTop meanwhile
+                uint64_t w = tp[col];
+                tp[col] = kHeapTop;
+                uint64_t c = cb[lane];
                 for (int e = 0; e < n; ++e) {
-                    uint64_t c = cb[e * 64 + lane];
-                    if (c > hp[col]) heap_sift_down(hp, col, k, c);
+                    // the next candidate's load goes out before this one's replay
+                    const uint64_t cn = cb[min(e + 1, SLOTS - 1) * 64 + lane];
+                    const uint64_t x = tree_key(c, lb);
+                    if (x > w) w = tree_replace<LBMAX>(tp, col, lb, x | (w & leaf_mask), (int)(w & leaf_mask));
+                    c = cn;
                 }
+                tp[col] = w;
             }
-            // The heaps are private to this wave, whose LDS instructions
+            // The trees are private to this wave, whose LDS instructions
             // execute in program order, so the next phase sees this phase's
-            // heap writes.  Only compiler reordering has to be fenced off.
+            // tree writes.  Only compiler reordering has to be fenced off.
             __builtin_amdgcn_wave_barrier();
         }
 #pragma unroll
         for (int b = 0; b < QB; ++b) {
             if (theta[b] != INFINITY) {
-                const uint64_t root = heaps[(size_t)b * hrows * 32 + col];
-                theta[b] = fmaxf(theta[b], root == 0ull ? -INFINITY : float_below(key_score(root)));
+                const uint64_t root = trees[(size_t)b * hrows * 32 + col];
+                theta[b] = fmaxf(theta[b], (root >> 32) == 0ull ? -INFINITY : float_below(key_score(root)));
             }
             cnt[b] = 0;
         }
@@ -815,22 +862,20 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         pacer_update(&pacers[xcd], now, nt, now - item_start);
     }
 
-    // Drain each heap in increasing order into slots k-1 .. 0, which leaves
-    // the row sorted by (score desc, index asc); sentinels become -1.  The
-    // vacated last row takes kHeapTop, so the heap shrinks without a size.
+    // Drain each tree in increasing order into slots k-1 .. 0, which leaves
+    // the row sorted by (score desc, index asc); sentinels become -1.  Each
+    // winner taken is replaced by kHeapTop, which never wins again.
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
         const int qi = 32 * b + col;
         if (half == 0 && qi < q_count) {
-            uint64_t* hp = heaps + (size_t)b * hrows * 32;
+            uint64_t* tp = trees + (size_t)b * hrows * 32;
             int32_t* dst = topk_idx + ((size_t)qid[b] * H + head) * k;
+            uint64_t w = tp[col];
+            tp[col] = kHeapTop;
             for (int p = k - 1; p >= 0; --p) {
-                dst[p] = key_index(hp[col]);
-                if (p > 0) {
-                    const uint64_t last = hp[p * 32 + col];
-                    hp[p * 32 + col] = kHeapTop;
-                    heap_sift_down(hp, col, k, last);
-                }
+                dst[p] = tree_index(w, lb);
+                if (p > 0) w = tree_replace<LBMAX>(tp, col, lb, kHeapTop, (int)(w & leaf_mask));
             }
         }
     }
@@ -841,7 +886,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         const int lab = qlabel[(size_t)head * N + qid[0]];
         atomicCAS(&seed_ref[(size_t)head * kGroupCenters + lab], 0, qid[0] + 1);
     }
-    // The next item reinitialises the heaps this wave just drained.
+    // The next item reinitialises the trees this wave just drained.
     __builtin_amdgcn_wave_barrier();
     }  // item loop
 }
@@ -917,7 +962,9 @@ hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const T
 }  // namespace
 
 size_t select_lds_bytes(int32_t k, SelectShape shape) {
-    return (size_t)shape.qb * ((size_t)k * 32 + (size_t)shape.slots * 64) * sizeof(uint64_t);
+    size_t rows = 1;   // loser-tree rows: k rounded up to a power of two
+    while (rows < (size_t)k) rows <<= 1;
+    return (size_t)shape.qb * (rows * 32 + (size_t)shape.slots * 64) * sizeof(uint64_t);
 }
 
 hipError_t launch_pack_k(const void* K, const int32_t* perm, void* kp, int32_t N, int32_t H, int32_t d,
