@@ -22,7 +22,11 @@
  *    non-decreasing, o_G = N.  Query i of graph g attends only to keys in
  *    [o_g, o_{g+1}) (block-diagonal batching of many graphs).  NULL means a
  *    single graph of N nodes (num_graphs is then ignored).  Empty graphs are
- *    allowed.
+ *    allowed.  With several graphs the library builds a work list on the
+ *    host and uploads it on the caller's stream through pinned host memory
+ *    that it keeps (two buffers per device, grown on demand, until the
+ *    process ends), so that the call does not wait for the stream; the
+ *    offsets array may be reused as soon as the call returns.
  *  - Ties between equal scores go to the lower node id.  The query's own
  *    key is a candidate.  `scale` must be finite and > 0; selection uses the
  *    raw scores, which for scale > 0 is the same as the scaled scores.

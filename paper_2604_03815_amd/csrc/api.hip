@@ -4,6 +4,8 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -34,6 +36,50 @@ kmip_status_t hip_fail(hipError_t e, const char* what) {
 }
 
 constexpr size_t kAlign = 256;
+
+// Pinned host staging for the block-diagonal work list, so that its upload
+// is an asynchronous copy (a copy from pageable memory blocks the caller
+// until the stream reaches it).  Two buffers per device, used in turn; a
+// buffer is refilled only after the copy that last read it has completed
+// (an event recorded behind that copy).  Kept until the process ends.
+struct Staging {
+    void* buf[2] = {nullptr, nullptr};
+    size_t cap[2] = {0, 0};
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    int next = 0;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_stage_mu;
+Staging g_stage[kMaxDevices];
+
+// Copies `bytes` from host `src` to device `dst` on `stream` through the
+// calling device's staging buffers.
+hipError_t upload_async(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream);
+    std::lock_guard<std::mutex> lock(g_stage_mu);
+    Staging& st = g_stage[dev];
+    const int i = st.next;
+    st.next ^= 1;
+    if (st.ev[i] == nullptr) {
+        if ((e = hipEventCreateWithFlags(&st.ev[i], hipEventDisableTiming)) != hipSuccess) return e;
+    } else if ((e = hipEventSynchronize(st.ev[i])) != hipSuccess) {
+        return e;
+    }
+    if (st.cap[i] < bytes) {
+        if (st.buf[i] != nullptr && (e = hipHostFree(st.buf[i])) != hipSuccess) return e;
+        st.buf[i] = nullptr;
+        st.cap[i] = 0;
+        const size_t cap = std::max<size_t>(bytes, 64 * 1024);
+        if ((e = hipHostMalloc(&st.buf[i], cap, hipHostMallocDefault)) != hipSuccess) return e;
+        st.cap[i] = cap;
+    }
+    std::memcpy(st.buf[i], src, bytes);
+    if ((e = hipMemcpyAsync(dst, st.buf[i], bytes, hipMemcpyHostToDevice, stream)) != hipSuccess) return e;
+    return hipEventRecord(st.ev[i], stream);
+}
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -179,8 +225,7 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
         });
         ntasks = (int32_t)tasks.size();
         void* dst = ws + tiled_bytes(N, H, d) + kCounterBytes;
-        hipError_t e = hipMemcpyAsync(dst, tasks.data(), tasks.size() * sizeof(kmip::Task),
-                                      hipMemcpyHostToDevice, stream);
+        hipError_t e = upload_async(dst, tasks.data(), tasks.size() * sizeof(kmip::Task), stream);
         if (e != hipSuccess) return hip_fail(e, "work list upload");
         dtasks = reinterpret_cast<const kmip::Task*>(dst);
     } else {

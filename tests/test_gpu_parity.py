@@ -266,3 +266,23 @@ def test_full_size_sampled(cfg, sample):
     w = workloads.make(cfg)
     strict, loose = _check_all(w, _run(w), sample=sample)
     print(f"c{cfg}: sampled {strict} well-separated, {loose} near-tied query-heads")
+
+
+def test_peak_memory_linear_in_n():
+    # Peak device memory of a forward+backward step (inputs, outputs and the
+    # library's workspaces) grows linearly with N: the bytes per node at the
+    # 500k-node configuration stay within 10% of those at a quarter of it.
+    per_node = {}
+    for n in (125_000, 500_000):
+        w = workloads.make(4, n=n)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats(DEV)
+        base = torch.cuda.memory_allocated(DEV)
+        res = _run(w)
+        del res
+        torch.cuda.synchronize()
+        per_node[n] = (torch.cuda.max_memory_allocated(DEV) - base) / n
+        print(f"N={n}: {per_node[n]:.0f} peak bytes per node", flush=True)
+    assert per_node[500_000] <= 1.1 * per_node[125_000]
+    assert per_node[500_000] < 8192
