@@ -99,6 +99,27 @@ __device__ __forceinline__ float pick16(const f32x16& a, int r) {
     return __uint_as_float(bsel(m0, v2[1], v2[0]));
 }
 
+// Superblock rows of a bound tile whose bound beats a threshold: lane l
+// holds m, with bit 15 - r set when its row tile_row(r, l / 32) is needed
+// by its query.  ORs m over each half-wave (a prefix OR along each row of
+// 16 lanes with DPP shifts, then the rows' last lanes) and returns the
+// 32-bit row mask of the tile.
+__device__ __forceinline__ uint32_t half_or_rows(uint32_t m) {
+    m |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)m, 0x111, 0xF, 0xF, true);   // row_shr:1
+    m |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)m, 0x112, 0xF, 0xF, true);   // row_shr:2
+    m |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)m, 0x114, 0xF, 0xF, true);   // row_shr:4
+    m |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)m, 0x118, 0xF, 0xF, true);   // row_shr:8
+    const uint32_t h0 = (uint32_t)__builtin_amdgcn_readlane((int)m, 15) | (uint32_t)__builtin_amdgcn_readlane((int)m, 31);
+    const uint32_t h1 = (uint32_t)__builtin_amdgcn_readlane((int)m, 47) | (uint32_t)__builtin_amdgcn_readlane((int)m, 63);
+    // bit 15 - r -> bit r, then nibble a (rows 4a .. 4a+3 of the half) to
+    // rows 8a .. 8a+3 (half 0) or 8a+4 .. 8a+7 (half 1)
+    auto spread = [](uint32_t x) {
+        x = __builtin_bitreverse32(x) >> 16;
+        return (x & 0xFu) | ((x & 0xF0u) << 4) | ((x & 0xF00u) << 8) | ((x & 0xF000u) << 12);
+    };
+    return spread(h0) | (spread(h1) << 4);
+}
+
 // Loser tree in LDS: column `col` of a [KP][32] array of keys, KP = k rounded
 // up to a power of two, 2^lb.  Leaves 0 .. KP-1 (not stored) hold the k best
 // keys so far, or sentinels; internal node i (rows 1 .. KP-1) has children
@@ -520,6 +541,11 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     const uint4* btiles = bounds != nullptr ? bounds + (size_t)head * ctiles * (NC + 1) * 64 : nullptr;
     uint32_t mask_lo = 0, mask_hi = 0;
     int mask_batch = -1;
+    // The last masks compute_batch formed (before a warm-up replaced them):
+    // thresholds only rise, so when the same batch is formed again only
+    // windows that kept a superblock then can keep one now.
+    uint32_t full_lo = 0, full_hi = 0;
+    int full_batch = -1;
     // Superblocks of batch 0 already scanned by a warm-up (see below), as
     // window masks held like mask_lo / mask_hi; left out of every mask.
     uint32_t warm_lo = 0, warm_hi = 0;
@@ -543,27 +569,46 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
             best_v[b] = -INFINITY;
             best_sb[b] = -1;
         }
-        uint4 cn[2][NC + 1];
-        auto fetch = [&](int w) {
+        uint64_t todo = whi - wlo == 64 ? ~0ull : (1ull << (whi - wlo)) - 1ull;
+        if (full_batch == bt) todo &= __builtin_amdgcn_ballot_w64((full_lo | full_hi) != 0u);
+        // Bound tiles of the next windows to score, PD windows ahead (two
+        // where registers allow).
+        constexpr int PD = NC <= 2 ? 2 : 1;
+        uint4 cn[2][NC + 1], cn2[2][NC + 1];
+        auto fetch = [&](uint4 (&dst)[2][NC + 1], int w) {
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
                 const uint4* src = btiles + (size_t)(2 * w + ct) * (NC + 1) * 64 + lane;
 #pragma unroll
-                for (int c = 0; c <= NC; ++c) cn[ct][c] = src[c * 64];
+                for (int c = 0; c <= NC; ++c) dst[ct][c] = src[c * 64];
             }
         };
-        fetch(wlo);
-        for (int w = wlo; w < whi; ++w) {
+        if (todo != 0ull) fetch(cn, wlo + (int)__builtin_ctzll(todo));
+        if (PD == 2) {
+            const uint64_t t1 = todo & (todo - 1ull);
+            if (t1 != 0ull) fetch(cn2, wlo + (int)__builtin_ctzll(t1));
+        }
+        while (todo != 0ull) {
+            const int w = wlo + (int)__builtin_ctzll(todo);
+            todo &= todo - 1ull;
             uint4 cc[2][NC + 1];
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct)
 #pragma unroll
                 for (int c = 0; c <= NC; ++c) cc[ct][c] = cn[ct][c];
-            if (w + 1 < whi) fetch(w + 1);
+            if (PD == 2) {
+#pragma unroll
+                for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+                    for (int c = 0; c <= NC; ++c) cn[ct][c] = cn2[ct][c];
+                const uint64_t t1 = todo & (todo - 1ull);
+                if (t1 != 0ull) fetch(cn2, wlo + (int)__builtin_ctzll(t1));
+            } else if (todo != 0ull) {
+                fetch(cn, wlo + (int)__builtin_ctzll(todo));
+            }
             uint64_t m = 0;
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
-                uint32_t bits = 0;
                 f32x16 bacc[QB];
 #pragma unroll
                 for (int b = 0; b < QB; ++b) {
@@ -575,15 +620,17 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
                     bacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, cc[ct][NC]),
                                                                       qa[b], bacc[b], 0, 0, 0);
                 }
+                // bit 15 - r: some block's bound beats its theta (theta - bound
+                // is negative exactly then; -0 only adds a row)
+                uint32_t lm = 0;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    bool need = false;
+                    uint32_t any = 0;
 #pragma unroll
-                    for (int b = 0; b < QB; ++b) need = need || bacc[b][r] > theta[b];
-                    const uint64_t bal = __builtin_amdgcn_ballot_w64(need);
-                    bits |= ((uint32_t)bal != 0u ? 1u : 0u) << tile_row(r, 0);
-                    bits |= ((uint32_t)(bal >> 32) != 0u ? 1u : 0u) << tile_row(r, 1);
+                    for (int b = 0; b < QB; ++b) any |= __float_as_uint(theta[b] - bacc[b][r]);
+                    lm = __builtin_amdgcn_alignbit(lm, any, 31);
                 }
+                const uint32_t bits = half_or_rows(lm);
                 if (track) {
                     const int sb0 = 64 * w + 32 * ct;
 #pragma unroll
@@ -607,9 +654,9 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
             }
             needed += __builtin_popcountll(m);
         }
-        mask_lo = (uint32_t)mv;
-        mask_hi = (uint32_t)(mv >> 32);
-        mask_batch = bt;
+        mask_lo = full_lo = (uint32_t)mv;
+        mask_hi = full_hi = (uint32_t)(mv >> 32);
+        mask_batch = full_batch = bt;
         return needed;
     };
     auto read_mask = [&](int w) {
