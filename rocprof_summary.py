@@ -17,6 +17,12 @@
   python rocprof_summary.py pmc <results.db> <command...>
       per-kernel table (mean per dispatch) of every counter of one --pmc run.
 
+  python rocprof_summary.py derived <trace.db> <fetch.db> <write.db> <sq.db> <tcc.db> <copy_bytes>
+      per-kernel figures of the kernels above 0.1 ms: average duration (kernel
+      trace), calibrated fetch+write bytes, their rate, the L2 hit rate
+      (TCC_HIT/(TCC_HIT+TCC_MISS)) and the clock (GRBM_GUI_ACTIVE / 8 XCDs /
+      duration); then the MFMA, VALU, SALU and LDS figures of select_kernel.
+
 Reads the SQLite databases rocprofv3 writes by default.
 """
 from __future__ import annotations
@@ -138,11 +144,50 @@ def pmc(db: str, command: str) -> None:
         print(f"| `{k}` | " + " | ".join(f"{table[n].get(k, 0.0):.4g}" for n in names) + " |")
 
 
+def derived(trace_db: str, fetch_db: str, write_db: str, sq_db: str, tcc_db: str, copy_bytes: int) -> None:
+    c = sqlite3.connect(trace_db)
+    dur = {}
+    for name, avg in c.execute("select name, avg(end-start) from kernels group by name"):
+        dur[short(name)] = avg / 1e9
+    fetch = counter_per_dispatch(fetch_db, "FETCH_SIZE")
+    write = counter_per_dispatch(write_db, "WRITE_SIZE")
+    ck = [k for k in fetch if "elementwise" in k.lower()][0]
+    f_scale = copy_bytes / (fetch[ck] * 1024.0)
+    w_scale = copy_bytes / (write[ck] * 1024.0)
+    hit = counter_per_dispatch(tcc_db, "TCC_HIT_sum")
+    miss = counter_per_dispatch(tcc_db, "TCC_MISS_sum")
+    grbm = counter_per_dispatch(tcc_db, "GRBM_GUI_ACTIVE")
+    print("| kernel | avg ms | fetch+write bytes | GB/s | % of 8 TB/s | L2 hit | GPU clock GHz |")
+    print("|---|---|---|---|---|---|---|")
+    for k in sorted(dur, key=lambda k: -dur[k]):
+        if dur[k] < 1e-4 or k not in fetch:
+            continue
+        b = fetch[k] * 1024.0 * f_scale + write.get(k, 0.0) * 1024.0 * w_scale
+        h, m = hit.get(k, 0.0), miss.get(k, 0.0)
+        print(f"| `{k}` | {dur[k] * 1e3:.3f} | {b:.4g} | {b / dur[k] / 1e9:.0f} | {b / dur[k] / 8e12 * 100:.1f} | "
+              f"{100 * h / max(h + m, 1.0):.0f}% | {grbm.get(k, 0.0) / 8 / dur[k] / 1e9:.2f} |")
+    sq = {n: counter_per_dispatch(sq_db, n) for n in
+          ("SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU", "SQ_INSTS_SALU", "SQ_INSTS_LDS",
+           "SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES")}
+    sk = [k for k in sq["SQ_INSTS_MFMA"] if k.startswith("select_kernel")][0]
+    cycles = grbm[sk] / 8
+    flop = sq["SQ_INSTS_MFMA"][sk] * MFMA_FLOP
+    print(f"\n`{sk}`: {dur[sk] * 1e3:.3f} ms, {cycles:.4g} cycles per XCD")
+    print(f"- MFMA: {sq['SQ_INSTS_MFMA'][sk]:.4g} instructions = {flop:.4g} FLOP executed "
+          f"({flop / dur[sk] / 1e12:.0f} TFLOP/s); busy {sq['SQ_VALU_MFMA_BUSY_CYCLES'][sk]:.4g} cycles = "
+          f"{100 * sq['SQ_VALU_MFMA_BUSY_CYCLES'][sk] / (1024 * cycles):.1f}% of 1024 SIMDs")
+    print(f"- VALU {sq['SQ_INSTS_VALU'][sk]:.4g}, SALU {sq['SQ_INSTS_SALU'][sk]:.4g}, "
+          f"LDS {sq['SQ_INSTS_LDS'][sk]:.4g} instructions; waiting "
+          f"{100 * sq['SQ_WAIT_INST_ANY'][sk] / sq['SQ_WAVE_CYCLES'][sk]:.1f}% of wave cycles")
+
+
 def main(argv):
     if len(argv) >= 4 and argv[1] == "stats":
         stats(argv[2], argv[3], " ".join(argv[4:]))
     elif len(argv) >= 6 and argv[1] == "counters":
         counters(argv[2], argv[3], argv[4], int(argv[5]), " ".join(argv[6:]))
+    elif len(argv) >= 8 and argv[1] == "derived":
+        derived(argv[2], argv[3], argv[4], argv[5], argv[6], int(argv[7]))
     elif len(argv) >= 3 and argv[1] == "pmc":
         pmc(argv[2], " ".join(argv[3:]))
     else:
