@@ -32,22 +32,52 @@ constexpr int kSlotsPerLane = (128 + 15) / 16;
 constexpr int kScanBlock = 1024;     // counts per block of the scan
 constexpr int kChunk = 1024;         // sorted pairs per wave in the reduction
 
+// Sum of a D-vector over the 16 lanes of a team, transposed: out[u] of lane
+// tl receives the team sum of dimension 16u + tl.  Recursive halving: at the
+// step with partner tl ^ m (m = 8, 4, 2, 1) a lane keeps the half of its
+// dimensions whose bit m matches its own and adds the partner's values of
+// that half, so the step exchanges half of what is left (15 shuffles per 16
+// dimensions, against 64 for a full butterfly per dimension).
+template <int N>
+__device__ __forceinline__ void halve_step(const float* in, float* outv, int tl, int m) {
+    const bool hi = (tl & m) != 0;
+#pragma unroll
+    for (int b = 0; b < N; b += 2 * m) {
+#pragma unroll
+        for (int j = 0; j < m; ++j) {
+            const float lo_v = in[b + j], hi_v = in[b + m + j];
+            const float own = hi ? hi_v : lo_v, other = hi ? lo_v : hi_v;
+            outv[b / 2 + j] = own + __shfl_xor(other, m, 16);
+        }
+    }
+}
+
+template <int D>
+__device__ __forceinline__ void team_sum_transpose(const float (&acc)[D], float (&out)[D / 16], int tl) {
+    float a8[D / 2], a4[D / 4], a2[D / 8];
+    halve_step<D>(acc, a8, tl, 8);
+    halve_step<D / 2>(a8, a4, tl, 4);
+    halve_step<D / 4>(a4, a2, tl, 2);
+    halve_step<D / 8>(a2, out, tl, 1);
+}
+
 // 1. Per (query, head), a team of 16 lanes with the slots on lanes.
 template <int D>
 __global__ __launch_bounds__(256) void csr_coef_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
     int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float2* __restrict__ coef,
-    uint16_t* __restrict__ Qt, uint16_t* __restrict__ dOt) {
+    uint16_t* __restrict__ QGt) {
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
     if (qh >= (int64_t)N * H) return;  // whole team exits together
     const int h = (int)(qh % H);
-    if (Qt != nullptr && tl < D / 8) {
-        // head-major copies [H][N][d] of the query and output-gradient rows
-        const size_t ht = ((size_t)h * N + (size_t)(qh / H)) * D;
-        reinterpret_cast<uint4*>(Qt + ht)[tl] = reinterpret_cast<const uint4*>(Q + (size_t)qh * D)[tl];
-        reinterpret_cast<uint4*>(dOt + ht)[tl] = reinterpret_cast<const uint4*>(dO + (size_t)qh * D)[tl];
+    if (QGt != nullptr && tl < D / 4) {
+        // head-major interleaved copy [H][N][2d]: row h*N + i holds q_i then
+        // dO_i of head h, so the reduction gathers both with one load
+        const size_t ht = ((size_t)h * N + (size_t)(qh / H)) * (2 * D);
+        const uint16_t* src = tl < D / 8 ? Q + (size_t)qh * D : dO + (size_t)qh * D;
+        reinterpret_cast<uint4*>(QGt + ht)[tl] = reinterpret_cast<const uint4*>(src)[tl & (D / 8 - 1)];
     }
     float q[D], g[D];
     load_row_f32<D>(q, Q + (size_t)qh * D);
@@ -96,17 +126,7 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
         }
     }
     float out[D / 16];
-#pragma unroll
-    for (int u = 0; u < D / 16; ++u) {
-        float v = 0.0f;
-#pragma unroll
-        for (int t = 0; t < 16; ++t) {
-            // lane tl keeps the team sum of dimension 16u + tl
-            const float tsum = group16_sum(acc[16 * u + t]);
-            if (t == tl) v = tsum;
-        }
-        out[u] = v;
-    }
+    team_sum_transpose<D>(acc, out, tl);
 #pragma unroll
     for (int u = 0; u < D / 16; ++u) dQ[(size_t)qh * D + 16 * u + tl] = scale * out[u];
 }
@@ -455,22 +475,48 @@ __global__ __launch_bounds__(256) void bkt_pieces_kernel(const int32_t* __restri
 //   1. counting sort of the piece's records by key row in LDS (claim_slot:
 //      a key most pairs share costs about one LDS atomic per wave);
 //   2. sixteen teams of 16 lanes walk contiguous stretches of the sorted
-//      order, dimensions on lanes, reading the query and output-gradient
-//      rows from head-major copies (a key's run of queries of one head then
-//      reads consecutive rows, not one row per 128-byte line), keep the sums of the current key row in
-//      registers and add them to dK and dV (zero at the start) with one
-//      atomic per dimension where the row changes or the stretch ends; a
-//      team loads the query rows of several pairs before adding them up.
+//      order.  A record's query row of the interleaved head-major copy
+//      (q then dO, 4d bytes) is one load per team, lane tl taking d/8
+//      elements: lanes 0-7 hold q and add a*q to dK, lanes 8-15 hold dO and
+//      add p*dO to dV.  Head-major rows let a key's run of queries of one
+//      head read consecutive rows.  A team keeps the sums of the current key
+//      row in registers and adds them to dK and dV (zero at the start) with
+//      one atomic per dimension where the row changes or the stretch ends; it
+//      loads the rows of eight pairs before adding them up.
+template <int E>
+struct RowChunk;   // E bf16 values, one load
+template <> struct RowChunk<2> { uint32_t w[1]; };
+template <> struct RowChunk<4> { uint32_t w[2]; };
+template <> struct RowChunk<8> { uint32_t w[4]; };
+
+template <int E>
+__device__ __forceinline__ RowChunk<E> load_chunk(const uint16_t* p) {
+    RowChunk<E> c;
+    if constexpr (E == 2) {
+        c.w[0] = *reinterpret_cast<const uint32_t*>(p);
+    } else if constexpr (E == 4) {
+        const uint2 v = *reinterpret_cast<const uint2*>(p);
+        c.w[0] = v.x;
+        c.w[1] = v.y;
+    } else {
+        const uint4 v = *reinterpret_cast<const uint4*>(p);
+        c.w[0] = v.x;
+        c.w[1] = v.y;
+        c.w[2] = v.z;
+        c.w[3] = v.w;
+    }
+    return c;
+}
+
 template <int D>
-__global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restrict__ Q,
-                                                         const uint16_t* __restrict__ dO,
+__global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restrict__ QG,
                                                          const PairRecord* __restrict__ rec,
                                                          const int32_t* __restrict__ sstart,
                                                          const int32_t* __restrict__ pstart, int32_t nbk,
                                                          float* __restrict__ dK, float* __restrict__ dV) {
     constexpr int RB = 4096 / D;
-    constexpr int U = D / 16;           // dims per lane of a team, for each of dK and dV
-    constexpr int G = 8 / U;            // pairs whose rows a team loads at once
+    constexpr int E = D / 8;            // elements of the interleaved row per lane
+    constexpr int G = 8;                // pairs whose rows a team loads at once
     __shared__ uint16_t ord[kPiece];
     __shared__ uint8_t lrow[kPiece];
     __shared__ int32_t cursor[RB];
@@ -529,19 +575,20 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
     // 2. teams walk the sorted order
     const int tl = t & 15;
     const int team = t >> 4;
+    const bool isq = tl < 8;
     const int span = (n + 15) / 16;
     const int p0 = min(n, team * span), p1 = min(n, p0 + span);
     int32_t cur = -1;
-    float ak[U], av[U];
+    float acc[E];
 #pragma unroll
-    for (int u = 0; u < U; ++u) ak[u] = av[u] = 0.0f;
+    for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+    float* const dst0 = (isq ? dK : dV) + (tl & 7) * E;
     auto flush = [&]() {
         if (cur >= 0) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                atomicAdd(dK + (size_t)cur * D + 16 * u + tl, ak[u]);
-                atomicAdd(dV + (size_t)cur * D + 16 * u + tl, av[u]);
-                ak[u] = av[u] = 0.0f;
+            for (int e = 0; e < E; ++e) {
+                atomicAdd(dst0 + (size_t)cur * D + e, acc[e]);
+                acc[e] = 0.0f;
             }
         }
     };
@@ -554,18 +601,20 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
         const int m = min(16, p1 - pb);
         for (int s0 = 0; s0 < m; s0 += G) {
             int32_t rt[G];
-            float at[G], pt[G], qv[G][U], ov[G][U];
+            float ct[G];
+            RowChunk<E> rv[G];
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 rt[g] = __shfl(r.row, s0 + g, 16);
                 const int32_t qt = __shfl(r.qh, s0 + g, 16);
-                at[g] = __shfl(r.a, s0 + g, 16);
-                pt[g] = __shfl(r.p, s0 + g, 16);
-                const size_t qrow = (size_t)qt * D + tl;
+                // lanes 0-7 take the record's a, lanes 8-15 its p
+                const float ca = __shfl(r.a, s0 + g, 16), cp = __shfl(r.p, s0 + g, 16);
+                ct[g] = isq ? ca : cp;
+                if (s0 + g < m) {
+                    rv[g] = load_chunk<E>(QG + (size_t)qt * (2 * D) + tl * E);
+                } else {
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    qv[g][u] = s0 + g < m ? bf16_bits_to_f32(Q[qrow + 16 * u]) : 0.0f;
-                    ov[g][u] = s0 + g < m ? bf16_bits_to_f32(dO[qrow + 16 * u]) : 0.0f;
+                    for (int w = 0; w < E / 2; ++w) rv[g].w[w] = 0u;
                 }
             }
 #pragma unroll
@@ -576,9 +625,9 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
                     cur = rt[g];
                 }
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    ak[u] = fmaf(at[g], qv[g][u], ak[u]);
-                    av[u] = fmaf(pt[g], ov[g][u], av[u]);
+                for (int w = 0; w < E / 2; ++w) {
+                    acc[2 * w] = fmaf(ct[g], bf16_bits_to_f32(rv[g].w[w] & 0xFFFFu), acc[2 * w]);
+                    acc[2 * w + 1] = fmaf(ct[g], bf16_bits_to_f32(rv[g].w[w] >> 16), acc[2 * w + 1]);
                 }
             }
         }
@@ -599,7 +648,7 @@ size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k) {
     const size_t nbk = (nh + bucket_rows(d) - 1) / bucket_rows(d);
     const size_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
     return al(pairs * sizeof(float2)) + al(pairs * sizeof(PairRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
-           al((nb + 1) * sizeof(int32_t)) + 2 * al(nh * d * sizeof(uint16_t));
+           al((nb + 1) * sizeof(int32_t)) + al(nh * 2 * d * sizeof(uint16_t));
 }
 
 hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const void* dO,
@@ -627,9 +676,7 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     p += al(((size_t)nbk + 1) * sizeof(int32_t));
     int32_t* sums = reinterpret_cast<int32_t*>(p);
     p += al(((size_t)nb + 1) * sizeof(int32_t));
-    uint16_t* qt = reinterpret_cast<uint16_t*>(p);   // Q and dO head-major, [H][N][d]
-    p += al((size_t)nh * d * sizeof(uint16_t));
-    uint16_t* gt = reinterpret_cast<uint16_t*>(p);
+    uint16_t* qg = reinterpret_cast<uint16_t*>(p);   // q and dO interleaved, head-major, [H][N][2d]
 
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
@@ -643,13 +690,13 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     const unsigned team_blocks = (unsigned)((nh + 15) / 16);
     if (d == 16)
         hipLaunchKernelGGL(csr_coef_kernel<16>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qt, gt);
+                           N, H, k, scale, dQ, coef, qg);
     else if (d == 32)
         hipLaunchKernelGGL(csr_coef_kernel<32>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qt, gt);
+                           N, H, k, scale, dQ, coef, qg);
     else
         hipLaunchKernelGGL(csr_coef_kernel<64>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qt, gt);
+                           N, H, k, scale, dQ, coef, qg);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // pairs per counting workgroup: about 1024 workgroups, 8192 .. 65536 pairs each
     const uint32_t per = (uint32_t)std::min<size_t>(65536, std::max<size_t>(8192, (pairs / 1024 + 255) / 256 * 256));
@@ -686,13 +733,13 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     // at most one piece per bucket plus one per kPiece pairs; the rest exit
     const unsigned rblocks = (unsigned)(nbk + (pairs + kPiece - 1) / kPiece);
     if (d == 16)
-        hipLaunchKernelGGL(bkt_reduce_kernel<16>, dim3(rblocks), dim3(256), 0, stream, qt, gt, rec, sstart,
+        hipLaunchKernelGGL(bkt_reduce_kernel<16>, dim3(rblocks), dim3(256), 0, stream, qg, rec, sstart,
                            pstart, nbk, dK, dV);
     else if (d == 32)
-        hipLaunchKernelGGL(bkt_reduce_kernel<32>, dim3(rblocks), dim3(256), 0, stream, qt, gt, rec, sstart,
+        hipLaunchKernelGGL(bkt_reduce_kernel<32>, dim3(rblocks), dim3(256), 0, stream, qg, rec, sstart,
                            pstart, nbk, dK, dV);
     else
-        hipLaunchKernelGGL(bkt_reduce_kernel<64>, dim3(rblocks), dim3(256), 0, stream, qt, gt, rec, sstart,
+        hipLaunchKernelGGL(bkt_reduce_kernel<64>, dim3(rblocks), dim3(256), 0, stream, qg, rec, sstart,
                            pstart, nbk, dK, dV);
     return hipGetLastError();
 }
@@ -736,15 +783,15 @@ hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const voi
     switch (d) {
         case 16:
             hipLaunchKernelGGL(csr_coef_kernel<16>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
-                               idx, lse, N, H, k, scale, dQ, coef, nullptr, nullptr);
+                               idx, lse, N, H, k, scale, dQ, coef, nullptr);
             break;
         case 32:
             hipLaunchKernelGGL(csr_coef_kernel<32>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
-                               idx, lse, N, H, k, scale, dQ, coef, nullptr, nullptr);
+                               idx, lse, N, H, k, scale, dQ, coef, nullptr);
             break;
         case 64:
             hipLaunchKernelGGL(csr_coef_kernel<64>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
-                               idx, lse, N, H, k, scale, dQ, coef, nullptr, nullptr);
+                               idx, lse, N, H, k, scale, dQ, coef, nullptr);
             break;
         default:
             return hipErrorInvalidValue;
