@@ -550,13 +550,20 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     // window masks held like mask_lo / mask_hi; left out of every mask.
     uint32_t warm_lo = 0, warm_hi = 0;
     // Masks of windows 64 bt .. 64 bt + 63; returns how many superblocks
-    // they keep.  Bound tile g holds superblocks 32 g .. 32 g + 31, scored
+    // they keep.  With lower, forms no masks and instead raises each query's
+    // theta from lower bounds: every key of a superblock also scores at
+    // least q.c - |q|_up R (the same MFMA with the sign of |q|_up flipped;
+    // the margins that make q.c + |q|_up R an upper bound of the fp32 scores
+    // bound the rounding in this direction as well).  A superblock that lies
+    // wholly inside the graph holds 256 keys, so when k <= 256 the largest
+    // such value over those superblocks is at most the query's k-th best
+    // score, and the float below it is a valid theta.  Bound tile g holds superblocks 32 g .. 32 g + 31, scored
     // like key tiles with the query's |q| bound entry as one more chunk; a
     // window's two tiles are loaded while the previous window is scored.
     // With track, each lane also notes, per query block, the superblock of
     // largest bound among its rows (best_sb, -1 for an invalid query).
     int best_sb[QB];
-    auto compute_batch = [&](int bt, bool track) {
+    auto compute_batch = [&](int bt, bool track, bool lower) {
         const int wlo = bt * 64;
         const int whi = min(nwin, wlo + 64);
         uint64_t mv = 0;
@@ -565,12 +572,16 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         float best_v[QB];
 #pragma unroll
         for (int b = 0; b < QB; ++b) {
-            qa[b] = __builtin_bit_cast(bf16x8, make_uint4(half == 0 ? qn_up[b] : 0u, 0u, 0u, 0u));
+            qa[b] = __builtin_bit_cast(bf16x8, make_uint4(half == 0 ? (lower ? (qn_up[b] | 0x8000u) : qn_up[b]) : 0u, 0u, 0u, 0u));
             best_v[b] = -INFINITY;
             best_sb[b] = -1;
         }
         uint64_t todo = whi - wlo == 64 ? ~0ull : (1ull << (whi - wlo)) - 1ull;
-        if (full_batch == bt) todo &= __builtin_amdgcn_ballot_w64((full_lo | full_hi) != 0u);
+        if (full_batch == bt && !lower) todo &= __builtin_amdgcn_ballot_w64((full_lo | full_hi) != 0u);
+        const int nfull = (key_hi - key_lo) / (32 * SBT);
+        float low_v[QB];
+#pragma unroll
+        for (int b = 0; b < QB; ++b) low_v[b] = -INFINITY;
         // Bound tiles of the next windows to score, PD windows ahead (two
         // where registers allow).
         constexpr int PD = NC <= 2 ? 2 : 1;
@@ -620,6 +631,16 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
                     bacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, cc[ct][NC]),
                                                                       qa[b], bacc[b], 0, 0, 0);
                 }
+                if (lower) {
+                    const int sb0 = 64 * w + 32 * ct;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const bool full = sb0 + tile_row(r, half) < nfull;
+#pragma unroll
+                        for (int b = 0; b < QB; ++b) low_v[b] = full ? fmaxf(low_v[b], bacc[b][r]) : low_v[b];
+                    }
+                    continue;
+                }
                 // bit 15 - r: some block's bound beats its theta (theta - bound
                 // is negative exactly then; -0 only adds a row)
                 uint32_t lm = 0;
@@ -646,6 +667,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
                 }
                 m |= (uint64_t)bits << (32 * ct);
             }
+            if (lower) continue;
             const int nv = nsb - 64 * w;
             if (nv < 64) m &= (1ull << nv) - 1ull;
             if (lane == w - wlo) {
@@ -653,6 +675,14 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
                 if (bt == 0) mv &= ~((uint64_t)warm_lo | ((uint64_t)warm_hi << 32));
             }
             needed += __builtin_popcountll(m);
+        }
+        if (lower) {
+#pragma unroll
+            for (int b = 0; b < QB; ++b) {
+                const float lv = fmaxf(low_v[b], __shfl_xor(low_v[b], 32));
+                if (theta[b] != INFINITY && lv > -INFINITY) theta[b] = fmaxf(theta[b], float_below(lv));
+            }
+            return 0;
         }
         mask_lo = full_lo = (uint32_t)mv;
         mask_hi = full_hi = (uint32_t)(mv >> 32);
@@ -693,7 +723,9 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         bool seeded = true;
 #pragma unroll
         for (int b = 0; b < QB; ++b) seeded = seeded && __builtin_amdgcn_ballot_w64(theta[b] == -INFINITY) == 0ull;
-        const int needed = compute_batch(0, nwin <= 64);
+        // (superblock s holds positions 256 s .. 256 s + 255 when key_lo = 0)
+        if (key_lo == 0 && k <= 32 * SBT) compute_batch(0, false, true);
+        const int needed = compute_batch(0, nwin <= 64, false);
         // Seeded items whose masks still keep more than half of the
         // superblocks warm up as well: a poorly seeded query widens the
         // masks of its whole wave.
@@ -835,7 +867,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
                 warm_pending = false;
                 finished = false;
                 stop_at = scanned + 16;
-                compute_batch(0, false);
+                compute_batch(0, false, false);
                 w = 0;
                 wv = 0;
                 wm = read_mask(0);
@@ -843,7 +875,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
             }
             if (scanned >= stop_at) stop_at = 4 * scanned;
             const int bt = wm != 0ull ? (w >> 6) : ((w + 1 == nwin ? 0 : w + 1) >> 6);
-            compute_batch(bt, false);
+            compute_batch(bt, false, false);
             if ((w >> 6) == bt) wm &= read_mask(w);
             continue;
         }

@@ -39,40 +39,75 @@ def _regs(text):
     return out
 
 
+LABEL = re.compile(r"^(\.LBB\w+|\.Ltmp\w+):")
+BRANCH = re.compile(r"^s_(c?branch)\w*\s+(\.\w+)")
+
+
 def early_reads(body):
-    """(load, offending instruction) pairs of one kernel's assembly lines."""
+    """(load, offending instruction) pairs of one kernel's assembly lines.
+
+    From every ring load, every control-flow path is followed (fall-through,
+    and the targets of s_branch and s_cbranch_*) up to a wait that covers the
+    load; a path that reads one of the load's registers first is reported.
+    Registers that a path overwrites drop out of that path's live set."""
+    labels = {}
+    for i, line in enumerate(body):
+        m = LABEL.match(line)
+        if m:
+            labels[m.group(1)] = i
     found = []
     for i, line in enumerate(body):
         m = RING_LOAD.match(line)
         if not m:
             continue
-        live = (set(range(int(m.group(1)), int(m.group(2)) + 1)) if m.group(1)
-                else {int(m.group(3))})
-        issued_after = 0
-        for x in body[i + 1:]:
-            if not x or x.startswith((";", ".")):
-                continue
-            w = WAIT.match(x)
-            if w and int(w.group(1)) <= issued_after:
-                break
-            op = x.split()[0]
-            if op.startswith(VMEM):
-                issued_after += 1
-            if op.startswith("s_"):
-                continue
-            fields = x.split(None, 1)
-            if len(fields) < 2:
-                continue
-            operands = fields[1].split(",")
-            stores = op.startswith(("global_store", "buffer_store", "flat_store", "ds_write"))
-            sources = fields[1] if stores else ",".join(operands[1:])
-            if _regs(sources) & live:
-                found.append((line, x))
-                break
-            if not stores and not op.startswith("v_cmp"):
-                live -= _regs(operands[0])
-                if not live:
+        live0 = frozenset(range(int(m.group(1)), int(m.group(2)) + 1)) if m.group(1) else frozenset({int(m.group(3))})
+        stack = [(i + 1, 0, live0)]
+        seen = set()
+        hit = None
+        while stack and hit is None:
+            pos, issued_after, live = stack.pop()
+            while pos < len(body):
+                state = (pos, min(issued_after, 64), live)
+                if state in seen:
                     break
+                seen.add(state)
+                x = body[pos]
+                if not x or x.startswith((";", ".")):
+                    pos += 1
+                    continue
+                w = WAIT.match(x)
+                if w and int(w.group(1)) <= issued_after:
+                    break
+                op = x.split()[0]
+                if op.startswith(VMEM):
+                    issued_after += 1
+                if op.startswith("s_"):
+                    br = BRANCH.match(x)
+                    if br and br.group(2) in labels:
+                        stack.append((labels[br.group(2)] + 1, issued_after, live))
+                        if br.group(1) == "branch":
+                            break          # unconditional: no fall-through
+                    elif op in ("s_endpgm", "s_setpc_b64"):
+                        break
+                    pos += 1
+                    continue
+                fields = x.split(None, 1)
+                if len(fields) < 2:
+                    pos += 1
+                    continue
+                operands = fields[1].split(",")
+                stores = op.startswith(("global_store", "buffer_store", "flat_store", "ds_write"))
+                sources = fields[1] if stores else ",".join(operands[1:])
+                if _regs(sources) & live:
+                    hit = (line, x)
+                    break
+                if not stores and not op.startswith("v_cmp"):
+                    live = live - _regs(operands[0])
+                    if not live:
+                        break
+                pos += 1
+        if hit is not None:
+            found.append(hit)
     return found
 
 
@@ -111,3 +146,29 @@ def test_checker_flags_a_copy_before_the_wait():
           "v_mov_b32_e32 v40, v6"]
     # v[2:5] is covered by vmcnt(1) (one load issued after it); v[6:9] is not
     assert early_reads(ok) == [(ok[1], ok[4])]
+
+
+def test_checker_follows_branches():
+    # a read of the ring register at a branch target is caught; one that only
+    # follows an unconditional branch in the layout is not on any path
+    body = ["global_load_dwordx4 v[2:5], v121, s[0:1] offset:0",
+            "s_cbranch_scc0 .LBB0_2",
+            "s_waitcnt vmcnt(0)",
+            "s_branch .LBB0_3",
+            "v_mov_b32_e32 v40, v2",
+            ".LBB0_2:",
+            "v_mov_b32_e32 v41, v3",
+            ".LBB0_3:",
+            "s_endpgm"]
+    assert early_reads(body) == [(body[0], body[6])]
+    body[1] = "s_cbranch_scc0 .LBB0_3"
+    assert early_reads(body) == []
+    # a loop back-edge that reaches the read before the wait
+    loop = [".LBB0_1:",
+            "v_mov_b32_e32 v41, v3",
+            "s_waitcnt vmcnt(0)",
+            "global_load_dwordx4 v[2:5], v121, s[0:1] offset:0",
+            "s_cbranch_scc1 .LBB0_1",
+            "s_waitcnt vmcnt(0)",
+            "s_endpgm"]
+    assert early_reads(loop) == [(loop[3], loop[1])]
