@@ -28,7 +28,6 @@
 namespace kmip {
 namespace {
 
-constexpr int kSlotsPerLane = (128 + 15) / 16;
 constexpr int kScanBlock = 1024;     // counts per block of the scan
 constexpr int kChunk = 1024;         // sorted pairs per wave in the reduction
 
@@ -61,13 +60,17 @@ __device__ __forceinline__ void team_sum_transpose(const float (&acc)[D], float 
     halve_step<D / 8>(a2, out, tl, 1);
 }
 
-// 1. Per (query, head), a team of 16 lanes with the slots on lanes.
-template <int D>
+// 1. Per (query, head), a team of 16 lanes with the slots on lanes, NS
+// slots per lane (k <= 16 NS).
+template <int D, int NS>
 __global__ __launch_bounds__(256) void csr_coef_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
     int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float2* __restrict__ coef,
     uint16_t* __restrict__ QGt) {
+    // key rows kept in registers for dQ when they take at most 64 dwords a
+    // lane; otherwise read again (from cache)
+    constexpr bool kKeep = D / 2 * NS <= 64;
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
     if (qh >= (int64_t)N * H) return;  // whole team exits together
@@ -83,21 +86,27 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
     load_row_f32<D>(q, Q + (size_t)qh * D);
     load_row_f32<D>(g, dO + (size_t)qh * D);
     const float l = lse[qh];
-    const int ns = (k + 15) >> 4;
-    float p[kSlotsPerLane], dp[kSlotsPerLane];
-    int32_t jj[kSlotsPerLane];
+    float p[NS], dp[NS];
+    int32_t jj[NS];
+    uint4 kw[kKeep ? NS : 1][D / 8];
     float dsum = 0.0f;
 #pragma unroll
-    for (int s = 0; s < kSlotsPerLane; ++s) {
+    for (int s = 0; s < NS; ++s) {
         p[s] = 0.0f;
         dp[s] = 0.0f;
         jj[s] = -1;
         const int slot = tl + 16 * s;
-        if (s < ns && slot < k && l != -INFINITY) {
+        if (slot < k && l != -INFINITY) {
             const int32_t j = idx[(size_t)qh * k + slot];
             if (j >= 0 && j < N) {
                 jj[s] = j;
-                const float z = scale * dot_row_bf16<D>(q, K + ((size_t)j * H + h) * D);
+                uint4 w[D / 8];
+                load_row_words<D>(w, K + ((size_t)j * H + h) * D);
+                if constexpr (kKeep) {
+#pragma unroll
+                    for (int c = 0; c < D / 8; ++c) kw[s][c] = w[c];
+                }
+                const float z = scale * dot_words_bf16<D>(q, w);
                 p[s] = __expf(z - l);
                 dp[s] = dot_row_bf16<D>(g, V + ((size_t)j * H + h) * D);
             }
@@ -105,23 +114,34 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
         dsum = fmaf(p[s], dp[s], dsum);
     }
     dsum = group16_sum(dsum);
-    // dQ: each slot lane adds g_s k_j over its own slots (the key row is read
-    // again, from cache), then the team reduces the D-vector so that lane tl
-    // ends up with dimensions tl, tl+16, ...
+    // dQ: each slot lane adds g_s k_j over its own slots, then the team
+    // reduces the D-vector so that lane tl ends up with dimensions tl, tl+16, ...
     float acc[D];
 #pragma unroll
     for (int t = 0; t < D; ++t) acc[t] = 0.0f;
 #pragma unroll
-    for (int s = 0; s < kSlotsPerLane; ++s) {
+    for (int s = 0; s < NS; ++s) {
         const int slot = tl + 16 * s;
-        if (s < ns && slot < k) {
+        if (slot < k) {
             const float gs = p[s] * (dp[s] - dsum);
             coef[(size_t)qh * k + slot] = make_float2(scale * gs, p[s]);
             if (jj[s] >= 0) {
-                float kr[D];
-                load_row_f32<D>(kr, K + ((size_t)jj[s] * H + h) * D);
+                uint4 w[D / 8];
+                if constexpr (kKeep) {
 #pragma unroll
-                for (int t = 0; t < D; ++t) acc[t] = fmaf(gs, kr[t], acc[t]);
+                    for (int c = 0; c < D / 8; ++c) w[c] = kw[s][c];
+                } else {
+                    load_row_words<D>(w, K + ((size_t)jj[s] * H + h) * D);
+                }
+#pragma unroll
+                for (int c = 0; c < D / 8; ++c) {
+                    const uint32_t ww[4] = {w[c].x, w[c].y, w[c].z, w[c].w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        acc[8 * c + 2 * e] = fmaf(gs, bf16_bits_to_f32(ww[e] & 0xFFFFu), acc[8 * c + 2 * e]);
+                        acc[8 * c + 2 * e + 1] = fmaf(gs, bf16_bits_to_f32(ww[e] >> 16), acc[8 * c + 2 * e + 1]);
+                    }
+                }
             }
         }
     }
@@ -129,6 +149,26 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
     team_sum_transpose<D>(acc, out, tl);
 #pragma unroll
     for (int u = 0; u < D / 16; ++u) dQ[(size_t)qh * D + 16 * u + tl] = scale * out[u];
+}
+
+// Launches csr_coef_kernel<D, NS> with NS the smallest power of two >= k/16.
+template <int D>
+void launch_coef(unsigned blocks, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
+                 const uint16_t* v, const uint16_t* g, const int32_t* idx, const float* lse, int32_t N,
+                 int32_t H, int32_t k, float scale, float* dQ, float2* coef, uint16_t* qg) {
+    const int ns = (k + 15) / 16;
+    if (ns <= 1)
+        hipLaunchKernelGGL((csr_coef_kernel<D, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse, N,
+                           H, k, scale, dQ, coef, qg);
+    else if (ns <= 2)
+        hipLaunchKernelGGL((csr_coef_kernel<D, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse, N,
+                           H, k, scale, dQ, coef, qg);
+    else if (ns <= 4)
+        hipLaunchKernelGGL((csr_coef_kernel<D, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse, N,
+                           H, k, scale, dQ, coef, qg);
+    else
+        hipLaunchKernelGGL((csr_coef_kernel<D, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse, N,
+                           H, k, scale, dQ, coef, qg);
 }
 
 // Key row of slot s of query-head qh, or -1 (padding).
@@ -689,14 +729,11 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     if ((e = launch_fill_zero(dV, (size_t)nh * d, stream)) != hipSuccess) return e;
     const unsigned team_blocks = (unsigned)((nh + 15) / 16);
     if (d == 16)
-        hipLaunchKernelGGL(csr_coef_kernel<16>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qg);
+        launch_coef<16>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, qg);
     else if (d == 32)
-        hipLaunchKernelGGL(csr_coef_kernel<32>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qg);
+        launch_coef<32>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, qg);
     else
-        hipLaunchKernelGGL(csr_coef_kernel<64>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qg);
+        launch_coef<64>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, qg);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // pairs per counting workgroup: about 1024 workgroups, 8192 .. 65536 pairs each
     const uint32_t per = (uint32_t)std::min<size_t>(65536, std::max<size_t>(8192, (pairs / 1024 + 255) / 256 * 256));
@@ -782,16 +819,13 @@ hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const voi
     const unsigned team_blocks = (unsigned)((nh + 15) / 16);
     switch (d) {
         case 16:
-            hipLaunchKernelGGL(csr_coef_kernel<16>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
-                               idx, lse, N, H, k, scale, dQ, coef, nullptr);
+            launch_coef<16>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, nullptr);
             break;
         case 32:
-            hipLaunchKernelGGL(csr_coef_kernel<32>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
-                               idx, lse, N, H, k, scale, dQ, coef, nullptr);
+            launch_coef<32>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, nullptr);
             break;
         case 64:
-            hipLaunchKernelGGL(csr_coef_kernel<64>, dim3(team_blocks), dim3(256), 0, stream, q, kk, v, g,
-                               idx, lse, N, H, k, scale, dQ, coef, nullptr);
+            launch_coef<64>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, nullptr);
             break;
         default:
             return hipErrorInvalidValue;

@@ -40,16 +40,23 @@ __device__ __forceinline__ float key_score(uint64_t key) {
     return score_from_code((uint32_t)(key >> 32));
 }
 
-// Dot product of a float32 query row held in registers with a bf16 row in
-// global memory, accumulated in float32 in dimension order t = 0..D-1.  Both
-// the aggregate and the backward kernels call this one function, so they see
+// A bf16 row of D values as D/8 16-byte words.
+template <int D>
+__device__ __forceinline__ void load_row_words(uint4 (&w)[D / 8], const uint16_t* __restrict__ row) {
+#pragma unroll
+    for (int c = 0; c < D / 8; ++c) w[c] = *reinterpret_cast<const uint4*>(row + 8 * c);
+}
+
+// Dot product of a float32 query row held in registers with a bf16 row,
+// accumulated in float32 in dimension order t = 0..D-1.  The aggregate and
+// the backward kernels both go through this one function, so they see
 // bit-identical scores.
 template <int D>
-__device__ __forceinline__ float dot_row_bf16(const float (&q)[D], const uint16_t* __restrict__ row) {
+__device__ __forceinline__ float dot_words_bf16(const float (&q)[D], const uint4 (&wv)[D / 8]) {
     float s = 0.0f;
 #pragma unroll
     for (int c = 0; c < D / 8; ++c) {
-        uint4 u = *reinterpret_cast<const uint4*>(row + 8 * c);
+        const uint4 u = wv[c];
         uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -58,6 +65,13 @@ __device__ __forceinline__ float dot_row_bf16(const float (&q)[D], const uint16_
         }
     }
     return s;
+}
+
+template <int D>
+__device__ __forceinline__ float dot_row_bf16(const float (&q)[D], const uint16_t* __restrict__ row) {
+    uint4 w[D / 8];
+    load_row_words<D>(w, row);
+    return dot_words_bf16<D>(q, w);
 }
 
 template <int D>
