@@ -6,24 +6,25 @@
 // scores are recomputed in fp32 from q_i and the gathered key rows, with the
 // same routine the backward uses, so the weights of the two passes agree.
 //
-// Mapping: a team of 16 lanes per (query, head), 16 teams per workgroup.
-// Phase 1 puts key slots on lanes (slot = lane + 16 s) to form the scores and
-// the softmax statistics with 16-lane butterflies; phase 2 puts output
-// dimensions on lanes (dim = lane + 16 u) and walks the slots, so each team
-// reads a gathered value row as one contiguous segment.
+// Mapping: a team of 16 lanes per (query, head), 16 teams per workgroup,
+// with the key slots on lanes (slot = lane + 16 s, NS slots per lane).  Each
+// lane gathers its slots' key rows and forms their scores; 16-lane
+// butterflies give the softmax statistics; each lane then adds its slots'
+// weighted value rows (gathered in the same round trip as the key rows when
+// they fit in 64 registers, else right after) into a D-vector, and a
+// transposed team reduction leaves dimensions tl, tl + 16, ... on lane tl.
 #include "kmip_device.h"
 #include "kmip_internal.h"
 
 namespace kmip {
 namespace {
 
-constexpr int kMaxSlotsPerLane = (128 + 15) / 16;
-
-template <int D>
+template <int D, int NS>
 __global__ __launch_bounds__(256) void attend_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const int32_t* __restrict__ idx, int32_t N, int32_t H, int32_t k, float scale,
     float* __restrict__ out, float* __restrict__ lse) {
+    constexpr bool kKeep = D / 2 * NS <= 64;
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
     if (qh >= (int64_t)N * H) return;  // whole team exits together
@@ -32,19 +33,20 @@ __global__ __launch_bounds__(256) void attend_kernel(
     float q[D];
     load_row_f32<D>(q, Q + (size_t)qh * D);
 
-    const int ns = (k + 15) >> 4;
-    float z[kMaxSlotsPerLane];
-    int32_t jj[kMaxSlotsPerLane];
+    float z[NS];
+    int32_t jj[NS];
+    uint4 vw[kKeep ? NS : 1][D / 8];
     float zmax = -INFINITY;
 #pragma unroll
-    for (int s = 0; s < kMaxSlotsPerLane; ++s) {
+    for (int s = 0; s < NS; ++s) {
         z[s] = -INFINITY;
         jj[s] = -1;
         const int slot = tl + 16 * s;
-        if (s < ns && slot < k) {
+        if (slot < k) {
             const int32_t j = idx[(size_t)qh * k + slot];
             if (j >= 0 && j < N) {
                 jj[s] = j;
+                if constexpr (kKeep) load_row_words<D>(vw[s], V + ((size_t)j * H + h) * D);
                 z[s] = scale * dot_row_bf16<D>(q, K + ((size_t)j * H + h) * D);
             }
         }
@@ -52,39 +54,66 @@ __global__ __launch_bounds__(256) void attend_kernel(
     }
     zmax = group16_max(zmax);
 
-    float w[kMaxSlotsPerLane];
+    float w[NS];
     float zs = 0.0f;
 #pragma unroll
-    for (int s = 0; s < kMaxSlotsPerLane; ++s) {
+    for (int s = 0; s < NS; ++s) {
         w[s] = jj[s] >= 0 ? __expf(z[s] - zmax) : 0.0f;
         zs += w[s];
     }
     zs = group16_sum(zs);
 
-    constexpr int U = D / 16;
-    float o[U];
+    float acc[D];
 #pragma unroll
-    for (int u = 0; u < U; ++u) o[u] = 0.0f;
+    for (int t = 0; t < D; ++t) acc[t] = 0.0f;
 #pragma unroll
-    for (int s = 0; s < kMaxSlotsPerLane; ++s) {
-        if (s < ns) {
-            for (int src = 0; src < 16; ++src) {
-                const float ws = __shfl(w[s], src, 16);
-                const int32_t js = __shfl(jj[s], src, 16);
-                if (js >= 0) {
-                    const uint16_t* vrow = V + ((size_t)js * H + h) * D + tl;
+    for (int s = 0; s < NS; ++s) {
+        if (jj[s] >= 0) {
+            uint4 wv[D / 8];
+            if constexpr (kKeep) {
 #pragma unroll
-                    for (int u = 0; u < U; ++u) o[u] = fmaf(ws, bf16_bits_to_f32(vrow[16 * u]), o[u]);
+                for (int c = 0; c < D / 8; ++c) wv[c] = vw[s][c];
+            } else {
+                load_row_words<D>(wv, V + ((size_t)jj[s] * H + h) * D);
+            }
+#pragma unroll
+            for (int c = 0; c < D / 8; ++c) {
+                const uint32_t ww[4] = {wv[c].x, wv[c].y, wv[c].z, wv[c].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[8 * c + 2 * e] = fmaf(w[s], bf16_bits_to_f32(ww[e] & 0xFFFFu), acc[8 * c + 2 * e]);
+                    acc[8 * c + 2 * e + 1] = fmaf(w[s], bf16_bits_to_f32(ww[e] >> 16), acc[8 * c + 2 * e + 1]);
                 }
             }
         }
     }
+    float o[D / 16];
+    team_sum_transpose<D>(acc, o, tl);
 
     const bool any = zmax != -INFINITY;
     const float inv = any ? 1.0f / zs : 0.0f;
 #pragma unroll
-    for (int u = 0; u < U; ++u) out[(size_t)qh * D + tl + 16 * u] = o[u] * inv;
+    for (int u = 0; u < D / 16; ++u) out[(size_t)qh * D + tl + 16 * u] = o[u] * inv;
     if (tl == 0) lse[qh] = any ? zmax + __logf(zs) : -INFINITY;
+}
+
+template <int D>
+void launch_attend_d(unsigned blocks, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
+                     const uint16_t* v, const int32_t* idx, int32_t N, int32_t H, int32_t k, float scale,
+                     float* out, float* lse) {
+    const int ns = (k + 15) / 16;
+    if (ns <= 1)
+        hipLaunchKernelGGL((attend_kernel<D, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H, k,
+                           scale, out, lse);
+    else if (ns <= 2)
+        hipLaunchKernelGGL((attend_kernel<D, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H, k,
+                           scale, out, lse);
+    else if (ns <= 4)
+        hipLaunchKernelGGL((attend_kernel<D, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H, k,
+                           scale, out, lse);
+    else
+        hipLaunchKernelGGL((attend_kernel<D, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H, k,
+                           scale, out, lse);
 }
 
 }  // namespace
@@ -100,16 +129,13 @@ hipError_t launch_attend(const void* Q, const void* K, const void* V, const int3
     const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
     switch (d) {
         case 16:
-            hipLaunchKernelGGL(attend_kernel<16>, dim3(blocks), dim3(256), 0, stream, q, kk, v, idx,
-                               N, H, k, scale, out, lse);
+            launch_attend_d<16>(blocks, stream, q, kk, v, idx, N, H, k, scale, out, lse);
             break;
         case 32:
-            hipLaunchKernelGGL(attend_kernel<32>, dim3(blocks), dim3(256), 0, stream, q, kk, v, idx,
-                               N, H, k, scale, out, lse);
+            launch_attend_d<32>(blocks, stream, q, kk, v, idx, N, H, k, scale, out, lse);
             break;
         case 64:
-            hipLaunchKernelGGL(attend_kernel<64>, dim3(blocks), dim3(256), 0, stream, q, kk, v, idx,
-                               N, H, k, scale, out, lse);
+            launch_attend_d<64>(blocks, stream, q, kk, v, idx, N, H, k, scale, out, lse);
             break;
         default:
             return hipErrorInvalidValue;

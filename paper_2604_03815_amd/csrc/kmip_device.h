@@ -101,4 +101,33 @@ __device__ __forceinline__ float group16_sum(float v) {
     return v;
 }
 
+// Sum of a D-vector over the 16 lanes of a team, transposed: out[u] of lane
+// tl receives the team sum of dimension 16u + tl.  Recursive halving: at the
+// step with partner tl ^ m (m = 8, 4, 2, 1) a lane keeps the half of its
+// dimensions whose bit m matches its own and adds the partner's values of
+// that half, so the step exchanges half of what is left (15 shuffles per 16
+// dimensions, against 64 for a full butterfly per dimension).
+template <int N>
+__device__ __forceinline__ void halve_step(const float* in, float* outv, int tl, int m) {
+    const bool hi = (tl & m) != 0;
+#pragma unroll
+    for (int b = 0; b < N; b += 2 * m) {
+#pragma unroll
+        for (int j = 0; j < m; ++j) {
+            const float lo_v = in[b + j], hi_v = in[b + m + j];
+            const float own = hi ? hi_v : lo_v, other = hi ? lo_v : hi_v;
+            outv[b / 2 + j] = own + __shfl_xor(other, m, 16);
+        }
+    }
+}
+
+template <int D>
+__device__ __forceinline__ void team_sum_transpose(const float (&acc)[D], float (&out)[D / 16], int tl) {
+    float a8[D / 2], a4[D / 4], a2[D / 8];
+    halve_step<D>(acc, a8, tl, 8);
+    halve_step<D / 2>(a8, a4, tl, 4);
+    halve_step<D / 4>(a4, a2, tl, 2);
+    halve_step<D / 8>(a2, out, tl, 1);
+}
+
 }  // namespace kmip
