@@ -20,10 +20,10 @@ namespace {
 constexpr int C = kGroupCenters;
 
 // centers[h][c][:] = unit vector of query row floor((2c+1) N / 2C) of head h
-// (zero if that row is zero).
+// (zero if that row is zero), rounded to bf16 (nearest even).
 __global__ __launch_bounds__(256) void group_centers_kernel(const uint16_t* __restrict__ Q,
                                                             int32_t N, int32_t H, int32_t d,
-                                                            float* __restrict__ centers) {
+                                                            uint16_t* __restrict__ centers) {
     const int c = threadIdx.x;
     const int h = blockIdx.x;
     const int64_t row = ((int64_t)(2 * c + 1) * N) / (2 * C);
@@ -34,56 +34,62 @@ __global__ __launch_bounds__(256) void group_centers_kernel(const uint16_t* __re
         ss = fmaf(x, x, ss);
     }
     const float inv = ss > 0.0f ? rsqrtf(ss) : 0.0f;
-    float* dst = centers + ((size_t)h * C + c) * d;
-    for (int t = 0; t < d; ++t) dst[t] = bf16_bits_to_f32(q[t]) * inv;
+    uint16_t* dst = centers + ((size_t)h * C + c) * d;
+    for (int t = 0; t < d; ++t) {
+        const uint32_t b = __float_as_uint(bf16_bits_to_f32(q[t]) * inv);
+        dst[t] = (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+    }
 }
 
 // label[h][i] = argmax_c <q_i, center_c> (lowest c on ties); hist[h][c] counts
-// the labels.  One block of 256 queries of one head; the head's centres pass
-// through LDS in chunks of at most 32 KB, and every thread reads the same
-// centre at a time (broadcast).
+// the labels.  A wave takes 32 queries of one head and scores them against
+// 32 centres at a time with one bf16 MFMA per 16 dimensions (A = centres,
+// B = queries, so lane l holds the scores of query l % 32); lanes l and
+// l + 32 hold different centres of the same query and merge their maxima.
+// The labels only decide which queries the select kernel groups together.
 template <int D>
 __global__ __launch_bounds__(256) void group_label_kernel(const uint16_t* __restrict__ Q,
-                                                          const float* __restrict__ centers,
+                                                          const uint16_t* __restrict__ centers,
                                                           int32_t N, int32_t H,
                                                           uint16_t* __restrict__ label,
                                                           int32_t* __restrict__ hist) {
-    constexpr int CH = (8192 / D) < C ? (8192 / D) : C;
-    __shared__ float cs[CH * D];
+    constexpr int NC = D / 16;
     __shared__ int32_t lh[C];
     const int h = blockIdx.y;
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int col = lane & 31, half = lane >> 5;
+    const int64_t i = (int64_t)blockIdx.x * 128 + (threadIdx.x >> 6) * 32 + col;
     const bool valid = i < N;
-    float q[D];
-    const uint16_t* row = Q + ((size_t)(valid ? i : 0) * H + h) * D;
-#pragma unroll
-    for (int c8 = 0; c8 < D / 8; ++c8) {
-        const uint4 u = *reinterpret_cast<const uint4*>(row + 8 * c8);
-        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            q[8 * c8 + 2 * e] = bf16_bits_to_f32(w[e] & 0xFFFFu);
-            q[8 * c8 + 2 * e + 1] = bf16_bits_to_f32(w[e] >> 16);
-        }
-    }
     lh[threadIdx.x] = 0;
+    bf16x8 bq[NC];
+    const uint16_t* row = Q + ((size_t)(valid ? i : 0) * H + h) * D + 8 * half;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) bq[c] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(row + 16 * c));
+    const uint16_t* ch = centers + (size_t)h * C * D + (size_t)col * D + 8 * half;
     float best = -INFINITY;
     int arg = 0;
-    for (int c0 = 0; c0 < C; c0 += CH) {
-        __syncthreads();
-        for (int e = threadIdx.x; e < CH * D; e += 256) cs[e] = centers[((size_t)h * C + c0) * D + e];
-        __syncthreads();
-        for (int c = 0; c < CH; ++c) {
-            float s = 0.0f;
+    for (int c0 = 0; c0 < C; c0 += 32) {
+        f32x16 acc = f32x16{};
 #pragma unroll
-            for (int t = 0; t < D; ++t) s = fmaf(q[t], cs[c * D + t], s);
-            if (s > best) {
-                best = s;
-                arg = c0 + c;
+        for (int c = 0; c < NC; ++c)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(ch + (size_t)c0 * D + 16 * c)), bq[c],
+                acc, 0, 0, 0);
+        // rows 8 (r / 4) + 4 half + r % 4 increase with r: strict > keeps the lowest centre
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int cc = c0 + 8 * (r >> 2) + 4 * half + (r & 3);
+            if (acc[r] > best) {
+                best = acc[r];
+                arg = cc;
             }
         }
     }
-    if (valid) {
+    const float ob = __shfl_xor(best, 32);
+    const int oa = __shfl_xor(arg, 32);
+    if (ob > best || (ob == best && oa < arg)) arg = oa;
+    __syncthreads();
+    if (valid && half == 0) {
         label[(size_t)h * N + i] = (uint16_t)arg;
         atomicAdd(&lh[arg], 1);
     }
@@ -147,7 +153,7 @@ __global__ __launch_bounds__(256) void group_scatter_kernel(const uint16_t* __re
 
 size_t group_workspace_bytes(int32_t N, int32_t H, int32_t d) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };
-    return al((size_t)H * C * d * sizeof(float)) + al((size_t)H * N * sizeof(uint16_t)) +
+    return al((size_t)H * C * d * sizeof(uint16_t)) + al((size_t)H * N * sizeof(uint16_t)) +
            al((size_t)2 * H * C * sizeof(int32_t)) + al((size_t)H * N * sizeof(int32_t));
 }
 
@@ -155,8 +161,8 @@ hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, 
                                 QueryGroups* out, hipStream_t stream) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };
     char* p = reinterpret_cast<char*>(ws);
-    float* centers = reinterpret_cast<float*>(p);
-    p += al((size_t)H * C * d * sizeof(float));
+    uint16_t* centers = reinterpret_cast<uint16_t*>(p);
+    p += al((size_t)H * C * d * sizeof(uint16_t));
     uint16_t* label = reinterpret_cast<uint16_t*>(p);
     p += al((size_t)H * N * sizeof(uint16_t));
     int32_t* hist = reinterpret_cast<int32_t*>(p);          // [H][C], then seed_ref [H][C]
@@ -172,7 +178,7 @@ hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, 
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(group_centers_kernel, dim3(H), dim3(C), 0, stream, q, N, H, d, centers);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const dim3 grid((unsigned)((N + 255) / 256), (unsigned)H);
+    const dim3 grid((unsigned)((N + 127) / 128), (unsigned)H);
     if (d == 16)
         hipLaunchKernelGGL(group_label_kernel<16>, grid, dim3(256), 0, stream, q, centers, N, H, label, hist);
     else if (d == 32)

@@ -21,6 +21,8 @@
 // only decides which tiles the select kernel visits together: it records
 // each candidate by its original key index, so the result does not depend
 // on it.
+#include <utility>
+
 #include "kmip_device.h"
 #include "kmip_internal.h"
 
@@ -114,8 +116,7 @@ __device__ __forceinline__ float wave_min(float v) {
 // from the mean), the quantisation range of the sample's projections, and
 // zeroed histograms and counters.
 template <int D>
-__global__ __launch_bounds__(64) void tree_axis_kernel(const uint16_t* __restrict__ K,
-                                                       const int32_t* __restrict__ perm, int32_t N,
+__global__ __launch_bounds__(64) void tree_axis_kernel(const uint16_t* __restrict__ kp, int32_t N,
                                                        int32_t H, int32_t lev, int32_t width,
                                                        float* __restrict__ nodef,
                                                        int32_t* __restrict__ nodeh) {
@@ -131,7 +132,7 @@ __global__ __launch_bounds__(64) void tree_axis_kernel(const uint16_t* __restric
     float x[D];
     if (act) {
         const int p = lo + (int)(((int64_t)(2 * t + 1) * n) / (2 * S));
-        load_row_f32<D>(x, K + ((size_t)perm[(size_t)h * N + p] * H + h) * D);
+        load_row_f32<D>(x, kp + ((size_t)h * N + p) * D);
     } else {
 #pragma unroll
         for (int i = 0; i < D; ++i) x[i] = 0.0f;
@@ -239,8 +240,7 @@ __device__ __forceinline__ int wave_ticket(int32_t* addr, bool active) {
 // Level lev: the 16-bit projection code of the key at each position of a
 // split node, and the histogram of its high byte per node.
 template <int D>
-__global__ __launch_bounds__(256) void tree_project_kernel(const uint16_t* __restrict__ K,
-                                                           const int32_t* __restrict__ perm, int32_t N,
+__global__ __launch_bounds__(256) void tree_project_kernel(const uint16_t* __restrict__ kp, int32_t N,
                                                            int32_t H, int32_t lev, int32_t width,
                                                            const float* __restrict__ nodef,
                                                            int32_t* __restrict__ nodeh,
@@ -258,7 +258,7 @@ __global__ __launch_bounds__(256) void tree_project_kernel(const uint16_t* __res
         int lo, n, idx;
         if (p >= N || !node_of(p, N, lev, lo, n, idx)) continue;
         float x[D];
-        load_row_f32<D>(x, K + ((size_t)perm[(size_t)h * N + p] * H + h) * D);
+        load_row_f32<D>(x, kp + ((size_t)h * N + p) * D);
         const uint32_t q = quantise<D>(nodef + ((size_t)h * width + idx) * (2 * D + 2), x);
         code[(size_t)h * N + p] = (uint16_t)q;
         if (agg && idx == idx0)
@@ -348,11 +348,15 @@ __global__ __launch_bounds__(256) void tree_hist2_kernel(int32_t N, int32_t lev,
 // one it starts in) tells its nodes apart.
 constexpr int kSlots = kBlockPos / (SBK + 1) + 2;
 
+// The key rows of the head-major copy move with their keys.
+template <int D>
 __global__ __launch_bounds__(256) void tree_scatter_kernel(int32_t N, int32_t lev, int32_t width,
                                                            int32_t* __restrict__ nodeh,
                                                            const uint16_t* __restrict__ code,
                                                            const int32_t* __restrict__ perm_in,
-                                                           int32_t* __restrict__ perm_out) {
+                                                           int32_t* __restrict__ perm_out,
+                                                           const uint16_t* __restrict__ kp_in,
+                                                           uint16_t* __restrict__ kp_out) {
     __shared__ int32_t cnt[kSlots][2];
     __shared__ int32_t sidx[kSlots];
     const int h = blockIdx.y;
@@ -394,13 +398,27 @@ __global__ __launch_bounds__(256) void tree_scatter_kernel(int32_t N, int32_t le
         const int p = base + i * 256 + t;
         if (p >= N) continue;
         const int32_t key = perm_in[(size_t)h * N + p];
-        perm_out[(size_t)h * N + dst[i] + (slot[i] >= 0 ? cnt[slot[i]][side[i]] : 0)] = key;
+        const size_t to = (size_t)h * N + dst[i] + (slot[i] >= 0 ? cnt[slot[i]][side[i]] : 0);
+        perm_out[to] = key;
+        const uint4* src = reinterpret_cast<const uint4*>(kp_in + ((size_t)h * N + p) * D);
+        uint4* out = reinterpret_cast<uint4*>(kp_out + to * D);
+#pragma unroll
+        for (int c = 0; c < D / 8; ++c) out[c] = src[c];
     }
 }
 
-__global__ __launch_bounds__(256) void iota_kernel(int32_t N, int32_t* __restrict__ perm) {
+// perm[h][p] = p and the head-major copy kp[h][p] = K row (p, h).
+template <int D>
+__global__ __launch_bounds__(256) void tree_init_kernel(const uint16_t* __restrict__ K, int32_t N, int32_t H,
+                                                        int32_t* __restrict__ perm, uint16_t* __restrict__ kp) {
     const int p = blockIdx.x * 256 + threadIdx.x;
-    if (p < N) perm[(size_t)blockIdx.y * N + p] = p;
+    const int h = blockIdx.y;
+    if (p >= N) return;
+    perm[(size_t)h * N + p] = p;
+    const uint4* src = reinterpret_cast<const uint4*>(K + ((size_t)p * H + h) * D);
+    uint4* dst = reinterpret_cast<uint4*>(kp + ((size_t)h * N + p) * D);
+#pragma unroll
+    for (int c = 0; c < D / 8; ++c) dst[c] = src[c];
 }
 
 // bf16 bits of x rounded to nearest even (finite x).
@@ -433,8 +451,7 @@ __device__ __forceinline__ uint16_t bf16_up(float x) {
 // only raises the bound further.  An empty superblock gets c = 0, R = 0;
 // the select kernel never scans superblocks past the last one anyway.
 template <int D>
-__global__ __launch_bounds__(256) void sb_bounds_kernel(const uint16_t* __restrict__ K,
-                                                        const int32_t* __restrict__ perm, int32_t N,
+__global__ __launch_bounds__(256) void sb_bounds_kernel(const uint16_t* __restrict__ kp, int32_t N,
                                                         int32_t H, int32_t ctiles,
                                                         uint16_t* __restrict__ bounds) {
     constexpr int NC = D / 16;
@@ -449,7 +466,7 @@ __global__ __launch_bounds__(256) void sb_bounds_kernel(const uint16_t* __restri
     const bool valid = pos < N;
     float x[D];
     if (valid) {
-        load_row_f32<D>(x, K + ((size_t)perm[(size_t)h * N + pos] * H + h) * D);
+        load_row_f32<D>(x, kp + ((size_t)h * N + pos) * D);
     } else {
 #pragma unroll
         for (int i = 0; i < D; ++i) x[i] = 0.0f;
@@ -518,7 +535,8 @@ size_t key_order_workspace_bytes(int32_t N, int32_t H, int32_t d) {
     const size_t ctiles = (size_t)key_order_ctiles(ntiles);
     int32_t levels, width;
     tree_shape(N, levels, width);
-    return 2 * al((size_t)H * N * sizeof(int32_t)) + al((size_t)H * N * sizeof(uint16_t)) +
+    return 2 * al((size_t)H * N * sizeof(int32_t)) + 2 * al((size_t)H * N * d * sizeof(uint16_t)) +
+           al((size_t)H * N * sizeof(uint16_t)) +
            al((size_t)H * width * (2 * d + 2) * sizeof(float)) +
            al((size_t)H * width * kNodeInts * sizeof(int32_t)) + al((size_t)H * sizeof(int32_t)) +
            al((size_t)H * ctiles * (d / 16 + 1) * 64 * 16);
@@ -535,6 +553,10 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
     p += al((size_t)H * N * sizeof(int32_t));
     int32_t* perm_b = reinterpret_cast<int32_t*>(p);
     p += al((size_t)H * N * sizeof(int32_t));
+    uint16_t* kp_a = reinterpret_cast<uint16_t*>(p);   // head-major key rows in the current order
+    p += al((size_t)H * N * d * sizeof(uint16_t));
+    uint16_t* kp_b = reinterpret_cast<uint16_t*>(p);
+    p += al((size_t)H * N * d * sizeof(uint16_t));
     uint16_t* code = reinterpret_cast<uint16_t*>(p);
     p += al((size_t)H * N * sizeof(uint16_t));
     float* nodef = reinterpret_cast<float*>(p);
@@ -550,17 +572,24 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)((N + 255) / 256), (unsigned)H);
     const dim3 pgrid((unsigned)((N + kBlockPos - 1) / kBlockPos), (unsigned)H);
-    hipLaunchKernelGGL(iota_kernel, grid, dim3(256), 0, stream, N, perm_a);
+    if (d == 16)
+        hipLaunchKernelGGL(tree_init_kernel<16>, grid, dim3(256), 0, stream, k, N, H, perm_a, kp_a);
+    else if (d == 32)
+        hipLaunchKernelGGL(tree_init_kernel<32>, grid, dim3(256), 0, stream, k, N, H, perm_a, kp_a);
+    else
+        hipLaunchKernelGGL(tree_init_kernel<64>, grid, dim3(256), 0, stream, k, N, H, perm_a, kp_a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     int32_t* cur = perm_a;
     int32_t* nxt = perm_b;
+    uint16_t* kcur = kp_a;
+    uint16_t* knxt = kp_b;
     for (int lev = 0; lev < levels; ++lev) {
         const dim3 ngrid((unsigned)(1 << lev), (unsigned)H);
 #define KMIP_TREE_LEVEL(DD)                                                                          \
-    hipLaunchKernelGGL(tree_axis_kernel<DD>, ngrid, dim3(64), 0, stream, k, cur, N, H, lev, width,   \
+    hipLaunchKernelGGL(tree_axis_kernel<DD>, ngrid, dim3(64), 0, stream, kcur, N, H, lev, width,     \
                        nodef, nodeh);                                                                \
     if ((e = hipGetLastError()) != hipSuccess) return e;                                             \
-    hipLaunchKernelGGL(tree_project_kernel<DD>, pgrid, dim3(256), 0, stream, k, cur, N, H, lev, width, \
+    hipLaunchKernelGGL(tree_project_kernel<DD>, pgrid, dim3(256), 0, stream, kcur, N, H, lev, width,   \
                        nodef, nodeh, code);
         if (d == 16) {
             KMIP_TREE_LEVEL(16)
@@ -577,12 +606,18 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
         if ((e = hipGetLastError()) != hipSuccess) return e;
         hipLaunchKernelGGL(tree_find_kernel, ngrid, dim3(256), 0, stream, N, lev, width, 1, nodeh);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(tree_scatter_kernel, pgrid, dim3(256), 0, stream, N, lev, width, nodeh, code, cur,
-                           nxt);
+        if (d == 16)
+            hipLaunchKernelGGL(tree_scatter_kernel<16>, pgrid, dim3(256), 0, stream, N, lev, width, nodeh, code,
+                               cur, nxt, kcur, knxt);
+        else if (d == 32)
+            hipLaunchKernelGGL(tree_scatter_kernel<32>, pgrid, dim3(256), 0, stream, N, lev, width, nodeh, code,
+                               cur, nxt, kcur, knxt);
+        else
+            hipLaunchKernelGGL(tree_scatter_kernel<64>, pgrid, dim3(256), 0, stream, N, lev, width, nodeh, code,
+                               cur, nxt, kcur, knxt);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        int32_t* tmp = cur;
-        cur = nxt;
-        nxt = tmp;
+        std::swap(cur, nxt);
+        std::swap(kcur, knxt);
     }
     out->perm = cur;
     out->bounds = reinterpret_cast<const uint4*>(bounds);
@@ -590,11 +625,11 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
     out->ctiles = ctiles;
     const dim3 sgrid((unsigned)(ctiles * 32), (unsigned)H);
     if (d == 16)
-        hipLaunchKernelGGL(sb_bounds_kernel<16>, sgrid, dim3(256), 0, stream, k, cur, N, H, ctiles, bounds);
+        hipLaunchKernelGGL(sb_bounds_kernel<16>, sgrid, dim3(256), 0, stream, kcur, N, H, ctiles, bounds);
     else if (d == 32)
-        hipLaunchKernelGGL(sb_bounds_kernel<32>, sgrid, dim3(256), 0, stream, k, cur, N, H, ctiles, bounds);
+        hipLaunchKernelGGL(sb_bounds_kernel<32>, sgrid, dim3(256), 0, stream, kcur, N, H, ctiles, bounds);
     else
-        hipLaunchKernelGGL(sb_bounds_kernel<64>, sgrid, dim3(256), 0, stream, k, cur, N, H, ctiles, bounds);
+        hipLaunchKernelGGL(sb_bounds_kernel<64>, sgrid, dim3(256), 0, stream, kcur, N, H, ctiles, bounds);
     return hipGetLastError();
 }
 

@@ -49,16 +49,18 @@ def test_workspace_size(lib):
     n = lib.kmip_topk_workspace_size(500_000, 4, 16, 32, 1)
     packed = 4 * (15625 + 16) * 32 * 16 * 2 + 512   # tiled K, then 512 B of work counters
     # one graph of >= 8192 nodes: query grouping adds reference directions
-    # [H][256][d] f32, labels [H][N] u16, a histogram and the seed references
+    # [H][256][d] bf16, labels [H][N] u16, a histogram and the seed references
     # [2][H][256] i32 and the permutation [H][N] i32, each 256-byte aligned
-    grouping = 4 * 256 * 16 * 4 + 4 * 500_000 * 2 + 2 * 4 * 256 * 4 + 4 * 500_000 * 4
-    # ... and the stored key order: two position buffers [H][N] i32, projection
+    grouping = 4 * 256 * 16 * 2 + 4 * 500_000 * 2 + 2 * 4 * 256 * 4 + 4 * 500_000 * 4
+    # ... and the stored key order: two position buffers [H][N] i32, two
+    # head-major copies of the key rows in that order [H][N][d] bf16, projection
     # codes [H][N] u16, per-node data of the widest tree level (1954
     # superblocks -> 11 levels, 1024 nodes) [H][1024][2d + 2] f32 and
     # [H][1024][520] i32, votes [H] i32 (padded to 256 B), and the bound tiles:
     # 1954 superblocks of 256 keys -> 31 windows of 64 -> 62 tiles per head of
     # (d/16 + 1) chunks of 64 x 16 B
-    key_order = (2 * 4 * 500_000 * 4 + 4 * 500_000 * 2 + 4 * 1024 * 34 * 4 + 4 * 1024 * 520 * 4
+    key_order = (2 * 4 * 500_000 * 4 + 2 * 4 * 500_000 * 16 * 2 + 4 * 500_000 * 2 + 4 * 1024 * 34 * 4
+                 + 4 * 1024 * 520 * 4
                  + 256 + 4 * 62 * 2 * 64 * 16)
     assert n == packed + grouping + key_order
     assert lib.kmip_topk_workspace_size(8191, 1, 16, 4, 1) == (256 + 16) * 32 * 16 * 2 + 512
@@ -69,9 +71,9 @@ def test_workspace_size(lib):
     assert lib.kmip_topk_workspace_size(-1, 1, 16, 4, 1) == 0
     assert lib.kmip_fwd_workspace_size(1000, 2, 32, 16, 1) == lib.kmip_topk_workspace_size(1000, 2, 32, 16, 1)
     # backward: per-pair atomics need none; key aggregation groups the queries
-    # (reference directions, labels, histogram + seed slots, permutation)
+    # (reference directions in bf16, labels, histogram + seed slots, permutation)
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 1) == 0
-    agg = 2 * 256 * 32 * 4 + 4096 + 2 * 2 * 256 * 4 + 8192
+    agg = 2 * 256 * 32 * 2 + 4096 + 2 * 2 * 256 * 4 + 8192
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 2) == agg
     # the segmented reduction: pair coefficients (2 f32), the key-sorted pair
     # records (16 B), per-key counts and the scan's block sums, each 256-byte
@@ -80,8 +82,8 @@ def test_workspace_size(lib):
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 3) == csr
     # the bucketed reduction: pair coefficients, the bucket-sorted records,
     # three arrays over the 2000 / (4096 / 32) = 16 key-row buckets (+1:
-    # counts, kept starts, pieces), the scan's block sums and head-major
-    # copies of Q and dO (bf16)
+    # counts, kept starts, pieces), the scan's block sums and the head-major
+    # interleaved copy of Q and dO (bf16, 2d per query-head)
     bucket = 32000 * 8 + 32000 * 16 + 3 * 256 + 256 + 2 * 2000 * 32 * 2
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 4) == bucket
     # the library picks the bucketed reduction where it fits
