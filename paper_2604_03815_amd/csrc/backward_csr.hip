@@ -359,6 +359,19 @@ constexpr int kMaxBuckets = 8192;
 __host__ __device__ __forceinline__ int bucket_rows(int d) { return 4096 / d; }
 __host__ __device__ __forceinline__ int bucket_shift(int d) { return d == 16 ? 8 : (d == 32 ? 7 : 6); }
 
+// A pair record of the bucketed sort, 12 bytes: the key row's offset in its
+// bucket (below 2^8) in bits 21..28 and the head-major query row h*N + i in
+// bits 0..20 (the bucketed variant takes N*H <= kMaxBuckets * 4096 / d,
+// at most 2^21), then the coefficients.
+struct BucketRecord {
+    uint32_t packed;
+    float a;
+    float p;
+};
+constexpr int kQRowBits = 21;
+static_assert(sizeof(BucketRecord) == 12, "packed record");
+static_assert((int64_t)kMaxBuckets * 4096 / 16 <= (int64_t)1 << kQRowBits, "query rows fit 21 bits");
+
 // Takes one slot of LDS counter ctr[bk] for each lane with bk >= 0 and
 // returns its number (kReturn) or nothing.  Lanes of a wave that share a bucket are served
 // by one atomic while the group the wave's first pending lane belongs to
@@ -406,7 +419,7 @@ __global__ __launch_bounds__(256) void bkt_count_kernel(const int32_t* __restric
                                                         const float2* __restrict__ coef, int32_t N,
                                                         int32_t H, int32_t k, int32_t shift, int32_t nbk,
                                                         uint32_t per, int32_t* __restrict__ gcnt,
-                                                        PairRecord* __restrict__ rec) {
+                                                        BucketRecord* __restrict__ rec) {
     __shared__ int32_t hist[kMaxBuckets];
     __shared__ int32_t base[kPlace ? kMaxBuckets : 1];
     const int t = threadIdx.x;
@@ -460,7 +473,8 @@ __global__ __launch_bounds__(256) void bkt_count_kernel(const int32_t* __restric
                 if (bk >= 0) {
                     const uint32_t qh = e / (uint32_t)k;
                     const int32_t ht = (int32_t)((qh % (uint32_t)H) * (uint32_t)N + qh / (uint32_t)H);
-                    rec[base[bk] + slot] = PairRecord{r[u], ht, c[u].x, c[u].y};
+                    const uint32_t off = (uint32_t)r[u] & ((1u << shift) - 1u);
+                    rec[base[bk] + slot] = BucketRecord{(off << kQRowBits) | (uint32_t)ht, c[u].x, c[u].y};
                 }
             }
         }
@@ -521,7 +535,7 @@ __device__ __forceinline__ RowChunk<E> load_chunk(const uint16_t* p) {
 
 template <int D>
 __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restrict__ QG,
-                                                         const PairRecord* __restrict__ rec,
+                                                         const BucketRecord* __restrict__ rec,
                                                          const int32_t* __restrict__ sstart,
                                                          const int32_t* __restrict__ pstart, int32_t nbk,
                                                          float* __restrict__ dK, float* __restrict__ dV) {
@@ -552,7 +566,7 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int i = base + 256 * u + t;
-            row[u] = i < n ? (rec[e0 + i].row & (RB - 1)) : -1;
+            row[u] = i < n ? (int32_t)(rec[e0 + i].packed >> kQRowBits) : -1;
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -603,11 +617,12 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
             }
         }
     };
-    PairRecord next{-1, 0, 0.0f, 0.0f};
+    const int32_t row0 = lo * RB;   // first key row of the bucket
+    BucketRecord next{0u, 0.0f, 0.0f};
     if (p0 + tl < p1) next = rec[e0 + ord[p0 + tl]];
     for (int pb = p0; pb < p1; pb += 16) {
-        const PairRecord r = next;   // this batch's records; the next batch's are fetched now
-        next = PairRecord{-1, 0, 0.0f, 0.0f};
+        const BucketRecord r = next;   // this batch's records; the next batch's are fetched now
+        next = BucketRecord{0u, 0.0f, 0.0f};
         if (pb + 16 + tl < p1) next = rec[e0 + ord[pb + 16 + tl]];
         const int m = min(16, p1 - pb);
         for (int s0 = 0; s0 < m; s0 += G) {
@@ -616,8 +631,9 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
             RowChunk<E> rv[G];
 #pragma unroll
             for (int g = 0; g < G; ++g) {
-                rt[g] = __shfl(r.row, s0 + g, 16);
-                const int32_t qt = __shfl(r.qh, s0 + g, 16);
+                const uint32_t pk = (uint32_t)__shfl((int32_t)r.packed, s0 + g, 16);
+                rt[g] = row0 + (int32_t)(pk >> kQRowBits);
+                const int32_t qt = (int32_t)(pk & ((1u << kQRowBits) - 1u));
                 // lanes 0-7 take the record's a, lanes 8-15 its p
                 const float ca = __shfl(r.a, s0 + g, 16), cp = __shfl(r.p, s0 + g, 16);
                 ct[g] = isq ? ca : cp;
@@ -658,7 +674,7 @@ size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k) {
     const size_t nh = (size_t)N * H, pairs = nh * k;
     const size_t nbk = (nh + bucket_rows(d) - 1) / bucket_rows(d);
     const size_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
-    return al(pairs * sizeof(float2)) + al(pairs * sizeof(PairRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
+    return al(pairs * sizeof(float2)) + al(pairs * sizeof(BucketRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
            al((nb + 1) * sizeof(int32_t)) + al(nh * 2 * d * sizeof(uint16_t));
 }
 
@@ -677,8 +693,8 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     char* p = reinterpret_cast<char*>(ws);
     float2* coef = reinterpret_cast<float2*>(p);
     p += al(pairs * sizeof(float2));
-    PairRecord* rec = reinterpret_cast<PairRecord*>(p);
-    p += al(pairs * sizeof(PairRecord));
+    BucketRecord* rec = reinterpret_cast<BucketRecord*>(p);
+    p += al(pairs * sizeof(BucketRecord));
     int32_t* gcnt = reinterpret_cast<int32_t*>(p);   // counts, then starts (nbk + 1 entries)
     p += al(((size_t)nbk + 1) * sizeof(int32_t));
     int32_t* sstart = reinterpret_cast<int32_t*>(p);   // kept starts
