@@ -216,19 +216,24 @@ __global__ __launch_bounds__(256) void bwd_agg_kernel(
     }
 }
 
-__global__ __launch_bounds__(256) void fill_zero_kernel(float4* __restrict__ p, size_t n4) {
+// Zeroes p[0 .. n): a float4 store per thread where four elements remain,
+// single stores for a tail of one to three (p is 16-byte aligned).
+__global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ p, size_t n) {
     const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-    if (i < n4) p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    const size_t e = 4 * i;
+    if (e + 4 <= n) {
+        reinterpret_cast<float4*>(p)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    } else {
+        for (size_t j = e; j < n; ++j) p[j] = 0.0f;
+    }
 }
 
 }  // namespace
 
 hipError_t launch_fill_zero(float* p, size_t n, hipStream_t stream) {
-    // n is a multiple of 16 here (rows of d >= 16 floats), so float4 stores cover it.
-    const size_t n4 = n / 4;
-    if (n4 == 0) return hipSuccess;
-    hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream,
-                       reinterpret_cast<float4*>(p), n4);
+    if (n == 0) return hipSuccess;
+    const size_t n4 = (n + 3) / 4;
+    hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream, p, n);
     return hipGetLastError();
 }
 

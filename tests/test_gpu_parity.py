@@ -268,6 +268,31 @@ def test_full_size_sampled(cfg, sample):
     print(f"c{cfg}: sampled {strict} well-separated, {loose} near-tied query-heads")
 
 
+def test_stale_workspace_does_not_change_selection():
+    # The library clears every counter it reads (work counters, dense-mode
+    # votes, seed slots) at the start of each call, whatever the workspace
+    # held before: a workspace filled with 0x7f bytes (counters reading as
+    # huge values) gives the same index sets as a zeroed one, and the select
+    # kernel takes about as long.  A one-head graph takes the per-head
+    # counters' shortest fill (one entry).
+    w = workloads.make(5, n=65536)
+    q, k = _dev(w.q), _dev(w.kk)
+    ws = kmip.Workspace(DEV)
+    buf = ws.get(kmip.topk_workspace_size(w.N, w.H, w.d, w.k, 1))
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    times, sets = {}, {}
+    for fill in (0, 0x7F, 0, 0x7F):
+        idx = torch.empty((w.N, w.H, w.k), dtype=torch.int32, device=DEV)
+        buf.fill_(fill)
+        kmip.topk(q, k, w.k, graph_offsets=w.offsets, idx=idx, workspace=ws, select_events=evs)
+        torch.cuda.synchronize()
+        times.setdefault(fill, []).append(evs[0].elapsed_time(evs[1]))
+        sets[fill] = torch.sort(idx, -1).values.cpu()
+    print(f"select ms, zeroed workspace {times[0]}, 0x7f-filled {times[0x7F]}", flush=True)
+    assert torch.equal(sets[0], sets[0x7F])
+    assert min(times[0x7F]) < 1.5 * min(times[0]) + 0.1
+
+
 def test_peak_memory_linear_in_n():
     # Peak device memory of a forward+backward step (inputs, outputs and the
     # library's workspaces) grows linearly with N: the bytes per node at the
