@@ -563,6 +563,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     // With track, each lane also notes, per query block, the superblock of
     // largest bound among its rows (best_sb, -1 for an invalid query).
     int best_sb[QB];
+    float best_b[QB];   // with track: each query's largest superblock bound
     auto compute_batch = [&](int bt, bool track, bool lower) {
         const int wlo = bt * 64;
         const int whi = min(nwin, wlo + 64);
@@ -684,6 +685,10 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
             }
             return 0;
         }
+        if (track) {
+#pragma unroll
+            for (int b = 0; b < QB; ++b) best_b[b] = fmaxf(best_v[b], __shfl_xor(best_v[b], 32));
+        }
         mask_lo = full_lo = (uint32_t)mv;
         mask_hi = full_hi = (uint32_t)(mv >> 32);
         mask_batch = full_batch = bt;
@@ -749,6 +754,26 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
             warm_pending = true;
         } else if (!seeded) {
             stop_at = 16;
+        } else if (nwin <= 64 && 8 * needed > nsb) {
+            // Seeded items whose masks keep more than an eighth of the
+            // superblocks warm up on a hot set first: the superblocks whose
+            // bound, for some query, lies in the upper half of the gap between
+            // that query's theta and its best bound.  The thresholds rise on
+            // the likeliest keys, and the masks formed after the warm-up (which
+            // leave the hot set out) keep fewer superblocks.
+            float th0[QB];
+#pragma unroll
+            for (int b = 0; b < QB; ++b) {
+                th0[b] = theta[b];
+                if (theta[b] != INFINITY && best_b[b] > theta[b]) theta[b] = 0.5f * (theta[b] + best_b[b]);
+            }
+            compute_batch(0, false, false);
+#pragma unroll
+            for (int b = 0; b < QB; ++b) theta[b] = th0[b];
+            full_batch = -1;
+            warm_lo = mask_lo;
+            warm_hi = mask_hi;
+            warm_pending = true;
         }
         if (seeded && lane == 0) atomicAdd(&votes[head], needed * 4 > min(nsb, 64 * 64) * 3 ? 1 : -1);
         wm = read_mask(0);
