@@ -348,16 +348,38 @@ __global__ __launch_bounds__(256) void csr_reduce_kernel(
 //
 // The key rows are cut into buckets of RB = 4096 / d consecutive rows, at
 // most kMaxBuckets of them.  The pairs are counting-sorted by bucket only: a
-// workgroup takes a range of consecutive pairs and counts or places them
-// with an LDS histogram over the buckets, one global atomic per bucket it
-// touches (against one per key row and workgroup for the full sort, whose
-// per-row tables overflow when pairs spread over many keys).  Each bucket's
-// records are then cut into pieces that one workgroup sorts by key row in
-// LDS and reduces like the full sort's reduction.
+// counting pass takes ranges of consecutive pairs and counts them with an
+// LDS histogram over the buckets, one global atomic per bucket it touches
+// (against one per key row and workgroup for the full sort, whose per-row
+// tables overflow when pairs spread over many keys); two placement passes
+// (below) then write the records in bucket order.  Each bucket's records are
+// cut into pieces that one workgroup sorts by key row in LDS and reduces
+// like the full sort's reduction.
 constexpr int kMaxBuckets = 8192;
 
 __host__ __device__ __forceinline__ int bucket_rows(int d) { return 4096 / d; }
 __host__ __device__ __forceinline__ int bucket_shift(int d) { return d == 16 ? 8 : (d == 32 ? 7 : 6); }
+
+// Division of a dividend below 2^31 by a fixed divisor d >= 1 as a multiply
+// and shift: with l = ceil(log2 d) and m = ceil(2^(32+l) / d) (at most 2^33),
+// floor(n m / 2^(32+l)) = floor(n / d) for every n < 2^32 (the round-up
+// method of Granlund and Montgomery); n < 2^31 keeps n m below 2^64.
+struct FastDiv {
+    uint64_t m;
+    uint32_t s;
+    uint32_t d;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;
+    const unsigned __int128 num = (unsigned __int128)1 << (32 + l);
+    return FastDiv{(uint64_t)((num + d - 1) / d), 32 + l, d};
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
+    return (uint32_t)(((uint64_t)n * f.m) >> f.s);
+}
 
 // A pair record of the bucketed sort, 12 bytes: the key row's offset in its
 // bucket (below 2^8) in bits 21..28 and the head-major query row h*N + i in
@@ -408,20 +430,14 @@ __device__ __forceinline__ int32_t claim_slot(int32_t* ctr, int32_t bk) {
     return slot;
 }
 
-// Counting (kPlace false) and placing (true) pass over a range of `per`
-// consecutive pairs (pair e = query-head e / k, slot e % k, so that lanes
-// read idx and the coefficients contiguously): the workgroup counts its
-// pairs per bucket in LDS, adds the counts to the global ones (count) or
-// reserves a range of each bucket's positions with one atomic (place) and
-// writes each pair's record at the next position of its range.
-template <bool kPlace>
-__global__ __launch_bounds__(256) void bkt_count_kernel(const int32_t* __restrict__ idx,
-                                                        const float2* __restrict__ coef, int32_t N,
-                                                        int32_t H, int32_t k, int32_t shift, int32_t nbk,
-                                                        uint32_t per, int32_t* __restrict__ gcnt,
-                                                        BucketRecord* __restrict__ rec) {
+// Counting pass over a range of `per` consecutive pairs (pair e =
+// query-head e / k, slot e % k, so that lanes read idx contiguously): the
+// workgroup counts its pairs per bucket in LDS and adds the counts to the
+// global ones, one atomic per bucket it touches.
+__global__ __launch_bounds__(256) void bkt_count_kernel(const int32_t* __restrict__ idx, int32_t N, int32_t H,
+                                                        int32_t k, FastDiv divk, FastDiv divh, int32_t shift,
+                                                        int32_t nbk, uint32_t per, int32_t* __restrict__ gcnt) {
     __shared__ int32_t hist[kMaxBuckets];
-    __shared__ int32_t base[kPlace ? kMaxBuckets : 1];
     const int t = threadIdx.x;
     const uint32_t P = (uint32_t)N * (uint32_t)H * (uint32_t)k;
     const uint32_t p0 = blockIdx.x * per;
@@ -429,8 +445,8 @@ __global__ __launch_bounds__(256) void bkt_count_kernel(const int32_t* __restric
     auto row_of = [&](uint32_t e) -> int32_t {
         if (e >= p1) return -1;
         const int32_t j = idx[e];
-        const uint32_t qh = e / (uint32_t)k;
-        return (j >= 0 && j < N) ? j * H + (int32_t)(qh % (uint32_t)H) : -1;
+        const uint32_t qh = fdiv(e, divk);
+        return (j >= 0 && j < N) ? j * H + (int32_t)(qh - fdiv(qh, divh) * (uint32_t)H) : -1;
     };
     for (int e = t; e < nbk; e += 256) hist[e] = 0;
     __syncthreads();
@@ -446,38 +462,239 @@ __global__ __launch_bounds__(256) void bkt_count_kernel(const int32_t* __restric
     __syncthreads();
     for (int e = t; e < nbk; e += 256) {
         const int32_t c = hist[e];
-        if (c == 0) continue;
-        if (kPlace)
-            base[e] = atomicAdd(&gcnt[e], c);
-        else
-            atomicAdd(&gcnt[e], c);
+        if (c != 0) atomicAdd(&gcnt[e], c);
     }
-    if constexpr (kPlace) {
-        __syncthreads();
-        for (int e = t; e < nbk; e += 256) hist[e] = 0;
-        __syncthreads();
-        for (uint32_t pb = p0; pb < p1; pb += 1024) {
-            int32_t r[4];
-            float2 c[4];
+}
+
+
+// Placing the records in bucket order takes two passes with coalesced
+// stores (a single pass that sends each pair to its bucket directly makes
+// one scattered store per pair).  Pass 1 sorts each chunk of kSplitChunk
+// consecutive pairs by super-bucket (kSupBuckets consecutive buckets, at
+// most kMaxBuckets / kSupBuckets of them) in LDS, reserves each
+// super-bucket's range with one atomic and writes the chunk out as runs;
+// pass 2 does the same for each piece of kSplitChunk records of one
+// super-bucket, by bucket, and writes the final records.
+constexpr int kSplitChunk = 2048;
+constexpr int kSupBuckets = 128;
+constexpr int kMaxSup = kMaxBuckets / kSupBuckets;
+static_assert(kMaxSup == 64 && kSupBuckets == 128, "6-bit super-bucket and 7-bit bucket digits; one-wave scans");
+
+// Exclusive prefix sum over the 64 lanes of a wave; *total (lane 63's
+// inclusive sum) for every lane.
+__device__ __forceinline__ int32_t wave_exclusive_sum(int32_t v, int32_t* total) {
+    const int lane = threadIdx.x & 63;
+    int32_t x = v;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const uint32_t e = pb + 256 * u + t;
-                r[u] = row_of(e);
-                c[u] = e < p1 ? coef[e] : make_float2(0.0f, 0.0f);
-            }
+    for (int off = 1; off < 64; off <<= 1) {
+        const int32_t y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+    }
+    *total = __shfl(x, 63, 64);
+    return x - v;
+}
+
+// Slot of each lane with digit >= 0 (a value below 2^NB) in LDS counter
+// ctr[digit]: the lanes of the wave with equal digits are found with NB
+// ballots, and one leader per digit takes the group's slots with a single
+// atomic (lanes with equal digits never meet at one counter in an atomic).
+template <int NB>
+__device__ __forceinline__ int32_t wave_rank(int32_t* ctr, int32_t digit) {
+    const int lane = threadIdx.x & 63;
+    uint64_t same = __ballot(digit >= 0);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const uint32_t e = pb + 256 * u + t;
-                const int32_t bk = r[u] >= 0 ? r[u] >> shift : -1;
-                const int32_t slot = claim_slot<true>(hist, bk);
-                if (bk >= 0) {
-                    const uint32_t qh = e / (uint32_t)k;
-                    const int32_t ht = (int32_t)((qh % (uint32_t)H) * (uint32_t)N + qh / (uint32_t)H);
-                    const uint32_t off = (uint32_t)r[u] & ((1u << shift) - 1u);
-                    rec[base[bk] + slot] = BucketRecord{(off << kQRowBits) | (uint32_t)ht, c[u].x, c[u].y};
-                }
+    for (int b = 0; b < NB; ++b) {
+        const bool bit = ((digit >> b) & 1) != 0;
+        const uint64_t bb = __ballot(bit);
+        same &= bit ? bb : ~bb;
+    }
+    const int leader = same != 0ull ? __ffsll((unsigned long long)same) - 1 : lane;
+    int32_t base = 0;
+    if (digit >= 0 && lane == leader) base = atomicAdd(&ctr[digit], (int32_t)__popcll(same));
+    base = __shfl(base, leader, 64);
+    return base + (int32_t)__popcll(same & ((1ull << lane) - 1ull));
+}
+
+// Pass 1: a workgroup takes kSplitPer consecutive pairs.  It counts them per
+// super-bucket, reserves each super-bucket's range with one atomic, then
+// sorts and writes them out kSplitChunk at a time at running offsets.
+constexpr int kSplitPer = 16 * kSplitChunk;
+
+__global__ __launch_bounds__(256) void bkt_split1_kernel(const int32_t* __restrict__ idx,
+                                                         const float2* __restrict__ coef, int32_t N,
+                                                         int32_t H, int32_t k, FastDiv divk, FastDiv divh,
+                                                         int32_t shift, int32_t* __restrict__ supcur,
+                                                         PairRecord* __restrict__ mid) {
+    constexpr int R = kSplitChunk / 256;
+    __shared__ int32_t cnt[kMaxSup], lstart[kMaxSup], gbase[kMaxSup];
+    __shared__ PairRecord stage[kSplitChunk];
+    __shared__ int32_t total;
+    const int t = threadIdx.x;
+    const uint32_t P = (uint32_t)N * (uint32_t)H * (uint32_t)k;
+    const uint32_t r0 = blockIdx.x * (uint32_t)kSplitPer;
+    const uint32_t r1 = min(P, r0 + (uint32_t)kSplitPer);
+    auto sup_of = [&](uint32_t e, int32_t& row) -> int32_t {
+        row = -1;
+        if (e >= r1) return -1;
+        const int32_t j = idx[e];
+        if (j < 0 || j >= N) return -1;
+        const uint32_t qh = fdiv(e, divk);
+        row = j * H + (int32_t)(qh - fdiv(qh, divh) * (uint32_t)H);
+        return (row >> shift) / kSupBuckets;
+    };
+    if (t < kMaxSup) cnt[t] = 0;
+    __syncthreads();
+    // count the range, reserve
+    for (uint32_t c0 = r0; c0 < r1; c0 += kSplitChunk) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            int32_t row;
+            wave_rank<6>(cnt, sup_of(c0 + u * 256 + t, row));
+        }
+    }
+    __syncthreads();
+    if (t < kMaxSup) {
+        const int32_t c = cnt[t];
+        gbase[t] = c != 0 ? atomicAdd(&supcur[t], c) : 0;
+        cnt[t] = 0;
+    }
+    __syncthreads();
+    for (uint32_t c0 = r0; c0 < r1; c0 += kSplitChunk) {
+        PairRecord rr[R];
+        int32_t sup[R], slot[R];
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            const uint32_t e = c0 + u * 256 + t;
+            int32_t row;
+            sup[u] = sup_of(e, row);
+            rr[u] = PairRecord{-1, 0, 0.0f, 0.0f};
+            if (sup[u] >= 0) {
+                const uint32_t qh = fdiv(e, divk);
+                const uint32_t i = fdiv(qh, divh);
+                const float2 c = coef[e];
+                rr[u] = PairRecord{row, (int32_t)((qh - i * (uint32_t)H) * (uint32_t)N + i), c.x, c.y};
             }
         }
+#pragma unroll
+        for (int u = 0; u < R; ++u) slot[u] = wave_rank<6>(cnt, sup[u]);
+        __syncthreads();
+        if (t < 64) {
+            const int32_t c = t < kMaxSup ? cnt[t] : 0;
+            int32_t tot;
+            const int32_t ex = wave_exclusive_sum(c, &tot);
+            if (t < kMaxSup) lstart[t] = ex;
+            if (t == 0) total = tot;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < R; ++u)
+            if (sup[u] >= 0) stage[lstart[sup[u]] + slot[u]] = rr[u];
+        __syncthreads();
+        const int n = total;
+        for (int i = t; i < n; i += 256) {
+            const PairRecord r = stage[i];
+            const int sp = (r.row >> shift) / kSupBuckets;
+            mid[gbase[sp] + (i - lstart[sp])] = r;
+        }
+        __syncthreads();
+        // the next chunk continues each super-bucket's range
+        if (t < kMaxSup) {
+            gbase[t] += cnt[t];
+            cnt[t] = 0;
+        }
+        __syncthreads();
+    }
+}
+
+// Per super-bucket: its first record (supst, nsup + 1 entries), the cursor
+// pass 1 reserves from (supcur), and the scanned number of pass-2 pieces
+// (pstart2, nsup + 1 entries).  One wave.
+__global__ __launch_bounds__(64) void bkt_split_setup_kernel(const int32_t* __restrict__ sstart, int32_t nbk,
+                                                             int32_t nsup, int32_t* __restrict__ supst,
+                                                             int32_t* __restrict__ supcur,
+                                                             int32_t* __restrict__ pstart2) {
+    const int s = threadIdx.x;
+    const int32_t a = sstart[min(s * kSupBuckets, nbk)];
+    const int32_t b = sstart[min((s + 1) * kSupBuckets, nbk)];
+    const int32_t np = s < nsup ? (b - a + kSplitChunk - 1) / kSplitChunk : 0;
+    int32_t tot;
+    const int32_t ex = wave_exclusive_sum(np, &tot);
+    if (s < nsup) {
+        supst[s] = a;
+        supcur[s] = a;
+        pstart2[s] = ex;
+    }
+    if (s == 0) {
+        supst[nsup] = sstart[nbk];
+        pstart2[nsup] = tot;
+    }
+}
+
+// Pass 2: one workgroup per piece of at most kSplitChunk records of one
+// super-bucket; bcur holds the buckets' cursors (their starts, advanced
+// here).
+__global__ __launch_bounds__(256) void bkt_split2_kernel(const PairRecord* __restrict__ mid,
+                                                         const int32_t* __restrict__ supst,
+                                                         const int32_t* __restrict__ pstart2, int32_t nsup,
+                                                         int32_t shift, int32_t* __restrict__ bcur,
+                                                         BucketRecord* __restrict__ rec) {
+    constexpr int R = kSplitChunk / 256;
+    __shared__ int32_t cnt[kSupBuckets], lstart[kSupBuckets], gbase[kSupBuckets];
+    __shared__ BucketRecord stage[kSplitChunk];
+    __shared__ uint8_t sbk[kSplitChunk];
+    const int t = threadIdx.x;
+    const int w = blockIdx.x;
+    if (w >= pstart2[nsup]) return;
+    int lo = 0, hi = nsup;
+    while (hi - lo > 1) {
+        const int m = (lo + hi) >> 1;
+        if (pstart2[m] <= w) lo = m; else hi = m;
+    }
+    const int32_t e0 = supst[lo] + (w - pstart2[lo]) * kSplitChunk;
+    const int32_t n = min(supst[lo + 1] - e0, kSplitChunk);
+    const int32_t b0 = lo * kSupBuckets;
+    if (t < kSupBuckets) cnt[t] = 0;
+    __syncthreads();
+    BucketRecord fr[R];
+    int32_t bk[R], slot[R];
+    const uint32_t offmask = (1u << shift) - 1u;
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+        const int i = u * 256 + t;
+        bk[u] = -1;
+        fr[u] = BucketRecord{0u, 0.0f, 0.0f};
+        if (i < n) {
+            const PairRecord r = mid[e0 + i];
+            bk[u] = (r.row >> shift) - b0;
+            fr[u] = BucketRecord{(((uint32_t)r.row & offmask) << kQRowBits) | (uint32_t)r.qh, r.a, r.p};
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < R; ++u) slot[u] = wave_rank<7>(cnt, bk[u]);
+    __syncthreads();
+    if (t < 64) {
+        // two halves of kSupBuckets = 128 counters, one wave
+        const int32_t c0 = cnt[t], c1 = cnt[t + 64];
+        int32_t tot0, tot1;
+        const int32_t ex0 = wave_exclusive_sum(c0, &tot0);
+        const int32_t ex1 = wave_exclusive_sum(c1, &tot1);
+        lstart[t] = ex0;
+        lstart[t + 64] = tot0 + ex1;
+        gbase[t] = c0 != 0 ? atomicAdd(&bcur[b0 + t], c0) : 0;
+        gbase[t + 64] = c1 != 0 ? atomicAdd(&bcur[b0 + t + 64], c1) : 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+        if (bk[u] >= 0) {
+            stage[lstart[bk[u]] + slot[u]] = fr[u];
+            sbk[lstart[bk[u]] + slot[u]] = (uint8_t)bk[u];
+        }
+    }
+    __syncthreads();
+    for (int i = t; i < n; i += 256) {
+        const int b = sbk[i];
+        rec[gbase[b] + (i - lstart[b])] = stage[i];
     }
 }
 
@@ -675,7 +892,8 @@ size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k) {
     const size_t nbk = (nh + bucket_rows(d) - 1) / bucket_rows(d);
     const size_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
     return al(pairs * sizeof(float2)) + al(pairs * sizeof(BucketRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
-           al((nb + 1) * sizeof(int32_t)) + al(nh * 2 * d * sizeof(uint16_t));
+           al((nb + 1) * sizeof(int32_t)) + al(nh * 2 * d * sizeof(uint16_t)) + al(pairs * sizeof(PairRecord)) +
+           3 * al((kMaxSup + 1) * sizeof(int32_t));
 }
 
 hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const void* dO,
@@ -704,6 +922,14 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     int32_t* sums = reinterpret_cast<int32_t*>(p);
     p += al(((size_t)nb + 1) * sizeof(int32_t));
     uint16_t* qg = reinterpret_cast<uint16_t*>(p);   // q and dO interleaved, head-major, [H][N][2d]
+    p += al((size_t)nh * 2 * d * sizeof(uint16_t));
+    PairRecord* mid = reinterpret_cast<PairRecord*>(p);   // records in super-bucket order (pass 1)
+    p += al(pairs * sizeof(PairRecord));
+    int32_t* supst = reinterpret_cast<int32_t*>(p);
+    p += al((kMaxSup + 1) * sizeof(int32_t));
+    int32_t* supcur = reinterpret_cast<int32_t*>(p);
+    p += al((kMaxSup + 1) * sizeof(int32_t));
+    int32_t* pstart2 = reinterpret_cast<int32_t*>(p);
 
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
@@ -726,8 +952,9 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     const uint32_t per = (uint32_t)std::min<size_t>(65536, std::max<size_t>(8192, (pairs / 1024 + 255) / 256 * 256));
     const unsigned cblocks = (unsigned)((pairs + per - 1) / per);
     const int32_t shift = bucket_shift(d);
-    hipLaunchKernelGGL(bkt_count_kernel<false>, dim3(cblocks), dim3(256), 0, stream, idx, coef, N, H, k, shift,
-                       nbk, per, gcnt, rec);
+    const FastDiv divk = make_fastdiv((uint32_t)k), divh = make_fastdiv((uint32_t)H);
+    hipLaunchKernelGGL(bkt_count_kernel, dim3(cblocks), dim3(256), 0, stream, idx, N, H, k, divk, divh, shift,
+                       nbk, per, gcnt);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // exclusive scan of the nbk counts; gcnt[nbk] (zero) becomes the total
     hipLaunchKernelGGL(scan_blocks_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, stream, gcnt,
@@ -750,9 +977,16 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     hipLaunchKernelGGL(scan_apply_kernel, dim3((unsigned)nb), dim3(kScanBlock), 0, stream, pstart,
                        (int64_t)nbk + 1, sums);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // the place pass advances each bucket's start to its end
-    hipLaunchKernelGGL(bkt_count_kernel<true>, dim3(cblocks), dim3(256), 0, stream, idx, coef, N, H, k, shift,
-                       nbk, per, gcnt, rec);
+    // the two split passes; pass 2 advances each bucket's start to its end
+    const int32_t nsup = (nbk + kSupBuckets - 1) / kSupBuckets;
+    hipLaunchKernelGGL(bkt_split_setup_kernel, dim3(1), dim3(64), 0, stream, sstart, nbk, nsup, supst, supcur,
+                       pstart2);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(bkt_split1_kernel, dim3((unsigned)((pairs + kSplitPer - 1) / kSplitPer)), dim3(256), 0,
+                       stream, idx, coef, N, H, k, divk, divh, shift, supcur, mid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(bkt_split2_kernel, dim3((unsigned)(nsup + (pairs + kSplitChunk - 1) / kSplitChunk)), dim3(256),
+                       0, stream, mid, supst, pstart2, nsup, shift, gcnt, rec);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // at most one piece per bucket plus one per kPiece pairs; the rest exit
     const unsigned rblocks = (unsigned)(nbk + (pairs + kPiece - 1) / kPiece);

@@ -85,7 +85,9 @@ def test_workspace_size(lib):
     # three arrays over the 2000 / (4096 / 32) = 16 key-row buckets (+1:
     # counts, kept starts, pieces), the scan's block sums and the head-major
     # interleaved copy of Q and dO (bf16, 2d per query-head)
-    bucket = 32000 * 8 + 32000 * 12 + 3 * 256 + 256 + 2 * 2000 * 32 * 2
+    # ... and the records in super-bucket order between the two placement
+    # passes (16 B), with three arrays of 65 super-bucket entries
+    bucket = 32000 * 8 + 32000 * 12 + 3 * 256 + 256 + 2 * 2000 * 32 * 2 + 32000 * 16 + 3 * 512
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 4) == bucket
     # the library picks the bucketed reduction where it fits
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == bucket
