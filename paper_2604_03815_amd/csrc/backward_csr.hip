@@ -32,19 +32,20 @@ constexpr int kScanBlock = 1024;     // counts per block of the scan
 constexpr int kChunk = 1024;         // sorted pairs per wave in the reduction
 
 // 1. Per (query, head), a team of 16 lanes with the slots on lanes, NS
-// slots per lane (k <= 16 NS).
+// slots per lane (k <= 16 NS): p, dp, D, g of each selected pair, dQ_i, and
+// the head-major interleaved copy of q_i and dO_i.  Slot tl + 16 s of query-
+// head qh leaves its key index in jj[s] (-1: none) and its coefficients
+// a = scale g, p in ca[s], cp[s].
 template <int D, int NS>
-__global__ __launch_bounds__(256) void csr_coef_kernel(
-    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
-    const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
-    int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float2* __restrict__ coef,
-    uint16_t* __restrict__ QGt) {
+__device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+                                         const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
+                                         const int32_t* __restrict__ idx, const float* __restrict__ lse,
+                                         int32_t N, int32_t H, int32_t k, float scale, int64_t qh, int tl,
+                                         float* __restrict__ dQ, uint16_t* __restrict__ QGt, int32_t (&jj)[NS],
+                                         float (&ca)[NS], float (&cp)[NS]) {
     // key rows kept in registers for dQ when they take at most 64 dwords a
     // lane; otherwise read again (from cache)
     constexpr bool kKeep = D / 2 * NS <= 64;
-    const int tl = threadIdx.x & 15;
-    const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
-    if (qh >= (int64_t)N * H) return;  // whole team exits together
     const int h = (int)(qh % H);
     if (QGt != nullptr && tl < D / 4) {
         // head-major interleaved copy [H][N][2d]: row h*N + i holds q_i then
@@ -58,7 +59,6 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
     load_row_f32<D>(g, dO + (size_t)qh * D);
     const float l = lse[qh];
     float p[NS], dp[NS];
-    int32_t jj[NS];
     uint4 kw[kKeep ? NS : 1][D / 8];
     float dsum = 0.0f;
 #pragma unroll
@@ -67,10 +67,12 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
         dp[s] = 0.0f;
         jj[s] = -1;
         const int slot = tl + 16 * s;
-        if (slot < k && l != -INFINITY) {
-            const int32_t j = idx[(size_t)qh * k + slot];
-            if (j >= 0 && j < N) {
-                jj[s] = j;
+        // a pair exists wherever its index lies in [0, N), as the counting
+        // pass sees it; its weight is zero if lse says no key was kept
+        const int32_t j = slot < k ? idx[(size_t)qh * k + slot] : -1;
+        if (j >= 0 && j < N) jj[s] = j;
+        if (j >= 0 && j < N && l != -INFINITY) {
+            {   // the key row (kept for dQ) and the two dot products
                 uint4 w[D / 8];
                 load_row_words<D>(w, K + ((size_t)j * H + h) * D);
                 if constexpr (kKeep) {
@@ -92,26 +94,24 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
     for (int t = 0; t < D; ++t) acc[t] = 0.0f;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-        const int slot = tl + 16 * s;
-        if (slot < k) {
-            const float gs = p[s] * (dp[s] - dsum);
-            coef[(size_t)qh * k + slot] = make_float2(scale * gs, p[s]);
-            if (jj[s] >= 0) {
-                uint4 w[D / 8];
-                if constexpr (kKeep) {
+        const float gs = p[s] * (dp[s] - dsum);
+        ca[s] = scale * gs;
+        cp[s] = p[s];
+        if (jj[s] >= 0 && l != -INFINITY) {
+            uint4 w[D / 8];
+            if constexpr (kKeep) {
 #pragma unroll
-                    for (int c = 0; c < D / 8; ++c) w[c] = kw[s][c];
-                } else {
-                    load_row_words<D>(w, K + ((size_t)jj[s] * H + h) * D);
-                }
+                for (int c = 0; c < D / 8; ++c) w[c] = kw[s][c];
+            } else {
+                load_row_words<D>(w, K + ((size_t)jj[s] * H + h) * D);
+            }
 #pragma unroll
-                for (int c = 0; c < D / 8; ++c) {
-                    const uint32_t ww[4] = {w[c].x, w[c].y, w[c].z, w[c].w};
+            for (int c = 0; c < D / 8; ++c) {
+                const uint32_t ww[4] = {w[c].x, w[c].y, w[c].z, w[c].w};
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        acc[8 * c + 2 * e] = fmaf(gs, bf16_bits_to_f32(ww[e] & 0xFFFFu), acc[8 * c + 2 * e]);
-                        acc[8 * c + 2 * e + 1] = fmaf(gs, bf16_bits_to_f32(ww[e] >> 16), acc[8 * c + 2 * e + 1]);
-                    }
+                for (int e = 0; e < 4; ++e) {
+                    acc[8 * c + 2 * e] = fmaf(gs, bf16_bits_to_f32(ww[e] & 0xFFFFu), acc[8 * c + 2 * e]);
+                    acc[8 * c + 2 * e + 1] = fmaf(gs, bf16_bits_to_f32(ww[e] >> 16), acc[8 * c + 2 * e + 1]);
                 }
             }
         }
@@ -120,6 +120,26 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
     team_sum_transpose<D>(acc, out, tl);
 #pragma unroll
     for (int u = 0; u < D / 16; ++u) dQ[(size_t)qh * D + 16 * u + tl] = scale * out[u];
+}
+
+// The coefficients of every pair, in pair order (variant 3).
+template <int D, int NS>
+__global__ __launch_bounds__(256) void csr_coef_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
+    const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
+    int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float2* __restrict__ coef,
+    uint16_t* __restrict__ QGt) {
+    const int tl = threadIdx.x & 15;
+    const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+    if (qh >= (int64_t)N * H) return;  // whole team exits together
+    int32_t jj[NS];
+    float ca[NS], cp[NS];
+    coef_one<D, NS>(Q, K, V, dO, idx, lse, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const int slot = tl + 16 * s;
+        if (slot < k) coef[(size_t)qh * k + slot] = make_float2(ca[s], cp[s]);
+    }
 }
 
 // Launches csr_coef_kernel<D, NS> with NS the smallest power of two >= k/16.
@@ -469,12 +489,13 @@ __global__ __launch_bounds__(256) void bkt_count_kernel(const int32_t* __restric
 
 // Placing the records in bucket order takes two passes with coalesced
 // stores (a single pass that sends each pair to its bucket directly makes
-// one scattered store per pair).  Pass 1 sorts each chunk of kSplitChunk
-// consecutive pairs by super-bucket (kSupBuckets consecutive buckets, at
-// most kMaxBuckets / kSupBuckets of them) in LDS, reserves each
-// super-bucket's range with one atomic and writes the chunk out as runs;
-// pass 2 does the same for each piece of kSplitChunk records of one
-// super-bucket, by bucket, and writes the final records.
+// one scattered store per pair).  Pass 1, fused with the coefficient pass
+// (coef_split_kernel), sorts each chunk of kSplitChunk pairs by super-bucket
+// (kSupBuckets consecutive buckets, at most kMaxBuckets / kSupBuckets of
+// them) in LDS, reserves each super-bucket's range with one atomic and
+// writes the chunk out as runs; pass 2 does the same for each piece of
+// kSplitChunk records of one super-bucket, by bucket, and writes the final
+// records.
 constexpr int kSplitChunk = 2048;
 constexpr int kSupBuckets = 128;
 constexpr int kMaxSup = kMaxBuckets / kSupBuckets;
@@ -515,95 +536,98 @@ __device__ __forceinline__ int32_t wave_rank(int32_t* ctr, int32_t digit) {
     return base + (int32_t)__popcll(same & ((1ull << lane) - 1ull));
 }
 
-// Pass 1: a workgroup takes kSplitPer consecutive pairs.  It counts them per
-// super-bucket, reserves each super-bucket's range with one atomic, then
-// sorts and writes them out kSplitChunk at a time at running offsets.
-constexpr int kSplitPer = 16 * kSplitChunk;
-
-__global__ __launch_bounds__(256) void bkt_split1_kernel(const int32_t* __restrict__ idx,
-                                                         const float2* __restrict__ coef, int32_t N,
-                                                         int32_t H, int32_t k, FastDiv divk, FastDiv divh,
-                                                         int32_t shift, int32_t* __restrict__ supcur,
-                                                         PairRecord* __restrict__ mid) {
-    constexpr int R = kSplitChunk / 256;
+// The coefficient pass fused with placement pass 1: a
+// workgroup takes 128 / NS query-heads (8 / NS per team, at most 2048
+// pairs), computes their coefficients, dQ and the interleaved copy, and
+// writes their records in super-bucket order: one record per lane and
+// round for 8 rounds, ranked by ballots, staged in LDS and written as runs
+// into ranges the workgroup reserves with one atomic per super-bucket.  The
+// coefficients never go to memory.
+template <int D, int NS>
+__global__ __launch_bounds__(256) void coef_split_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
+    const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
+    int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, uint16_t* __restrict__ QGt,
+    int32_t shift, int32_t* __restrict__ supcur, PairRecord* __restrict__ mid) {
+    constexpr int TQ = 8 / NS;   // query-heads per team
+    constexpr int R = TQ * NS;   // records per lane: 8
+    static_assert(256 * R == kSplitChunk, "one staging chunk per workgroup");
     __shared__ int32_t cnt[kMaxSup], lstart[kMaxSup], gbase[kMaxSup];
     __shared__ PairRecord stage[kSplitChunk];
     __shared__ int32_t total;
     const int t = threadIdx.x;
-    const uint32_t P = (uint32_t)N * (uint32_t)H * (uint32_t)k;
-    const uint32_t r0 = blockIdx.x * (uint32_t)kSplitPer;
-    const uint32_t r1 = min(P, r0 + (uint32_t)kSplitPer);
-    auto sup_of = [&](uint32_t e, int32_t& row) -> int32_t {
-        row = -1;
-        if (e >= r1) return -1;
-        const int32_t j = idx[e];
-        if (j < 0 || j >= N) return -1;
-        const uint32_t qh = fdiv(e, divk);
-        row = j * H + (int32_t)(qh - fdiv(qh, divh) * (uint32_t)H);
-        return (row >> shift) / kSupBuckets;
-    };
+    const int tl = t & 15, team = t >> 4;
+    const int64_t nh = (int64_t)N * H;
     if (t < kMaxSup) cnt[t] = 0;
-    __syncthreads();
-    // count the range, reserve
-    for (uint32_t c0 = r0; c0 < r1; c0 += kSplitChunk) {
+    PairRecord rr[R];
+    int32_t sup[R], slot[R];
 #pragma unroll
-        for (int u = 0; u < R; ++u) {
-            int32_t row;
-            wave_rank<6>(cnt, sup_of(c0 + u * 256 + t, row));
-        }
-    }
-    __syncthreads();
-    if (t < kMaxSup) {
-        const int32_t c = cnt[t];
-        gbase[t] = c != 0 ? atomicAdd(&supcur[t], c) : 0;
-        cnt[t] = 0;
-    }
-    __syncthreads();
-    for (uint32_t c0 = r0; c0 < r1; c0 += kSplitChunk) {
-        PairRecord rr[R];
-        int32_t sup[R], slot[R];
+    for (int it = 0; it < TQ; ++it) {
+        const int64_t qh = (int64_t)blockIdx.x * (16 * TQ) + it * 16 + team;
+        int32_t jj[NS];
+        float ca[NS], cp[NS];
 #pragma unroll
-        for (int u = 0; u < R; ++u) {
-            const uint32_t e = c0 + u * 256 + t;
-            int32_t row;
-            sup[u] = sup_of(e, row);
-            rr[u] = PairRecord{-1, 0, 0.0f, 0.0f};
-            if (sup[u] >= 0) {
-                const uint32_t qh = fdiv(e, divk);
-                const uint32_t i = fdiv(qh, divh);
-                const float2 c = coef[e];
-                rr[u] = PairRecord{row, (int32_t)((qh - i * (uint32_t)H) * (uint32_t)N + i), c.x, c.y};
+        for (int s2 = 0; s2 < NS; ++s2) jj[s2] = -1;
+        if (qh < nh) coef_one<D, NS>(Q, K, V, dO, idx, lse, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
+        const int32_t h = (int32_t)(qh % H), i = (int32_t)(qh / H);
+#pragma unroll
+        for (int s2 = 0; s2 < NS; ++s2) {
+            const int r = it * NS + s2;
+            sup[r] = -1;
+            rr[r] = PairRecord{-1, 0, 0.0f, 0.0f};
+            if (qh < nh && jj[s2] >= 0) {
+                const int32_t row = jj[s2] * H + h;
+                rr[r] = PairRecord{row, h * N + i, ca[s2], cp[s2]};
+                sup[r] = (row >> shift) / kSupBuckets;
             }
         }
-#pragma unroll
-        for (int u = 0; u < R; ++u) slot[u] = wave_rank<6>(cnt, sup[u]);
-        __syncthreads();
-        if (t < 64) {
-            const int32_t c = t < kMaxSup ? cnt[t] : 0;
-            int32_t tot;
-            const int32_t ex = wave_exclusive_sum(c, &tot);
-            if (t < kMaxSup) lstart[t] = ex;
-            if (t == 0) total = tot;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int u = 0; u < R; ++u)
-            if (sup[u] >= 0) stage[lstart[sup[u]] + slot[u]] = rr[u];
-        __syncthreads();
-        const int n = total;
-        for (int i = t; i < n; i += 256) {
-            const PairRecord r = stage[i];
-            const int sp = (r.row >> shift) / kSupBuckets;
-            mid[gbase[sp] + (i - lstart[sp])] = r;
-        }
-        __syncthreads();
-        // the next chunk continues each super-bucket's range
-        if (t < kMaxSup) {
-            gbase[t] += cnt[t];
-            cnt[t] = 0;
-        }
-        __syncthreads();
     }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < R; ++r) slot[r] = wave_rank<6>(cnt, sup[r]);
+    __syncthreads();
+    if (t < 64) {
+        const int32_t c = t < kMaxSup ? cnt[t] : 0;
+        int32_t tot;
+        const int32_t ex = wave_exclusive_sum(c, &tot);
+        if (t < kMaxSup) {
+            lstart[t] = ex;
+            gbase[t] = c != 0 ? atomicAdd(&supcur[t], c) : 0;
+        }
+        if (t == 0) total = tot;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        if (sup[r] >= 0) stage[lstart[sup[r]] + slot[r]] = rr[r];
+    __syncthreads();
+    const int n = total;
+    for (int j = t; j < n; j += 256) {
+        const PairRecord rec = stage[j];
+        const int sp = (rec.row >> shift) / kSupBuckets;
+        mid[gbase[sp] + (j - lstart[sp])] = rec;
+    }
+}
+
+template <int D>
+hipError_t launch_coef_split(int32_t nh, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
+                             const uint16_t* v, const uint16_t* g, const int32_t* idx, const float* lse,
+                             int32_t N, int32_t H, int32_t k, float scale, float* dQ, uint16_t* qg,
+                             int32_t shift, int32_t* supcur, PairRecord* mid) {
+    const int ns = (k + 15) / 16;
+#define KMIP_COEF_SPLIT(NSV)                                                                           \
+    hipLaunchKernelGGL((coef_split_kernel<D, NSV>), dim3((unsigned)((nh + 128 / NSV - 1) / (128 / NSV))),   \
+                       dim3(256), 0, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur, mid)
+    if (ns <= 1)
+        KMIP_COEF_SPLIT(1);
+    else if (ns <= 2)
+        KMIP_COEF_SPLIT(2);
+    else if (ns <= 4)
+        KMIP_COEF_SPLIT(4);
+    else
+        KMIP_COEF_SPLIT(8);
+#undef KMIP_COEF_SPLIT
+    return hipGetLastError();
 }
 
 // Per super-bucket: its first record (supst, nsup + 1 entries), the cursor
@@ -891,7 +915,7 @@ size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k) {
     const size_t nh = (size_t)N * H, pairs = nh * k;
     const size_t nbk = (nh + bucket_rows(d) - 1) / bucket_rows(d);
     const size_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
-    return al(pairs * sizeof(float2)) + al(pairs * sizeof(BucketRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
+    return al(pairs * sizeof(BucketRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
            al((nb + 1) * sizeof(int32_t)) + al(nh * 2 * d * sizeof(uint16_t)) + al(pairs * sizeof(PairRecord)) +
            3 * al((kMaxSup + 1) * sizeof(int32_t));
 }
@@ -909,8 +933,6 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     if (nbk > kMaxBuckets) return hipErrorInvalidValue;
     const int32_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
     char* p = reinterpret_cast<char*>(ws);
-    float2* coef = reinterpret_cast<float2*>(p);
-    p += al(pairs * sizeof(float2));
     BucketRecord* rec = reinterpret_cast<BucketRecord*>(p);
     p += al(pairs * sizeof(BucketRecord));
     int32_t* gcnt = reinterpret_cast<int32_t*>(p);   // counts, then starts (nbk + 1 entries)
@@ -940,14 +962,6 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
         return e;
     if ((e = launch_fill_zero(dK, (size_t)nh * d, stream)) != hipSuccess) return e;
     if ((e = launch_fill_zero(dV, (size_t)nh * d, stream)) != hipSuccess) return e;
-    const unsigned team_blocks = (unsigned)((nh + 15) / 16);
-    if (d == 16)
-        launch_coef<16>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, qg);
-    else if (d == 32)
-        launch_coef<32>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, qg);
-    else
-        launch_coef<64>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, qg);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     // pairs per counting workgroup: about 1024 workgroups, 8192 .. 65536 pairs each
     const uint32_t per = (uint32_t)std::min<size_t>(65536, std::max<size_t>(8192, (pairs / 1024 + 255) / 256 * 256));
     const unsigned cblocks = (unsigned)((pairs + per - 1) / per);
@@ -982,9 +996,17 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     hipLaunchKernelGGL(bkt_split_setup_kernel, dim3(1), dim3(64), 0, stream, sstart, nbk, nsup, supst, supcur,
                        pstart2);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(bkt_split1_kernel, dim3((unsigned)((pairs + kSplitPer - 1) / kSplitPer)), dim3(256), 0,
-                       stream, idx, coef, N, H, k, divk, divh, shift, supcur, mid);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // coefficients, dQ and the interleaved copy, fused with placement pass 1
+    if (d == 16)
+        e = launch_coef_split<16>((int32_t)nh, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur,
+                                  mid);
+    else if (d == 32)
+        e = launch_coef_split<32>((int32_t)nh, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur,
+                                  mid);
+    else
+        e = launch_coef_split<64>((int32_t)nh, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur,
+                                  mid);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(bkt_split2_kernel, dim3((unsigned)(nsup + (pairs + kSplitChunk - 1) / kSplitChunk)), dim3(256),
                        0, stream, mid, supst, pstart2, nsup, shift, gcnt, rec);
     if ((e = hipGetLastError()) != hipSuccess) return e;

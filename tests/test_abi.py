@@ -80,14 +80,14 @@ def test_workspace_size(lib):
     # aligned
     csr = 32000 * 8 + 32000 * 16 + 8192 + 256
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 3) == csr
-    # the bucketed reduction: pair coefficients, the bucket-sorted records
-    # (12 B: packed key-row offset and query row, then the coefficients),
+    # the bucketed reduction: the bucket-sorted records (12 B: packed
+    # key-row offset and query row, then the coefficients),
     # three arrays over the 2000 / (4096 / 32) = 16 key-row buckets (+1:
     # counts, kept starts, pieces), the scan's block sums and the head-major
     # interleaved copy of Q and dO (bf16, 2d per query-head)
     # ... and the records in super-bucket order between the two placement
     # passes (16 B), with three arrays of 65 super-bucket entries
-    bucket = 32000 * 8 + 32000 * 12 + 3 * 256 + 256 + 2 * 2000 * 32 * 2 + 32000 * 16 + 3 * 512
+    bucket = 32000 * 12 + 3 * 256 + 256 + 2 * 2000 * 32 * 2 + 32000 * 16 + 3 * 512
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 4) == bucket
     # the library picks the bucketed reduction where it fits
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == bucket
