@@ -245,7 +245,8 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
         e = kmip::launch_key_order(K, n32, H, d, ntiles, kws, &keys, stream);
         if (e != hipSuccess) return hip_fail(e, "key order launch");
     }
-    hipError_t e = kmip::launch_pack_k(K, grouped ? keys.perm : nullptr, kp, n32, H, d, ntiles, stream);
+    hipError_t e = kmip::launch_pack_k(K, grouped ? keys.perm : nullptr, grouped ? keys.rows : nullptr, kp, n32, H, d, ntiles,
+                                          stream);
     if (e != hipSuccess) return hip_fail(e, "pack_k launch");
     int32_t* work_ctr = reinterpret_cast<int32_t*>(ws + tiled_bytes(N, H, d));
     e = kmip::launch_select(kp, Q, K, dtasks, grouped ? &groups : nullptr, grouped ? &keys : nullptr,

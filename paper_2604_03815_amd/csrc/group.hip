@@ -42,11 +42,14 @@ __global__ __launch_bounds__(256) void group_centers_kernel(const uint16_t* __re
 }
 
 // label[h][i] = argmax_c <q_i, center_c> (lowest c on ties); hist[h][c] counts
-// the labels.  A wave takes 32 queries of one head and scores them against
+// the labels (a block of 4 waves labels kLabelRounds * 128 queries, then adds
+// its 256 counts).  A wave takes 32 queries of one head and scores them against
 // 32 centres at a time with one bf16 MFMA per 16 dimensions (A = centres,
 // B = queries, so lane l holds the scores of query l % 32); lanes l and
 // l + 32 hold different centres of the same query and merge their maxima.
 // The labels only decide which queries the select kernel groups together.
+constexpr int kLabelRounds = 8;   // rounds of 128 queries per labelling block
+
 template <int D>
 __global__ __launch_bounds__(256) void group_label_kernel(const uint16_t* __restrict__ Q,
                                                           const uint16_t* __restrict__ centers,
@@ -54,44 +57,59 @@ __global__ __launch_bounds__(256) void group_label_kernel(const uint16_t* __rest
                                                           uint16_t* __restrict__ label,
                                                           int32_t* __restrict__ hist) {
     constexpr int NC = D / 16;
+    constexpr int TB = 4;   // the loads of four centre tiles go out together
+    static_assert(C % (32 * TB) == 0, "whole groups of centre tiles");
     __shared__ int32_t lh[C];
     const int h = blockIdx.y;
     const int lane = threadIdx.x & 63;
     const int col = lane & 31, half = lane >> 5;
-    const int64_t i = (int64_t)blockIdx.x * 128 + (threadIdx.x >> 6) * 32 + col;
-    const bool valid = i < N;
     lh[threadIdx.x] = 0;
-    bf16x8 bq[NC];
-    const uint16_t* row = Q + ((size_t)(valid ? i : 0) * H + h) * D + 8 * half;
-#pragma unroll
-    for (int c = 0; c < NC; ++c) bq[c] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(row + 16 * c));
+    __syncthreads();
     const uint16_t* ch = centers + (size_t)h * C * D + (size_t)col * D + 8 * half;
-    float best = -INFINITY;
-    int arg = 0;
-    for (int c0 = 0; c0 < C; c0 += 32) {
-        f32x16 acc = f32x16{};
+    for (int rd = 0; rd < kLabelRounds; ++rd) {
+        const int64_t i = ((int64_t)blockIdx.x * kLabelRounds + rd) * 128 + (threadIdx.x >> 6) * 32 + col;
+        const bool valid = i < N;
+        bf16x8 bq[NC];
+        const uint16_t* row = Q + ((size_t)(valid ? i : 0) * H + h) * D + 8 * half;
 #pragma unroll
         for (int c = 0; c < NC; ++c)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(ch + (size_t)c0 * D + 16 * c)), bq[c],
-                acc, 0, 0, 0);
-        // rows 8 (r / 4) + 4 half + r % 4 increase with r: strict > keeps the lowest centre
+            bq[c] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(row + 16 * c));
+        float best = -INFINITY;
+        int arg = 0;
+        for (int c0 = 0; c0 < C; c0 += 32 * TB) {
+            uint4 ct[TB][NC];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int cc = c0 + 8 * (r >> 2) + 4 * half + (r & 3);
-            if (acc[r] > best) {
-                best = acc[r];
-                arg = cc;
+            for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    ct[tb][c] = *reinterpret_cast<const uint4*>(ch + (size_t)(c0 + 32 * tb) * D + 16 * c);
+#pragma unroll
+            for (int tb = 0; tb < TB; ++tb) {
+                f32x16 acc = f32x16{};
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ct[tb][c]), bq[c], acc,
+                                                                  0, 0, 0);
+                // rows 8 (r / 4) + 4 half + r % 4 increase with r: strict >
+                // keeps the lowest centre
+                const int cb = c0 + 32 * tb;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int cc = cb + 8 * (r >> 2) + 4 * half + (r & 3);
+                    if (acc[r] > best) {
+                        best = acc[r];
+                        arg = cc;
+                    }
+                }
             }
         }
-    }
-    const float ob = __shfl_xor(best, 32);
-    const int oa = __shfl_xor(arg, 32);
-    if (ob > best || (ob == best && oa < arg)) arg = oa;
-    __syncthreads();
-    if (valid && half == 0) {
-        label[(size_t)h * N + i] = (uint16_t)arg;
-        atomicAdd(&lh[arg], 1);
+        const float ob = __shfl_xor(best, 32);
+        const int oa = __shfl_xor(arg, 32);
+        if (ob > best || (ob == best && oa < arg)) arg = oa;
+        if (valid && half == 0) {
+            label[(size_t)h * N + i] = (uint16_t)arg;
+            atomicAdd(&lh[arg], 1);
+        }
     }
     __syncthreads();
     if (lh[threadIdx.x] != 0) atomicAdd(&hist[(size_t)h * C + threadIdx.x], lh[threadIdx.x]);
@@ -178,7 +196,7 @@ hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, 
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(group_centers_kernel, dim3(H), dim3(C), 0, stream, q, N, H, d, centers);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const dim3 grid((unsigned)((N + 127) / 128), (unsigned)H);
+    const dim3 grid((unsigned)((N + 128 * kLabelRounds - 1) / (128 * kLabelRounds)), (unsigned)H);
     if (d == 16)
         hipLaunchKernelGGL(group_label_kernel<16>, grid, dim3(256), 0, stream, q, centers, N, H, label, hist);
     else if (d == 32)

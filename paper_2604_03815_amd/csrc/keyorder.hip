@@ -620,6 +620,7 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
         std::swap(kcur, knxt);
     }
     out->perm = cur;
+    out->rows = kcur;
     out->bounds = reinterpret_cast<const uint4*>(bounds);
     out->votes = votes;
     out->ctiles = ctiles;

@@ -32,9 +32,10 @@ struct Task {
 // tile t (32 positions), chunk c of 16 dims, lane l holds 8 bf16 of the key at
 // position p = 32t + l%32, dims 16c + 8(l/32) .. +8.  Position p holds key
 // perm[h][p] (key p when perm is NULL); positions >= N are zero; each head has
-// ntiles + kPadTiles tiles.
-hipError_t launch_pack_k(const void* K, const int32_t* perm, void* kp, int32_t N, int32_t H, int32_t d,
-                         int32_t ntiles, hipStream_t stream);
+// ntiles + kPadTiles tiles.  rows, when not NULL, holds those keys' rows
+// already in position order, head-major [H][N][d], and is read instead.
+hipError_t launch_pack_k(const void* K, const int32_t* perm, const uint16_t* rows, void* kp, int32_t N,
+                         int32_t H, int32_t d, int32_t ntiles, hipStream_t stream);
 
 // Stored key order with superblock bounds (keyorder.hip): the leaf order of
 // a balanced space-partitioning tree whose leaves are superblocks of
@@ -53,6 +54,7 @@ constexpr int kDenseVotes = 16;
 //   votes  [H]  dense-mode votes (zero before the select launch).
 struct KeyOrder {
     const int32_t* perm;
+    const uint16_t* rows;   // key rows in the stored order, head-major [H][N][d]
     const uint4* bounds;
     int32_t* votes;
     int32_t ctiles;

@@ -997,8 +997,11 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
 
 // Tiles t >= ntiles of each head (the kPadTiles padding) are written as zeros.
 // Position p of head h holds key perm[h][p] (key p without perm).
+// With rows (the key rows already in the stored order, head-major [H][N][d])
+// position p of head h is read from there, in sequence.
 __global__ __launch_bounds__(256) void pack_k_kernel(const uint16_t* __restrict__ K,
                                                      const int32_t* __restrict__ perm,
+                                                     const uint16_t* __restrict__ rows,
                                                      uint4* __restrict__ kp, int32_t N, int32_t H,
                                                      int32_t nchunk, int32_t ntiles) {
     const int32_t ntiles_all = ntiles + kPadTiles;
@@ -1015,8 +1018,12 @@ __global__ __launch_bounds__(256) void pack_k_kernel(const uint16_t* __restrict_
     uint4 v = make_uint4(0, 0, 0, 0);
     if (pos < N) {
         const int d = nchunk * 16;
-        const int key = perm != nullptr ? perm[(size_t)h * N + pos] : pos;
-        v = *reinterpret_cast<const uint4*>(K + ((size_t)key * H + h) * d + 16 * c + 8 * (lane >> 5));
+        if (rows != nullptr) {
+            v = *reinterpret_cast<const uint4*>(rows + ((size_t)h * N + pos) * d + 16 * c + 8 * (lane >> 5));
+        } else {
+            const int key = perm != nullptr ? perm[(size_t)h * N + pos] : pos;
+            v = *reinterpret_cast<const uint4*>(K + ((size_t)key * H + h) * d + 16 * c + 8 * (lane >> 5));
+        }
     }
     kp[u] = v;
 }
@@ -1071,14 +1078,14 @@ size_t select_lds_bytes(int32_t k, SelectShape shape) {
     return (size_t)shape.qb * (rows * 32 + (size_t)shape.slots * 64) * sizeof(uint64_t);
 }
 
-hipError_t launch_pack_k(const void* K, const int32_t* perm, void* kp, int32_t N, int32_t H, int32_t d,
+hipError_t launch_pack_k(const void* K, const int32_t* perm, const uint16_t* rows, void* kp, int32_t N, int32_t H, int32_t d,
                          int32_t ntiles, hipStream_t stream) {
     const int nchunk = d / 16;
     const size_t total = (size_t)H * (ntiles + kPadTiles) * nchunk * 64;
     if (total == 0) return hipSuccess;
     const unsigned blocks = (unsigned)((total + 255) / 256);
     hipLaunchKernelGGL(pack_k_kernel, dim3(blocks), dim3(256), 0, stream,
-                       reinterpret_cast<const uint16_t*>(K), perm, reinterpret_cast<uint4*>(kp), N, H,
+                       reinterpret_cast<const uint16_t*>(K), perm, rows, reinterpret_cast<uint4*>(kp), N, H,
                        nchunk, ntiles);
     return hipGetLastError();
 }
