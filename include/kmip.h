@@ -142,10 +142,12 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
  *                sorted by key and each key's run is summed in registers,
  *                one atomic per run piece of 256 pairs;
  *            4 = bucketed: the pairs are counting-sorted by buckets of
- *                4096/d consecutive key rows (j*H + h), each bucket's
- *                records are sorted by key row in LDS, at most 8192 at a
- *                time, and reduced as in 3; needs N*H <= 8192*4096/d
- *                (else KMIP_ERR_UNSUPPORTED and workspace size 0);
+ *                consecutive key rows (j*H + h), 4096/d of them, doubled
+ *                up to 512 while N*H would need more than 8192 buckets;
+ *                each bucket's records are sorted by key row in LDS, at
+ *                most 8192 at a time, and reduced as in 3; needs
+ *                N*H <= 8192*512 (else KMIP_ERR_UNSUPPORTED and workspace
+ *                size 0);
  *            0 = library's choice: 4 where it is supported, else 3;
  *            others UNSUPPORTED.
  *   workspace: kmip_bwd_workspace_size(variant) bytes, 256-byte aligned

@@ -335,7 +335,7 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
                                  dV, workspace, stream);
     } else if (v == 4) {
         if (!kmip::bwd_bucket_supported((int32_t)N, H, d))
-            return fail(KMIP_ERR_UNSUPPORTED, "variant 4 needs N*H/(4096/d) <= 8192 key-row buckets");
+            return fail(KMIP_ERR_UNSUPPORTED, "variant 4 needs N*H <= 8192*512 (key-row buckets of at most 512 rows)");
         e = kmip::launch_bwd_bucket(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
                                     dV, workspace, stream);
     } else if (v == 3) {

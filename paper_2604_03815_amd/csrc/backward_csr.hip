@@ -24,6 +24,7 @@
 #include "kmip_internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace kmip {
 namespace {
@@ -366,8 +367,9 @@ __global__ __launch_bounds__(256) void csr_reduce_kernel(
 
 // ---- Variant 4: pairs bucketed by blocks of key rows, sorted in LDS ----
 //
-// The key rows are cut into buckets of RB = 4096 / d consecutive rows, at
-// most kMaxBuckets of them.  The pairs are counting-sorted by bucket only: a
+// The key rows are cut into buckets of RB consecutive rows, at most
+// kMaxBuckets of them: RB = 4096 / d, doubled (up to kMaxBucketRows) while
+// N*H would need more buckets.  The pairs are counting-sorted by bucket only: a
 // counting pass takes ranges of consecutive pairs and counts them with an
 // LDS histogram over the buckets, one global atomic per bucket it touches
 // (against one per key row and workgroup for the full sort, whose per-row
@@ -376,9 +378,15 @@ __global__ __launch_bounds__(256) void csr_reduce_kernel(
 // cut into pieces that one workgroup sorts by key row in LDS and reduces
 // like the full sort's reduction.
 constexpr int kMaxBuckets = 8192;
+constexpr int kMaxBucketRows = 512;
 
-__host__ __device__ __forceinline__ int bucket_rows(int d) { return 4096 / d; }
-__host__ __device__ __forceinline__ int bucket_shift(int d) { return d == 16 ? 8 : (d == 32 ? 7 : 6); }
+// log2 of the bucket rows for N*H key rows at width d (the bucketed variant
+// takes N*H <= kMaxBuckets * kMaxBucketRows).
+inline int bucket_shift(int64_t nh, int d) {
+    int sh = d == 16 ? 8 : (d == 32 ? 7 : 6);
+    while ((nh + (1 << sh) - 1) >> sh > kMaxBuckets && (1 << sh) < kMaxBucketRows) ++sh;
+    return sh;
+}
 
 // Division of a dividend below 2^31 by a fixed divisor d >= 1 as a multiply
 // and shift: with l = ceil(log2 d) and m = ceil(2^(32+l) / d) (at most 2^33),
@@ -402,17 +410,18 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
 }
 
 // A pair record of the bucketed sort, 12 bytes: the key row's offset in its
-// bucket (below 2^8) in bits 21..28 and the head-major query row h*N + i in
-// bits 0..20 (the bucketed variant takes N*H <= kMaxBuckets * 4096 / d,
-// at most 2^21), then the coefficients.
+// bucket (below kMaxBucketRows = 2^9) in bits 22..30 and the head-major query
+// row h*N + i in bits 0..21 (the bucketed variant takes N*H <= kMaxBuckets *
+// kMaxBucketRows = 2^22), then the coefficients.
 struct BucketRecord {
     uint32_t packed;
     float a;
     float p;
 };
-constexpr int kQRowBits = 21;
+constexpr int kQRowBits = 22;
 static_assert(sizeof(BucketRecord) == 12, "packed record");
-static_assert((int64_t)kMaxBuckets * 4096 / 16 <= (int64_t)1 << kQRowBits, "query rows fit 21 bits");
+static_assert((int64_t)kMaxBuckets * kMaxBucketRows <= (int64_t)1 << kQRowBits, "query rows fit 22 bits");
+static_assert(kMaxBucketRows <= 1 << (32 - kQRowBits), "bucket offsets fit the other 10 bits");
 
 // Takes one slot of LDS counter ctr[bk] for each lane with bk >= 0 and
 // returns its number (kReturn) or nothing.  Lanes of a wave that share a bucket are served
@@ -774,17 +783,18 @@ __device__ __forceinline__ RowChunk<E> load_chunk(const uint16_t* p) {
     return c;
 }
 
-template <int D>
+template <int D, int RB>
 __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restrict__ QG,
                                                          const BucketRecord* __restrict__ rec,
                                                          const int32_t* __restrict__ sstart,
                                                          const int32_t* __restrict__ pstart, int32_t nbk,
                                                          float* __restrict__ dK, float* __restrict__ dV) {
-    constexpr int RB = 4096 / D;
     constexpr int E = D / 8;            // elements of the interleaved row per lane
     constexpr int G = 8;                // pairs whose rows a team loads at once
+    constexpr int CPT = (RB + 255) / 256;   // cursors per thread in the scan
+    using LRow = typename std::conditional<(RB <= 256), uint8_t, uint16_t>::type;
     __shared__ uint16_t ord[kPiece];
-    __shared__ uint8_t lrow[kPiece];
+    __shared__ LRow lrow[kPiece];
     __shared__ int32_t cursor[RB];
     __shared__ int32_t sh[256];
     const int t = threadIdx.x;
@@ -798,7 +808,7 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
     }
     const int32_t e0 = sstart[lo] + (w - pstart[lo]) * kPiece;
     const int32_t n = min(sstart[lo + 1] - e0, kPiece);
-    if (t < RB) cursor[t] = 0;
+    for (int r = t; r < RB; r += 256) cursor[r] = 0;
     __syncthreads();
 
     // 1a. records per key row; the rows (local to the bucket) are kept in LDS
@@ -812,13 +822,16 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int i = base + 256 * u + t;
-            if (row[u] >= 0) lrow[i] = (uint8_t)row[u];
+            if (row[u] >= 0) lrow[i] = (LRow)row[u];
             claim_slot<false>(cursor, row[u]);
         }
     }
     __syncthreads();
-    // 1b. exclusive scan of the counts: the cursors
-    const int32_t c = t < RB ? cursor[t] : 0;
+    // 1b. exclusive scan of the counts: the cursors (thread t owns cursors
+    // CPT t .. CPT t + CPT - 1)
+    int32_t c = 0;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) c += CPT * t + j < RB ? cursor[CPT * t + j] : 0;
     sh[t] = c;
     __syncthreads();
     for (int off = 1; off < 256; off <<= 1) {
@@ -827,7 +840,15 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
         sh[t] += add;
         __syncthreads();
     }
-    if (t < RB) cursor[t] = sh[t] - c;
+    int32_t run = sh[t] - c;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+        if (CPT * t + j < RB) {
+            const int32_t v = cursor[CPT * t + j];
+            cursor[CPT * t + j] = run;
+            run += v;
+        }
+    }
     __syncthreads();
     // 1c. place the record numbers in key-row order
     for (int base = 0; base < n; base += 256) {
@@ -906,14 +927,15 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
 }  // namespace
 
 bool bwd_bucket_supported(int32_t N, int32_t H, int32_t d) {
-    const int64_t nbk = ((int64_t)N * H + bucket_rows(d) - 1) / bucket_rows(d);
-    return nbk <= kMaxBuckets;
+    const int64_t nh = (int64_t)N * H;
+    const int sh = bucket_shift(nh, d);
+    return ((nh + (1 << sh) - 1) >> sh) <= kMaxBuckets;
 }
 
 size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };
     const size_t nh = (size_t)N * H, pairs = nh * k;
-    const size_t nbk = (nh + bucket_rows(d) - 1) / bucket_rows(d);
+    const size_t nbk = (nh + ((size_t)1 << bucket_shift((int64_t)nh, d)) - 1) >> bucket_shift((int64_t)nh, d);
     const size_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
     return al(pairs * sizeof(BucketRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
            al((nb + 1) * sizeof(int32_t)) + al(nh * 2 * d * sizeof(uint16_t)) + al(pairs * sizeof(PairRecord)) +
@@ -928,7 +950,8 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     const int64_t nh = (int64_t)N * H;
     if (nh == 0) return hipSuccess;
     const size_t pairs = (size_t)nh * k;
-    const int32_t rb = bucket_rows(d);
+    const int32_t shift = bucket_shift(nh, d);
+    const int32_t rb = 1 << shift;
     const int32_t nbk = (int32_t)((nh + rb - 1) / rb);
     if (nbk > kMaxBuckets) return hipErrorInvalidValue;
     const int32_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
@@ -965,7 +988,6 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     // pairs per counting workgroup: about 1024 workgroups, 8192 .. 65536 pairs each
     const uint32_t per = (uint32_t)std::min<size_t>(65536, std::max<size_t>(8192, (pairs / 1024 + 255) / 256 * 256));
     const unsigned cblocks = (unsigned)((pairs + per - 1) / per);
-    const int32_t shift = bucket_shift(d);
     const FastDiv divk = make_fastdiv((uint32_t)k), divh = make_fastdiv((uint32_t)H);
     hipLaunchKernelGGL(bkt_count_kernel, dim3(cblocks), dim3(256), 0, stream, idx, N, H, k, divk, divh, shift,
                        nbk, per, gcnt);
@@ -1012,15 +1034,20 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // at most one piece per bucket plus one per kPiece pairs; the rest exit
     const unsigned rblocks = (unsigned)(nbk + (pairs + kPiece - 1) / kPiece);
-    if (d == 16)
-        hipLaunchKernelGGL(bkt_reduce_kernel<16>, dim3(rblocks), dim3(256), 0, stream, qg, rec, sstart,
+#define KMIP_BKT_REDUCE(DD, RBV)                                                                       \
+    if (d == DD && rb == RBV)                                                                          \
+        hipLaunchKernelGGL((bkt_reduce_kernel<DD, RBV>), dim3(rblocks), dim3(256), 0, stream, qg, rec, sstart, \
                            pstart, nbk, dK, dV);
-    else if (d == 32)
-        hipLaunchKernelGGL(bkt_reduce_kernel<32>, dim3(rblocks), dim3(256), 0, stream, qg, rec, sstart,
-                           pstart, nbk, dK, dV);
-    else
-        hipLaunchKernelGGL(bkt_reduce_kernel<64>, dim3(rblocks), dim3(256), 0, stream, qg, rec, sstart,
-                           pstart, nbk, dK, dV);
+    KMIP_BKT_REDUCE(16, 256)
+    KMIP_BKT_REDUCE(16, 512)
+    KMIP_BKT_REDUCE(32, 128)
+    KMIP_BKT_REDUCE(32, 256)
+    KMIP_BKT_REDUCE(32, 512)
+    KMIP_BKT_REDUCE(64, 64)
+    KMIP_BKT_REDUCE(64, 128)
+    KMIP_BKT_REDUCE(64, 256)
+    KMIP_BKT_REDUCE(64, 512)
+#undef KMIP_BKT_REDUCE
     return hipGetLastError();
 }
 

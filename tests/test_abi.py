@@ -91,11 +91,13 @@ def test_workspace_size(lib):
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 4) == bucket
     # the library picks the bucketed reduction where it fits
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == bucket
-    # more than 8192 buckets: unsupported, size 0; the library picks the
-    # full key sort
-    assert lib.kmip_bwd_workspace_size(1_000_000, 4, 16, 16, 4) == 0
-    assert (lib.kmip_bwd_workspace_size(1_000_000, 4, 16, 16, 0)
-            == lib.kmip_bwd_workspace_size(1_000_000, 4, 16, 16, 3) > 0)
+    # buckets widen up to 512 key rows: N*H = 4M still fits 8192 buckets;
+    # beyond that the variant is unsupported (size 0) and the library picks
+    # the full key sort
+    assert lib.kmip_bwd_workspace_size(1_000_000, 4, 16, 16, 4) > 0
+    assert lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, 4) == 0
+    assert (lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, 0)
+            == lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, 3) > 0)
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 5) == 0
 
 

@@ -268,6 +268,19 @@ def test_full_size_sampled(cfg, sample):
     print(f"c{cfg}: sampled {strict} well-separated, {loose} near-tied query-heads")
 
 
+@pytest.mark.parametrize("n,h,d,k", [(600_000, 4, 16, 32), (70_000, 32, 64, 16)])
+def test_backward_wide_buckets(n, h, d, k):
+    # N*H above 8192 * 4096/d key rows: the bucketed backward (the default
+    # variant) widens its buckets to 512 key rows.  Index sets on sampled
+    # query-heads, structure on all; out, lse and every gradient on every
+    # query-head against the oracle on the GPU's own sets.
+    w = workloads.make(4, n=n) if d == 16 else workloads.iid(n, h, d, k, seed=11)
+    assert w.N * w.H > 8192 * 4096 // w.d
+    res = _run(w)
+    strict, loose = _check_all(w, res, sample=256)
+    print(f"N={w.N} H={w.H} d={w.d}: sampled {strict} well-separated, {loose} near-tied query-heads")
+
+
 def test_stale_workspace_does_not_change_selection():
     # The library clears every counter it reads (work counters, dense-mode
     # votes, seed slots) at the start of each call, whatever the workspace
