@@ -16,7 +16,7 @@ import numpy as np
 from ._lib import KmipError, MAX_K, check, load
 
 __all__ = [
-    "KmipError", "MAX_K", "topk", "attend", "fwd", "bwd", "topk_workspace_size",
+    "KmipError", "MAX_K", "topk", "attend", "fwd", "bwd", "attention", "topk_workspace_size",
     "bwd_workspace_size", "Workspace", "load",
 ]
 
@@ -161,3 +161,31 @@ def bwd(q, k_, v, dout, idx, lse, scale: float, variant: int = 0, dq=None, dk=No
                           int(variant), ctypes.c_void_p(buf.data_ptr() if buf is not None else 0),
                           0 if buf is None else buf.numel(), _stream_ptr()))
     return dq, dk, dv
+
+
+def attention(q, k_, v, kk: int, scale: float, graph_offsets=None, variant: int = 0, workspace=None):
+    """Differentiable k-MIP attention for training: returns out (float32 [N, H, d]).
+
+    The forward is ``fwd``; autograd's backward calls ``bwd`` with the saved
+    (topk_idx, lse), so the index set is held fixed and no gradient flows
+    through the selection (Section 3.1 and Appendix E of arXiv 2604.03815).
+    The incoming output gradient is rounded to bf16, the type the library's
+    backward reads, and dQ, dK, dV are returned in the dtype of Q, K, V.
+    """
+    torch = _torch()
+
+    class _Attention(torch.autograd.Function):
+        @staticmethod
+        def forward(ctx, q_, k2, v_):
+            out, idx, lse = fwd(q_, k2, v_, kk, scale, graph_offsets=graph_offsets, workspace=workspace)
+            ctx.save_for_backward(q_, k2, v_, idx, lse)
+            return out
+
+        @staticmethod
+        def backward(ctx, dout):
+            q_, k2, v_, idx, lse = ctx.saved_tensors
+            dq, dk, dv = bwd(q_, k2, v_, dout.to(torch.bfloat16).contiguous(), idx, lse, scale,
+                             variant=variant, workspace=workspace)
+            return dq.to(q_.dtype), dk.to(k2.dtype), dv.to(v_.dtype)
+
+    return _Attention.apply(q, k_, v)

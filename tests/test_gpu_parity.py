@@ -281,6 +281,30 @@ def test_backward_wide_buckets(n, h, d, k):
     print(f"N={w.N} H={w.H} d={w.d}: sampled {strict} well-separated, {loose} near-tied query-heads")
 
 
+def test_autograd_wrapper_matches_backward_and_oracle():
+    # kmip.attention under torch autograd: the loss sum(out * dO) gives
+    # Q, K, V gradients equal to kmip.bwd's rounded to bf16, the inputs'
+    # dtype (dQ bit for bit; dK and dV sum with atomics, so to within a bf16
+    # rounding), and within tolerance of the oracle's on the GPU's index sets.
+    w = workloads.iid(300, 2, 32, 16, seed=3, sizes=[120, 1, 179])
+    q, k, v = (_dev(a).requires_grad_() for a in (w.q, w.kk, w.v))
+    g = _dev(w.dout)
+    out = kmip.attention(q, k, v, w.k, w.scale, graph_offsets=w.offsets)
+    (out * g.float()).sum().backward()
+    out2, idx, lse = kmip.fwd(q.detach(), k.detach(), v.detach(), w.k, w.scale, graph_offsets=w.offsets)
+    dq, dk, dv = kmip.bwd(q.detach(), k.detach(), v.detach(), g, idx, lse, w.scale)
+    torch.cuda.synchronize()
+    assert torch.equal(out.detach(), out2)
+    assert q.grad.dtype == k.grad.dtype == v.grad.dtype == torch.bfloat16
+    assert torch.equal(q.grad, dq.to(torch.bfloat16))
+    for got, ref in ((k.grad, dk), (v.grad, dv)):
+        assert torch.allclose(got.float(), ref, rtol=2.0 ** -7, atol=1e-6)
+    Qd, Kd, Vd, dOd = _f64(w)
+    rq, rk, rv = oracle.backward(Qd, Kd, Vd, dOd, idx.cpu().numpy(), w.scale)
+    for name, got, ref in (("dQ", q.grad, rq), ("dK", k.grad, rk), ("dV", v.grad, rv)):
+        allclose_report(name, got.float().cpu().numpy(), ref)
+
+
 def test_stale_workspace_does_not_change_selection():
     # The library clears every counter it reads (work counters, dense-mode
     # votes, seed slots) at the start of each call, whatever the workspace
