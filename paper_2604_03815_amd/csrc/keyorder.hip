@@ -93,56 +93,62 @@ __device__ __forceinline__ bool node_by_index(int idx, int N, int lev, int& lo, 
     return n > SBK;
 }
 
+// Reductions over the 64 lanes of a wave (all active), returning the same
+// value to every lane: an inclusive scan within each row of 16 lanes by DPP
+// row shifts (lanes shifted in from outside the row contribute `fill`, the
+// operation's identity), then the four row totals (lanes 15, 31, 47, 63)
+// read as scalars.  The chain is four dependent DPP steps, far shorter than
+// a butterfly through the LDS crossbar.
+template <int CTRL>
+__device__ __forceinline__ float dpp_row_shr(float v, float fill) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(fill), __float_as_int(v), CTRL, 0xf,
+                                                      0xf, false));
+}
+
+__device__ __forceinline__ float lane_f(float v, int lane) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-    return v;
+    v += dpp_row_shr<0x111>(v, 0.0f);
+    v += dpp_row_shr<0x112>(v, 0.0f);
+    v += dpp_row_shr<0x114>(v, 0.0f);
+    v += dpp_row_shr<0x118>(v, 0.0f);
+    return (lane_f(v, 15) + lane_f(v, 31)) + (lane_f(v, 47) + lane_f(v, 63));
 }
 
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
-    return v;
+    v = fmaxf(v, dpp_row_shr<0x111>(v, -INFINITY));
+    v = fmaxf(v, dpp_row_shr<0x112>(v, -INFINITY));
+    v = fmaxf(v, dpp_row_shr<0x114>(v, -INFINITY));
+    v = fmaxf(v, dpp_row_shr<0x118>(v, -INFINITY));
+    return fmaxf(fmaxf(lane_f(v, 15), lane_f(v, 31)), fmaxf(lane_f(v, 47), lane_f(v, 63)));
 }
 
 __device__ __forceinline__ float wave_min(float v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v = fminf(v, __shfl_xor(v, m));
-    return v;
+    v = fminf(v, dpp_row_shr<0x111>(v, INFINITY));
+    v = fminf(v, dpp_row_shr<0x112>(v, INFINITY));
+    v = fminf(v, dpp_row_shr<0x114>(v, INFINITY));
+    v = fminf(v, dpp_row_shr<0x118>(v, INFINITY));
+    return fminf(fminf(lane_f(v, 15), lane_f(v, 31)), fminf(lane_f(v, 47), lane_f(v, 63)));
 }
 
-// Level lev, one wave per node: the node's mean and principal axis from an
-// evenly spaced sample of its keys (power iteration from the sample farthest
-// from the mean), the quantisation range of the sample's projections, and
-// zeroed histograms and counters.
+// One wave: the mean and principal axis of the S <= 64 sample rows x held by
+// the active lanes (power iteration from the sample farthest from the mean),
+// and the quantisation range of the sample's projections.  The lane with
+// `writer` set stores the node record nf: mean[D], axis[D], qlo, qinv (codes
+// map a projection p to clamp((p - qlo) * qinv) in 0 .. 65535).  x comes
+// back mean-centred.
 template <int D>
-__global__ __launch_bounds__(64) void tree_axis_kernel(const uint16_t* __restrict__ kp, int32_t N,
-                                                       int32_t H, int32_t lev, int32_t width,
-                                                       float* __restrict__ nodef,
-                                                       int32_t* __restrict__ nodeh) {
-    const int idx = blockIdx.x;
-    const int h = blockIdx.y;
-    const int t = threadIdx.x;
-    int lo, n;
-    if (!node_by_index(idx, N, lev, lo, n)) return;
-    int32_t* nh = nodeh + ((size_t)h * width + idx) * kNodeInts;
-    for (int e = t; e < kNodeInts; e += 64) nh[e] = 0;
-    const int S = n < kSample ? n : kSample;
-    const bool act = t < S;
-    float x[D];
-    if (act) {
-        const int p = lo + (int)(((int64_t)(2 * t + 1) * n) / (2 * S));
-        load_row_f32<D>(x, kp + ((size_t)h * N + p) * D);
-    } else {
-#pragma unroll
-        for (int i = 0; i < D; ++i) x[i] = 0.0f;
-    }
-    float mu[D];
+__device__ __forceinline__ void sample_axis(float (&x)[D], bool act, int S, bool writer,
+                                            float* __restrict__ nf) {
     const float inv_s = 1.0f / (float)S;
+    // static indices keep the arrays in registers
 #pragma unroll
     for (int i = 0; i < D; ++i) {
-        mu[i] = wave_sum(x[i]) * inv_s;
-        x[i] = act ? x[i] - mu[i] : 0.0f;
+        const float mu = wave_sum(x[i]) * inv_s;
+        if (writer) nf[i] = mu;
+        x[i] = act ? x[i] - mu : 0.0f;
     }
     float dd = 0.0f;
 #pragma unroll
@@ -179,20 +185,43 @@ __global__ __launch_bounds__(64) void tree_axis_kernel(const uint16_t* __restric
 #pragma unroll
     for (int i = 0; i < D; ++i) pr = fmaf(x[i], axis[i], pr);
     const float pmin = wave_min(act ? pr : INFINITY), pmax = wave_max(act ? pr : -INFINITY);
-    if (t == 0) {
-        float* nf = nodef + ((size_t)h * width + idx) * (2 * D + 2);
-        // static indices keep the arrays in registers
+    if (writer) {
 #pragma unroll
-        for (int i = 0; i < D; ++i) {
-            nf[i] = mu[i];
-            nf[D + i] = axis[i];
-        }
+        for (int i = 0; i < D; ++i) nf[D + i] = axis[i];
         // the mean-centred projection of the sample, widened a little so that
         // most keys fall inside the quantised range
         const float span = pmax - pmin;
         nf[2 * D] = pmin - 0.0625f * span;
         nf[2 * D + 1] = span > 0.0f ? 65535.0f / (1.125f * span) : 0.0f;
     }
+}
+
+// Level lev, one wave per node: the node's mean and principal axis from an
+// evenly spaced sample of its keys, the quantisation range, and zeroed
+// histograms and counters.
+template <int D>
+__global__ __launch_bounds__(64) void tree_axis_kernel(const uint16_t* __restrict__ kp, int32_t N,
+                                                       int32_t H, int32_t lev, int32_t width,
+                                                       float* __restrict__ nodef,
+                                                       int32_t* __restrict__ nodeh) {
+    const int idx = blockIdx.x;
+    const int h = blockIdx.y;
+    const int t = threadIdx.x;
+    int lo, n;
+    if (!node_by_index(idx, N, lev, lo, n)) return;
+    int32_t* nh = nodeh + ((size_t)h * width + idx) * kNodeInts;
+    for (int e = t; e < kNodeInts; e += 64) nh[e] = 0;
+    const int S = n < kSample ? n : kSample;
+    const bool act = t < S;
+    float x[D];
+    if (act) {
+        const int p = lo + (int)(((int64_t)(2 * t + 1) * n) / (2 * S));
+        load_row_f32<D>(x, kp + ((size_t)h * N + p) * D);
+    } else {
+#pragma unroll
+        for (int i = 0; i < D; ++i) x[i] = 0.0f;
+    }
+    sample_axis<D>(x, act, S, t == 0, nodef + ((size_t)h * width + idx) * (2 * D + 2));
 }
 
 template <int D>
@@ -407,6 +436,220 @@ __global__ __launch_bounds__(256) void tree_scatter_kernel(int32_t N, int32_t le
     }
 }
 
+// The bottom levels in one launch.  Once every split node of level lev0
+// holds at most kLocalRows(D) keys (their rows fill 128 KB of LDS), one
+// block per node loads the node's rows and runs all remaining levels in LDS:
+// the same sample axis, quantisation and exact two-pass split as the
+// per-level kernels, with the keys of the split value assigned to the left
+// side in position order.  Only a permutation of the node's positions moves
+// between levels; at the end the rows and key ids are written back in their
+// final order, in place (blocks own disjoint position ranges).
+//
+// Sub-nodes: a node of n <= 256 MS keys (MS a power of two) has every
+// sub-node at depth j at most 256 MS / 2^j keys (the left part rounds half
+// up to whole superblocks, which keeps that bound), so sub-nodes that are
+// still split (more than 256 keys) occur only at depths with 2^j <= MS / 2,
+// and their path index is below MS.
+template <int D>
+constexpr int kLocalRows = 65536 / D;
+
+template <int D>
+__global__ __launch_bounds__(512) void tree_local_kernel(int32_t N, int32_t lev0,
+                                                         uint16_t* __restrict__ kp,
+                                                         int32_t* __restrict__ perm) {
+    constexpr int NL = kLocalRows<D>;
+    constexpr int NT = 512;
+    constexpr int NW = NT / 64;
+    constexpr int PT = NL / NT;   // positions per thread, consecutive
+    constexpr int MS = NL / SBK;  // bound on the index of a split sub-node
+    constexpr int RW = D / 8;     // uint4 per row
+    __shared__ uint4 rows[NL * RW];
+    __shared__ uint16_t ord[2][NL];      // ord[.][position] = row of the node in LDS
+    __shared__ uint32_t hist[MS][128];   // two 16-bit bins per word
+    __shared__ float subf[MS][2 * D + 2];
+    __shared__ int32_t subi[MS][4];      // split value, ties to the left, high byte, prefix base
+    __shared__ uint32_t wtot[NW];
+    const int h = blockIdx.y;
+    const int t = threadIdx.x;
+    const int wave = t >> 6, lane = t & 63;
+    int lo, n;
+    if (!node_by_index(blockIdx.x, N, lev0, lo, n)) return;
+    if (n > NL) return;   // the host starts at a level where no node is larger
+    const uint4* src = reinterpret_cast<const uint4*>(kp + ((size_t)h * N + lo) * D);
+    // eight loads in flight per thread before their LDS stores
+    static_assert(NL * RW % (8 * NT) == 0, "whole rounds of eight");
+    for (int e0 = 0; e0 < NL * RW; e0 += 8 * NT) {
+        uint4 buf[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int e = e0 + u * NT + t;
+            if (e < n * RW) buf[u] = src[e];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int e = e0 + u * NT + t;
+            if (e < n * RW) rows[e] = buf[u];
+        }
+    }
+    for (int p = t; p < n; p += NT) ord[0][p] = (uint16_t)p;
+    __syncthreads();
+    int cb = 0;
+    for (int j = 0;; ++j) {
+        // the left-most sub-node is the largest of its depth
+        int big = n;
+        for (int l = 0; l < j && big > SBK; ++l) big = split_left(big);
+        if (big <= SBK) break;
+        // sample axis of every split sub-node, one wave each; clear its histogram
+        for (int sidx = wave; sidx < MS && sidx < (1 << j); sidx += NW) {
+            int slo, sn;
+            if (!node_by_index(sidx, n, j, slo, sn)) continue;
+            float x[D];
+            const int p = slo + (int)(((int64_t)(2 * lane + 1) * sn) / (2 * kSample));
+            load_row_f32<D>(x, reinterpret_cast<const uint16_t*>(&rows[(int)ord[cb][p] * RW]));
+            sample_axis<D>(x, true, kSample, lane == 0, subf[sidx]);
+            hist[sidx][2 * lane] = 0u;
+            hist[sidx][2 * lane + 1] = 0u;
+        }
+        __syncthreads();
+        // codes and the high-byte histograms
+        int code[PT], sid[PT], sblo[PT], sbn[PT];
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int p = t * PT + i;
+            int slo = 0, sn = 0, sidx = -1;
+            code[i] = 0;
+            if (p < n && node_of(p, n, j, slo, sn, sidx) && sidx < MS) {
+                float x[D];
+                load_row_f32<D>(x, reinterpret_cast<const uint16_t*>(&rows[(int)ord[cb][p] * RW]));
+                code[i] = (int)quantise<D>(subf[sidx], x);
+                atomicAdd(&hist[sidx][code[i] >> 9], 1u << (((code[i] >> 8) & 1) << 4));
+            } else {
+                sidx = -1;
+            }
+            sid[i] = sidx;
+            sblo[i] = slo;
+            sbn[i] = sn;
+        }
+        __syncthreads();
+        // two passes of the split search, one wave per split sub-node: the
+        // bin that holds the target rank, then the value within that bin
+        for (int pass = 0; pass < 2; ++pass) {
+            for (int sidx = wave; sidx < MS && sidx < (1 << j); sidx += NW) {
+                int slo, sn;
+                if (!node_by_index(sidx, n, j, slo, sn)) continue;
+                const int target = pass == 0 ? split_left(sn) : subi[sidx][1];
+                const uint32_t w0 = hist[sidx][2 * lane], w1 = hist[sidx][2 * lane + 1];
+                const int c[4] = {(int)(w0 & 0xFFFFu), (int)(w0 >> 16), (int)(w1 & 0xFFFFu), (int)(w1 >> 16)};
+                const int mine = c[0] + c[1] + c[2] + c[3];
+                int incl = mine;
+#pragma unroll
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int o = __shfl_up(incl, off);
+                    if (lane >= off) incl += o;
+                }
+                int below = incl - mine;
+                if (target >= below && target < incl) {
+                    int b = 0;
+                    if (target >= below + c[0]) {
+                        below += c[0];
+                        b = 1;
+                        if (target >= below + c[1]) {
+                            below += c[1];
+                            b = 2;
+                            if (target >= below + c[2]) {
+                                below += c[2];
+                                b = 3;
+                            }
+                        }
+                    }
+                    const int bin = 4 * lane + b;
+                    if (pass == 0) {
+                        subi[sidx][2] = bin;
+                    } else {
+                        subi[sidx][0] = (subi[sidx][2] << 8) | bin;
+                    }
+                    subi[sidx][1] = target - below;
+                }
+                hist[sidx][2 * lane] = 0u;
+                hist[sidx][2 * lane + 1] = 0u;
+            }
+            __syncthreads();
+            if (pass == 0) {
+#pragma unroll
+                for (int i = 0; i < PT; ++i) {
+                    if (sid[i] >= 0 && (code[i] >> 8) == subi[sid[i]][2])
+                        atomicAdd(&hist[sid[i]][(code[i] & 255) >> 1], 1u << ((code[i] & 1) << 4));
+                }
+                __syncthreads();
+            }
+        }
+        // partition: a block-wide scan of (code < v) + (code == v) << 16
+        uint32_t pre[PT];
+        uint32_t tot = 0u;
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            pre[i] = tot;
+            if (sid[i] >= 0) {
+                const int v = subi[sid[i]][0];
+                tot += code[i] < v ? 1u : (code[i] == v ? 0x10000u : 0u);
+            }
+        }
+        uint32_t incl = tot;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t o = __shfl_up(incl, off);
+            if (lane >= off) incl += o;
+        }
+        if (lane == 63) wtot[wave] = incl;
+        __syncthreads();
+        uint32_t base = incl - tot;
+        for (int w = 0; w < wave; ++w) base += wtot[w];
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            if (sid[i] >= 0 && t * PT + i == sblo[i]) subi[sid[i]][3] = (int)(base + pre[i]);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int p = t * PT + i;
+            if (p >= n) continue;
+            int dst = p;
+            if (sid[i] >= 0) {
+                const int s2 = sid[i];
+                const uint32_t rel = base + pre[i] - (uint32_t)subi[s2][3];
+                const int ltb = (int)(rel & 0xFFFFu), tieb = (int)(rel >> 16);
+                const int tl = subi[s2][1];
+                const int v = subi[s2][0];
+                const int leftb = ltb + (tieb < tl ? tieb : tl);
+                const bool left = code[i] < v || (code[i] == v && tieb < tl);
+                dst = left ? sblo[i] + leftb : sblo[i] + split_left(sbn[i]) + (p - sblo[i] - leftb);
+            }
+            ord[cb ^ 1][dst] = ord[cb][p];
+        }
+        __syncthreads();
+        cb ^= 1;
+    }
+    // write back: read every key id first, then overwrite the node's range
+    int32_t* pk = perm + (size_t)h * N + lo;
+    int32_t key[PT];
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+        const int p = t + i * NT;
+        key[i] = p < n ? pk[(int)ord[cb][p]] : 0;
+    }
+    __syncthreads();
+    uint4* dstr = reinterpret_cast<uint4*>(kp + ((size_t)h * N + lo) * D);
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+        const int p = t + i * NT;
+        if (p >= n) continue;
+        pk[p] = key[i];
+        const int r = (int)ord[cb][p];
+#pragma unroll
+        for (int c = 0; c < RW; ++c) dstr[p * RW + c] = rows[r * RW + c];
+    }
+}
+
 // perm[h][p] = p and the head-major copy kp[h][p] = K row (p, h).
 template <int D>
 __global__ __launch_bounds__(256) void tree_init_kernel(const uint16_t* __restrict__ K, int32_t N, int32_t H,
@@ -522,6 +765,17 @@ void tree_shape(int32_t N, int32_t& levels, int32_t& width) {
     width = levels > 0 ? (1 << (levels - 1)) : 1;
 }
 
+// First level at which every split node fits tree_local_kernel (nl keys),
+// or levels.  The left-most node of a level is its largest.
+int32_t tree_local_level(int32_t N, int32_t levels, int32_t nl) {
+    int32_t big = N;
+    for (int32_t lev = 0; lev < levels; ++lev) {
+        if (big <= nl) return lev;
+        big = big > SBK ? split_left(big) : big;
+    }
+    return levels;
+}
+
 }  // namespace
 
 int32_t key_order_ctiles(int32_t ntiles) {
@@ -583,7 +837,9 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
     int32_t* nxt = perm_b;
     uint16_t* kcur = kp_a;
     uint16_t* knxt = kp_b;
-    for (int lev = 0; lev < levels; ++lev) {
+    const int32_t lev0 =
+        tree_local_level(N, levels, d == 16 ? kLocalRows<16> : (d == 32 ? kLocalRows<32> : kLocalRows<64>));
+    for (int lev = 0; lev < lev0; ++lev) {
         const dim3 ngrid((unsigned)(1 << lev), (unsigned)H);
 #define KMIP_TREE_LEVEL(DD)                                                                          \
     hipLaunchKernelGGL(tree_axis_kernel<DD>, ngrid, dim3(64), 0, stream, kcur, N, H, lev, width,     \
@@ -618,6 +874,16 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
         if ((e = hipGetLastError()) != hipSuccess) return e;
         std::swap(cur, nxt);
         std::swap(kcur, knxt);
+    }
+    if (lev0 < levels) {
+        const dim3 lgrid((unsigned)(1 << lev0), (unsigned)H);
+        if (d == 16)
+            hipLaunchKernelGGL(tree_local_kernel<16>, lgrid, dim3(512), 0, stream, N, lev0, kcur, cur);
+        else if (d == 32)
+            hipLaunchKernelGGL(tree_local_kernel<32>, lgrid, dim3(512), 0, stream, N, lev0, kcur, cur);
+        else
+            hipLaunchKernelGGL(tree_local_kernel<64>, lgrid, dim3(512), 0, stream, N, lev0, kcur, cur);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     out->perm = cur;
     out->rows = kcur;
