@@ -85,6 +85,31 @@ def test_small_cases_full(case):
     _check_all(w, _run(w))
 
 
+@pytest.mark.parametrize("n,d,k", [(8193, 16, 32), (12345, 32, 16), (9001, 64, 128)])
+def test_key_tree_odd_sizes_full(n, d, k):
+    # Single graphs just above the size from which the keys are stored in
+    # tree order: nodes of odd sizes, a partial last superblock, and both the
+    # per-level splits and the levels finished in LDS.  Full comparison.
+    w = workloads.iid(n, 2, d, k, seed=n + d)
+    _check_all(w, _run(w))
+
+
+def test_identical_keys_tree():
+    # Every key row equal: every projection ties, so each split of the key
+    # tree is decided by the tie count alone, and every score of a query
+    # ties, so every query keeps keys 0 .. k-1 in that order.
+    N, H, d, k = 20000, 2, 32, 16
+    rng = np.random.default_rng(3)
+    row = rng.standard_normal((1, H, d)).astype(np.float32)
+    w = workloads.Workload("same_keys", N, H, d, k, 0.25, None,
+                           workloads.bf16_round(rng.standard_normal((N, H, d)).astype(np.float32)),
+                           workloads.bf16_round(np.repeat(row, N, axis=0)),
+                           workloads.bf16_round(rng.standard_normal((N, H, d)).astype(np.float32)),
+                           None, False)
+    res = _run(w, backward=False)
+    assert (res["idx"] == np.arange(k, dtype=np.int32)).all()
+
+
 def test_config1_full():
     w = workloads.make(1)
     strict, loose = _check_all(w, _run(w, backward=False))
