@@ -104,7 +104,8 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
-              "(the k-MIP path here is single-GPU; see DESIGN.md for how it would shard)",
+              "(the k-MIP path here is single-GPU; several graphs would shard by whole "
+              "graphs, one large graph by query ranges after an all-gather of K and V)",
               file=sys.stderr)
         sys.exit(2)
 
