@@ -47,7 +47,7 @@ def parse():
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-sample", type=int, default=2048, help="query-heads in the oracle sample")
-    p.add_argument("--bwd-variant", type=int, default=0, help="backward: 0 library choice, 1 per-pair atomics, 2 key-aggregated, 3 key-sorted segmented, 4 bucketed")
+    p.add_argument("--bwd-variant", type=int, default=0, help="backward: 0 library choice, 1 per-pair atomics, 2 key-sorted segmented, 3 bucketed, 4 key-aggregated")
     p.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                    help="before the warm-up, run one plain copy kernel that reads and writes MIB MiB "
                         "(the reference for the FETCH_SIZE/WRITE_SIZE counter runs)")

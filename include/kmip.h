@@ -130,30 +130,48 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
  *   in:  dOut bf16 [N, H, d]; topk_idx [N, H, k] and lse [N, H] as written
  *        by the forward.
  *   out: dQ, dK, dV float32 [N, H, d], overwritten.
- *   variant: how dK and dV are summed over the queries that selected a
- *            key (all use fp32 atomics somewhere, so the summation order is
- *            not fixed and results may differ in the last bits from call to
- *            call):
- *            1 = every selected pair adds its rows with atomics;
- *            2 = key-aggregated: queries are grouped by direction, each
- *                workgroup of 256 queries sums its pairs per key in LDS and
- *                adds each key's sums once;
- *            3 = key-sorted segmented reduction: the pairs are counting-
- *                sorted by key and each key's run is summed in registers,
- *                one atomic per run piece of 256 pairs;
- *            4 = bucketed: the pairs are counting-sorted by buckets of
- *                consecutive key rows (j*H + h), 4096/d of them, doubled
- *                up to 512 while N*H would need more than 8192 buckets;
- *                each bucket's records are sorted by key row in LDS, at
- *                most 8192 at a time, and reduced as in 3; needs
+ *
+ * Parameters compared with the forward's: there is no graph_offsets,
+ * num_graphs or out.  The saved indices are global node ids that already
+ * lie in their query's graph, so the batch structure is not needed again;
+ * and D_i = sum_j p_j dp_j comes from the dp_j that g_j needs anyway, so
+ * the forward's out (whose dot product with dOut_i is the same D_i) is not
+ * read.  The order is (inputs, saved tensors, sizes, scale, outputs,
+ * variant, workspace, stream).
+ *
+ *   variant (kmip_bwd_variant_t): how dK and dV are summed over the queries
+ *            that selected a key.  All use fp32 atomics somewhere, so the
+ *            summation order is not fixed and results may differ in the
+ *            last bits from call to call.
+ *            KMIP_BWD_ATOMIC: every selected pair adds its rows with
+ *                atomics;
+ *            KMIP_BWD_SEGMENTED: the pairs are counting-sorted by key row
+ *                and each key's run is summed in registers, one atomic per
+ *                run piece of 256 pairs;
+ *            KMIP_BWD_BUCKETED: the pairs are counting-sorted by buckets of
+ *                consecutive key rows (j*H + h), 4096/d of them, doubled up
+ *                to 512 while N*H would need more than 8192 buckets; each
+ *                bucket's records are sorted by key row in LDS, at most 8192
+ *                at a time, and reduced as in SEGMENTED; needs
  *                N*H <= 8192*512 (else KMIP_ERR_UNSUPPORTED and workspace
  *                size 0);
- *            0 = library's choice: 4 where it is supported, else 3;
- *            others UNSUPPORTED.
+ *            KMIP_BWD_KEY_AGGREGATED: queries are grouped by direction, each
+ *                workgroup of 256 queries sums its pairs per key in LDS and
+ *                adds each key's sums once;
+ *            KMIP_BWD_AUTO: BUCKETED where it is supported, else SEGMENTED;
+ *            any other value: KMIP_ERR_UNSUPPORTED.
  *   workspace: kmip_bwd_workspace_size(variant) bytes, 256-byte aligned
- *              (0 for variant 1, which accepts NULL); too small or
+ *              (0 for KMIP_BWD_ATOMIC, which accepts NULL); too small or
  *              misaligned -> KMIP_ERR_WORKSPACE.
  */
+typedef enum {
+    KMIP_BWD_AUTO = 0,
+    KMIP_BWD_ATOMIC = 1,
+    KMIP_BWD_SEGMENTED = 2,
+    KMIP_BWD_BUCKETED = 3,
+    KMIP_BWD_KEY_AGGREGATED = 4
+} kmip_bwd_variant_t;
+
 size_t kmip_bwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t variant);
 kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* dOut,
                        const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,

@@ -31,15 +31,32 @@ def _stream_ptr():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-def _dev(t, dtype, name):
+def _validate(*specs):
+    """Checks (tensor, name, dtype, shape) specs before anything is allocated
+    or launched: every tensor must have its dtype and shape (None: any) and
+    be contiguous, and then all must sit on the same GPU.  The C ABI cannot
+    see buffer sizes, so a size mismatch has to be caught here, before a
+    kernel would read or write out of bounds."""
     torch = _torch()
-    if not isinstance(t, torch.Tensor) or not t.is_cuda:
-        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
-    if t.dtype != dtype:
-        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
-    if not t.is_contiguous():
-        raise ValueError(f"{name} must be contiguous")
-    return ctypes.c_void_p(t.data_ptr())
+    for t, name, dtype, shape in specs:
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a torch tensor")
+        if t.dtype != dtype:
+            raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+        if shape is not None and tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    dev = specs[0][0].device
+    for t, name, _, _ in specs:
+        if not t.is_cuda:
+            raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+        if t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, expected {dev} (the device of {specs[0][1]})")
+
+
+def _ptr(t):
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
 
 
 def _offsets(graph_offsets):
@@ -72,10 +89,30 @@ class Workspace:
         return self.buf
 
 
-def _shape(q):
-    if q.dim() != 3:
-        raise ValueError("Q must be [N, H, d]")
-    return q.shape
+def _nhd(q, name="Q"):
+    torch = _torch()
+    if not isinstance(q, torch.Tensor) or q.dim() != 3:
+        raise ValueError(f"{name} must be a tensor [N, H, d]")
+    return tuple(int(x) for x in q.shape)
+
+
+def _kk(idx, name="topk_idx"):
+    torch = _torch()
+    if not isinstance(idx, torch.Tensor) or idx.dim() != 3:
+        raise ValueError(f"{name} must be a tensor [N, H, k]")
+    return int(idx.shape[-1])
+
+
+def _workspace(ws, nbytes, device):
+    """Device buffer of at least nbytes from ws (a Workspace, or None for a
+    fresh one), or None when nbytes is 0."""
+    if nbytes == 0:
+        return None
+    buf = (ws or Workspace(device)).get(nbytes)
+    _validate((buf, "workspace", _torch().uint8, None))
+    if buf.device != device:
+        raise ValueError(f"workspace is on {buf.device}, expected {device}")
+    return buf
 
 
 def topk(q, k_, kk: int, graph_offsets: Optional[Sequence[int]] = None, idx=None,
@@ -86,16 +123,20 @@ def topk(q, k_, kk: int, graph_offsets: Optional[Sequence[int]] = None, idx=None
     stream right before and after the score+select kernel (not the pre-passes).
     """
     torch = _torch()
-    N, H, d = _shape(q)
+    N, H, d = _nhd(q)
+    kk = int(kk)
+    specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d))]
+    if idx is not None:
+        specs.append((idx, "topk_idx", torch.int32, (N, H, kk)))
+    _validate(*specs)
+    o, optr, G = _offsets(graph_offsets)
+    if o is not None and (o.ndim != 1 or len(o) < 2):
+        raise ValueError("graph_offsets must be a 1-D sequence of at least two entries")
     if idx is None:
         idx = torch.empty((N, H, kk), dtype=torch.int32, device=q.device)
-    o, optr, G = _offsets(graph_offsets)
-    ws = workspace or Workspace(q.device)
-    nbytes = topk_workspace_size(N, H, d, kk, G)
-    buf = ws.get(nbytes)
-    args = (_dev(q, torch.bfloat16, "Q"), _dev(k_, torch.bfloat16, "K"), optr, G, N, H, d, kk,
-            _dev(idx, torch.int32, "topk_idx"), ctypes.c_void_p(buf.data_ptr()), buf.numel(),
-            _stream_ptr())
+    buf = _workspace(workspace, topk_workspace_size(N, H, d, kk, G), q.device)
+    args = (_ptr(q), _ptr(k_), optr, G, N, H, d, kk, _ptr(idx), _ptr(buf),
+            0 if buf is None else buf.numel(), _stream_ptr())
     if select_events is None:
         check(load().kmip_topk(*args))
     else:
@@ -111,34 +152,41 @@ def topk(q, k_, kk: int, graph_offsets: Optional[Sequence[int]] = None, idx=None
 def attend(q, k_, v, idx, scale: float, out=None, lse=None):
     """Gather-softmax-aggregate on a given index set: returns (out, lse)."""
     torch = _torch()
-    N, H, d = _shape(q)
-    kk = idx.shape[-1]
+    N, H, d = _nhd(q)
+    kk = _kk(idx)
+    specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d)),
+             (v, "V", torch.bfloat16, (N, H, d)), (idx, "topk_idx", torch.int32, (N, H, kk))]
+    if out is not None:
+        specs.append((out, "out", torch.float32, (N, H, d)))
+    if lse is not None:
+        specs.append((lse, "lse", torch.float32, (N, H)))
+    _validate(*specs)
     if out is None:
         out = torch.empty((N, H, d), dtype=torch.float32, device=q.device)
     if lse is None:
         lse = torch.empty((N, H), dtype=torch.float32, device=q.device)
-    check(load().kmip_attend(_dev(q, torch.bfloat16, "Q"), _dev(k_, torch.bfloat16, "K"),
-                             _dev(v, torch.bfloat16, "V"), N, H, d, kk, float(scale),
-                             _dev(idx, torch.int32, "topk_idx"), _dev(out, torch.float32, "out"),
-                             _dev(lse, torch.float32, "lse"), _stream_ptr()))
+    check(load().kmip_attend(_ptr(q), _ptr(k_), _ptr(v), N, H, d, kk, float(scale), _ptr(idx),
+                             _ptr(out), _ptr(lse), _stream_ptr()))
     return out, lse
 
 
 def fwd(q, k_, v, kk: int, scale: float, graph_offsets=None, workspace=None):
     """Full forward: returns (out, topk_idx, lse)."""
     torch = _torch()
-    N, H, d = _shape(q)
+    N, H, d = _nhd(q)
+    kk = int(kk)
+    _validate((q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d)),
+              (v, "V", torch.bfloat16, (N, H, d)))
+    o, optr, G = _offsets(graph_offsets)
+    if o is not None and (o.ndim != 1 or len(o) < 2):
+        raise ValueError("graph_offsets must be a 1-D sequence of at least two entries")
     out = torch.empty((N, H, d), dtype=torch.float32, device=q.device)
     idx = torch.empty((N, H, kk), dtype=torch.int32, device=q.device)
     lse = torch.empty((N, H), dtype=torch.float32, device=q.device)
-    o, optr, G = _offsets(graph_offsets)
-    ws = workspace or Workspace(q.device)
-    buf = ws.get(topk_workspace_size(N, H, d, kk, G))
-    check(load().kmip_fwd(_dev(q, torch.bfloat16, "Q"), _dev(k_, torch.bfloat16, "K"),
-                          _dev(v, torch.bfloat16, "V"), optr, G, N, H, d, kk, float(scale),
-                          _dev(out, torch.float32, "out"), _dev(idx, torch.int32, "topk_idx"),
-                          _dev(lse, torch.float32, "lse"), ctypes.c_void_p(buf.data_ptr()),
-                          buf.numel(), _stream_ptr()))
+    buf = _workspace(workspace, topk_workspace_size(N, H, d, kk, G), q.device)
+    check(load().kmip_fwd(_ptr(q), _ptr(k_), _ptr(v), optr, G, N, H, d, kk, float(scale), _ptr(out),
+                          _ptr(idx), _ptr(lse), _ptr(buf), 0 if buf is None else buf.numel(),
+                          _stream_ptr()))
     return out, idx, lse
 
 
@@ -146,19 +194,23 @@ def bwd(q, k_, v, dout, idx, lse, scale: float, variant: int = 0, dq=None, dk=No
         workspace=None):
     """Backward with the index set held fixed: returns (dQ, dK, dV) float32."""
     torch = _torch()
-    N, H, d = _shape(q)
-    kk = idx.shape[-1]
-    dq = dq if dq is not None else torch.empty((N, H, d), dtype=torch.float32, device=q.device)
-    dk = dk if dk is not None else torch.empty((N, H, d), dtype=torch.float32, device=q.device)
-    dv = dv if dv is not None else torch.empty((N, H, d), dtype=torch.float32, device=q.device)
-    nbytes = bwd_workspace_size(N, H, d, kk, variant)
-    buf = (workspace or Workspace(q.device)).get(nbytes) if nbytes else None
-    check(load().kmip_bwd(_dev(q, torch.bfloat16, "Q"), _dev(k_, torch.bfloat16, "K"),
-                          _dev(v, torch.bfloat16, "V"), _dev(dout, torch.bfloat16, "dOut"),
-                          _dev(idx, torch.int32, "topk_idx"), _dev(lse, torch.float32, "lse"),
-                          N, H, d, kk, float(scale), _dev(dq, torch.float32, "dQ"),
-                          _dev(dk, torch.float32, "dK"), _dev(dv, torch.float32, "dV"),
-                          int(variant), ctypes.c_void_p(buf.data_ptr() if buf is not None else 0),
+    N, H, d = _nhd(q)
+    kk = _kk(idx)
+    nd = (N, H, d)
+    specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, nd), (v, "V", torch.bfloat16, nd),
+             (dout, "dOut", torch.bfloat16, nd), (idx, "topk_idx", torch.int32, (N, H, kk)),
+             (lse, "lse", torch.float32, (N, H))]
+    for t, name in ((dq, "dQ"), (dk, "dK"), (dv, "dV")):
+        if t is not None:
+            specs.append((t, name, torch.float32, nd))
+    _validate(*specs)
+    dev = q.device
+    dq = dq if dq is not None else torch.empty(nd, dtype=torch.float32, device=dev)
+    dk = dk if dk is not None else torch.empty(nd, dtype=torch.float32, device=dev)
+    dv = dv if dv is not None else torch.empty(nd, dtype=torch.float32, device=dev)
+    buf = _workspace(workspace, bwd_workspace_size(N, H, d, kk, variant), dev)
+    check(load().kmip_bwd(_ptr(q), _ptr(k_), _ptr(v), _ptr(dout), _ptr(idx), _ptr(lse), N, H, d, kk,
+                          float(scale), _ptr(dq), _ptr(dk), _ptr(dv), int(variant), _ptr(buf),
                           0 if buf is None else buf.numel(), _stream_ptr()))
     return dq, dk, dv
 

@@ -14,6 +14,13 @@ KMIP_ERR_WORKSPACE = 3
 KMIP_ERR_HIP = 4
 MAX_K = 128
 
+# kmip_bwd_variant_t
+BWD_AUTO = 0
+BWD_ATOMIC = 1
+BWD_SEGMENTED = 2
+BWD_BUCKETED = 3
+BWD_KEY_AGGREGATED = 4
+
 # Every symbol declared in include/kmip.h.
 EXPORTS = (
     "kmip_topk_workspace_size", "kmip_topk", "kmip_topk_with_events", "kmip_attend", "kmip_fwd_workspace_size",

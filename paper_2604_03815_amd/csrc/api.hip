@@ -289,20 +289,20 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
     return kmip_attend(Q, K, V, N, H, d, k, scale, topk_idx, out, lse, stream);
 }
 
-// Backward variant the library picks (variant 0): the bucketed reduction
+// Backward variant the library picks (KMIP_BWD_AUTO): the bucketed reduction
 // where the key rows fit its bucket table, else the full key sort.
 static int32_t default_bwd_variant(int64_t N, int32_t H, int32_t d) {
-    return kmip::bwd_bucket_supported((int32_t)N, H, d) ? 4 : 3;
+    return kmip::bwd_bucket_supported((int32_t)N, H, d) ? KMIP_BWD_BUCKETED : KMIP_BWD_SEGMENTED;
 }
 
 size_t kmip_bwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t variant) {
     if (check_sizes(N, H, d, k) != KMIP_OK) return 0;
-    const int32_t v = variant == 0 ? default_bwd_variant(N, H, d) : variant;
-    if (v == 2) return align_up(kmip::bwd_agg_workspace_bytes((int32_t)N, H, d));
-    if (v == 3) return align_up(kmip::bwd_csr_workspace_bytes((int32_t)N, H, k));
-    if (v == 4) return kmip::bwd_bucket_supported((int32_t)N, H, d)
-                           ? align_up(kmip::bwd_bucket_workspace_bytes((int32_t)N, H, d, k))
-                           : 0;
+    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d) : variant;
+    if (v == KMIP_BWD_KEY_AGGREGATED) return align_up(kmip::bwd_agg_workspace_bytes((int32_t)N, H, d));
+    if (v == KMIP_BWD_SEGMENTED) return align_up(kmip::bwd_csr_workspace_bytes((int32_t)N, H, k));
+    if (v == KMIP_BWD_BUCKETED) return kmip::bwd_bucket_supported((int32_t)N, H, d)
+                                         ? align_up(kmip::bwd_bucket_workspace_bytes((int32_t)N, H, d, k))
+                                         : 0;
     return 0;
 }
 
@@ -313,32 +313,33 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
-    if (variant < 0 || variant > 4) return fail(KMIP_ERR_UNSUPPORTED, "backward variant %d", variant);
+    if (variant < KMIP_BWD_AUTO || variant > KMIP_BWD_KEY_AGGREGATED)
+        return fail(KMIP_ERR_UNSUPPORTED, "backward variant %d", variant);
     if (N == 0) return ok();
     if (!Q || !K || !V || !dOut || !topk_idx || !lse || !dQ || !dK || !dV)
         return fail(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_bwd");
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(dOut))
         return fail(KMIP_ERR_INVALID_ARG, "Q, K, V and dOut must be 16-byte aligned");
     if (!aligned16(dK) || !aligned16(dV)) return fail(KMIP_ERR_INVALID_ARG, "dK and dV must be 16-byte aligned");
-    const int32_t v = variant == 0 ? default_bwd_variant(N, H, d) : variant;
+    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d) : variant;
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
     hipError_t e;
-    if (v != 1) {
+    if (v != KMIP_BWD_ATOMIC) {
         const size_t need = kmip_bwd_workspace_size(N, H, d, k, v);
         if (workspace == nullptr || workspace_bytes < need)
             return fail(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
         if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0)
             return fail(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
     }
-    if (v == 2) {
+    if (v == KMIP_BWD_KEY_AGGREGATED) {
         e = kmip::launch_bwd_agg(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
                                  dV, workspace, stream);
-    } else if (v == 4) {
+    } else if (v == KMIP_BWD_BUCKETED) {
         if (!kmip::bwd_bucket_supported((int32_t)N, H, d))
-            return fail(KMIP_ERR_UNSUPPORTED, "variant 4 needs N*H <= 8192*512 (key-row buckets of at most 512 rows)");
+            return fail(KMIP_ERR_UNSUPPORTED, "the bucketed variant needs N*H <= 8192*512 (key-row buckets of at most 512 rows)");
         e = kmip::launch_bwd_bucket(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
                                     dV, workspace, stream);
-    } else if (v == 3) {
+    } else if (v == KMIP_BWD_SEGMENTED) {
         e = kmip::launch_bwd_csr(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
                                  dV, workspace, stream);
     } else {

@@ -74,12 +74,12 @@ def test_workspace_size(lib):
     # (reference directions in bf16, labels, histogram + seed slots, permutation)
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 1) == 0
     agg = 2 * 256 * 32 * 2 + 4096 + 2 * 2 * 256 * 4 + 8192
-    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 2) == agg
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, _lib.BWD_KEY_AGGREGATED) == agg
     # the segmented reduction: pair coefficients (2 f32), the key-sorted pair
     # records (16 B), per-key counts and the scan's block sums, each 256-byte
     # aligned
     csr = 32000 * 8 + 32000 * 16 + 8192 + 256
-    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 3) == csr
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, _lib.BWD_SEGMENTED) == csr
     # the bucketed reduction: the bucket-sorted records (12 B: packed
     # key-row offset and query row, then the coefficients),
     # three arrays over the 2000 / (4096 / 32) = 16 key-row buckets (+1:
@@ -88,16 +88,16 @@ def test_workspace_size(lib):
     # ... and the records in super-bucket order between the two placement
     # passes (16 B), with three arrays of 65 super-bucket entries
     bucket = 32000 * 12 + 3 * 256 + 256 + 2 * 2000 * 32 * 2 + 32000 * 16 + 3 * 512
-    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 4) == bucket
+    assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, _lib.BWD_BUCKETED) == bucket
     # the library picks the bucketed reduction where it fits
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == bucket
     # buckets widen up to 512 key rows: N*H = 4M still fits 8192 buckets;
     # beyond that the variant is unsupported (size 0) and the library picks
     # the full key sort
-    assert lib.kmip_bwd_workspace_size(1_000_000, 4, 16, 16, 4) > 0
-    assert lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, 4) == 0
+    assert lib.kmip_bwd_workspace_size(1_000_000, 4, 16, 16, _lib.BWD_BUCKETED) > 0
+    assert lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, _lib.BWD_BUCKETED) == 0
     assert (lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, 0)
-            == lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, 3) > 0)
+            == lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, _lib.BWD_SEGMENTED) > 0)
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 5) == 0
 
 
@@ -141,9 +141,9 @@ def test_bwd_rejects(lib):
     f = ctypes.c_float
     args = [FAKE] * 6 + [64, 1, 16, 4, f(1.0), FAKE, FAKE, FAKE]
     assert lib.kmip_bwd(*args, 7, None, 0, None) == 2            # unknown variant
-    assert lib.kmip_bwd(*args, 3, None, 0, None) == 3            # segmented needs workspace
-    assert lib.kmip_bwd(*args, 2, None, 0, None) == 3            # aggregated needs workspace
-    assert lib.kmip_bwd(*args, 4, None, 0, None) == 3            # bucketed needs workspace
+    assert lib.kmip_bwd(*args, _lib.BWD_SEGMENTED, None, 0, None) == 3        # needs workspace
+    assert lib.kmip_bwd(*args, _lib.BWD_KEY_AGGREGATED, None, 0, None) == 3   # needs workspace
+    assert lib.kmip_bwd(*args, _lib.BWD_BUCKETED, None, 0, None) == 3         # needs workspace
     assert lib.kmip_bwd(*args, 0, FAKE, 16, None) == 3           # workspace too small
     bad = list(args)
     bad[3] = None                                                 # dOut
@@ -159,3 +159,39 @@ def test_fwd_validates_before_launch(lib):
                         FAKE, 1 << 20, None) == 1
     assert lib.kmip_fwd(FAKE, FAKE, FAKE, None, 1, 64, 1, 16, 4, f(-1.0), FAKE, FAKE, FAKE,
                         FAKE, 1 << 20, None) == 1
+
+
+def _prototypes():
+    """{function name: [parameter names]} of every prototype in include/kmip.h."""
+    with open(os.path.join(ROOT, "include", "kmip.h")) as f:
+        text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+    protos = {}
+    for m in re.finditer(r"\b(kmip_[a-z_]+)\s*\(([^)]*)\)\s*;", text):
+        params = [p.strip() for p in m.group(2).split(",") if p.strip() and p.strip() != "void"]
+        protos[m.group(1)] = [re.findall(r"[A-Za-z_][A-Za-z_0-9]*", p)[-1] for p in params]
+    return protos
+
+
+def test_bwd_signature_as_documented():
+    # kmip_bwd takes (inputs, saved tensors, sizes, scale, outputs, variant,
+    # workspace, stream); the forward's graph_offsets and out are not
+    # parameters (the header states why).
+    assert _prototypes()["kmip_bwd"] == [
+        "Q", "K", "V", "dOut", "topk_idx", "lse", "N", "H", "d", "k", "scale", "dQ", "dK", "dV",
+        "variant", "workspace", "workspace_bytes", "stream"]
+
+
+def test_bwd_variant_codes_as_documented():
+    with open(os.path.join(ROOT, "include", "kmip.h")) as f:
+        text = f.read()
+    codes = dict((n, int(v)) for n, v in re.findall(r"\b(KMIP_BWD_[A-Z_]+)\s*=\s*(\d+)", text))
+    assert codes == {"KMIP_BWD_AUTO": 0, "KMIP_BWD_ATOMIC": 1, "KMIP_BWD_SEGMENTED": 2,
+                     "KMIP_BWD_BUCKETED": 3, "KMIP_BWD_KEY_AGGREGATED": 4}
+    assert (_lib.BWD_AUTO, _lib.BWD_ATOMIC, _lib.BWD_SEGMENTED, _lib.BWD_BUCKETED,
+            _lib.BWD_KEY_AGGREGATED) == (0, 1, 2, 3, 4)
+
+
+def test_binding_argument_counts_match_header(lib):
+    for name, params in _prototypes().items():
+        argtypes = getattr(lib, name).argtypes
+        assert argtypes is not None and len(argtypes) == len(params), name

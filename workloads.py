@@ -5,10 +5,10 @@ none of the attention arithmetic: both the CPU oracle and the GPU path take
 the arrays it returns, so that the two sides see bit-identical inputs.
 
 The paper's efficiency study samples Q, K and V from a standard normal
-distribution (Appendix I.2, "Objective 1: Computational efficiency"); its
+distribution (Appendix H.2, "Objective 1: Computational efficiency"); its
 real workloads are superpixel graphs (LRGB), city road networks with Fourier
-position encodings (Appendix I.3) and point clouds with xyz inputs
-(Appendix I.4).  None of those datasets is available here, so each
+position encodings (Appendix H.4, City-Networks) and point clouds with xyz
+inputs (Appendix H.5, point cloud datasets).  None of those datasets is available here, so each
 configuration below is a synthetic stand-in with the same shapes and value
 structure:
 
