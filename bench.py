@@ -8,11 +8,15 @@ region starts.
 
 Prints ONE JSON line on stdout.  Extra detail goes to stderr.
   value        whole-job node-queries per second (N / step time; every head)
-  roofline     the score+select kernel against the bf16 MFMA peak, from HIP
+  roofline     the score+select kernel against the bf16 MFMA peak: the MFMA
+               work it executes (counted by rocprofv3 on the same sources,
+               profiles/select_counters.json) over its duration, from HIP
                events the library records around that kernel's launch on
-               the stream it runs on; the work counted is every (query,
-               key) pair of each graph (a dense scan), of which the kernel
-               executes the fraction its bounds cannot rule out
+               the stream it runs on; the kernel skips the key blocks its
+               bounds rule out, so this is less than a dense scan of every
+               (query, key) pair, whose rate over the same time is reported
+               separately as the effective rate; `limiter` gives the busy
+               fractions of the MFMA and VALU units from the same counters
   cpu_baseline the float64 CPU oracle on a bounded sample of the same
                workload (not an optimisation target)
 """
@@ -54,17 +58,29 @@ def parse():
     return p.parse_args()
 
 
-def measured_counters():
-    """Counter figures of the score+select kernel from profiles/select_counters.json
-    (HBM bytes per launch, MFMA instructions per launch), or None when there
-    are none or the select sources changed since they were taken."""
+def measured_counters(config):
+    """Counter figures of the score+select kernel on workload `config` from
+    profiles/select_counters.json (HBM bytes, MFMA instructions, busy
+    fractions per launch), or None when there are none or the select
+    sources changed since they were taken."""
     path = os.path.join(ROOT, "profiles", "select_counters.json")
     if not os.path.exists(path):
         return None
     import rocprof_summary
     with open(path) as f:
-        rec = json.load(f)
-    return rec if rec.get("sources_sha256") == rocprof_summary.sources_hash() else None
+        rec = json.load(f).get(f"c{config}")
+    return rec if rec and rec.get("sources_sha256") == rocprof_summary.sources_hash() else None
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(w, sample):
@@ -94,6 +110,8 @@ def cpu_baseline(w, sample):
     per_query = w.H * t_fwd / m + t_bwd / w.N
     return {
         "value": 1.0 / per_query, "unit": "queries/s", "cores": oracle.threads(), "kind": "oracle",
+        "cpu_model": cpu_model(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS", "unset"),
+        "host_cpus": os.cpu_count(),
         "sample": (f"full-sort top-k + aggregate on {m} seeded query-heads of the same workload "
                    f"({t_fwd:.2f} s), backward on all {w.N * w.H} query-heads ({t_bwd:.2f} s); "
                    f"per node-query cost = H*fwd/query-head + bwd/node"),
@@ -188,9 +206,10 @@ def main():
     flops = 2.0 * H * pairs * d
     tflops = flops / (sel_ms * 1e-3) / 1e12
     # MFMA work the kernel actually executed (32x32x16 bf16 MFMAs counted by
-    # rocprofv3 on the same sources), when a counter run is on record
-    counters = measured_counters() if args.config == 4 and args.n is None else None
+    # rocprofv3 on the same sources and workload), when a counter run is on record
+    counters = measured_counters(args.config) if args.n is None and args.seed == 0 else None
     executed = counters["mfma_flop_per_launch"] if counters else None
+    exec_tflops = None if executed is None else executed / (sel_ms * 1e-3) / 1e12
     topk_ms = sum(t_topk) / len(t_topk)
     att_ms = sum(t_att) / len(t_att)
     bwd_ms = sum(t_bwd) / len(t_bwd) if backward else 0.0
@@ -246,16 +265,32 @@ def main():
         },
         "peak_mem_bytes": peak_mem,
         "roofline": {
-            "bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": tflops / PEAK_BF16_TFLOPS,
+            "bound": "mfma", "achieved": exec_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": None if exec_tflops is None else exec_tflops / PEAK_BF16_TFLOPS,
             "traffic": counters["bytes_per_launch"] if counters else None,
             "kernel": ("select_kernel (score+select) alone, between events recorded around its "
                        "launch; the kmip_topk call also runs the query-grouping, key-tree and "
                        "key-tiling pre-passes (kernel_ms.topk)"),
-            "algorithmic": (f"2*H*sum(n_g^2)*d = {flops:.4g} FLOP per launch: every (query, key) "
-                            "pair of each graph, the work of a dense scan"),
+            "work": ("MFMA FLOP the kernel executes per launch (SQ_INSTS_MFMA x 32768, rocprofv3 "
+                     "on the same sources and workload; null if none is on record): the scan of "
+                     "the key blocks its bounds do not rule out, plus the bound and seed tiles"),
             "executed_mfma_flop": executed,
-            "executed_frac": None if executed is None else executed / flops,
+            "limiter": None if counters is None else {
+                "mfma_busy_frac": counters["mfma_busy_frac"],
+                "valu_issue_frac": counters["valu_issue_frac"],
+                "bound_by": ("valu" if counters["valu_issue_frac"] > counters["mfma_busy_frac"]
+                             else "mfma"),
+                "note": ("busy fractions from the same counter runs: MFMA busy cycles over 1024 "
+                         "SIMDs, VALU instructions over one issue per CU per cycle"),
+            },
+            "effective": {
+                "tflops": tflops, "pct_bf16_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
+                "flop": flops,
+                "what": (f"2*H*sum(n_g^2)*d = {flops:.4g} FLOP, every (query, key) pair of each "
+                         "graph (a dense scan), over the select kernel's time; above the peak when "
+                         "the bounds skip more than the kernel's shortfall from it"),
+            },
+            "executed_frac_of_dense": None if executed is None else executed / flops,
         },
         "cpu_baseline": cpu,
     }

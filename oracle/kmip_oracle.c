@@ -341,12 +341,15 @@ int oracle_check_set(const double* Q, const double* K, const int32_t* offsets, i
             }
             int64_t want = n < k ? n : k;
             if (distinct != want) f |= 4;
+            /* largest score of a graph key outside the set; membership is
+               looked up only for a score that would raise the maximum */
             double mx = -INFINITY;
             for (int64_t j = lo; j < hi; ++j) {
+                double s = oracle_score(Q, K, H, d, i, j, h);
+                if (!(s > mx)) continue;
                 int32_t jj = (int32_t)j;
                 if (bsearch(&jj, set, (size_t)m, sizeof(int32_t), oracle_int_order)) continue;
-                double s = oracle_score(Q, K, H, d, i, j, h);
-                if (s > mx) mx = s;
+                mx = s;
             }
             min_in[r] = mn;
             max_out[r] = mx;
