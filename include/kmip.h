@@ -36,7 +36,9 @@
  *    asynchronous on `stream`; the caller synchronises.
  *  - Ownership: the caller allocates every buffer (inputs, outputs and the
  *    workspace); the library allocates no device memory and keeps no state
- *    between calls.  Outputs are overwritten, never accumulated.
+ *    between calls (apart from kmip_fwd_noalloc's fixed per-device array,
+ *    which holds no state from one call to the next).  Outputs are
+ *    overwritten, never accumulated.
  *  - Errors: arguments are validated on the host before any launch; on
  *    error nothing is launched and outputs are untouched.  Index entries
  *    read by kmip_attend / kmip_bwd that fall outside [0, N) are treated as
@@ -177,6 +179,34 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
                        const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
                        int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
                        int32_t variant, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Forward (kmip_fwd) of one graph without a caller workspace and without
+ * allocating anything, for callers that cannot allocate device or pinned
+ * memory during the call: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation.
+ *   The score + select pass keeps its working data (tiled keys, query
+ *   grouping, key order, work counters) in a fixed device array of
+ *   KMIP_NOALLOC_SCRATCH_BYTES bytes inside this library, one per GPU the
+ *   library runs on, held until the process ends.  Its device address is
+ *   looked up on the first call on each device.
+ *   Arguments, layouts and results are kmip_fwd's for graph_offsets = NULL:
+ *   Q, K, V bf16 [N, H, d]; out float32 [N, H, d], topk_idx int32 [N, H, k],
+ *   lse float32 [N, H], all caller-owned device memory.  Block-diagonal
+ *   batches are not taken (their work list is uploaded through pinned host
+ *   memory that kmip_fwd allocates): use kmip_fwd for them.
+ *   Sizes whose kmip_fwd_workspace_size(N, H, d, k, 1) exceeds
+ *   KMIP_NOALLOC_SCRATCH_BYTES return KMIP_ERR_UNSUPPORTED (N = 500,000,
+ *   H = 4, d = 16, k = 32 needs 223 MiB) before anything is launched.
+ *   Every call on one GPU shares that GPU's array: calls that overlap on
+ *   one GPU (on different streams, or from different host threads without
+ *   ordering) race and give undefined results.  Calls ordered on one
+ *   stream are safe; each call clears the counters it reads.
+ */
+#define KMIP_NOALLOC_SCRATCH_BYTES (256u * 1024u * 1024u)
+kmip_status_t kmip_fwd_noalloc(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
+                               int32_t d, int32_t k, float scale, float* out, int32_t* topk_idx,
+                               float* lse, void* stream);
 
 /* Static description of a status code. */
 const char* kmip_status_string(kmip_status_t status);

@@ -13,11 +13,11 @@ from typing import Optional, Sequence
 
 import numpy as np
 
-from ._lib import KmipError, MAX_K, check, load
+from ._lib import KmipError, MAX_K, NOALLOC_SCRATCH_BYTES, check, load
 
 __all__ = [
-    "KmipError", "MAX_K", "topk", "attend", "fwd", "bwd", "attention", "topk_workspace_size",
-    "bwd_workspace_size", "Workspace", "load",
+    "KmipError", "MAX_K", "NOALLOC_SCRATCH_BYTES", "topk", "attend", "fwd", "fwd_noalloc", "bwd",
+    "attention", "topk_workspace_size", "bwd_workspace_size", "Workspace", "load",
 ]
 
 
@@ -187,6 +187,22 @@ def fwd(q, k_, v, kk: int, scale: float, graph_offsets=None, workspace=None):
     check(load().kmip_fwd(_ptr(q), _ptr(k_), _ptr(v), optr, G, N, H, d, kk, float(scale), _ptr(out),
                           _ptr(idx), _ptr(lse), _ptr(buf), 0 if buf is None else buf.numel(),
                           _stream_ptr()))
+    return out, idx, lse
+
+
+def fwd_noalloc(q, k_, v, kk: int, scale: float, out, idx, lse):
+    """Forward of one graph into caller-allocated out [N, H, d] float32,
+    idx [N, H, kk] int32 and lse [N, H] float32, through kmip_fwd_noalloc:
+    the library allocates nothing (its working data lives in a fixed
+    per-device array).  Calls that overlap on one GPU race."""
+    torch = _torch()
+    N, H, d = _nhd(q)
+    kk = int(kk)
+    _validate((q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d)),
+              (v, "V", torch.bfloat16, (N, H, d)), (out, "out", torch.float32, (N, H, d)),
+              (idx, "topk_idx", torch.int32, (N, H, kk)), (lse, "lse", torch.float32, (N, H)))
+    check(load().kmip_fwd_noalloc(_ptr(q), _ptr(k_), _ptr(v), N, H, d, kk, float(scale), _ptr(out),
+                                  _ptr(idx), _ptr(lse), _stream_ptr()))
     return out, idx, lse
 
 

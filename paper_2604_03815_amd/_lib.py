@@ -24,9 +24,12 @@ BWD_KEY_AGGREGATED = 4
 # Every symbol declared in include/kmip.h.
 EXPORTS = (
     "kmip_topk_workspace_size", "kmip_topk", "kmip_topk_with_events", "kmip_attend", "kmip_fwd_workspace_size",
-    "kmip_fwd", "kmip_bwd_workspace_size", "kmip_bwd", "kmip_status_string",
+    "kmip_fwd", "kmip_bwd_workspace_size", "kmip_bwd", "kmip_fwd_noalloc", "kmip_status_string",
     "kmip_last_error",
 )
+
+# bytes of the fixed per-device array kmip_fwd_noalloc works in
+NOALLOC_SCRATCH_BYTES = 256 * 1024 * 1024
 
 _lib = None
 
@@ -60,7 +63,9 @@ def load(path: str = LIB_PATH):
     lib.kmip_attend.argtypes = [P, P, P, i64, i32, i32, i32, f32, P, P, P, P]
     lib.kmip_fwd.argtypes = [P, P, P, P, i32, i64, i32, i32, i32, f32, P, P, P, P, sz, P]
     lib.kmip_bwd.argtypes = [P, P, P, P, P, P, i64, i32, i32, i32, f32, P, P, P, i32, P, sz, P]
-    for f in ("kmip_topk", "kmip_topk_with_events", "kmip_attend", "kmip_fwd", "kmip_bwd"):
+    lib.kmip_fwd_noalloc.argtypes = [P, P, P, i64, i32, i32, i32, f32, P, P, P, P]
+    for f in ("kmip_topk", "kmip_topk_with_events", "kmip_attend", "kmip_fwd", "kmip_bwd",
+              "kmip_fwd_noalloc"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kmip_status_string.argtypes = [ctypes.c_int]
     lib.kmip_status_string.restype = ctypes.c_char_p

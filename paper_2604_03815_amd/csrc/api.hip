@@ -13,10 +13,12 @@
 #include "kmip_internal.h"
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
 
-kmip_status_t fail(kmip_status_t s, const char* fmt, ...) {
+namespace kmip {
+
+kmip_status_t record_error(kmip_status_t s, const char* fmt, ...) {
     char buf[512];
     va_list ap;
     va_start(ap, fmt);
@@ -26,13 +28,19 @@ kmip_status_t fail(kmip_status_t s, const char* fmt, ...) {
     return s;
 }
 
+}  // namespace kmip
+
+namespace {
+
+using kmip::record_error;
+
 kmip_status_t ok() {
     g_last_error.clear();
     return KMIP_OK;
 }
 
 kmip_status_t hip_fail(hipError_t e, const char* what) {
-    return fail(KMIP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return record_error(KMIP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
 constexpr size_t kAlign = 256;
@@ -87,28 +95,28 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 // Sizes shared by all entry points.
 kmip_status_t check_sizes(int64_t N, int32_t H, int32_t d, int32_t k) {
-    if (N < 0 || N >= (int64_t(1) << 31)) return fail(KMIP_ERR_INVALID_ARG, "N=%lld out of range", (long long)N);
-    if (H < 1) return fail(KMIP_ERR_INVALID_ARG, "H=%d must be >= 1", H);
-    if (k < 1) return fail(KMIP_ERR_INVALID_ARG, "k=%d must be >= 1", k);
-    if (d != 16 && d != 32 && d != 64) return fail(KMIP_ERR_UNSUPPORTED, "d=%d not in {16, 32, 64}", d);
-    if (k > KMIP_MAX_K) return fail(KMIP_ERR_UNSUPPORTED, "k=%d exceeds %d", k, KMIP_MAX_K);
+    if (N < 0 || N >= (int64_t(1) << 31)) return record_error(KMIP_ERR_INVALID_ARG, "N=%lld out of range", (long long)N);
+    if (H < 1) return record_error(KMIP_ERR_INVALID_ARG, "H=%d must be >= 1", H);
+    if (k < 1) return record_error(KMIP_ERR_INVALID_ARG, "k=%d must be >= 1", k);
+    if (d != 16 && d != 32 && d != 64) return record_error(KMIP_ERR_UNSUPPORTED, "d=%d not in {16, 32, 64}", d);
+    if (k > KMIP_MAX_K) return record_error(KMIP_ERR_UNSUPPORTED, "k=%d exceeds %d", k, KMIP_MAX_K);
     const int64_t wide = N * (int64_t)H * std::max<int64_t>(d, k);
-    if (wide >= (int64_t(1) << 31)) return fail(KMIP_ERR_INVALID_ARG, "N*H*max(d,k) >= 2^31");
+    if (wide >= (int64_t(1) << 31)) return record_error(KMIP_ERR_INVALID_ARG, "N*H*max(d,k) >= 2^31");
     return KMIP_OK;
 }
 
 kmip_status_t check_scale(float scale) {
-    if (!std::isfinite(scale) || !(scale > 0.0f)) return fail(KMIP_ERR_INVALID_ARG, "scale must be finite and > 0");
+    if (!std::isfinite(scale) || !(scale > 0.0f)) return record_error(KMIP_ERR_INVALID_ARG, "scale must be finite and > 0");
     return KMIP_OK;
 }
 
 kmip_status_t check_offsets(const int32_t* off, int32_t G, int64_t N) {
     if (off == nullptr) return KMIP_OK;
-    if (G < 1) return fail(KMIP_ERR_INVALID_ARG, "num_graphs=%d must be >= 1 with offsets", G);
-    if (off[0] != 0) return fail(KMIP_ERR_INVALID_ARG, "graph_offsets[0]=%d must be 0", off[0]);
+    if (G < 1) return record_error(KMIP_ERR_INVALID_ARG, "num_graphs=%d must be >= 1 with offsets", G);
+    if (off[0] != 0) return record_error(KMIP_ERR_INVALID_ARG, "graph_offsets[0]=%d must be 0", off[0]);
     for (int32_t g = 0; g < G; ++g)
-        if (off[g + 1] < off[g]) return fail(KMIP_ERR_INVALID_ARG, "graph_offsets decrease at %d", g);
-    if (off[G] != N) return fail(KMIP_ERR_INVALID_ARG, "graph_offsets[G]=%d != N=%lld", off[G], (long long)N);
+        if (off[g + 1] < off[g]) return record_error(KMIP_ERR_INVALID_ARG, "graph_offsets decrease at %d", g);
+    if (off[G] != N) return record_error(KMIP_ERR_INVALID_ARG, "graph_offsets[G]=%d != N=%lld", off[G], (long long)N);
     return KMIP_OK;
 }
 
@@ -190,14 +198,14 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
     if (s != KMIP_OK) return s;
     if ((s = check_offsets(graph_offsets, num_graphs, N)) != KMIP_OK) return s;
     if (N == 0) return ok();
-    if (!Q || !K || !topk_idx) return fail(KMIP_ERR_INVALID_ARG, "null Q, K or topk_idx");
-    if (!aligned16(Q) || !aligned16(K)) return fail(KMIP_ERR_INVALID_ARG, "Q and K must be 16-byte aligned");
+    if (!Q || !K || !topk_idx) return record_error(KMIP_ERR_INVALID_ARG, "null Q, K or topk_idx");
+    if (!aligned16(Q) || !aligned16(K)) return record_error(KMIP_ERR_INVALID_ARG, "Q and K must be 16-byte aligned");
     const int32_t G = graph_offsets ? num_graphs : 1;
     const size_t need = kmip_topk_workspace_size(N, H, d, k, G);
     if (workspace == nullptr || workspace_bytes < need)
-        return fail(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
+        return record_error(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
     if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0)
-        return fail(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+        return record_error(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
 
     const int32_t n32 = (int32_t)N;
@@ -265,9 +273,9 @@ kmip_status_t kmip_attend(const void* Q, const void* K, const void* V, int64_t N
     if ((s = check_scale(scale)) != KMIP_OK) return s;
     if (N == 0) return ok();
     if (!Q || !K || !V || !topk_idx || !out || !lse)
-        return fail(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_attend");
+        return record_error(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_attend");
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V))
-        return fail(KMIP_ERR_INVALID_ARG, "Q, K and V must be 16-byte aligned");
+        return record_error(KMIP_ERR_INVALID_ARG, "Q, K and V must be 16-byte aligned");
     hipError_t e = kmip::launch_attend(Q, K, V, topk_idx, (int32_t)N, H, d, k, scale, out, lse,
                                        reinterpret_cast<hipStream_t>(stream_));
     if (e != hipSuccess) return hip_fail(e, "attend launch");
@@ -281,8 +289,8 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
-    if (N > 0 && (!V || !out || !lse)) return fail(KMIP_ERR_INVALID_ARG, "null V, out or lse");
-    if (N > 0 && !aligned16(V)) return fail(KMIP_ERR_INVALID_ARG, "V must be 16-byte aligned");
+    if (N > 0 && (!V || !out || !lse)) return record_error(KMIP_ERR_INVALID_ARG, "null V, out or lse");
+    if (N > 0 && !aligned16(V)) return record_error(KMIP_ERR_INVALID_ARG, "V must be 16-byte aligned");
     s = kmip_topk(Q, K, graph_offsets, num_graphs, N, H, d, k, topk_idx, workspace,
                   workspace_bytes, stream);
     if (s != KMIP_OK) return s;
@@ -314,29 +322,29 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
     if (s != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
     if (variant < KMIP_BWD_AUTO || variant > KMIP_BWD_KEY_AGGREGATED)
-        return fail(KMIP_ERR_UNSUPPORTED, "backward variant %d", variant);
+        return record_error(KMIP_ERR_UNSUPPORTED, "backward variant %d", variant);
     if (N == 0) return ok();
     if (!Q || !K || !V || !dOut || !topk_idx || !lse || !dQ || !dK || !dV)
-        return fail(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_bwd");
+        return record_error(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_bwd");
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(dOut))
-        return fail(KMIP_ERR_INVALID_ARG, "Q, K, V and dOut must be 16-byte aligned");
-    if (!aligned16(dK) || !aligned16(dV)) return fail(KMIP_ERR_INVALID_ARG, "dK and dV must be 16-byte aligned");
+        return record_error(KMIP_ERR_INVALID_ARG, "Q, K, V and dOut must be 16-byte aligned");
+    if (!aligned16(dK) || !aligned16(dV)) return record_error(KMIP_ERR_INVALID_ARG, "dK and dV must be 16-byte aligned");
     const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d) : variant;
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
     hipError_t e;
     if (v != KMIP_BWD_ATOMIC) {
         const size_t need = kmip_bwd_workspace_size(N, H, d, k, v);
         if (workspace == nullptr || workspace_bytes < need)
-            return fail(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
+            return record_error(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
         if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0)
-            return fail(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+            return record_error(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
     }
     if (v == KMIP_BWD_KEY_AGGREGATED) {
         e = kmip::launch_bwd_agg(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
                                  dV, workspace, stream);
     } else if (v == KMIP_BWD_BUCKETED) {
         if (!kmip::bwd_bucket_supported((int32_t)N, H, d))
-            return fail(KMIP_ERR_UNSUPPORTED, "the bucketed variant needs N*H <= 8192*512 (key-row buckets of at most 512 rows)");
+            return record_error(KMIP_ERR_UNSUPPORTED, "the bucketed variant needs N*H <= 8192*512 (key-row buckets of at most 512 rows)");
         e = kmip::launch_bwd_bucket(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
                                     dV, workspace, stream);
     } else if (v == KMIP_BWD_SEGMENTED) {

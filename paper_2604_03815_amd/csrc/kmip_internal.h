@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kmip.h"
+
 namespace kmip {
 
 // Zero tiles appended to each head of the tiled key buffer, so that key
@@ -146,5 +148,9 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
                              hipStream_t stream);
 
 hipError_t launch_fill_zero(float* p, size_t n, hipStream_t stream);
+
+// Sets the calling thread's kmip_last_error() text (printf-style) and
+// returns s.
+kmip_status_t record_error(kmip_status_t s, const char* fmt, ...);
 
 }  // namespace kmip

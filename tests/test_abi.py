@@ -195,3 +195,27 @@ def test_binding_argument_counts_match_header(lib):
     for name, params in _prototypes().items():
         argtypes = getattr(lib, name).argtypes
         assert argtypes is not None and len(argtypes) == len(params), name
+
+
+def test_noalloc_scratch_size_matches_header():
+    with open(os.path.join(ROOT, "include", "kmip.h")) as f:
+        m = re.search(r"#define KMIP_NOALLOC_SCRATCH_BYTES \((\d+)u \* (\d+)u \* (\d+)u\)", f.read())
+    assert m and int(m.group(1)) * int(m.group(2)) * int(m.group(3)) == _lib.NOALLOC_SCRATCH_BYTES
+
+
+def test_noalloc_validates_before_launch(lib):
+    f = ctypes.c_float
+    # sizes whose working data exceed the fixed array: rejected with a clear
+    # error before any HIP call (this host has no GPU)
+    assert lib.kmip_fwd_noalloc(FAKE, FAKE, FAKE, 1_000_000, 4, 16, 32, f(0.25), FAKE, FAKE, FAKE, None) == 2
+    assert b"scratch" in lib.kmip_last_error()
+    assert lib.kmip_fwd_workspace_size(1_000_000, 4, 16, 32, 1) > _lib.NOALLOC_SCRATCH_BYTES
+    # the benchmark's workload fits
+    assert 0 < lib.kmip_fwd_workspace_size(500_000, 4, 16, 32, 1) <= _lib.NOALLOC_SCRATCH_BYTES
+    # argument errors come first
+    assert lib.kmip_fwd_noalloc(FAKE, FAKE, None, 64, 1, 16, 4, f(1.0), FAKE, FAKE, FAKE, None) == 1
+    assert lib.kmip_fwd_noalloc(FAKE, FAKE, FAKE, 64, 1, 16, 4, f(-1.0), FAKE, FAKE, FAKE, None) == 1
+    assert lib.kmip_fwd_noalloc(FAKE, FAKE, FAKE, 64, 1, 24, 4, f(1.0), FAKE, FAKE, FAKE, None) == 2
+    assert lib.kmip_fwd_noalloc(P(258), FAKE, FAKE, 64, 1, 16, 4, f(1.0), FAKE, FAKE, FAKE, None) == 1
+    # nothing to do
+    assert lib.kmip_fwd_noalloc(None, None, None, 0, 1, 16, 4, f(1.0), None, None, None, None) == 0
