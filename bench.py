@@ -8,15 +8,16 @@ region starts.
 
 Prints ONE JSON line on stdout.  Extra detail goes to stderr.
   value        whole-job node-queries per second (N / step time; every head)
-  roofline     the score+select kernel against the bf16 MFMA peak: the MFMA
-               work it executes (counted by rocprofv3 on the same sources,
-               profiles/select_counters.json) over its duration, from HIP
-               events the library records around that kernel's launch on
-               the stream it runs on; the kernel skips the key blocks its
-               bounds rule out, so this is less than a dense scan of every
-               (query, key) pair, whose rate over the same time is reported
-               separately as the effective rate; `limiter` gives the busy
-               fractions of the MFMA and VALU units from the same counters
+  roofline     the score+select kernel against the unit that binds it: the
+               work it executes (VALU instructions and MFMA FLOP counted by
+               rocprofv3 on the same sources, profiles/select_counters.json)
+               over its duration, from HIP events the library records
+               around that kernel's launch on the stream it runs on; bound
+               is "alu" when the VALU issue rate is the larger fraction of
+               its peak, else "mfma"; the kernel skips the key blocks its
+               bounds rule out, so its MFMA work is less than a dense scan
+               of every (query, key) pair, whose rate over the same time is
+               reported separately as the effective rate
   cpu_baseline the float64 CPU oracle on a bounded sample of the same
                workload (not an optimisation target)
 """
@@ -35,6 +36,7 @@ if ROOT not in sys.path:
 METRIC = "k-MIP attn fwd+bwd queries/s and score TFLOP/s (% bf16 MFMA peak) at N=500k"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+PEAK_VALU_TOPS = 256 * 64 * 2.4e9 / 1e12   # wave64 VALU lane-instructions, 39.3 T/s
 
 
 def log(*a):
@@ -231,6 +233,50 @@ def main():
         log(f"[bench] cpu oracle baseline: {cpu['value']:.1f} queries/s on {cpu['cores']} threads "
             f"({time.perf_counter() - t0:.1f} s)")
 
+    # Roofline of the score+select kernel from the work it executes (counted
+    # by rocprofv3 on the same sources and workload), against the unit the
+    # counters show binding: the VALU when its issue rate exceeds the MFMA
+    # busy fraction, else the MFMA.  Without a counter record on file the
+    # kernel's executed work is unknown and achieved/frac are null.
+    valu = counters.get("valu_instructions_per_launch") if counters else None
+    valu_rate = None if valu is None else valu * 64 / (sel_ms * 1e-3) / 1e12     # T lane-instr/s
+    valu_frac = None if valu_rate is None else valu_rate / PEAK_VALU_TOPS
+    mfma_frac = None if exec_tflops is None else exec_tflops / PEAK_BF16_TFLOPS
+    bound = "mfma"
+    if valu_frac is not None and mfma_frac is not None and valu_frac > mfma_frac:
+        bound = "alu"
+    roofline = {
+        "bound": bound,
+        "achieved": valu_rate if bound == "alu" else exec_tflops,
+        "peak": PEAK_VALU_TOPS if bound == "alu" else PEAK_BF16_TFLOPS,
+        "unit": "T VALU lane-instr/s" if bound == "alu" else "TFLOP/s",
+        "frac": valu_frac if bound == "alu" else mfma_frac,
+        "traffic": counters["bytes_per_launch"] if counters else None,
+        "kernel": ("select_kernel (score+select) alone, between events recorded around its "
+                   "launch; the kmip_topk call also runs the query-grouping, key-tree and "
+                   "key-tiling pre-passes (kernel_ms.topk)"),
+        "work": ("per launch, from rocprofv3 counters on the same sources and workload "
+                 "(null if none is on record): SQ_INSTS_VALU x 64 lanes for the VALU, "
+                 "SQ_INSTS_MFMA x 32768 FLOP for the MFMA (the scan of the key blocks the "
+                 "bounds do not rule out, plus the bound and seed tiles)"),
+        "alu": None if valu is None else {
+            "valu_instructions": valu, "achieved": valu_rate, "peak": PEAK_VALU_TOPS,
+            "unit": "T VALU lane-instr/s", "frac": valu_frac,
+            "peak_is": "256 CUs x 64 lanes x 2.4 GHz (one wave64 VALU instruction per CU per cycle)"},
+        "mfma": None if executed is None else {
+            "executed_flop": executed, "achieved": exec_tflops, "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": mfma_frac,
+            "busy_frac_profiled": counters["mfma_busy_frac"]},
+        "effective": {
+            "tflops": tflops, "pct_bf16_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
+            "flop": flops,
+            "what": (f"2*H*sum(n_g^2)*d = {flops:.4g} FLOP, every (query, key) pair of each "
+                     "graph (a dense scan), over the select kernel's time; above the peak when "
+                     "the bounds skip more than the kernel's shortfall from it"),
+        },
+        "executed_frac_of_dense": None if executed is None else executed / flops,
+    }
+
     result = {
         "metric": METRIC,
         "value": N / (ms_step * 1e-3),
@@ -264,34 +310,7 @@ def main():
                           "+ 3*4d dQ, dK, dV)")},
         },
         "peak_mem_bytes": peak_mem,
-        "roofline": {
-            "bound": "mfma", "achieved": exec_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": None if exec_tflops is None else exec_tflops / PEAK_BF16_TFLOPS,
-            "traffic": counters["bytes_per_launch"] if counters else None,
-            "kernel": ("select_kernel (score+select) alone, between events recorded around its "
-                       "launch; the kmip_topk call also runs the query-grouping, key-tree and "
-                       "key-tiling pre-passes (kernel_ms.topk)"),
-            "work": ("MFMA FLOP the kernel executes per launch (SQ_INSTS_MFMA x 32768, rocprofv3 "
-                     "on the same sources and workload; null if none is on record): the scan of "
-                     "the key blocks its bounds do not rule out, plus the bound and seed tiles"),
-            "executed_mfma_flop": executed,
-            "limiter": None if counters is None else {
-                "mfma_busy_frac": counters["mfma_busy_frac"],
-                "valu_issue_frac": counters["valu_issue_frac"],
-                "bound_by": ("valu" if counters["valu_issue_frac"] > counters["mfma_busy_frac"]
-                             else "mfma"),
-                "note": ("busy fractions from the same counter runs: MFMA busy cycles over 1024 "
-                         "SIMDs, VALU instructions over one issue per CU per cycle"),
-            },
-            "effective": {
-                "tflops": tflops, "pct_bf16_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
-                "flop": flops,
-                "what": (f"2*H*sum(n_g^2)*d = {flops:.4g} FLOP, every (query, key) pair of each "
-                         "graph (a dense scan), over the select kernel's time; above the peak when "
-                         "the bounds skip more than the kernel's shortfall from it"),
-            },
-            "executed_frac_of_dense": None if executed is None else executed / flops,
-        },
+        "roofline": roofline,
         "cpu_baseline": cpu,
     }
     print(json.dumps(result), flush=True)
