@@ -54,6 +54,13 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-sample", type=int, default=2048, help="query-heads in the oracle sample")
     p.add_argument("--bwd-variant", type=int, default=0, help="backward: 0 library choice, 1 per-pair atomics, 2 key-sorted segmented, 3 bucketed, 4 key-aggregated")
+    p.add_argument("--compare-dense", action="store_true",
+                   help="instead of the step benchmark: k-MIP (k=10, d=16, H=1) against dense "
+                        "softmax attention (torch SDPA, flash or memory-efficient kernels) over the "
+                        "efficiency study's grid of N; prints one JSON line with the table")
+    p.add_argument("--dense-exps", type=str, default="2,3,4,4.5,5,5.5,6",
+                   help="log10 N of the --compare-dense grid (dense attention only up to --dense-max)")
+    p.add_argument("--dense-max", type=float, default=6.0, help="largest log10 N run densely")
     p.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                    help="before the warm-up, run one plain copy kernel that reads and writes MIB MiB "
                         "(the reference for the FETCH_SIZE/WRITE_SIZE counter runs)")
@@ -120,6 +127,120 @@ def cpu_baseline(w, sample):
     }
 
 
+def _time_ms(fn, reps):
+    """Mean ms of fn() over reps runs after one warm-up, by events on the current stream."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(reps):
+        fn()
+    ev[1].record()
+    torch.cuda.synchronize()
+    return ev[0].elapsed_time(ev[1]) / reps
+
+
+def _peak_bytes(fn):
+    """Peak device memory fn() allocates beyond what is already allocated."""
+    import torch
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    fn()
+    torch.cuda.synchronize()
+    return torch.cuda.max_memory_allocated() - base
+
+
+def compare_dense(args):
+    """k-MIP attention against dense softmax attention on one MI355X.
+
+    The efficiency study (Section 5.1, "Objective 1", and the detailed
+    measurements of Appendix H.2 / I) times one graph with Q, K, V ~ N(0, 1),
+    one head, k = 10, over N = 10^2 .. 10^7, for inference (forward) and
+    training (forward + backward), with peak memory.  Here d = 16 (the
+    smallest head size the library compiles; the paper used 10) and bf16
+    inputs.  Dense attention is torch's scaled_dot_product_attention held to
+    its flash / memory-efficient kernels (linear memory, no N x N matrix);
+    the math fallback is not allowed, so a size it cannot take is reported
+    as an error rather than timed on another algorithm."""
+    import numpy as np
+    import torch
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    import torch.nn.functional as F
+
+    import paper_2604_03815_amd as kmip
+    import workloads
+
+    dev = torch.device("cuda:0")
+    d, kk = 16, 10
+    scale = 1.0 / np.sqrt(d)
+    rows = []
+    for e in (float(x) for x in args.dense_exps.split(",")):
+        N = int(round(10 ** e))
+        w = workloads.iid(N, 1, d, kk, seed=args.seed, name="grid")
+        q, k, v, g = (torch.from_numpy(getattr(w, n).view(np.int16)).view(torch.bfloat16).to(dev)
+                      for n in ("q", "kk", "v", "dout"))
+        reps = 5 if N <= 10 ** 5 else (2 if N <= 10 ** 6 else 1)
+        row = {"log10_N": e, "N": N}
+        ws = kmip.Workspace(dev)
+        ws.get(max(kmip.topk_workspace_size(N, 1, d, kk), kmip.bwd_workspace_size(N, 1, d, kk)))
+        out = torch.empty((N, 1, d), dtype=torch.float32, device=dev)
+        idx = torch.empty((N, 1, kk), dtype=torch.int32, device=dev)
+        lse = torch.empty((N, 1), dtype=torch.float32, device=dev)
+        grads = [torch.empty((N, 1, d), dtype=torch.float32, device=dev) for _ in range(3)]
+
+        def kmip_inf():
+            kmip.topk(q, k, kk, idx=idx, workspace=ws)
+            kmip.attend(q, k, v, idx, scale, out=out, lse=lse)
+
+        def kmip_train():
+            kmip_inf()
+            kmip.bwd(q, k, v, g, idx, lse, scale, dq=grads[0], dk=grads[1], dv=grads[2], workspace=ws)
+
+        row["kmip_inference_ms"] = _time_ms(kmip_inf, reps)
+        row["kmip_training_ms"] = _time_ms(kmip_train, reps)
+        row["kmip_training_peak_bytes"] = _peak_bytes(kmip_train) + ws.buf.numel() + 4 * (
+            out.numel() + idx.numel() + lse.numel() + sum(x.numel() for x in grads))
+        if e <= args.dense_max + 1e-9:
+            # [batch 1, heads 1, N, d]
+            qd, kd, vd, gd = (x.view(N, d).unsqueeze(0).unsqueeze(0) for x in (q, k, v, g))
+            try:
+                with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+                    def dense_inf():
+                        with torch.no_grad():
+                            F.scaled_dot_product_attention(qd, kd, vd, scale=scale)
+
+                    qg, kg, vg = (x.detach().clone().requires_grad_() for x in (qd, kd, vd))
+
+                    def dense_train():
+                        o = F.scaled_dot_product_attention(qg, kg, vg, scale=scale)
+                        o.backward(gd)
+                        qg.grad = kg.grad = vg.grad = None
+
+                    row["dense_inference_ms"] = _time_ms(dense_inf, reps)
+                    row["dense_training_ms"] = _time_ms(dense_train, reps)
+                    row["dense_training_peak_bytes"] = _peak_bytes(dense_train) + 3 * 2 * N * d
+                    row["speedup_inference"] = row["dense_inference_ms"] / row["kmip_inference_ms"]
+                    row["speedup_training"] = row["dense_training_ms"] / row["kmip_training_ms"]
+            except RuntimeError as ex:
+                row["dense_error"] = str(ex).splitlines()[0][:200]
+        log("[dense] " + json.dumps(row))
+        rows.append(row)
+        del q, k, v, g, out, idx, lse, grads, ws
+        torch.cuda.empty_cache()
+    result = {
+        "metric": "k-MIP vs dense softmax attention, inference and training ms and peak memory",
+        "unit": "ms", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "one graph, H=1, d=16, k=10, Q/K/V/dOut ~ N(0,1) -> bf16, seed "
+                               f"{args.seed}; dense = torch SDPA (flash / memory-efficient kernels)",
+                   "grid_log10_N": args.dense_exps, "dense_max_log10_N": args.dense_max},
+        "rows": rows,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -128,6 +249,10 @@ def main():
               "graphs, one large graph by query ranges after an all-gather of K and V)",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.compare_dense:
+        compare_dense(args)
+        return
 
     import numpy as np
     import torch
