@@ -6,7 +6,9 @@ and wraps it with ctypes.  Only the test suite, ``__graft_entry__.smoke()``
 and the benchmark's CPU-baseline leg may import it.  The GPU library never
 links or calls it, and the two share no code.
 
-Inputs are float64 arrays [N, H, d] (node-major).  ``from_bf16`` widens the
+Inputs are float64 arrays, node-major: Q and K [N, H, d_K], V and the output
+gradient [N, H, d_V] (the value width may differ from the key width, Section
+3.1).  ``from_bf16`` widens the
 raw bfloat16 bits that the GPU path receives, exactly, so both sides see the
 same values.
 """
@@ -44,9 +46,9 @@ def _load():
         P = ctypes.c_void_p
         i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
         lib.oracle_topk.argtypes = [P, P, P, i32, i64, i32, i32, i32, i64, P, P, P, P]
-        lib.oracle_attend.argtypes = [P, P, P, i64, i32, i32, i32, f64, i64, P, P, P, P]
-        lib.oracle_forward.argtypes = [P, P, P, P, i32, i64, i32, i32, i32, f64, P, P, P]
-        lib.oracle_backward.argtypes = [P, P, P, P, i64, i32, i32, i32, f64, P, P, P, P]
+        lib.oracle_attend.argtypes = [P, P, P, i64, i32, i32, i32, i32, f64, i64, P, P, P, P]
+        lib.oracle_forward.argtypes = [P, P, P, P, i32, i64, i32, i32, i32, i32, f64, P, P, P]
+        lib.oracle_backward.argtypes = [P, P, P, P, i64, i32, i32, i32, i32, f64, P, P, P, P]
         lib.oracle_check_set.argtypes = [P, P, P, i32, i64, i32, i32, i32, i64, P, P, P, P, P]
         lib.oracle_threads.argtypes = []
         for f in ("oracle_threads", "oracle_topk", "oracle_attend", "oracle_forward", "oracle_backward",
@@ -114,29 +116,44 @@ def topk(Q, K, k: int, offsets=None, sel=None):
     return idx, sc, nx
 
 
+def _value_width(V, N, H, name="V"):
+    if V.ndim != 3 or V.shape[0] != N or V.shape[1] != H:
+        raise ValueError(f"{name} must be [N, H, d_V] with the N and H of Q")
+    return V.shape[2]
+
+
+def _key_shape(K, N, H, d):
+    if K.shape != (N, H, d):
+        raise ValueError("K must have the shape of Q")
+
+
 def attend(Q, K, V, idx, scale: float, sel=None):
-    """Softmax + aggregate on a given index set.  Returns (out [nsel,d], lse [nsel])."""
+    """Softmax + aggregate on a given index set.  Returns (out [nsel,d_V], lse [nsel])."""
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     N, H, d = _shape(Q)
+    _key_shape(K, N, H, d)
+    dv = _value_width(V, N, H)
     s, n = _sel(sel, N, H)
     idx = np.ascontiguousarray(idx, dtype=np.int32).reshape(n, -1)
     k = idx.shape[1]
-    out = np.empty((n, d), np.float64)
+    out = np.empty((n, dv), np.float64)
     lse = np.empty(n, np.float64)
-    _load().oracle_attend(_ptr(Q), _ptr(K), _ptr(V), N, H, d, k, float(scale), n, _ptr(s),
+    _load().oracle_attend(_ptr(Q), _ptr(K), _ptr(V), N, H, d, dv, k, float(scale), n, _ptr(s),
                           _ptr(idx), _ptr(out), _ptr(lse))
     return out, lse
 
 
 def forward(Q, K, V, k: int, scale: float, offsets=None):
-    """Full forward.  Returns (out [N,H,d], idx [N,H,k], lse [N,H])."""
+    """Full forward.  Returns (out [N,H,d_V], idx [N,H,k], lse [N,H])."""
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     N, H, d = _shape(Q)
+    _key_shape(K, N, H, d)
+    dv = _value_width(V, N, H)
     o, G = _offsets(offsets, N)
     idx = np.empty((N, H, k), np.int32)
-    out = np.empty((N, H, d), np.float64)
+    out = np.empty((N, H, dv), np.float64)
     lse = np.empty((N, H), np.float64)
-    rc = _load().oracle_forward(_ptr(Q), _ptr(K), _ptr(V), _ptr(o), G, N, H, d, k,
+    rc = _load().oracle_forward(_ptr(Q), _ptr(K), _ptr(V), _ptr(o), G, N, H, d, dv, k,
                                 float(scale), _ptr(idx), _ptr(out), _ptr(lse))
     if rc != 0:
         raise MemoryError("oracle_forward could not allocate")
@@ -144,15 +161,19 @@ def forward(Q, K, V, k: int, scale: float, offsets=None):
 
 
 def backward(Q, K, V, dO, idx, scale: float):
-    """Gradients with the index set held fixed.  Returns (dQ, dK, dV), each [N,H,d]."""
+    """Gradients with the index set held fixed.  Returns (dQ [N,H,d_K], dK [N,H,d_K], dV [N,H,d_V])."""
     Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
     N, H, d = _shape(Q)
+    _key_shape(K, N, H, d)
+    dv = _value_width(V, N, H)
+    if dO.shape != V.shape:
+        raise ValueError("dO must have the shape of V")
     idx = np.ascontiguousarray(idx, dtype=np.int32).reshape(N, H, -1)
     k = idx.shape[2]
     dQ = np.empty((N, H, d), np.float64)
     dK = np.empty((N, H, d), np.float64)
-    dV = np.empty((N, H, d), np.float64)
-    rc = _load().oracle_backward(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO), N, H, d, k,
+    dV = np.empty((N, H, dv), np.float64)
+    rc = _load().oracle_backward(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO), N, H, d, dv, k,
                                  float(scale), _ptr(idx), _ptr(dQ), _ptr(dK), _ptr(dV))
     if rc != 0:
         raise MemoryError("oracle_backward could not allocate")

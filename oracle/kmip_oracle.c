@@ -29,9 +29,12 @@
  *   - scale must be > 0, so selecting on raw scores equals selecting on
  *     scaled scores.
  *
- * All inputs are float64 arrays [N, H, d], node-major (row i, head h, dim t
- * at ((i * H) + h) * d + t).  Exact bf16 values widen to float64 without
- * rounding, so the oracle sees the same numbers as the GPU path.
+ * All inputs are float64 arrays, node-major (row i, head h, dim t at
+ * ((i * H) + h) * width + t): Q and K [N, H, d] with d = d_K, V and dO
+ * [N, H, dv] with dv = d_V (Section 3.1 lets the value width differ from the
+ * query/key width: W_V maps to d_V dimensions, W_Q and W_K to d_K).  Exact
+ * bf16 values widen to float64 without rounding, so the oracle sees the same
+ * numbers as the GPU path.
  */
 #include <math.h>
 #include <omp.h>
@@ -143,11 +146,11 @@ int oracle_topk(const double* Q, const double* K, const int32_t* offsets, int32_
  * Softmax over the kept scores and the weighted sum of gathered value rows
  * (Algorithm 1: GatherRows, softmax, Einsum nk,nkv->nv), for a given index
  * set.  Slots holding -1 are empty (their weight is exp(-inf) = 0).
- *   out [nsel, d], lse [nsel] (natural log of sum_j exp(scale * s_ij)).
+ *   out [nsel, dv], lse [nsel] (natural log of sum_j exp(scale * s_ij)).
  * A row with no valid index gets out = 0 and lse = -inf.
  */
 int oracle_attend(const double* Q, const double* K, const double* V, int64_t N, int32_t H,
-                  int32_t d, int32_t k, double scale, int64_t nsel, const int64_t* sel,
+                  int32_t d, int32_t dv, int32_t k, double scale, int64_t nsel, const int64_t* sel,
                   const int32_t* idx, double* out, double* lse) {
     if (sel == NULL) nsel = N * (int64_t)H;
 #pragma omp parallel
@@ -164,8 +167,8 @@ int oracle_attend(const double* Q, const double* K, const double* V, int64_t N, 
                 z[t] = row[t] >= 0 ? scale * oracle_score(Q, K, H, d, i, row[t], h) : -INFINITY;
                 if (z[t] > zmax) zmax = z[t];
             }
-            double* o = out + r * d;
-            for (int32_t c = 0; c < d; ++c) o[c] = 0.0;
+            double* o = out + r * dv;
+            for (int32_t c = 0; c < dv; ++c) o[c] = 0.0;
             if (zmax == -INFINITY) {
                 lse[r] = -INFINITY;
                 continue;
@@ -175,8 +178,8 @@ int oracle_attend(const double* Q, const double* K, const double* V, int64_t N, 
             for (int32_t t = 0; t < k; ++t) {
                 if (row[t] < 0) continue;
                 double p = exp(z[t] - zmax) / Z;
-                const double* vr = V + ((size_t)row[t] * H + h) * d;
-                for (int32_t c = 0; c < d; ++c) o[c] += p * vr[c];
+                const double* vr = V + ((size_t)row[t] * H + h) * dv;
+                for (int32_t c = 0; c < dv; ++c) o[c] += p * vr[c];
             }
             lse[r] = zmax + log(Z);
         }
@@ -187,13 +190,13 @@ int oracle_attend(const double* Q, const double* K, const double* V, int64_t N, 
 
 /*
  * Full forward: RowwiseTopK for every query-head, then oracle_attend.
- * idx [N, H, k], out [N, H, d], lse [N, H].
+ * idx [N, H, k], out [N, H, dv], lse [N, H].
  */
 int oracle_forward(const double* Q, const double* K, const double* V, const int32_t* offsets,
-                   int32_t G, int64_t N, int32_t H, int32_t d, int32_t k, double scale,
+                   int32_t G, int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, double scale,
                    int32_t* idx, double* out, double* lse) {
     if (oracle_topk(Q, K, offsets, G, N, H, d, k, 0, NULL, idx, NULL, NULL) != 0) return -1;
-    return oracle_attend(Q, K, V, N, H, d, k, scale, 0, NULL, idx, out, lse);
+    return oracle_attend(Q, K, V, N, H, d, dv, k, scale, 0, NULL, idx, out, lse);
 }
 
 /*
@@ -206,12 +209,14 @@ int oracle_forward(const double* Q, const double* K, const double* V, const int3
  *   dQ_i  = sum_j g_j * scale * k_j
  *   dK_j += g_j * scale * q_i
  *   dV_j += p_j * dO_i
- * idx [N, H, k]; dQ, dK, dV [N, H, d] are overwritten.
+ * (the dot product dp_j runs over the dv value dimensions, dQ and dK have
+ * the d query/key dimensions, dV the dv value dimensions).
+ * idx [N, H, k]; dQ, dK [N, H, d] and dV [N, H, dv] are overwritten.
  * Per-query terms are computed in parallel; the scatter into dK and dV runs
  * in one thread in query order.
  */
 int oracle_backward(const double* Q, const double* K, const double* V, const double* dO,
-                    int64_t N, int32_t H, int32_t d, int32_t k, double scale,
+                    int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, double scale,
                     const int32_t* idx, double* dQ, double* dK, double* dV) {
     int64_t NH = N * (int64_t)H;
     double* P = (double*)malloc(sizeof(double) * (size_t)(NH * k > 0 ? NH * k : 1));
@@ -223,7 +228,7 @@ int oracle_backward(const double* Q, const double* K, const double* V, const dou
     }
     memset(dQ, 0, sizeof(double) * (size_t)(NH * d));
     memset(dK, 0, sizeof(double) * (size_t)(NH * d));
-    memset(dV, 0, sizeof(double) * (size_t)(NH * d));
+    memset(dV, 0, sizeof(double) * (size_t)(NH * dv));
 #pragma omp parallel
     {
         double* z = (double*)malloc(sizeof(double) * (size_t)(k > 0 ? k : 1));
@@ -246,14 +251,14 @@ int oracle_backward(const double* Q, const double* K, const double* V, const dou
             }
             double Z = 0.0;
             for (int32_t t = 0; t < k; ++t) Z += row[t] >= 0 ? exp(z[t] - zmax) : 0.0;
-            const double* dOi = dO + (size_t)qh * d;
+            const double* dOi = dO + (size_t)qh * dv;
             double D = 0.0;
             for (int32_t t = 0; t < k; ++t) {
                 p[t] = row[t] >= 0 ? exp(z[t] - zmax) / Z : 0.0;
                 dp[t] = 0.0;
                 if (row[t] >= 0) {
-                    const double* vr = V + ((size_t)row[t] * H + h) * d;
-                    for (int32_t c = 0; c < d; ++c) dp[t] += dOi[c] * vr[c];
+                    const double* vr = V + ((size_t)row[t] * H + h) * dv;
+                    for (int32_t c = 0; c < dv; ++c) dp[t] += dOi[c] * vr[c];
                 }
                 D += p[t] * dp[t];
             }
@@ -272,16 +277,14 @@ int oracle_backward(const double* Q, const double* K, const double* V, const dou
         int32_t h = (int32_t)(qh % H);
         const int32_t* row = idx + qh * k;
         const double* qi = Q + (size_t)qh * d;
-        const double* dOi = dO + (size_t)qh * d;
+        const double* dOi = dO + (size_t)qh * dv;
         for (int32_t t = 0; t < k; ++t) {
             if (row[t] < 0) continue;
-            double* dk = dK + ((size_t)row[t] * H + h) * d;
-            double* dv = dV + ((size_t)row[t] * H + h) * d;
+            double* dkr = dK + ((size_t)row[t] * H + h) * d;
+            double* dvr = dV + ((size_t)row[t] * H + h) * dv;
             double gs = Gr[qh * k + t] * scale, pt = P[qh * k + t];
-            for (int32_t c = 0; c < d; ++c) {
-                dk[c] += gs * qi[c];
-                dv[c] += pt * dOi[c];
-            }
+            for (int32_t c = 0; c < d; ++c) dkr[c] += gs * qi[c];
+            for (int32_t c = 0; c < dv; ++c) dvr[c] += pt * dOi[c];
         }
     }
     free(P);

@@ -115,7 +115,7 @@ def test_golden_tiny_ties():
 
 def _sdpa_per_graph(Q, K, V, offsets, scale):
     N, H, d = Q.shape
-    out = np.zeros_like(Q)
+    out = np.zeros((N, H, V.shape[2]))
     lse = np.zeros((N, H))
     for (lo, hi) in _graphs(offsets, N):
         if hi == lo:
@@ -379,3 +379,93 @@ def test_check_set_detects_bad_sets():
     assert fl[0] & 2 and fl[0] & 4
     assert fl[1] & 8 and fl[1] & 4
     assert fl[2] & 1
+
+
+# ---- value rows of another width than the query/key rows (Section 3.1:
+# W_Q, W_K map to d_K dimensions, W_V to d_V) ----
+
+@pytest.mark.parametrize("d,dv", [(4, 7), (6, 2)])
+def test_value_width_k_equals_n_is_softmax_attention(d, dv):
+    rng = np.random.default_rng(d * 10 + dv)
+    sizes = [5, 9, 1, 12]
+    N, H = sum(sizes), 2
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    Q, K = (rng.standard_normal((N, H, d)) for _ in range(2))
+    V = rng.standard_normal((N, H, dv))
+    out, idx, lse = oracle.forward(Q, K, V, max(sizes), 0.45, offsets=offsets)
+    assert out.shape == (N, H, dv)
+    want_out, want_lse = _sdpa_per_graph(Q, K, V, offsets, 0.45)
+    np.testing.assert_allclose(out, want_out, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(lse, want_lse, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("d,dv", [(5, 3), (3, 8)])
+def test_value_width_masked_dense_and_autograd(d, dv):
+    rng = np.random.default_rng(300 + d + dv)
+    N, H, k = 31, 2, 6
+    Qn, Kn = (rng.standard_normal((N, H, d)) for _ in range(2))
+    Vn, dOn = (rng.standard_normal((N, H, dv)) for _ in range(2))
+    scale = 0.7
+    out, idx, lse = oracle.forward(Qn, Kn, Vn, k, scale)
+    dQ, dK, dV = oracle.backward(Qn, Kn, Vn, dOn, idx, scale)
+    assert dQ.shape == dK.shape == (N, H, d) and dV.shape == (N, H, dv)
+    Q, K, V = (torch.from_numpy(x).clone().requires_grad_(True) for x in (Qn, Kn, Vn))
+    want_out, want_lse, top = _masked_dense_torch(Q, K, V, k, scale)
+    np.testing.assert_allclose(out, want_out.detach().numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(lse, want_lse.detach().numpy(), rtol=1e-12, atol=1e-12)
+    (want_out * torch.from_numpy(dOn)).sum().backward()
+    np.testing.assert_allclose(dQ, Q.grad.numpy(), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(dK, K.grad.numpy(), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(dV, V.grad.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def test_value_width_backward_finite_differences():
+    rng = np.random.default_rng(21)
+    N, H, d, dv, k = 12, 1, 3, 5, 3
+    offsets = np.array([0, 5, 12], np.int32)
+    Q, K = (rng.standard_normal((N, H, d)) for _ in range(2))
+    V, dO = (rng.standard_normal((N, H, dv)) for _ in range(2))
+    scale = 0.9
+    _, idx, _ = oracle.forward(Q, K, V, k, scale, offsets=offsets)
+    dQ, dK, dV = oracle.backward(Q, K, V, dO, idx, scale)
+    eps = 1e-6
+    for name, X, G in (("Q", Q, dQ), ("K", K, dK), ("V", V, dV)):
+        num = np.zeros_like(X)
+        for pos in np.ndindex(X.shape):
+            args = [{"Q": Q, "K": K, "V": V} for _ in range(2)]
+            for a, sgn in zip(args, (1.0, -1.0)):
+                Xs = X.copy()
+                Xs[pos] += sgn * eps
+                a[name] = Xs
+            num[pos] = (_loss(args[0]["Q"], args[0]["K"], args[0]["V"], dO, k, scale, offsets)
+                        - _loss(args[1]["Q"], args[1]["K"], args[1]["V"], dO, k, scale, offsets)) / (2 * eps)
+        np.testing.assert_allclose(G, num, rtol=1e-6, atol=1e-7, err_msg=name)
+
+
+def test_value_columns_split_and_gradient_invariants():
+    # out and dV are linear in the value columns: splitting V (and dO) into
+    # column blocks gives the column blocks of the full result, while dQ and
+    # dK add up over the blocks (dp sums over the value dimensions)
+    rng = np.random.default_rng(22)
+    N, H, d, dv, k = 26, 2, 4, 9, 5
+    offsets = np.array([0, 10, 26], np.int32)
+    Q, K = (rng.standard_normal((N, H, d)) for _ in range(2))
+    V, dO = (rng.standard_normal((N, H, dv)) for _ in range(2))
+    out, idx, _ = oracle.forward(Q, K, V, k, 0.6, offsets=offsets)
+    dQ, dK, dV = oracle.backward(Q, K, V, dO, idx, 0.6)
+    parts = [(0, 4), (4, 9)]
+    sq = np.zeros_like(dQ)
+    sk = np.zeros_like(dK)
+    for a, b in parts:
+        o, ix, _ = oracle.forward(Q, K, V[:, :, a:b], k, 0.6, offsets=offsets)
+        np.testing.assert_array_equal(ix, idx)
+        np.testing.assert_allclose(o, out[:, :, a:b], rtol=1e-13, atol=1e-13)
+        pq, pk, pv = oracle.backward(Q, K, V[:, :, a:b], dO[:, :, a:b], idx, 0.6)
+        np.testing.assert_allclose(pv, dV[:, :, a:b], rtol=1e-13, atol=1e-13)
+        sq += pq
+        sk += pk
+    np.testing.assert_allclose(sq, dQ, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(sk, dK, rtol=1e-11, atol=1e-12)
+    for (lo, hi) in _graphs(offsets, N):
+        np.testing.assert_allclose(dK[lo:hi].sum(axis=0), 0.0, atol=1e-12)
+        np.testing.assert_allclose(dV[lo:hi].sum(axis=0), dO[lo:hi].sum(axis=0), atol=1e-12)
