@@ -123,6 +123,21 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * kmip_attend and kmip_fwd with value rows of their own width (Section 3.1:
+ * W_Q and W_K project to d_K dimensions, W_V to d_V).  Q and K are
+ * [N, H, d] with d = d_K, which alone decides the selection; V and out are
+ * [N, H, dv] with dv = d_V in {16, 32, 64}.  kmip_attend / kmip_fwd are the
+ * case dv = d.  Same workspace as kmip_topk; N * H * dv < 2^31.
+ */
+kmip_status_t kmip_attend_dv(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
+                             int32_t d, int32_t dv, int32_t k, float scale, const int32_t* topk_idx,
+                             float* out, float* lse, void* stream);
+kmip_status_t kmip_fwd_dv(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
+                          int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k,
+                          float scale, float* out, int32_t* topk_idx, float* lse, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/*
  * Backward with the forward's index set held fixed (Section 3.1, last
  * paragraph, and Appendix E, last paragraph: the top-k indices are reused,
  * so only the k selected pairs of each query carry gradient).  With p_j the
@@ -179,6 +194,21 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
                        const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
                        int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
                        int32_t variant, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * kmip_bwd with value rows of their own width dv = d_V in {16, 32, 64}
+ * (Section 3.1): V, dOut bf16 [N, H, dv] and dV float32 [N, H, dv]; Q, K,
+ * dQ, dK stay [N, H, d].  dp_j = dOut_i . v_j runs over the dv value
+ * dimensions.  KMIP_BWD_BUCKETED needs dv == d (else KMIP_ERR_UNSUPPORTED
+ * and workspace size 0): its interleaved copy of q_i and dOut_i assumes
+ * equal widths; KMIP_BWD_AUTO then picks KMIP_BWD_SEGMENTED.  kmip_bwd and
+ * kmip_bwd_workspace_size are the case dv = d.
+ */
+size_t kmip_bwd_dv_workspace_size(int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, int32_t variant);
+kmip_status_t kmip_bwd_dv(const void* Q, const void* K, const void* V, const void* dOut,
+                          const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
+                          int32_t d, int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV,
+                          int32_t variant, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Forward (kmip_fwd) of one graph without a caller workspace and without

@@ -2,8 +2,10 @@
 
 Every function marshals torch tensors into the C ABI of include/kmip.h and
 launches on the current HIP stream; all arithmetic runs in the library's HIP
-kernels.  Tensors: Q, K, V, dOut are bf16 [N, H, d] on the GPU; out, dQ, dK,
-dV are float32 [N, H, d]; topk_idx is int32 [N, H, k]; lse is float32 [N, H].
+kernels.  Tensors: Q, K are bf16 [N, H, d] (d = d_K), V and dOut bf16
+[N, H, dv] (dv = d_V, the value width; dv = d unless the caller's V is
+narrower or wider) on the GPU; out and dV are float32 [N, H, dv], dQ and dK
+float32 [N, H, d]; topk_idx is int32 [N, H, k]; lse is float32 [N, H].
 ``graph_offsets`` is a host-side int32 sequence [G+1] (or None for one graph).
 """
 from __future__ import annotations
@@ -70,8 +72,8 @@ def topk_workspace_size(N: int, H: int, d: int, k: int, num_graphs: int = 1) -> 
     return int(load().kmip_topk_workspace_size(N, H, d, k, num_graphs))
 
 
-def bwd_workspace_size(N: int, H: int, d: int, k: int, variant: int = 0) -> int:
-    return int(load().kmip_bwd_workspace_size(N, H, d, k, variant))
+def bwd_workspace_size(N: int, H: int, d: int, k: int, variant: int = 0, dv: Optional[int] = None) -> int:
+    return int(load().kmip_bwd_dv_workspace_size(N, H, d, d if dv is None else dv, k, variant))
 
 
 class Workspace:
@@ -94,6 +96,14 @@ def _nhd(q, name="Q"):
     if not isinstance(q, torch.Tensor) or q.dim() != 3:
         raise ValueError(f"{name} must be a tensor [N, H, d]")
     return tuple(int(x) for x in q.shape)
+
+
+def _dv(v, N, H, name="V"):
+    """Value width of v, which must be [N, H, dv]."""
+    torch = _torch()
+    if not isinstance(v, torch.Tensor) or v.dim() != 3 or tuple(v.shape[:2]) != (N, H):
+        raise ValueError(f"{name} must be a tensor [N, H, d_V] with N={N}, H={H}")
+    return int(v.shape[2])
 
 
 def _kk(idx, name="topk_idx"):
@@ -153,20 +163,21 @@ def attend(q, k_, v, idx, scale: float, out=None, lse=None):
     """Gather-softmax-aggregate on a given index set: returns (out, lse)."""
     torch = _torch()
     N, H, d = _nhd(q)
+    dv = _dv(v, N, H)
     kk = _kk(idx)
     specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d)),
-             (v, "V", torch.bfloat16, (N, H, d)), (idx, "topk_idx", torch.int32, (N, H, kk))]
+             (v, "V", torch.bfloat16, (N, H, dv)), (idx, "topk_idx", torch.int32, (N, H, kk))]
     if out is not None:
-        specs.append((out, "out", torch.float32, (N, H, d)))
+        specs.append((out, "out", torch.float32, (N, H, dv)))
     if lse is not None:
         specs.append((lse, "lse", torch.float32, (N, H)))
     _validate(*specs)
     if out is None:
-        out = torch.empty((N, H, d), dtype=torch.float32, device=q.device)
+        out = torch.empty((N, H, dv), dtype=torch.float32, device=q.device)
     if lse is None:
         lse = torch.empty((N, H), dtype=torch.float32, device=q.device)
-    check(load().kmip_attend(_ptr(q), _ptr(k_), _ptr(v), N, H, d, kk, float(scale), _ptr(idx),
-                             _ptr(out), _ptr(lse), _stream_ptr()))
+    check(load().kmip_attend_dv(_ptr(q), _ptr(k_), _ptr(v), N, H, d, dv, kk, float(scale), _ptr(idx),
+                                _ptr(out), _ptr(lse), _stream_ptr()))
     return out, lse
 
 
@@ -174,19 +185,20 @@ def fwd(q, k_, v, kk: int, scale: float, graph_offsets=None, workspace=None):
     """Full forward: returns (out, topk_idx, lse)."""
     torch = _torch()
     N, H, d = _nhd(q)
+    dv = _dv(v, N, H)
     kk = int(kk)
     _validate((q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d)),
-              (v, "V", torch.bfloat16, (N, H, d)))
+              (v, "V", torch.bfloat16, (N, H, dv)))
     o, optr, G = _offsets(graph_offsets)
     if o is not None and (o.ndim != 1 or len(o) < 2):
         raise ValueError("graph_offsets must be a 1-D sequence of at least two entries")
-    out = torch.empty((N, H, d), dtype=torch.float32, device=q.device)
+    out = torch.empty((N, H, dv), dtype=torch.float32, device=q.device)
     idx = torch.empty((N, H, kk), dtype=torch.int32, device=q.device)
     lse = torch.empty((N, H), dtype=torch.float32, device=q.device)
     buf = _workspace(workspace, topk_workspace_size(N, H, d, kk, G), q.device)
-    check(load().kmip_fwd(_ptr(q), _ptr(k_), _ptr(v), optr, G, N, H, d, kk, float(scale), _ptr(out),
-                          _ptr(idx), _ptr(lse), _ptr(buf), 0 if buf is None else buf.numel(),
-                          _stream_ptr()))
+    check(load().kmip_fwd_dv(_ptr(q), _ptr(k_), _ptr(v), optr, G, N, H, d, dv, kk, float(scale), _ptr(out),
+                             _ptr(idx), _ptr(lse), _ptr(buf), 0 if buf is None else buf.numel(),
+                             _stream_ptr()))
     return out, idx, lse
 
 
@@ -211,23 +223,24 @@ def bwd(q, k_, v, dout, idx, lse, scale: float, variant: int = 0, dq=None, dk=No
     """Backward with the index set held fixed: returns (dQ, dK, dV) float32."""
     torch = _torch()
     N, H, d = _nhd(q)
+    wv = _dv(v, N, H)
     kk = _kk(idx)
-    nd = (N, H, d)
-    specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, nd), (v, "V", torch.bfloat16, nd),
-             (dout, "dOut", torch.bfloat16, nd), (idx, "topk_idx", torch.int32, (N, H, kk)),
+    nd, nv = (N, H, d), (N, H, wv)
+    specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, nd), (v, "V", torch.bfloat16, nv),
+             (dout, "dOut", torch.bfloat16, nv), (idx, "topk_idx", torch.int32, (N, H, kk)),
              (lse, "lse", torch.float32, (N, H))]
-    for t, name in ((dq, "dQ"), (dk, "dK"), (dv, "dV")):
+    for t, name, shp in ((dq, "dQ", nd), (dk, "dK", nd), (dv, "dV", nv)):
         if t is not None:
-            specs.append((t, name, torch.float32, nd))
+            specs.append((t, name, torch.float32, shp))
     _validate(*specs)
     dev = q.device
     dq = dq if dq is not None else torch.empty(nd, dtype=torch.float32, device=dev)
     dk = dk if dk is not None else torch.empty(nd, dtype=torch.float32, device=dev)
-    dv = dv if dv is not None else torch.empty(nd, dtype=torch.float32, device=dev)
-    buf = _workspace(workspace, bwd_workspace_size(N, H, d, kk, variant), dev)
-    check(load().kmip_bwd(_ptr(q), _ptr(k_), _ptr(v), _ptr(dout), _ptr(idx), _ptr(lse), N, H, d, kk,
-                          float(scale), _ptr(dq), _ptr(dk), _ptr(dv), int(variant), _ptr(buf),
-                          0 if buf is None else buf.numel(), _stream_ptr()))
+    dv = dv if dv is not None else torch.empty(nv, dtype=torch.float32, device=dev)
+    buf = _workspace(workspace, bwd_workspace_size(N, H, d, kk, variant, dv=wv), dev)
+    check(load().kmip_bwd_dv(_ptr(q), _ptr(k_), _ptr(v), _ptr(dout), _ptr(idx), _ptr(lse), N, H, d, wv, kk,
+                             float(scale), _ptr(dq), _ptr(dk), _ptr(dv), int(variant), _ptr(buf),
+                             0 if buf is None else buf.numel(), _stream_ptr()))
     return dq, dk, dv
 
 

@@ -105,6 +105,13 @@ kmip_status_t check_sizes(int64_t N, int32_t H, int32_t d, int32_t k) {
     return KMIP_OK;
 }
 
+// The value width, besides the sizes check_sizes covers.
+kmip_status_t check_value_width(int64_t N, int32_t H, int32_t dv) {
+    if (dv != 16 && dv != 32 && dv != 64) return record_error(KMIP_ERR_UNSUPPORTED, "d_V=%d not in {16, 32, 64}", dv);
+    if (N * (int64_t)H * dv >= (int64_t(1) << 31)) return record_error(KMIP_ERR_INVALID_ARG, "N*H*d_V >= 2^31");
+    return KMIP_OK;
+}
+
 kmip_status_t check_scale(float scale) {
     if (!std::isfinite(scale) || !(scale > 0.0f)) return record_error(KMIP_ERR_INVALID_ARG, "scale must be finite and > 0");
     return KMIP_OK;
@@ -265,82 +272,106 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
     return ok();
 }
 
-kmip_status_t kmip_attend(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
-                          int32_t d, int32_t k, float scale, const int32_t* topk_idx, float* out,
-                          float* lse, void* stream_) {
+kmip_status_t kmip_attend_dv(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
+                             int32_t d, int32_t dv, int32_t k, float scale, const int32_t* topk_idx,
+                             float* out, float* lse, void* stream_) {
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
+    if ((s = check_value_width(N, H, dv)) != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
     if (N == 0) return ok();
     if (!Q || !K || !V || !topk_idx || !out || !lse)
         return record_error(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_attend");
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V))
         return record_error(KMIP_ERR_INVALID_ARG, "Q, K and V must be 16-byte aligned");
-    hipError_t e = kmip::launch_attend(Q, K, V, topk_idx, (int32_t)N, H, d, k, scale, out, lse,
+    hipError_t e = kmip::launch_attend(Q, K, V, topk_idx, (int32_t)N, H, d, dv, k, scale, out, lse,
                                        reinterpret_cast<hipStream_t>(stream_));
     if (e != hipSuccess) return hip_fail(e, "attend launch");
     return ok();
 }
 
-kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
-                       int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
-                       float scale, float* out, int32_t* topk_idx, float* lse, void* workspace,
-                       size_t workspace_bytes, void* stream) {
+kmip_status_t kmip_attend(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
+                          int32_t d, int32_t k, float scale, const int32_t* topk_idx, float* out,
+                          float* lse, void* stream) {
+    return kmip_attend_dv(Q, K, V, N, H, d, d, k, scale, topk_idx, out, lse, stream);
+}
+
+kmip_status_t kmip_fwd_dv(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
+                          int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k,
+                          float scale, float* out, int32_t* topk_idx, float* lse, void* workspace,
+                          size_t workspace_bytes, void* stream) {
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
+    if ((s = check_value_width(N, H, dv)) != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
     if (N > 0 && (!V || !out || !lse)) return record_error(KMIP_ERR_INVALID_ARG, "null V, out or lse");
     if (N > 0 && !aligned16(V)) return record_error(KMIP_ERR_INVALID_ARG, "V must be 16-byte aligned");
     s = kmip_topk(Q, K, graph_offsets, num_graphs, N, H, d, k, topk_idx, workspace,
                   workspace_bytes, stream);
     if (s != KMIP_OK) return s;
-    return kmip_attend(Q, K, V, N, H, d, k, scale, topk_idx, out, lse, stream);
+    return kmip_attend_dv(Q, K, V, N, H, d, dv, k, scale, topk_idx, out, lse, stream);
+}
+
+kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
+                       int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
+                       float scale, float* out, int32_t* topk_idx, float* lse, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+    return kmip_fwd_dv(Q, K, V, graph_offsets, num_graphs, N, H, d, d, k, scale, out, topk_idx, lse,
+                       workspace, workspace_bytes, stream);
 }
 
 // Backward variant the library picks (KMIP_BWD_AUTO): the bucketed reduction
-// where the key rows fit its bucket table, else the full key sort.
-static int32_t default_bwd_variant(int64_t N, int32_t H, int32_t d) {
-    return kmip::bwd_bucket_supported((int32_t)N, H, d) ? KMIP_BWD_BUCKETED : KMIP_BWD_SEGMENTED;
+// where the key rows fit its bucket table and the value width equals the
+// key width, else the full key sort.
+static int32_t default_bwd_variant(int64_t N, int32_t H, int32_t d, int32_t dv) {
+    return dv == d && kmip::bwd_bucket_supported((int32_t)N, H, d) ? KMIP_BWD_BUCKETED : KMIP_BWD_SEGMENTED;
 }
 
-size_t kmip_bwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t variant) {
-    if (check_sizes(N, H, d, k) != KMIP_OK) return 0;
-    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d) : variant;
+size_t kmip_bwd_dv_workspace_size(int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, int32_t variant) {
+    if (check_sizes(N, H, d, k) != KMIP_OK || check_value_width(N, H, dv) != KMIP_OK) return 0;
+    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d, dv) : variant;
     if (v == KMIP_BWD_KEY_AGGREGATED) return align_up(kmip::bwd_agg_workspace_bytes((int32_t)N, H, d));
     if (v == KMIP_BWD_SEGMENTED) return align_up(kmip::bwd_csr_workspace_bytes((int32_t)N, H, k));
-    if (v == KMIP_BWD_BUCKETED) return kmip::bwd_bucket_supported((int32_t)N, H, d)
+    if (v == KMIP_BWD_BUCKETED) return dv == d && kmip::bwd_bucket_supported((int32_t)N, H, d)
                                          ? align_up(kmip::bwd_bucket_workspace_bytes((int32_t)N, H, d, k))
                                          : 0;
     return 0;
 }
 
-kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* dOut,
-                       const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
-                       int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
-                       int32_t variant, void* workspace, size_t workspace_bytes, void* stream_) {
+size_t kmip_bwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t variant) {
+    return kmip_bwd_dv_workspace_size(N, H, d, d, k, variant);
+}
+
+kmip_status_t kmip_bwd_dv(const void* Q, const void* K, const void* V, const void* dOut,
+                          const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
+                          int32_t d, int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV,
+                          int32_t variant, void* workspace, size_t workspace_bytes, void* stream_) {
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
+    if ((s = check_value_width(N, H, dv)) != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
     if (variant < KMIP_BWD_AUTO || variant > KMIP_BWD_KEY_AGGREGATED)
         return record_error(KMIP_ERR_UNSUPPORTED, "backward variant %d", variant);
+    if (variant == KMIP_BWD_BUCKETED && dv != d)
+        return record_error(KMIP_ERR_UNSUPPORTED, "the bucketed variant needs d_V == d_K (got %d, %d)", dv, d);
     if (N == 0) return ok();
     if (!Q || !K || !V || !dOut || !topk_idx || !lse || !dQ || !dK || !dV)
         return record_error(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_bwd");
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(dOut))
         return record_error(KMIP_ERR_INVALID_ARG, "Q, K, V and dOut must be 16-byte aligned");
     if (!aligned16(dK) || !aligned16(dV)) return record_error(KMIP_ERR_INVALID_ARG, "dK and dV must be 16-byte aligned");
-    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d) : variant;
+    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d, dv) : variant;
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
     hipError_t e;
     if (v != KMIP_BWD_ATOMIC) {
-        const size_t need = kmip_bwd_workspace_size(N, H, d, k, v);
+        const size_t need = kmip_bwd_dv_workspace_size(N, H, d, dv, k, v);
         if (workspace == nullptr || workspace_bytes < need)
             return record_error(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
         if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0)
             return record_error(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
     }
     if (v == KMIP_BWD_KEY_AGGREGATED) {
-        e = kmip::launch_bwd_agg(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
+        e = kmip::launch_bwd_agg(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, dv, k, scale, dQ, dK,
                                  dV, workspace, stream);
     } else if (v == KMIP_BWD_BUCKETED) {
         if (!kmip::bwd_bucket_supported((int32_t)N, H, d))
@@ -348,14 +379,22 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
         e = kmip::launch_bwd_bucket(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
                                     dV, workspace, stream);
     } else if (v == KMIP_BWD_SEGMENTED) {
-        e = kmip::launch_bwd_csr(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
+        e = kmip::launch_bwd_csr(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, dv, k, scale, dQ, dK,
                                  dV, workspace, stream);
     } else {
-        e = kmip::launch_bwd_atomic(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ,
+        e = kmip::launch_bwd_atomic(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, dv, k, scale, dQ,
                                     dK, dV, stream);
     }
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     return ok();
+}
+
+kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* dOut,
+                       const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
+                       int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
+                       int32_t variant, void* workspace, size_t workspace_bytes, void* stream) {
+    return kmip_bwd_dv(Q, K, V, dOut, topk_idx, lse, N, H, d, d, k, scale, dQ, dK, dV, variant, workspace,
+                       workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -8,23 +8,24 @@
 //
 // Mapping: a team of 16 lanes per (query, head), 16 teams per workgroup,
 // with the key slots on lanes (slot = lane + 16 s, NS slots per lane).  Each
-// lane gathers its slots' key rows and forms their scores; 16-lane
-// butterflies give the softmax statistics; each lane then adds its slots'
-// weighted value rows (gathered in the same round trip as the key rows when
-// they fit in 64 registers, else right after) into a D-vector, and a
-// transposed team reduction leaves dimensions tl, tl + 16, ... on lane tl.
+// lane gathers its slots' key rows (D = d_K wide) and forms their scores;
+// 16-lane butterflies give the softmax statistics; each lane then adds its
+// slots' weighted value rows (DV = d_V wide, gathered in the same round trip
+// as the key rows when they fit in 64 registers, else right after) into a
+// DV-vector, and a transposed team reduction leaves dimensions tl, tl + 16,
+// ... on lane tl.
 #include "kmip_device.h"
 #include "kmip_internal.h"
 
 namespace kmip {
 namespace {
 
-template <int D, int NS>
+template <int D, int DV, int NS>
 __global__ __launch_bounds__(256) void attend_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const int32_t* __restrict__ idx, int32_t N, int32_t H, int32_t k, float scale,
     float* __restrict__ out, float* __restrict__ lse) {
-    constexpr bool kKeep = D / 2 * NS <= 64;
+    constexpr bool kKeep = DV / 2 * NS <= 64;
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
     if (qh >= (int64_t)N * H) return;  // whole team exits together
@@ -35,7 +36,7 @@ __global__ __launch_bounds__(256) void attend_kernel(
 
     float z[NS];
     int32_t jj[NS];
-    uint4 vw[kKeep ? NS : 1][D / 8];
+    uint4 vw[kKeep ? NS : 1][DV / 8];
     float zmax = -INFINITY;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
@@ -46,7 +47,7 @@ __global__ __launch_bounds__(256) void attend_kernel(
             const int32_t j = idx[(size_t)qh * k + slot];
             if (j >= 0 && j < N) {
                 jj[s] = j;
-                if constexpr (kKeep) load_row_words<D>(vw[s], V + ((size_t)j * H + h) * D);
+                if constexpr (kKeep) load_row_words<DV>(vw[s], V + ((size_t)j * H + h) * DV);
                 z[s] = scale * dot_row_bf16<D>(q, K + ((size_t)j * H + h) * D);
             }
         }
@@ -63,21 +64,21 @@ __global__ __launch_bounds__(256) void attend_kernel(
     }
     zs = group16_sum(zs);
 
-    float acc[D];
+    float acc[DV];
 #pragma unroll
-    for (int t = 0; t < D; ++t) acc[t] = 0.0f;
+    for (int t = 0; t < DV; ++t) acc[t] = 0.0f;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         if (jj[s] >= 0) {
-            uint4 wv[D / 8];
+            uint4 wv[DV / 8];
             if constexpr (kKeep) {
 #pragma unroll
-                for (int c = 0; c < D / 8; ++c) wv[c] = vw[s][c];
+                for (int c = 0; c < DV / 8; ++c) wv[c] = vw[s][c];
             } else {
-                load_row_words<D>(wv, V + ((size_t)jj[s] * H + h) * D);
+                load_row_words<DV>(wv, V + ((size_t)jj[s] * H + h) * DV);
             }
 #pragma unroll
-            for (int c = 0; c < D / 8; ++c) {
+            for (int c = 0; c < DV / 8; ++c) {
                 const uint32_t ww[4] = {wv[c].x, wv[c].y, wv[c].z, wv[c].w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -87,39 +88,39 @@ __global__ __launch_bounds__(256) void attend_kernel(
             }
         }
     }
-    float o[D / 16];
-    team_sum_transpose<D>(acc, o, tl);
+    float o[DV / 16];
+    team_sum_transpose<DV>(acc, o, tl);
 
     const bool any = zmax != -INFINITY;
     const float inv = any ? 1.0f / zs : 0.0f;
 #pragma unroll
-    for (int u = 0; u < D / 16; ++u) out[(size_t)qh * D + tl + 16 * u] = o[u] * inv;
+    for (int u = 0; u < DV / 16; ++u) out[(size_t)qh * DV + tl + 16 * u] = o[u] * inv;
     if (tl == 0) lse[qh] = any ? zmax + __logf(zs) : -INFINITY;
 }
 
-template <int D>
+template <int D, int DV>
 void launch_attend_d(unsigned blocks, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
                      const uint16_t* v, const int32_t* idx, int32_t N, int32_t H, int32_t k, float scale,
                      float* out, float* lse) {
     const int ns = (k + 15) / 16;
     if (ns <= 1)
-        hipLaunchKernelGGL((attend_kernel<D, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H, k,
-                           scale, out, lse);
+        hipLaunchKernelGGL((attend_kernel<D, DV, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H,
+                           k, scale, out, lse);
     else if (ns <= 2)
-        hipLaunchKernelGGL((attend_kernel<D, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H, k,
-                           scale, out, lse);
+        hipLaunchKernelGGL((attend_kernel<D, DV, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H,
+                           k, scale, out, lse);
     else if (ns <= 4)
-        hipLaunchKernelGGL((attend_kernel<D, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H, k,
-                           scale, out, lse);
+        hipLaunchKernelGGL((attend_kernel<D, DV, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H,
+                           k, scale, out, lse);
     else
-        hipLaunchKernelGGL((attend_kernel<D, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H, k,
-                           scale, out, lse);
+        hipLaunchKernelGGL((attend_kernel<D, DV, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H,
+                           k, scale, out, lse);
 }
 
 }  // namespace
 
 hipError_t launch_attend(const void* Q, const void* K, const void* V, const int32_t* idx,
-                         int32_t N, int32_t H, int32_t d, int32_t k, float scale, float* out,
+                         int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* out,
                          float* lse, hipStream_t stream) {
     const int64_t nqh = (int64_t)N * H;
     if (nqh == 0) return hipSuccess;
@@ -127,20 +128,18 @@ hipError_t launch_attend(const void* Q, const void* K, const void* V, const int3
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
     const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
-    switch (d) {
-        case 16:
-            launch_attend_d<16>(blocks, stream, q, kk, v, idx, N, H, k, scale, out, lse);
-            break;
-        case 32:
-            launch_attend_d<32>(blocks, stream, q, kk, v, idx, N, H, k, scale, out, lse);
-            break;
-        case 64:
-            launch_attend_d<64>(blocks, stream, q, kk, v, idx, N, H, k, scale, out, lse);
-            break;
-        default:
-            return hipErrorInvalidValue;
+#define KMIP_ATTEND_CASE(DD, DVV)                                                              \
+    if (d == DD && dv == DVV) {                                                                \
+        launch_attend_d<DD, DVV>(blocks, stream, q, kk, v, idx, N, H, k, scale, out, lse);    \
+        return hipGetLastError();                                                              \
     }
-    return hipGetLastError();
+#define KMIP_ATTEND_D(DD) KMIP_ATTEND_CASE(DD, 16) KMIP_ATTEND_CASE(DD, 32) KMIP_ATTEND_CASE(DD, 64)
+    KMIP_ATTEND_D(16)
+    KMIP_ATTEND_D(32)
+    KMIP_ATTEND_D(64)
+#undef KMIP_ATTEND_D
+#undef KMIP_ATTEND_CASE
+    return hipErrorInvalidValue;
 }
 
 }  // namespace kmip

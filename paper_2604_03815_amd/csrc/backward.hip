@@ -8,6 +8,8 @@
 //   dQ_i = scale sum_j g_j k_j      (row-local, plain store)
 //   dK_j += scale g_j q_i,  dV_j += p_j dO_i   (scatter)
 //
+// D is the query/key width d_K, DV the value width d_V (dp_j and dV run over
+// DV dimensions, dQ and dK over D).
 // Mapping: a team of 16 lanes per (query, head) as in the aggregate kernel:
 // slots on lanes for the per-pair scalars, dimensions on lanes for the
 // row-vector updates.  Two ways to scatter:
@@ -33,17 +35,18 @@ constexpr int kMaxSlotsPerLane = (128 + 15) / 16;
 // per key in a table of kSlots keys (32 KB of sums).
 constexpr int kAggQueries = 256;
 
-template <int D>
+template <int D, int DV>
 struct AggTable {
-    static constexpr int kSlots = D == 16 ? 256 : D == 32 ? 128 : 64;
+    // the largest power of two with kSlots (D + DV) floats <= 32 KB
+    static constexpr int kSlots = D + DV <= 32 ? 256 : D + DV <= 64 ? 128 : 64;
     static constexpr int kProbes = 8;
 };
 
-// LDS table of one workgroup: key row index and the 2D sums (dK, then dV).
-template <int D>
+// LDS table of one workgroup: key row index and the D + DV sums (dK, then dV).
+template <int D, int DV>
 struct AggLds {
-    int32_t key[AggTable<D>::kSlots];
-    float acc[AggTable<D>::kSlots][2 * D];
+    int32_t key[AggTable<D, DV>::kSlots];
+    float acc[AggTable<D, DV>::kSlots][D + DV];
 };
 
 // Finds or claims the table slot of key row js; -1 when all probes are taken
@@ -52,11 +55,11 @@ struct AggLds {
 // empty slot is claimed with a compare-and-swap.  Every lane of a team runs
 // the same probes, and a claim by one of them reads back as the key itself
 // for the others.
-template <int D>
-__device__ __forceinline__ int agg_slot(AggLds<D>* t, int32_t js) {
-    constexpr int C = AggTable<D>::kSlots;
+template <int D, int DV>
+__device__ __forceinline__ int agg_slot(AggLds<D, DV>* t, int32_t js) {
+    constexpr int C = AggTable<D, DV>::kSlots;
     const uint32_t hsh = ((uint32_t)js * 0x9E3779B1u) >> (32 - __builtin_ctz(C));
-    for (int p = 0; p < AggTable<D>::kProbes; ++p) {
+    for (int p = 0; p < AggTable<D, DV>::kProbes; ++p) {
         const int ts = (int)((hsh + p) & (C - 1));
         const int32_t cur = __hip_atomic_load(&t->key[ts], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         if (cur == js) return ts;
@@ -74,16 +77,17 @@ __device__ __forceinline__ int agg_slot(AggLds<D>* t, int32_t js) {
 // lanes.  All 16 pairs' key elements for dQ are loaded before any is used.
 // With tab != nullptr the dK/dV sums go to the workgroup's table when the
 // key has a slot there.
-template <int D>
+template <int D, int DV>
 __device__ __forceinline__ void bwd_query(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
     int64_t qh, int h, int tl, int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ,
-    float* __restrict__ dK, float* __restrict__ dV, AggLds<D>* tab) {
+    float* __restrict__ dK, float* __restrict__ dV, AggLds<D, DV>* tab) {
     constexpr int U = D / 16;
-    float q[D], g[D];
+    constexpr int UV = DV / 16;
+    float q[D], g[DV];
     load_row_f32<D>(q, Q + (size_t)qh * D);
-    load_row_f32<D>(g, dO + (size_t)qh * D);
+    load_row_f32<DV>(g, dO + (size_t)qh * DV);
     const float l = lse[qh];
 
     const int ns = (k + 15) >> 4;
@@ -102,25 +106,26 @@ __device__ __forceinline__ void bwd_query(
                 jj[s] = j;
                 const float z = scale * dot_row_bf16<D>(q, K + ((size_t)j * H + h) * D);
                 p[s] = __expf(z - l);
-                dp[s] = dot_row_bf16<D>(g, V + ((size_t)j * H + h) * D);
+                dp[s] = dot_row_bf16<DV>(g, V + ((size_t)j * H + h) * DV);
             }
         }
         dsum = fmaf(p[s], dp[s], dsum);
     }
     dsum = group16_sum(dsum);
 
-    float qd[U], gd[U], dq[U];
+    float qd[U], gd[UV], dq[U];
     {
         // this lane's dimensions of q_i and dO_i, read straight from memory so
         // that no runtime register indexing is needed
         const uint16_t* qrow = Q + (size_t)qh * D + tl;
-        const uint16_t* grow = dO + (size_t)qh * D + tl;
+        const uint16_t* grow = dO + (size_t)qh * DV + tl;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             qd[u] = bf16_bits_to_f32(qrow[16 * u]);
-            gd[u] = bf16_bits_to_f32(grow[16 * u]);
             dq[u] = 0.0f;
         }
+#pragma unroll
+        for (int u = 0; u < UV; ++u) gd[u] = bf16_bits_to_f32(grow[16 * u]);
     }
 #pragma unroll
     for (int s = 0; s < kMaxSlotsPerLane; ++s) {
@@ -143,20 +148,19 @@ __device__ __forceinline__ void bwd_query(
 #pragma unroll
             for (int src = 0; src < 16; ++src) {
                 if (js[src] < 0) continue;
-                const int ts = tab != nullptr ? agg_slot<D>(tab, js[src]) : -1;
+                const int ts = tab != nullptr ? agg_slot<D, DV>(tab, js[src]) : -1;
                 if (ts >= 0) {
 #pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        atomicAdd(&tab->acc[ts][16 * u + tl], scale * gsv[src] * qd[u]);
-                        atomicAdd(&tab->acc[ts][D + 16 * u + tl], ps[src] * gd[u]);
-                    }
+                    for (int u = 0; u < U; ++u) atomicAdd(&tab->acc[ts][16 * u + tl], scale * gsv[src] * qd[u]);
+#pragma unroll
+                    for (int u = 0; u < UV; ++u) atomicAdd(&tab->acc[ts][D + 16 * u + tl], ps[src] * gd[u]);
                 } else {
                     const size_t base = ((size_t)js[src] * H + h) * D + tl;
+                    const size_t basev = ((size_t)js[src] * H + h) * DV + tl;
 #pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        atomicAdd(dK + base + 16 * u, scale * gsv[src] * qd[u]);
-                        atomicAdd(dV + base + 16 * u, ps[src] * gd[u]);
-                    }
+                    for (int u = 0; u < U; ++u) atomicAdd(dK + base + 16 * u, scale * gsv[src] * qd[u]);
+#pragma unroll
+                    for (int u = 0; u < UV; ++u) atomicAdd(dV + basev + 16 * u, ps[src] * gd[u]);
                 }
             }
 #pragma unroll
@@ -170,7 +174,7 @@ __device__ __forceinline__ void bwd_query(
 }
 
 // Per-pair scatter: one team per (query, head), 16 per workgroup.
-template <int D>
+template <int D, int DV>
 __global__ __launch_bounds__(256) void bwd_atomic_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
@@ -179,39 +183,42 @@ __global__ __launch_bounds__(256) void bwd_atomic_kernel(
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
     if (qh >= (int64_t)N * H) return;  // whole team exits together
-    bwd_query<D>(Q, K, V, dO, idx, lse, qh, (int)(qh % H), tl, N, H, k, scale, dQ, dK, dV, nullptr);
+    bwd_query<D, DV>(Q, K, V, dO, idx, lse, qh, (int)(qh % H), tl, N, H, k, scale, dQ, dK, dV, nullptr);
 }
 
 // Key-aggregated scatter: one workgroup per kAggQueries positions of head
 // blockIdx.y in the grouped order.
-template <int D>
+template <int D, int DV>
 __global__ __launch_bounds__(256) void bwd_agg_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
     const int32_t* __restrict__ perm, int32_t N, int32_t H, int32_t k, float scale,
     float* __restrict__ dQ, float* __restrict__ dK, float* __restrict__ dV) {
-    constexpr int C = AggTable<D>::kSlots;
-    __shared__ AggLds<D> tab;
+    constexpr int C = AggTable<D, DV>::kSlots;
+    constexpr int W = D + DV;
+    __shared__ AggLds<D, DV> tab;
     const int tl = threadIdx.x & 15;
     const int team = threadIdx.x >> 4;
     const int h = blockIdx.y;
     for (int e = threadIdx.x; e < C; e += 256) tab.key[e] = -1;
-    for (int e = threadIdx.x; e < C * 2 * D; e += 256) (&tab.acc[0][0])[e] = 0.0f;
+    for (int e = threadIdx.x; e < C * W; e += 256) (&tab.acc[0][0])[e] = 0.0f;
     __syncthreads();
     for (int round = 0; round < kAggQueries / 16; ++round) {
         const int64_t pos = (int64_t)blockIdx.x * kAggQueries + round * 16 + team;
         if (pos >= N) break;  // positions grow with round: the team is done
         const int64_t qh = (int64_t)perm[(size_t)h * N + pos] * H + h;
-        bwd_query<D>(Q, K, V, dO, idx, lse, qh, h, tl, N, H, k, scale, dQ, dK, dV, &tab);
+        bwd_query<D, DV>(Q, K, V, dO, idx, lse, qh, h, tl, N, H, k, scale, dQ, dK, dV, &tab);
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < C * 2 * D; e += 256) {
-        const int s = e / (2 * D), c = e - s * 2 * D;
+    for (int e = threadIdx.x; e < C * W; e += 256) {
+        const int s = e / W, c = e - s * W;
         const int32_t j = tab.key[s];
         const float v = (&tab.acc[0][0])[e];
         if (j >= 0 && v != 0.0f) {
-            float* dst = c < D ? dK : dV;
-            atomicAdd(dst + ((size_t)j * H + h) * D + (c < D ? c : c - D), v);
+            if (c < D)
+                atomicAdd(dK + ((size_t)j * H + h) * D + c, v);
+            else
+                atomicAdd(dV + ((size_t)j * H + h) * DV + (c - D), v);
         }
     }
 }
@@ -239,36 +246,32 @@ hipError_t launch_fill_zero(float* p, size_t n, hipStream_t stream) {
 
 hipError_t launch_bwd_atomic(const void* Q, const void* K, const void* V, const void* dO,
                              const int32_t* idx, const float* lse, int32_t N, int32_t H,
-                             int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
+                             int32_t d, int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV,
                              hipStream_t stream) {
     const int64_t nqh = (int64_t)N * H;
     if (nqh == 0) return hipSuccess;
     hipError_t e = launch_fill_zero(dK, (size_t)nqh * d, stream);
     if (e != hipSuccess) return e;
-    e = launch_fill_zero(dV, (size_t)nqh * d, stream);
+    e = launch_fill_zero(dV, (size_t)nqh * dv, stream);
     if (e != hipSuccess) return e;
     const unsigned blocks = (unsigned)((nqh + 15) / 16);
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
     const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
     const uint16_t* g = reinterpret_cast<const uint16_t*>(dO);
-    switch (d) {
-        case 16:
-            hipLaunchKernelGGL(bwd_atomic_kernel<16>, dim3(blocks), dim3(256), 0, stream, q, kk, v,
-                               g, idx, lse, N, H, k, scale, dQ, dK, dV);
-            break;
-        case 32:
-            hipLaunchKernelGGL(bwd_atomic_kernel<32>, dim3(blocks), dim3(256), 0, stream, q, kk, v,
-                               g, idx, lse, N, H, k, scale, dQ, dK, dV);
-            break;
-        case 64:
-            hipLaunchKernelGGL(bwd_atomic_kernel<64>, dim3(blocks), dim3(256), 0, stream, q, kk, v,
-                               g, idx, lse, N, H, k, scale, dQ, dK, dV);
-            break;
-        default:
-            return hipErrorInvalidValue;
+#define KMIP_BWD_ATOMIC_CASE(DD, DVV)                                                                  \
+    if (d == DD && dv == DVV) {                                                                        \
+        hipLaunchKernelGGL((bwd_atomic_kernel<DD, DVV>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, \
+                           idx, lse, N, H, k, scale, dQ, dK, dV);                                      \
+        return hipGetLastError();                                                                      \
     }
-    return hipGetLastError();
+#define KMIP_BWD_ATOMIC_D(DD) KMIP_BWD_ATOMIC_CASE(DD, 16) KMIP_BWD_ATOMIC_CASE(DD, 32) KMIP_BWD_ATOMIC_CASE(DD, 64)
+    KMIP_BWD_ATOMIC_D(16)
+    KMIP_BWD_ATOMIC_D(32)
+    KMIP_BWD_ATOMIC_D(64)
+#undef KMIP_BWD_ATOMIC_D
+#undef KMIP_BWD_ATOMIC_CASE
+    return hipErrorInvalidValue;
 }
 
 }  // namespace kmip
@@ -279,7 +282,7 @@ size_t bwd_agg_workspace_bytes(int32_t N, int32_t H, int32_t d) { return group_w
 
 hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const void* dO,
                           const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                          int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
+                          int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
                           hipStream_t stream) {
     const int64_t nqh = (int64_t)N * H;
     if (nqh == 0) return hipSuccess;
@@ -287,29 +290,25 @@ hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const voi
     hipError_t e = launch_group_queries(Q, N, H, d, ws, &groups, stream);
     if (e != hipSuccess) return e;
     if ((e = launch_fill_zero(dK, (size_t)nqh * d, stream)) != hipSuccess) return e;
-    if ((e = launch_fill_zero(dV, (size_t)nqh * d, stream)) != hipSuccess) return e;
+    if ((e = launch_fill_zero(dV, (size_t)nqh * dv, stream)) != hipSuccess) return e;
     const dim3 grid((unsigned)((N + kAggQueries - 1) / kAggQueries), (unsigned)H);
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
     const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
     const uint16_t* g = reinterpret_cast<const uint16_t*>(dO);
-    switch (d) {
-        case 16:
-            hipLaunchKernelGGL(bwd_agg_kernel<16>, grid, dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                               groups.perm, N, H, k, scale, dQ, dK, dV);
-            break;
-        case 32:
-            hipLaunchKernelGGL(bwd_agg_kernel<32>, grid, dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                               groups.perm, N, H, k, scale, dQ, dK, dV);
-            break;
-        case 64:
-            hipLaunchKernelGGL(bwd_agg_kernel<64>, grid, dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                               groups.perm, N, H, k, scale, dQ, dK, dV);
-            break;
-        default:
-            return hipErrorInvalidValue;
+#define KMIP_BWD_AGG_CASE(DD, DVV)                                                                       \
+    if (d == DD && dv == DVV) {                                                                          \
+        hipLaunchKernelGGL((bwd_agg_kernel<DD, DVV>), grid, dim3(256), 0, stream, q, kk, v, g, idx, lse, \
+                           groups.perm, N, H, k, scale, dQ, dK, dV);                                     \
+        return hipGetLastError();                                                                        \
     }
-    return hipGetLastError();
+#define KMIP_BWD_AGG_D(DD) KMIP_BWD_AGG_CASE(DD, 16) KMIP_BWD_AGG_CASE(DD, 32) KMIP_BWD_AGG_CASE(DD, 64)
+    KMIP_BWD_AGG_D(16)
+    KMIP_BWD_AGG_D(32)
+    KMIP_BWD_AGG_D(64)
+#undef KMIP_BWD_AGG_D
+#undef KMIP_BWD_AGG_CASE
+    return hipErrorInvalidValue;
 }
 
 }  // namespace kmip

@@ -34,10 +34,11 @@ constexpr int kChunk = 1024;         // sorted pairs per wave in the reduction
 
 // 1. Per (query, head), a team of 16 lanes with the slots on lanes, NS
 // slots per lane (k <= 16 NS): p, dp, D, g of each selected pair, dQ_i, and
-// the head-major interleaved copy of q_i and dO_i.  Slot tl + 16 s of query-
-// head qh leaves its key index in jj[s] (-1: none) and its coefficients
-// a = scale g, p in ca[s], cp[s].
-template <int D, int NS>
+// (QGt != nullptr, value width DV = D only) the head-major interleaved copy
+// of q_i and dO_i.  D is the query/key width, DV the value width (dp_j runs
+// over it).  Slot tl + 16 s of query-head qh leaves its key index in jj[s]
+// (-1: none) and its coefficients a = scale g, p in ca[s], cp[s].
+template <int D, int DV, int NS>
 __device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                                          const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
                                          const int32_t* __restrict__ idx, const float* __restrict__ lse,
@@ -48,16 +49,16 @@ __device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const u
     // lane; otherwise read again (from cache)
     constexpr bool kKeep = D / 2 * NS <= 64;
     const int h = (int)(qh % H);
-    if (QGt != nullptr && tl < D / 4) {
+    if (DV == D && QGt != nullptr && tl < D / 4) {
         // head-major interleaved copy [H][N][2d]: row h*N + i holds q_i then
         // dO_i of head h, so the reduction gathers both with one load
         const size_t ht = ((size_t)h * N + (size_t)(qh / H)) * (2 * D);
         const uint16_t* src = tl < D / 8 ? Q + (size_t)qh * D : dO + (size_t)qh * D;
         reinterpret_cast<uint4*>(QGt + ht)[tl] = reinterpret_cast<const uint4*>(src)[tl & (D / 8 - 1)];
     }
-    float q[D], g[D];
+    float q[D], g[DV];
     load_row_f32<D>(q, Q + (size_t)qh * D);
-    load_row_f32<D>(g, dO + (size_t)qh * D);
+    load_row_f32<DV>(g, dO + (size_t)qh * DV);
     const float l = lse[qh];
     float p[NS], dp[NS];
     uint4 kw[kKeep ? NS : 1][D / 8];
@@ -82,7 +83,7 @@ __device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const u
                 }
                 const float z = scale * dot_words_bf16<D>(q, w);
                 p[s] = __expf(z - l);
-                dp[s] = dot_row_bf16<D>(g, V + ((size_t)j * H + h) * D);
+                dp[s] = dot_row_bf16<DV>(g, V + ((size_t)j * H + h) * DV);
             }
         }
         dsum = fmaf(p[s], dp[s], dsum);
@@ -123,8 +124,8 @@ __device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const u
     for (int u = 0; u < D / 16; ++u) dQ[(size_t)qh * D + 16 * u + tl] = scale * out[u];
 }
 
-// The coefficients of every pair, in pair order (variant 3).
-template <int D, int NS>
+// The coefficients of every pair, in pair order (the segmented variant).
+template <int D, int DV, int NS>
 __global__ __launch_bounds__(256) void csr_coef_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
@@ -135,7 +136,7 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
     if (qh >= (int64_t)N * H) return;  // whole team exits together
     int32_t jj[NS];
     float ca[NS], cp[NS];
-    coef_one<D, NS>(Q, K, V, dO, idx, lse, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
+    coef_one<D, DV, NS>(Q, K, V, dO, idx, lse, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         const int slot = tl + 16 * s;
@@ -143,24 +144,24 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
     }
 }
 
-// Launches csr_coef_kernel<D, NS> with NS the smallest power of two >= k/16.
-template <int D>
+// Launches csr_coef_kernel<D, DV, NS> with NS the smallest power of two >= k/16.
+template <int D, int DV>
 void launch_coef(unsigned blocks, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
                  const uint16_t* v, const uint16_t* g, const int32_t* idx, const float* lse, int32_t N,
                  int32_t H, int32_t k, float scale, float* dQ, float2* coef, uint16_t* qg) {
     const int ns = (k + 15) / 16;
     if (ns <= 1)
-        hipLaunchKernelGGL((csr_coef_kernel<D, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse, N,
-                           H, k, scale, dQ, coef, qg);
+        hipLaunchKernelGGL((csr_coef_kernel<D, DV, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                           N, H, k, scale, dQ, coef, qg);
     else if (ns <= 2)
-        hipLaunchKernelGGL((csr_coef_kernel<D, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse, N,
-                           H, k, scale, dQ, coef, qg);
+        hipLaunchKernelGGL((csr_coef_kernel<D, DV, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                           N, H, k, scale, dQ, coef, qg);
     else if (ns <= 4)
-        hipLaunchKernelGGL((csr_coef_kernel<D, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse, N,
-                           H, k, scale, dQ, coef, qg);
+        hipLaunchKernelGGL((csr_coef_kernel<D, DV, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                           N, H, k, scale, dQ, coef, qg);
     else
-        hipLaunchKernelGGL((csr_coef_kernel<D, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse, N,
-                           H, k, scale, dQ, coef, qg);
+        hipLaunchKernelGGL((csr_coef_kernel<D, DV, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
+                           N, H, k, scale, dQ, coef, qg);
 }
 
 // Key row of slot s of query-head qh, or -1 (padding).
@@ -313,28 +314,35 @@ __global__ __launch_bounds__(kScanBlock) void scan_apply_kernel(int32_t* __restr
 
 // 5.  A wave per chunk of kChunk sorted pairs, four teams per wave, each team
 // a contiguous quarter of the chunk.  `total` = number of sorted pairs.
-template <int D>
+template <int D, int DV>
 __global__ __launch_bounds__(256) void csr_reduce_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ dO,
     const PairRecord* __restrict__ rec, const int32_t* __restrict__ total,
     float* __restrict__ dK, float* __restrict__ dV) {
     constexpr int U = D / 16;
+    constexpr int UV = DV / 16;
     constexpr int kTeamSpan = kChunk / 4;
     const int tl = threadIdx.x & 15;
     const int team = (int)(blockIdx.x * 16 + (threadIdx.x >> 4));
     const int64_t e0 = (int64_t)team * kTeamSpan;
     const int64_t e1 = min((int64_t)*total, e0 + kTeamSpan);
     int32_t cur = -1;
-    float ak[U], av[U];
+    float ak[U], av[UV];
 #pragma unroll
-    for (int u = 0; u < U; ++u) ak[u] = av[u] = 0.0f;
+    for (int u = 0; u < U; ++u) ak[u] = 0.0f;
+#pragma unroll
+    for (int u = 0; u < UV; ++u) av[u] = 0.0f;
     auto flush = [&]() {
         if (cur >= 0) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 atomicAdd(dK + (size_t)cur * D + 16 * u + tl, ak[u]);
-                atomicAdd(dV + (size_t)cur * D + 16 * u + tl, av[u]);
-                ak[u] = av[u] = 0.0f;
+                ak[u] = 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < UV; ++u) {
+                atomicAdd(dV + (size_t)cur * DV + 16 * u + tl, av[u]);
+                av[u] = 0.0f;
             }
         }
     };
@@ -355,11 +363,11 @@ __global__ __launch_bounds__(256) void csr_reduce_kernel(
                 cur = rt;
             }
             const size_t qrow = (size_t)qt * D + tl;
+            const size_t grow = (size_t)qt * DV + tl;
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                ak[u] = fmaf(at, bf16_bits_to_f32(Q[qrow + 16 * u]), ak[u]);
-                av[u] = fmaf(pt, bf16_bits_to_f32(dO[qrow + 16 * u]), av[u]);
-            }
+            for (int u = 0; u < U; ++u) ak[u] = fmaf(at, bf16_bits_to_f32(Q[qrow + 16 * u]), ak[u]);
+#pragma unroll
+            for (int u = 0; u < UV; ++u) av[u] = fmaf(pt, bf16_bits_to_f32(dO[grow + 16 * u]), av[u]);
         }
     }
     flush();
@@ -577,7 +585,7 @@ __global__ __launch_bounds__(256) void coef_split_kernel(
         float ca[NS], cp[NS];
 #pragma unroll
         for (int s2 = 0; s2 < NS; ++s2) jj[s2] = -1;
-        if (qh < nh) coef_one<D, NS>(Q, K, V, dO, idx, lse, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
+        if (qh < nh) coef_one<D, D, NS>(Q, K, V, dO, idx, lse, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
         const int32_t h = (int32_t)(qh % H), i = (int32_t)(qh / H);
 #pragma unroll
         for (int s2 = 0; s2 < NS; ++s2) {
@@ -1061,7 +1069,7 @@ size_t bwd_csr_workspace_bytes(int32_t N, int32_t H, int32_t k) {
 
 hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const void* dO,
                           const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                          int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
+                          int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
                           hipStream_t stream) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };
     const int64_t nh = (int64_t)N * H;
@@ -1085,21 +1093,21 @@ hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const voi
     // counts are zeroed with the float fill (same bits); n padded to 4
     if ((e = launch_fill_zero(reinterpret_cast<float*>(cnt), ((size_t)nh + 3) / 4 * 4, stream)) != hipSuccess) return e;
     if ((e = launch_fill_zero(dK, (size_t)nh * d, stream)) != hipSuccess) return e;
-    if ((e = launch_fill_zero(dV, (size_t)nh * d, stream)) != hipSuccess) return e;
+    if ((e = launch_fill_zero(dV, (size_t)nh * dv, stream)) != hipSuccess) return e;
     const unsigned team_blocks = (unsigned)((nh + 15) / 16);
-    switch (d) {
-        case 16:
-            launch_coef<16>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, nullptr);
-            break;
-        case 32:
-            launch_coef<32>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, nullptr);
-            break;
-        case 64:
-            launch_coef<64>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, nullptr);
-            break;
-        default:
-            return hipErrorInvalidValue;
+    bool launched = false;
+#define KMIP_CSR_COEF(DD, DVV)                                                                          \
+    if (d == DD && dv == DVV) {                                                                         \
+        launch_coef<DD, DVV>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, nullptr); \
+        launched = true;                                                                                \
     }
+#define KMIP_CSR_COEF_D(DD) KMIP_CSR_COEF(DD, 16) KMIP_CSR_COEF(DD, 32) KMIP_CSR_COEF(DD, 64)
+    KMIP_CSR_COEF_D(16)
+    KMIP_CSR_COEF_D(32)
+    KMIP_CSR_COEF_D(64)
+#undef KMIP_CSR_COEF_D
+#undef KMIP_CSR_COEF
+    if (!launched) return hipErrorInvalidValue;
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned qh_blocks = (unsigned)((nh + 255) / 256);
     hipLaunchKernelGGL(csr_count_kernel<false>, dim3(qh_blocks), dim3(256), 0, stream, idx, coef, N, H,
@@ -1120,20 +1128,16 @@ hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const voi
     // every pair slot, teams past the total exit at once
     const unsigned red_blocks = (unsigned)((pairs + kChunk * 4 - 1) / (kChunk * 4));
     const int32_t* total = sums + nb;
-    switch (d) {
-        case 16:
-            hipLaunchKernelGGL(csr_reduce_kernel<16>, dim3(red_blocks), dim3(256), 0, stream, q, g, rec,
-                               total, dK, dV);
-            break;
-        case 32:
-            hipLaunchKernelGGL(csr_reduce_kernel<32>, dim3(red_blocks), dim3(256), 0, stream, q, g, rec,
-                               total, dK, dV);
-            break;
-        default:
-            hipLaunchKernelGGL(csr_reduce_kernel<64>, dim3(red_blocks), dim3(256), 0, stream, q, g, rec,
-                               total, dK, dV);
-            break;
-    }
+#define KMIP_CSR_REDUCE(DD, DVV)                                                                        \
+    if (d == DD && dv == DVV)                                                                           \
+        hipLaunchKernelGGL((csr_reduce_kernel<DD, DVV>), dim3(red_blocks), dim3(256), 0, stream, q, g, rec, \
+                           total, dK, dV);
+#define KMIP_CSR_REDUCE_D(DD) KMIP_CSR_REDUCE(DD, 16) KMIP_CSR_REDUCE(DD, 32) KMIP_CSR_REDUCE(DD, 64)
+    KMIP_CSR_REDUCE_D(16)
+    KMIP_CSR_REDUCE_D(32)
+    KMIP_CSR_REDUCE_D(64)
+#undef KMIP_CSR_REDUCE_D
+#undef KMIP_CSR_REDUCE
     return hipGetLastError();
 }
 

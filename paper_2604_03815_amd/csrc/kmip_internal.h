@@ -114,20 +114,24 @@ size_t group_workspace_bytes(int32_t N, int32_t H, int32_t d);
 hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, void* ws,
                                 QueryGroups* out, hipStream_t stream);
 
+// Gather-softmax-aggregate: Q, K [N,H,d] (d = d_K), V and out [N,H,dv]
+// (dv = d_V), each in {16, 32, 64}.
 hipError_t launch_attend(const void* Q, const void* K, const void* V, const int32_t* idx,
-                         int32_t N, int32_t H, int32_t d, int32_t k, float scale, float* out,
+                         int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* out,
                          float* lse, hipStream_t stream);
 
+// The backward launchers take the query/key width d and the value width dv
+// (each in {16, 32, 64}); the bucketed one needs dv == d.
 hipError_t launch_bwd_atomic(const void* Q, const void* K, const void* V, const void* dO,
                              const int32_t* idx, const float* lse, int32_t N, int32_t H,
-                             int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
+                             int32_t d, int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV,
                              hipStream_t stream);
 
 // Backward with key-aggregated scatter; ws holds bwd_agg_workspace_bytes().
 size_t bwd_agg_workspace_bytes(int32_t N, int32_t H, int32_t d);
 hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const void* dO,
                           const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                          int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
+                          int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
                           hipStream_t stream);
 
 // Backward with a key-sorted segmented reduction (backward_csr.hip); ws
@@ -135,7 +139,7 @@ hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const voi
 size_t bwd_csr_workspace_bytes(int32_t N, int32_t H, int32_t k);
 hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const void* dO,
                           const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                          int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
+                          int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
                           hipStream_t stream);
 
 // Backward with pairs bucketed by blocks of key rows and summed in LDS

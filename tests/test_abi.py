@@ -219,3 +219,22 @@ def test_noalloc_validates_before_launch(lib):
     assert lib.kmip_fwd_noalloc(P(258), FAKE, FAKE, 64, 1, 16, 4, f(1.0), FAKE, FAKE, FAKE, None) == 1
     # nothing to do
     assert lib.kmip_fwd_noalloc(None, None, None, 0, 1, 16, 4, f(1.0), None, None, None, None) == 0
+
+
+def test_value_width_entry_points_validate(lib):
+    f = ctypes.c_float
+    # value widths outside {16, 32, 64}
+    assert lib.kmip_attend_dv(FAKE, FAKE, FAKE, 64, 1, 16, 48, 4, f(1.0), FAKE, FAKE, FAKE, None) == 2
+    assert lib.kmip_fwd_dv(FAKE, FAKE, FAKE, None, 1, 64, 1, 16, 8, 4, f(1.0), FAKE, FAKE, FAKE,
+                           FAKE, 1 << 20, None) == 2
+    args = [FAKE] * 6 + [64, 1, 32, 16, 4, f(1.0), FAKE, FAKE, FAKE]
+    # the bucketed variant needs d_V == d_K; the others take any pair
+    assert lib.kmip_bwd_dv(*args, _lib.BWD_BUCKETED, FAKE, 1 << 30, None) == 2
+    assert lib.kmip_bwd_dv_workspace_size(64, 1, 32, 16, 4, _lib.BWD_BUCKETED) == 0
+    assert lib.kmip_bwd_dv_workspace_size(64, 1, 32, 16, 4, _lib.BWD_AUTO) == \
+        lib.kmip_bwd_dv_workspace_size(64, 1, 32, 16, 4, _lib.BWD_SEGMENTED) > 0
+    assert lib.kmip_bwd_dv(*args, _lib.BWD_SEGMENTED, None, 0, None) == 3
+    # d_V = d_K: the plain entry points are this case
+    for v in (0, 1, 2, 3, 4):
+        assert lib.kmip_bwd_dv_workspace_size(5000, 2, 32, 32, 16, v) == lib.kmip_bwd_workspace_size(5000, 2, 32, 16, v)
+    assert lib.kmip_attend_dv(FAKE, FAKE, FAKE, 64, 1, 16, 32, 4, f(-1.0), FAKE, FAKE, FAKE, None) == 1

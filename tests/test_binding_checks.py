@@ -79,9 +79,27 @@ def test_topk_and_fwd_reject_mismatch():
     with pytest.raises(ValueError):
         kmip.topk(a["q"], a["k_"], k, idx=i32(N, H, k + 1))
     with pytest.raises(ValueError):
-        kmip.fwd(a["q"], a["k_"], bf(N, H, d // 2), k, 0.25)
+        kmip.fwd(a["q"], a["k_"], bf(N, H + 1, d), k, 0.25)
     with pytest.raises(ValueError):
         kmip.fwd(bf(N, H * d), a["k_"], a["v"], k, 0.25)
+
+
+def test_value_width_of_its_own():
+    # V (and dOut, out, dV) may be wider or narrower than Q and K: only the
+    # device check is left to fail on host tensors; a dOut or dV whose width
+    # differs from V's is a mismatch
+    a = good()
+    wide = bf(N, H, 2 * d)
+    with pytest.raises(TypeError, match="CUDA"):
+        kmip.attend(a["q"], a["k_"], wide, a["idx"], 0.25)
+    with pytest.raises(TypeError, match="CUDA"):
+        kmip.bwd(a["q"], a["k_"], wide, bf(N, H, 2 * d), a["idx"], a["lse"], 0.25)
+    with pytest.raises(ValueError):
+        kmip.bwd(a["q"], a["k_"], wide, a["dout"], a["idx"], a["lse"], 0.25)
+    with pytest.raises(ValueError):
+        kmip.bwd(a["q"], a["k_"], wide, bf(N, H, 2 * d), a["idx"], a["lse"], 0.25, dv=f32(N, H, d))
+    with pytest.raises(ValueError):
+        kmip.attend(a["q"], a["k_"], wide, a["idx"], 0.25, out=f32(N, H, d))
 
 
 def test_matching_host_tensors_are_refused_as_not_on_the_gpu():

@@ -59,7 +59,7 @@ def _check_all(w, res, sample=None):
     print(f"[sets] {w.name}: {exact} exact by scores, {strict} well-separated, {loose} near-tied "
           f"query-heads of {w.N * w.H if sel is None else len(sel)} checked", flush=True)
     ref_out, ref_lse = oracle.attend(Qd, Kd, Vd, res["idx"], w.scale)
-    allclose_report("out", res["out"].reshape(-1, w.d), ref_out)
+    allclose_report("out", res["out"].reshape(-1, Vd.shape[2]), ref_out)
     allclose_report("lse", res["lse"].reshape(-1), ref_lse)
     if "dq" in res:
         rq, rk, rv = oracle.backward(Qd, Kd, Vd, dOd, res["idx"], w.scale)
@@ -396,6 +396,40 @@ def test_autograd_wrapper_matches_backward_and_oracle():
     rq, rk, rv = oracle.backward(Qd, Kd, Vd, dOd, idx.cpu().numpy(), w.scale)
     for name, got, ref in (("dQ", q.grad, rq), ("dK", k.grad, rk), ("dV", v.grad, rv)):
         allclose_report(name, got.float().cpu().numpy(), ref)
+
+
+# Value rows of another width than the query/key rows (Section 3.1: W_V maps
+# to d_V dimensions).  The index sets depend on Q and K only; out, lse and
+# the gradients are compared with the oracle on every query-head, for every
+# backward variant that takes d_V != d_K (the bucketed one needs them equal;
+# the library's choice then is the segmented one).
+VALUE_WIDTH = [
+    # (N, H, d, dv, k, sizes)
+    (3000, 2, 16, 32, 16, [1000, 7, 1993]),
+    (2500, 3, 32, 64, 32, None),
+    (1800, 2, 64, 16, 24, [900, 0, 900]),
+    (2100, 1, 32, 16, 128, [2100]),
+    (20000, 2, 16, 64, 32, None),       # one graph above the grouping size
+]
+
+
+@pytest.mark.parametrize("case", VALUE_WIDTH, ids=lambda c: "N%d_H%d_d%d_dv%d_k%d" % c[:5])
+def test_value_width_full(case):
+    N, H, d, dv, k, sizes = case
+    w = workloads.iid(N, H, d, k, seed=N + dv, sizes=sizes, dv=dv)
+    for variant in (0, 1, 2, 4):
+        res = _run(w, variant=variant)
+        assert res["out"].shape == (N, H, dv) and res["dv"].shape == (N, H, dv) and res["dk"].shape == (N, H, d)
+        _check_all(w, res)
+
+
+def test_value_width_bucketed_refused():
+    w = workloads.iid(500, 1, 16, 8, seed=1, dv=32)
+    q, k, v, g = _dev(w.q), _dev(w.kk), _dev(w.v), _dev(w.dout)
+    out, idx, lse = kmip.fwd(q, k, v, w.k, w.scale)
+    with pytest.raises(kmip.KmipError) as e:
+        kmip.bwd(q, k, v, g, idx, lse, w.scale, variant=3)
+    assert e.value.status == 2
 
 
 def test_stale_workspace_does_not_change_selection():

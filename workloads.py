@@ -101,10 +101,11 @@ def _normal(rng, shape, std=1.0):
 
 def iid(N: int, H: int, d: int, k: int, seed: int = 0, sizes=None,
         scale: Optional[float] = None, backward: bool = True, std: float = 1.0,
-        name: str = "iid") -> Workload:
+        name: str = "iid", dv: Optional[int] = None) -> Workload:
     """Q, K, V, dOut i.i.d. N(0, std^2) rounded to bf16.
 
     ``sizes`` (list of graph sizes) gives a block-diagonal batch; None means one graph.
+    ``dv`` is the width of V and dOut (default d).
     """
     rng = np.random.default_rng(seed)
     offsets = None
@@ -112,10 +113,11 @@ def iid(N: int, H: int, d: int, k: int, seed: int = 0, sizes=None,
         sizes = np.asarray(sizes, dtype=np.int64)
         assert int(sizes.sum()) == N
         offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    dv = d if dv is None else dv
     q = bf16_round(_normal(rng, (N, H, d), std))
     kk = bf16_round(_normal(rng, (N, H, d), std))
-    v = bf16_round(_normal(rng, (N, H, d)))
-    dout = bf16_round(_normal(rng, (N, H, d))) if backward else None
+    v = bf16_round(_normal(rng, (N, H, dv)))
+    dout = bf16_round(_normal(rng, (N, H, dv))) if backward else None
     return Workload(name, N, H, d, k, scale if scale is not None else 1.0 / math.sqrt(d),
                     offsets, q, kk, v, dout, backward)
 
