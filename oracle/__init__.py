@@ -46,9 +46,9 @@ def _load():
         P = ctypes.c_void_p
         i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
         lib.oracle_topk.argtypes = [P, P, P, i32, i64, i32, i32, i32, i64, P, P, P, P]
-        lib.oracle_attend.argtypes = [P, P, P, i64, i32, i32, i32, i32, f64, i64, P, P, P, P]
+        lib.oracle_attend.argtypes = [P, P, P, i64, i32, i32, i32, i32, f64, i64, P, P, P, f64, P, P]
         lib.oracle_forward.argtypes = [P, P, P, P, i32, i64, i32, i32, i32, i32, f64, P, P, P]
-        lib.oracle_backward.argtypes = [P, P, P, P, i64, i32, i32, i32, i32, f64, P, P, P, P]
+        lib.oracle_backward.argtypes = [P, P, P, P, i64, i32, i32, i32, i32, f64, P, P, f64, P, P, P]
         lib.oracle_check_set.argtypes = [P, P, P, i32, i64, i32, i32, i32, i64, P, P, P, P, P]
         lib.oracle_threads.argtypes = []
         for f in ("oracle_threads", "oracle_topk", "oracle_attend", "oracle_forward", "oracle_backward",
@@ -127,8 +127,23 @@ def _key_shape(K, N, H, d):
         raise ValueError("K must have the shape of Q")
 
 
-def attend(Q, K, V, idx, scale: float, sel=None):
-    """Softmax + aggregate on a given index set.  Returns (out [nsel,d_V], lse [nsel])."""
+def _keep(keep, n, k, drop_rate):
+    """Dropout keep draws as uint8 [n, k] (or None) and the scale 1/(1 - rate)."""
+    if not 0.0 <= drop_rate < 1.0:
+        raise ValueError("drop_rate must lie in [0, 1)")
+    if keep is None:
+        if drop_rate != 0.0:
+            raise ValueError("a drop rate needs keep draws")
+        return None, 1.0
+    keep = np.ascontiguousarray(keep, dtype=np.uint8).reshape(n, k)
+    return keep, 1.0 / (1.0 - drop_rate)
+
+
+def attend(Q, K, V, idx, scale: float, sel=None, keep=None, drop_rate: float = 0.0):
+    """Softmax + aggregate on a given index set.  Returns (out [nsel,d_V], lse [nsel]).
+
+    keep: optional dropout draws [nsel, k] (nonzero keeps a slot's weight,
+    scaled by 1/(1 - drop_rate))."""
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     N, H, d = _shape(Q)
     _key_shape(K, N, H, d)
@@ -136,10 +151,11 @@ def attend(Q, K, V, idx, scale: float, sel=None):
     s, n = _sel(sel, N, H)
     idx = np.ascontiguousarray(idx, dtype=np.int32).reshape(n, -1)
     k = idx.shape[1]
+    kp, ks = _keep(keep, n, k, drop_rate)
     out = np.empty((n, dv), np.float64)
     lse = np.empty(n, np.float64)
     _load().oracle_attend(_ptr(Q), _ptr(K), _ptr(V), N, H, d, dv, k, float(scale), n, _ptr(s),
-                          _ptr(idx), _ptr(out), _ptr(lse))
+                          _ptr(idx), _ptr(kp), ks, _ptr(out), _ptr(lse))
     return out, lse
 
 
@@ -160,8 +176,10 @@ def forward(Q, K, V, k: int, scale: float, offsets=None):
     return out, idx, lse
 
 
-def backward(Q, K, V, dO, idx, scale: float):
-    """Gradients with the index set held fixed.  Returns (dQ [N,H,d_K], dK [N,H,d_K], dV [N,H,d_V])."""
+def backward(Q, K, V, dO, idx, scale: float, keep=None, drop_rate: float = 0.0):
+    """Gradients with the index set held fixed.  Returns (dQ [N,H,d_K], dK [N,H,d_K], dV [N,H,d_V]).
+
+    keep, drop_rate: the forward's dropout draws [N, H, k] and rate."""
     Q, K, V, dO = _f64(Q), _f64(K), _f64(V), _f64(dO)
     N, H, d = _shape(Q)
     _key_shape(K, N, H, d)
@@ -170,11 +188,12 @@ def backward(Q, K, V, dO, idx, scale: float):
         raise ValueError("dO must have the shape of V")
     idx = np.ascontiguousarray(idx, dtype=np.int32).reshape(N, H, -1)
     k = idx.shape[2]
+    kp, ks = _keep(keep, N * H, k, drop_rate)
     dQ = np.empty((N, H, d), np.float64)
     dK = np.empty((N, H, d), np.float64)
     dV = np.empty((N, H, dv), np.float64)
     rc = _load().oracle_backward(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO), N, H, d, dv, k,
-                                 float(scale), _ptr(idx), _ptr(dQ), _ptr(dK), _ptr(dV))
+                                 float(scale), _ptr(idx), _ptr(kp), ks, _ptr(dQ), _ptr(dK), _ptr(dV))
     if rc != 0:
         raise MemoryError("oracle_backward could not allocate")
     return dQ, dK, dV

@@ -15,6 +15,12 @@
  *     GatherRows picks the value rows, softmax runs over the k kept scores,
  *     and an einsum sums the weighted value rows.
  *   - Appendix F: the symbolic matrix entry is E_ij = q_i . k_j.
+ *   - Attention dropout (the experimental details list an attention-dropout
+ *     rate r): each kept weight A_ij is multiplied by m_ij / (1 - r) with a
+ *     0/1 keep draw m_ij, inverted dropout as in Srivastava et al. (2014);
+ *     the draws are an input (keep [.., k] uint8 aligned with the index
+ *     slots, NULL for no dropout) so that both implementations see the same
+ *     ones.  The softmax statistics (lse) are those of A, before dropout.
  *   - Backward (Section 3.1, last paragraph; Appendix E, last paragraph):
  *     the selected indices are reused, so gradients flow only through the
  *     k selected pairs of each query and the selection itself is constant.
@@ -146,12 +152,14 @@ int oracle_topk(const double* Q, const double* K, const int32_t* offsets, int32_
  * Softmax over the kept scores and the weighted sum of gathered value rows
  * (Algorithm 1: GatherRows, softmax, Einsum nk,nkv->nv), for a given index
  * set.  Slots holding -1 are empty (their weight is exp(-inf) = 0).
+ *   keep [nsel, k] (NULL: no dropout): the weight of slot t is multiplied
+ *   by keep_scale when keep[t] != 0 and by 0 otherwise.
  *   out [nsel, dv], lse [nsel] (natural log of sum_j exp(scale * s_ij)).
  * A row with no valid index gets out = 0 and lse = -inf.
  */
 int oracle_attend(const double* Q, const double* K, const double* V, int64_t N, int32_t H,
                   int32_t d, int32_t dv, int32_t k, double scale, int64_t nsel, const int64_t* sel,
-                  const int32_t* idx, double* out, double* lse) {
+                  const int32_t* idx, const uint8_t* keep, double keep_scale, double* out, double* lse) {
     if (sel == NULL) nsel = N * (int64_t)H;
 #pragma omp parallel
     {
@@ -178,6 +186,7 @@ int oracle_attend(const double* Q, const double* K, const double* V, int64_t N, 
             for (int32_t t = 0; t < k; ++t) {
                 if (row[t] < 0) continue;
                 double p = exp(z[t] - zmax) / Z;
+                if (keep) p *= keep[r * k + t] ? keep_scale : 0.0;
                 const double* vr = V + ((size_t)row[t] * H + h) * dv;
                 for (int32_t c = 0; c < dv; ++c) o[c] += p * vr[c];
             }
@@ -196,7 +205,7 @@ int oracle_forward(const double* Q, const double* K, const double* V, const int3
                    int32_t G, int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, double scale,
                    int32_t* idx, double* out, double* lse) {
     if (oracle_topk(Q, K, offsets, G, N, H, d, k, 0, NULL, idx, NULL, NULL) != 0) return -1;
-    return oracle_attend(Q, K, V, N, H, d, dv, k, scale, 0, NULL, idx, out, lse);
+    return oracle_attend(Q, K, V, N, H, d, dv, k, scale, 0, NULL, idx, NULL, 1.0, out, lse);
 }
 
 /*
@@ -210,20 +219,26 @@ int oracle_forward(const double* Q, const double* K, const double* V, const int3
  *   dK_j += g_j * scale * q_i
  *   dV_j += p_j * dO_i
  * (the dot product dp_j runs over the dv value dimensions, dQ and dK have
- * the d query/key dimensions, dV the dv value dimensions).
+ * the d query/key dimensions, dV the dv value dimensions).  With dropout
+ * (keep [N, H, k] not NULL, f_j = keep_scale or 0 by keep), out_i sums
+ * p_j f_j v_j, so dV_j gets p_j f_j dO_i and the gradient of p_j is
+ * f_j dp_j, which replaces dp_j in D_i and g_j.
  * idx [N, H, k]; dQ, dK [N, H, d] and dV [N, H, dv] are overwritten.
  * Per-query terms are computed in parallel; the scatter into dK and dV runs
  * in one thread in query order.
  */
 int oracle_backward(const double* Q, const double* K, const double* V, const double* dO,
                     int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, double scale,
-                    const int32_t* idx, double* dQ, double* dK, double* dV) {
+                    const int32_t* idx, const uint8_t* keep, double keep_scale, double* dQ, double* dK,
+                    double* dV) {
     int64_t NH = N * (int64_t)H;
     double* P = (double*)malloc(sizeof(double) * (size_t)(NH * k > 0 ? NH * k : 1));
     double* Gr = (double*)malloc(sizeof(double) * (size_t)(NH * k > 0 ? NH * k : 1));
-    if (!P || !Gr) {
+    double* F = (double*)malloc(sizeof(double) * (size_t)(NH * k > 0 ? NH * k : 1));
+    if (!P || !Gr || !F) {
         free(P);
         free(Gr);
+        free(F);
         return -1;
     }
     memset(dQ, 0, sizeof(double) * (size_t)(NH * d));
@@ -240,6 +255,8 @@ int oracle_backward(const double* Q, const double* K, const double* V, const dou
             const int32_t* row = idx + qh * k;
             double* p = P + qh * k;
             double* g = Gr + qh * k;
+            double* f = F + qh * k;
+            for (int32_t t = 0; t < k; ++t) f[t] = keep ? (keep[qh * k + t] ? keep_scale : 0.0) : 1.0;
             double zmax = -INFINITY;
             for (int32_t t = 0; t < k; ++t) {
                 z[t] = row[t] >= 0 ? scale * oracle_score(Q, K, H, d, i, row[t], h) : -INFINITY;
@@ -259,6 +276,7 @@ int oracle_backward(const double* Q, const double* K, const double* V, const dou
                 if (row[t] >= 0) {
                     const double* vr = V + ((size_t)row[t] * H + h) * dv;
                     for (int32_t c = 0; c < dv; ++c) dp[t] += dOi[c] * vr[c];
+                    dp[t] *= f[t];
                 }
                 D += p[t] * dp[t];
             }
@@ -282,13 +300,14 @@ int oracle_backward(const double* Q, const double* K, const double* V, const dou
             if (row[t] < 0) continue;
             double* dkr = dK + ((size_t)row[t] * H + h) * d;
             double* dvr = dV + ((size_t)row[t] * H + h) * dv;
-            double gs = Gr[qh * k + t] * scale, pt = P[qh * k + t];
+            double gs = Gr[qh * k + t] * scale, pt = P[qh * k + t] * F[qh * k + t];
             for (int32_t c = 0; c < d; ++c) dkr[c] += gs * qi[c];
             for (int32_t c = 0; c < dv; ++c) dvr[c] += pt * dOi[c];
         }
     }
     free(P);
     free(Gr);
+    free(F);
     return 0;
 }
 

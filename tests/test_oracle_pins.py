@@ -469,3 +469,87 @@ def test_value_columns_split_and_gradient_invariants():
     for (lo, hi) in _graphs(offsets, N):
         np.testing.assert_allclose(dK[lo:hi].sum(axis=0), 0.0, atol=1e-12)
         np.testing.assert_allclose(dV[lo:hi].sum(axis=0), dO[lo:hi].sum(axis=0), atol=1e-12)
+
+
+# ---- attention dropout (inverted dropout on the kept weights, the keep
+# draws given) ----
+
+def _dropout_dense_torch(Q, K, V, k, scale, keep_dense, rate):
+    """Top-k masked dense attention with dropout on its weights, from torch
+    primitives: A = softmax(scale S + mask), out = (A * keep / (1 - rate)) V."""
+    q = Q.permute(1, 0, 2)
+    kk = K.permute(1, 0, 2)
+    v = V.permute(1, 0, 2).contiguous()
+    S = torch.matmul(q, kk.transpose(1, 2).contiguous())
+    top = torch.topk(S, k, dim=-1).indices
+    mask = torch.full_like(S, float("-inf"))
+    mask.scatter_(-1, top, 0.0)
+    A = torch.softmax(scale * S + mask, dim=-1)
+    out = torch.matmul(A * keep_dense / (1.0 - rate), v).permute(1, 0, 2)
+    return out
+
+
+def _dense_keep(idx, keep, N):
+    """The per-slot keep draws [N, H, k] scattered onto the dense [H, N, N] grid."""
+    Nq, H, k = idx.shape
+    dense = np.zeros((H, Nq, N))
+    for i in range(Nq):
+        for h in range(H):
+            for t in range(k):
+                if idx[i, h, t] >= 0:
+                    dense[h, i, idx[i, h, t]] = keep[i, h, t]
+    return torch.from_numpy(dense)
+
+
+@pytest.mark.parametrize("d,dv,rate", [(4, 4, 0.5), (3, 6, 0.25)])
+def test_dropout_matches_torch_autograd(d, dv, rate):
+    rng = np.random.default_rng(400 + d + dv)
+    N, H, k = 23, 2, 6
+    Qn, Kn = (rng.standard_normal((N, H, d)) for _ in range(2))
+    Vn, dOn = (rng.standard_normal((N, H, dv)) for _ in range(2))
+    scale = 0.7
+    _, idx, _ = oracle.forward(Qn, Kn, Vn, k, scale)
+    keep = (rng.random((N, H, k)) >= rate).astype(np.uint8)
+    out, lse = oracle.attend(Qn, Kn, Vn, idx, scale, keep=keep, drop_rate=rate)
+    dQ, dK, dV = oracle.backward(Qn, Kn, Vn, dOn, idx, scale, keep=keep, drop_rate=rate)
+    Q, K, V = (torch.from_numpy(x).clone().requires_grad_(True) for x in (Qn, Kn, Vn))
+    want = _dropout_dense_torch(Q, K, V, k, scale, _dense_keep(idx, keep, N), rate)
+    np.testing.assert_allclose(out, want.detach().numpy().reshape(N * H, dv), rtol=1e-12, atol=1e-12)
+    # lse is that of the weights before dropout
+    _, lse0 = oracle.attend(Qn, Kn, Vn, idx, scale)
+    np.testing.assert_array_equal(lse, lse0)
+    (want * torch.from_numpy(dOn)).sum().backward()
+    np.testing.assert_allclose(dQ, Q.grad.numpy(), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(dK, K.grad.numpy(), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(dV, V.grad.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def test_dropout_keep_all_is_no_dropout_and_finite_differences():
+    rng = np.random.default_rng(31)
+    N, H, d, k, rate = 11, 1, 3, 4, 0.3
+    Q, K, V, dO = (rng.standard_normal((N, H, d)) for _ in range(4))
+    _, idx, _ = oracle.forward(Q, K, V, k, 0.8)
+    ones = np.ones((N, H, k), np.uint8)
+    np.testing.assert_array_equal(oracle.attend(Q, K, V, idx, 0.8, keep=ones)[0], oracle.attend(Q, K, V, idx, 0.8)[0])
+    for a, b in zip(oracle.backward(Q, K, V, dO, idx, 0.8, keep=ones), oracle.backward(Q, K, V, dO, idx, 0.8)):
+        np.testing.assert_array_equal(a, b)
+    keep = (rng.random((N, H, k)) >= rate).astype(np.uint8)
+    dQ, dK, dV = oracle.backward(Q, K, V, dO, idx, 0.8, keep=keep, drop_rate=rate)
+
+    def loss(xs):
+        # the index set and the draws held fixed, as in the backward
+        o, _ = oracle.attend(xs["Q"], xs["K"], xs["V"], idx, 0.8, keep=keep, drop_rate=rate)
+        return float((o.reshape(N, H, d) * dO).sum())
+
+    eps = 1e-6
+    for name, X, G in (("Q", Q, dQ), ("K", K, dK), ("V", V, dV)):
+        num = np.zeros_like(X)
+        for pos in np.ndindex(X.shape):
+            vals = []
+            for sgn in (1.0, -1.0):
+                xs = {"Q": Q, "K": K, "V": V}
+                xs[name] = X.copy()
+                xs[name][pos] += sgn * eps
+                vals.append(loss(xs))
+            num[pos] = (vals[0] - vals[1]) / (2 * eps)
+        np.testing.assert_allclose(G, num, rtol=1e-6, atol=1e-7, err_msg=name)
