@@ -123,19 +123,28 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * kmip_attend and kmip_fwd with value rows of their own width (Section 3.1:
- * W_Q and W_K project to d_K dimensions, W_V to d_V).  Q and K are
- * [N, H, d] with d = d_K, which alone decides the selection; V and out are
- * [N, H, dv] with dv = d_V in {16, 32, 64}.  kmip_attend / kmip_fwd are the
- * case dv = d.  Same workspace as kmip_topk; N * H * dv < 2^31.
+ * Extended forward entry points for training use:
+ *  - value rows of their own width (Section 3.1: W_Q and W_K project to
+ *    d_K dimensions, W_V to d_V): Q and K are [N, H, d] with d = d_K, which
+ *    alone decides the selection; V and out are [N, H, dv] with
+ *    dv = d_V in {16, 32, 64};
+ *  - attention dropout (the experimental details list an attention-dropout
+ *    rate): keep is uint8 [N, H, k] device memory aligned with the topk_idx
+ *    slots, drawn by the caller (nonzero keeps the slot); the kept weights
+ *    are multiplied by 1 / (1 - drop_rate), the dropped ones by 0 (inverted
+ *    dropout).  lse stays that of the softmax before dropout.  keep = NULL
+ *    with drop_rate = 0 is no dropout; a drop_rate outside [0, 1), or > 0
+ *    without keep, is KMIP_ERR_INVALID_ARG.
+ * kmip_attend / kmip_fwd are the case dv = d, keep = NULL.  Same workspace
+ * as kmip_topk; N * H * dv < 2^31.
  */
-kmip_status_t kmip_attend_dv(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
+kmip_status_t kmip_attend_ex(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
                              int32_t d, int32_t dv, int32_t k, float scale, const int32_t* topk_idx,
-                             float* out, float* lse, void* stream);
-kmip_status_t kmip_fwd_dv(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
+                             const uint8_t* keep, float drop_rate, float* out, float* lse, void* stream);
+kmip_status_t kmip_fwd_ex(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
                           int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k,
-                          float scale, float* out, int32_t* topk_idx, float* lse, void* workspace,
-                          size_t workspace_bytes, void* stream);
+                          float scale, const uint8_t* keep, float drop_rate, float* out, int32_t* topk_idx,
+                          float* lse, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Backward with the forward's index set held fixed (Section 3.1, last
@@ -196,19 +205,23 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
                        int32_t variant, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * kmip_bwd with value rows of their own width dv = d_V in {16, 32, 64}
- * (Section 3.1): V, dOut bf16 [N, H, dv] and dV float32 [N, H, dv]; Q, K,
- * dQ, dK stay [N, H, d].  dp_j = dOut_i . v_j runs over the dv value
- * dimensions.  KMIP_BWD_BUCKETED needs dv == d (else KMIP_ERR_UNSUPPORTED
- * and workspace size 0): its interleaved copy of q_i and dOut_i assumes
- * equal widths; KMIP_BWD_AUTO then picks KMIP_BWD_SEGMENTED.  kmip_bwd and
- * kmip_bwd_workspace_size are the case dv = d.
+ * kmip_bwd for the extended forward: value rows of width dv = d_V in
+ * {16, 32, 64} (V, dOut bf16 [N, H, dv] and dV float32 [N, H, dv]; Q, K,
+ * dQ, dK stay [N, H, d]; dp_j = dOut_i . v_j runs over the dv value
+ * dimensions) and the forward's dropout draws keep / drop_rate (with
+ * f_j = 1/(1 - drop_rate) for a kept slot and 0 for a dropped one, dV_j gets
+ * p_j f_j dOut_i and f_j dp_j replaces dp_j in D_i and g_j).
+ * KMIP_BWD_BUCKETED needs dv == d (else KMIP_ERR_UNSUPPORTED and workspace
+ * size 0): its interleaved copy of q_i and dOut_i assumes equal widths;
+ * KMIP_BWD_AUTO then picks KMIP_BWD_SEGMENTED.  kmip_bwd and
+ * kmip_bwd_workspace_size are the case dv = d, keep = NULL.
  */
-size_t kmip_bwd_dv_workspace_size(int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, int32_t variant);
-kmip_status_t kmip_bwd_dv(const void* Q, const void* K, const void* V, const void* dOut,
-                          const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
-                          int32_t d, int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV,
-                          int32_t variant, void* workspace, size_t workspace_bytes, void* stream);
+size_t kmip_bwd_ex_workspace_size(int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, int32_t variant);
+kmip_status_t kmip_bwd_ex(const void* Q, const void* K, const void* V, const void* dOut,
+                          const int32_t* topk_idx, const float* lse, const uint8_t* keep, float drop_rate,
+                          int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* dQ,
+                          float* dK, float* dV, int32_t variant, void* workspace, size_t workspace_bytes,
+                          void* stream);
 
 /*
  * Forward (kmip_fwd) of one graph without a caller workspace and without

@@ -6,6 +6,9 @@ kernels.  Tensors: Q, K are bf16 [N, H, d] (d = d_K), V and dOut bf16
 [N, H, dv] (dv = d_V, the value width; dv = d unless the caller's V is
 narrower or wider) on the GPU; out and dV are float32 [N, H, dv], dQ and dK
 float32 [N, H, d]; topk_idx is int32 [N, H, k]; lse is float32 [N, H].
+Attention dropout: ``keep`` is a uint8 [N, H, k] tensor of draws aligned
+with the index slots (nonzero keeps a slot's weight, scaled by
+1/(1 - drop_rate)), drawn by the caller.
 ``graph_offsets`` is a host-side int32 sequence [G+1] (or None for one graph).
 """
 from __future__ import annotations
@@ -19,7 +22,8 @@ from ._lib import KmipError, MAX_K, NOALLOC_SCRATCH_BYTES, check, load
 
 __all__ = [
     "KmipError", "MAX_K", "NOALLOC_SCRATCH_BYTES", "topk", "attend", "fwd", "fwd_noalloc", "bwd",
-    "attention", "topk_workspace_size", "bwd_workspace_size", "Workspace", "load",
+    "attention", "topk_workspace_size", "bwd_workspace_size", "Workspace", "load", "KMIPAttention",
+    "linear_k_schedule",
 ]
 
 
@@ -73,7 +77,12 @@ def topk_workspace_size(N: int, H: int, d: int, k: int, num_graphs: int = 1) -> 
 
 
 def bwd_workspace_size(N: int, H: int, d: int, k: int, variant: int = 0, dv: Optional[int] = None) -> int:
-    return int(load().kmip_bwd_dv_workspace_size(N, H, d, d if dv is None else dv, k, variant))
+    return int(load().kmip_bwd_ex_workspace_size(N, H, d, d if dv is None else dv, k, variant))
+
+
+def _keep_spec(keep, N, H, kk):
+    torch = _torch()
+    return [] if keep is None else [(keep, "keep", torch.uint8, (N, H, kk))]
 
 
 class Workspace:
@@ -159,7 +168,7 @@ def topk(q, k_, kk: int, graph_offsets: Optional[Sequence[int]] = None, idx=None
     return idx
 
 
-def attend(q, k_, v, idx, scale: float, out=None, lse=None):
+def attend(q, k_, v, idx, scale: float, out=None, lse=None, keep=None, drop_rate: float = 0.0):
     """Gather-softmax-aggregate on a given index set: returns (out, lse)."""
     torch = _torch()
     N, H, d = _nhd(q)
@@ -167,6 +176,7 @@ def attend(q, k_, v, idx, scale: float, out=None, lse=None):
     kk = _kk(idx)
     specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d)),
              (v, "V", torch.bfloat16, (N, H, dv)), (idx, "topk_idx", torch.int32, (N, H, kk))]
+    specs += _keep_spec(keep, N, H, kk)
     if out is not None:
         specs.append((out, "out", torch.float32, (N, H, dv)))
     if lse is not None:
@@ -176,19 +186,20 @@ def attend(q, k_, v, idx, scale: float, out=None, lse=None):
         out = torch.empty((N, H, dv), dtype=torch.float32, device=q.device)
     if lse is None:
         lse = torch.empty((N, H), dtype=torch.float32, device=q.device)
-    check(load().kmip_attend_dv(_ptr(q), _ptr(k_), _ptr(v), N, H, d, dv, kk, float(scale), _ptr(idx),
-                                _ptr(out), _ptr(lse), _stream_ptr()))
+    check(load().kmip_attend_ex(_ptr(q), _ptr(k_), _ptr(v), N, H, d, dv, kk, float(scale), _ptr(idx),
+                                _ptr(keep), float(drop_rate), _ptr(out), _ptr(lse), _stream_ptr()))
     return out, lse
 
 
-def fwd(q, k_, v, kk: int, scale: float, graph_offsets=None, workspace=None):
+def fwd(q, k_, v, kk: int, scale: float, graph_offsets=None, workspace=None, keep=None,
+        drop_rate: float = 0.0):
     """Full forward: returns (out, topk_idx, lse)."""
     torch = _torch()
     N, H, d = _nhd(q)
     dv = _dv(v, N, H)
     kk = int(kk)
     _validate((q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d)),
-              (v, "V", torch.bfloat16, (N, H, dv)))
+              (v, "V", torch.bfloat16, (N, H, dv)), *_keep_spec(keep, N, H, kk))
     o, optr, G = _offsets(graph_offsets)
     if o is not None and (o.ndim != 1 or len(o) < 2):
         raise ValueError("graph_offsets must be a 1-D sequence of at least two entries")
@@ -196,9 +207,9 @@ def fwd(q, k_, v, kk: int, scale: float, graph_offsets=None, workspace=None):
     idx = torch.empty((N, H, kk), dtype=torch.int32, device=q.device)
     lse = torch.empty((N, H), dtype=torch.float32, device=q.device)
     buf = _workspace(workspace, topk_workspace_size(N, H, d, kk, G), q.device)
-    check(load().kmip_fwd_dv(_ptr(q), _ptr(k_), _ptr(v), optr, G, N, H, d, dv, kk, float(scale), _ptr(out),
-                             _ptr(idx), _ptr(lse), _ptr(buf), 0 if buf is None else buf.numel(),
-                             _stream_ptr()))
+    check(load().kmip_fwd_ex(_ptr(q), _ptr(k_), _ptr(v), optr, G, N, H, d, dv, kk, float(scale), _ptr(keep),
+                             float(drop_rate), _ptr(out), _ptr(idx), _ptr(lse), _ptr(buf),
+                             0 if buf is None else buf.numel(), _stream_ptr()))
     return out, idx, lse
 
 
@@ -219,7 +230,7 @@ def fwd_noalloc(q, k_, v, kk: int, scale: float, out, idx, lse):
 
 
 def bwd(q, k_, v, dout, idx, lse, scale: float, variant: int = 0, dq=None, dk=None, dv=None,
-        workspace=None):
+        workspace=None, keep=None, drop_rate: float = 0.0):
     """Backward with the index set held fixed: returns (dQ, dK, dV) float32."""
     torch = _torch()
     N, H, d = _nhd(q)
@@ -228,7 +239,7 @@ def bwd(q, k_, v, dout, idx, lse, scale: float, variant: int = 0, dq=None, dk=No
     nd, nv = (N, H, d), (N, H, wv)
     specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, nd), (v, "V", torch.bfloat16, nv),
              (dout, "dOut", torch.bfloat16, nv), (idx, "topk_idx", torch.int32, (N, H, kk)),
-             (lse, "lse", torch.float32, (N, H))]
+             (lse, "lse", torch.float32, (N, H))] + _keep_spec(keep, N, H, kk)
     for t, name, shp in ((dq, "dQ", nd), (dk, "dK", nd), (dv, "dV", nv)):
         if t is not None:
             specs.append((t, name, torch.float32, shp))
@@ -238,27 +249,31 @@ def bwd(q, k_, v, dout, idx, lse, scale: float, variant: int = 0, dq=None, dk=No
     dk = dk if dk is not None else torch.empty(nd, dtype=torch.float32, device=dev)
     dv = dv if dv is not None else torch.empty(nv, dtype=torch.float32, device=dev)
     buf = _workspace(workspace, bwd_workspace_size(N, H, d, kk, variant, dv=wv), dev)
-    check(load().kmip_bwd_dv(_ptr(q), _ptr(k_), _ptr(v), _ptr(dout), _ptr(idx), _ptr(lse), N, H, d, wv, kk,
-                             float(scale), _ptr(dq), _ptr(dk), _ptr(dv), int(variant), _ptr(buf),
-                             0 if buf is None else buf.numel(), _stream_ptr()))
+    check(load().kmip_bwd_ex(_ptr(q), _ptr(k_), _ptr(v), _ptr(dout), _ptr(idx), _ptr(lse), _ptr(keep),
+                             float(drop_rate), N, H, d, wv, kk, float(scale), _ptr(dq), _ptr(dk), _ptr(dv),
+                             int(variant), _ptr(buf), 0 if buf is None else buf.numel(), _stream_ptr()))
     return dq, dk, dv
 
 
-def attention(q, k_, v, kk: int, scale: float, graph_offsets=None, variant: int = 0, workspace=None):
-    """Differentiable k-MIP attention for training: returns out (float32 [N, H, d]).
+def attention(q, k_, v, kk: int, scale: float, graph_offsets=None, variant: int = 0, workspace=None,
+              keep=None, drop_rate: float = 0.0):
+    """Differentiable k-MIP attention for training: returns out (float32 [N, H, d_V]).
 
     The forward is ``fwd``; autograd's backward calls ``bwd`` with the saved
     (topk_idx, lse), so the index set is held fixed and no gradient flows
     through the selection (Section 3.1 and Appendix E of arXiv 2604.03815).
     The incoming output gradient is rounded to bf16, the type the library's
     backward reads, and dQ, dK, dV are returned in the dtype of Q, K, V.
+    keep / drop_rate: attention dropout draws uint8 [N, H, kk] and rate,
+    used by the forward and again by the backward.
     """
     torch = _torch()
 
     class _Attention(torch.autograd.Function):
         @staticmethod
         def forward(ctx, q_, k2, v_):
-            out, idx, lse = fwd(q_, k2, v_, kk, scale, graph_offsets=graph_offsets, workspace=workspace)
+            out, idx, lse = fwd(q_, k2, v_, kk, scale, graph_offsets=graph_offsets, workspace=workspace,
+                                keep=keep, drop_rate=drop_rate)
             ctx.save_for_backward(q_, k2, v_, idx, lse)
             return out
 
@@ -266,7 +281,10 @@ def attention(q, k_, v, kk: int, scale: float, graph_offsets=None, variant: int 
         def backward(ctx, dout):
             q_, k2, v_, idx, lse = ctx.saved_tensors
             dq, dk, dv = bwd(q_, k2, v_, dout.to(torch.bfloat16).contiguous(), idx, lse, scale,
-                             variant=variant, workspace=workspace)
+                             variant=variant, workspace=workspace, keep=keep, drop_rate=drop_rate)
             return dq.to(q_.dtype), dk.to(k2.dtype), dv.to(v_.dtype)
 
     return _Attention.apply(q, k_, v)
+
+
+from .layer import KMIPAttention, linear_k_schedule  # noqa: E402

@@ -18,7 +18,7 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # scores never hold NaN (finite bf16 inputs): lets max3 chains skip the
     # IEEE quieting of each operand
-    "-fno-honor-nans",
+    "-Xarch_device", "-fno-honor-nans",
     # keep MFMA results in ordinary VGPRs, next to the VALU code that reads them
     "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-Wall", "-Wno-unused-function",

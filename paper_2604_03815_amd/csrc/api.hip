@@ -112,8 +112,24 @@ kmip_status_t check_value_width(int64_t N, int32_t H, int32_t dv) {
     return KMIP_OK;
 }
 
+// Finite test on the bits: the sources are built with -fno-honor-nans (for
+// the kernels' max3 chains), under which std::isfinite may assume no NaN.
+bool finite_bits(float x) {
+    uint32_t b;
+    std::memcpy(&b, &x, sizeof(b));
+    return (b & 0x7F800000u) != 0x7F800000u;
+}
+
+// Attention dropout: a rate in [0, 1); keep draws are needed for a rate > 0.
+kmip_status_t check_dropout(const uint8_t* keep, float rate) {
+    if (!finite_bits(rate) || rate < 0.0f || rate >= 1.0f)
+        return record_error(KMIP_ERR_INVALID_ARG, "drop_rate must lie in [0, 1)");
+    if (keep == nullptr && rate != 0.0f) return record_error(KMIP_ERR_INVALID_ARG, "drop_rate > 0 needs keep draws");
+    return KMIP_OK;
+}
+
 kmip_status_t check_scale(float scale) {
-    if (!std::isfinite(scale) || !(scale > 0.0f)) return record_error(KMIP_ERR_INVALID_ARG, "scale must be finite and > 0");
+    if (!finite_bits(scale) || !(scale > 0.0f)) return record_error(KMIP_ERR_INVALID_ARG, "scale must be finite and > 0");
     return KMIP_OK;
 }
 
@@ -272,20 +288,21 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
     return ok();
 }
 
-kmip_status_t kmip_attend_dv(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
+kmip_status_t kmip_attend_ex(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
                              int32_t d, int32_t dv, int32_t k, float scale, const int32_t* topk_idx,
-                             float* out, float* lse, void* stream_) {
+                             const uint8_t* keep, float drop_rate, float* out, float* lse, void* stream_) {
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
     if ((s = check_value_width(N, H, dv)) != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
+    if ((s = check_dropout(keep, drop_rate)) != KMIP_OK) return s;
     if (N == 0) return ok();
     if (!Q || !K || !V || !topk_idx || !out || !lse)
         return record_error(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_attend");
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V))
         return record_error(KMIP_ERR_INVALID_ARG, "Q, K and V must be 16-byte aligned");
-    hipError_t e = kmip::launch_attend(Q, K, V, topk_idx, (int32_t)N, H, d, dv, k, scale, out, lse,
-                                       reinterpret_cast<hipStream_t>(stream_));
+    hipError_t e = kmip::launch_attend(Q, K, V, topk_idx, keep, 1.0f / (1.0f - drop_rate), (int32_t)N, H, d, dv,
+                                       k, scale, out, lse, reinterpret_cast<hipStream_t>(stream_));
     if (e != hipSuccess) return hip_fail(e, "attend launch");
     return ok();
 }
@@ -293,31 +310,32 @@ kmip_status_t kmip_attend_dv(const void* Q, const void* K, const void* V, int64_
 kmip_status_t kmip_attend(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
                           int32_t d, int32_t k, float scale, const int32_t* topk_idx, float* out,
                           float* lse, void* stream) {
-    return kmip_attend_dv(Q, K, V, N, H, d, d, k, scale, topk_idx, out, lse, stream);
+    return kmip_attend_ex(Q, K, V, N, H, d, d, k, scale, topk_idx, nullptr, 0.0f, out, lse, stream);
 }
 
-kmip_status_t kmip_fwd_dv(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
+kmip_status_t kmip_fwd_ex(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
                           int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k,
-                          float scale, float* out, int32_t* topk_idx, float* lse, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+                          float scale, const uint8_t* keep, float drop_rate, float* out, int32_t* topk_idx,
+                          float* lse, void* workspace, size_t workspace_bytes, void* stream) {
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
     if ((s = check_value_width(N, H, dv)) != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
+    if ((s = check_dropout(keep, drop_rate)) != KMIP_OK) return s;
     if (N > 0 && (!V || !out || !lse)) return record_error(KMIP_ERR_INVALID_ARG, "null V, out or lse");
     if (N > 0 && !aligned16(V)) return record_error(KMIP_ERR_INVALID_ARG, "V must be 16-byte aligned");
     s = kmip_topk(Q, K, graph_offsets, num_graphs, N, H, d, k, topk_idx, workspace,
                   workspace_bytes, stream);
     if (s != KMIP_OK) return s;
-    return kmip_attend_dv(Q, K, V, N, H, d, dv, k, scale, topk_idx, out, lse, stream);
+    return kmip_attend_ex(Q, K, V, N, H, d, dv, k, scale, topk_idx, keep, drop_rate, out, lse, stream);
 }
 
 kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
                        int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t k,
                        float scale, float* out, int32_t* topk_idx, float* lse, void* workspace,
                        size_t workspace_bytes, void* stream) {
-    return kmip_fwd_dv(Q, K, V, graph_offsets, num_graphs, N, H, d, d, k, scale, out, topk_idx, lse,
-                       workspace, workspace_bytes, stream);
+    return kmip_fwd_ex(Q, K, V, graph_offsets, num_graphs, N, H, d, d, k, scale, nullptr, 0.0f, out, topk_idx,
+                       lse, workspace, workspace_bytes, stream);
 }
 
 // Backward variant the library picks (KMIP_BWD_AUTO): the bucketed reduction
@@ -327,7 +345,7 @@ static int32_t default_bwd_variant(int64_t N, int32_t H, int32_t d, int32_t dv) 
     return dv == d && kmip::bwd_bucket_supported((int32_t)N, H, d) ? KMIP_BWD_BUCKETED : KMIP_BWD_SEGMENTED;
 }
 
-size_t kmip_bwd_dv_workspace_size(int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, int32_t variant) {
+size_t kmip_bwd_ex_workspace_size(int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, int32_t variant) {
     if (check_sizes(N, H, d, k) != KMIP_OK || check_value_width(N, H, dv) != KMIP_OK) return 0;
     const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d, dv) : variant;
     if (v == KMIP_BWD_KEY_AGGREGATED) return align_up(kmip::bwd_agg_workspace_bytes((int32_t)N, H, d));
@@ -339,17 +357,20 @@ size_t kmip_bwd_dv_workspace_size(int64_t N, int32_t H, int32_t d, int32_t dv, i
 }
 
 size_t kmip_bwd_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int32_t variant) {
-    return kmip_bwd_dv_workspace_size(N, H, d, d, k, variant);
+    return kmip_bwd_ex_workspace_size(N, H, d, d, k, variant);
 }
 
-kmip_status_t kmip_bwd_dv(const void* Q, const void* K, const void* V, const void* dOut,
-                          const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
-                          int32_t d, int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV,
-                          int32_t variant, void* workspace, size_t workspace_bytes, void* stream_) {
+kmip_status_t kmip_bwd_ex(const void* Q, const void* K, const void* V, const void* dOut,
+                          const int32_t* topk_idx, const float* lse, const uint8_t* keep, float drop_rate,
+                          int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* dQ,
+                          float* dK, float* dV, int32_t variant, void* workspace, size_t workspace_bytes,
+                          void* stream_) {
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
     if ((s = check_value_width(N, H, dv)) != KMIP_OK) return s;
     if ((s = check_scale(scale)) != KMIP_OK) return s;
+    if ((s = check_dropout(keep, drop_rate)) != KMIP_OK) return s;
+    const float keep_scale = 1.0f / (1.0f - drop_rate);
     if (variant < KMIP_BWD_AUTO || variant > KMIP_BWD_KEY_AGGREGATED)
         return record_error(KMIP_ERR_UNSUPPORTED, "backward variant %d", variant);
     if (variant == KMIP_BWD_BUCKETED && dv != d)
@@ -364,26 +385,26 @@ kmip_status_t kmip_bwd_dv(const void* Q, const void* K, const void* V, const voi
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
     hipError_t e;
     if (v != KMIP_BWD_ATOMIC) {
-        const size_t need = kmip_bwd_dv_workspace_size(N, H, d, dv, k, v);
+        const size_t need = kmip_bwd_ex_workspace_size(N, H, d, dv, k, v);
         if (workspace == nullptr || workspace_bytes < need)
             return record_error(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, need);
         if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0)
             return record_error(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
     }
     if (v == KMIP_BWD_KEY_AGGREGATED) {
-        e = kmip::launch_bwd_agg(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, dv, k, scale, dQ, dK,
-                                 dV, workspace, stream);
+        e = kmip::launch_bwd_agg(Q, K, V, dOut, topk_idx, lse, keep, keep_scale, (int32_t)N, H, d, dv, k, scale,
+                                 dQ, dK, dV, workspace, stream);
     } else if (v == KMIP_BWD_BUCKETED) {
         if (!kmip::bwd_bucket_supported((int32_t)N, H, d))
             return record_error(KMIP_ERR_UNSUPPORTED, "the bucketed variant needs N*H <= 8192*512 (key-row buckets of at most 512 rows)");
-        e = kmip::launch_bwd_bucket(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, k, scale, dQ, dK,
-                                    dV, workspace, stream);
+        e = kmip::launch_bwd_bucket(Q, K, V, dOut, topk_idx, lse, keep, keep_scale, (int32_t)N, H, d, k, scale,
+                                    dQ, dK, dV, workspace, stream);
     } else if (v == KMIP_BWD_SEGMENTED) {
-        e = kmip::launch_bwd_csr(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, dv, k, scale, dQ, dK,
-                                 dV, workspace, stream);
+        e = kmip::launch_bwd_csr(Q, K, V, dOut, topk_idx, lse, keep, keep_scale, (int32_t)N, H, d, dv, k, scale,
+                                 dQ, dK, dV, workspace, stream);
     } else {
-        e = kmip::launch_bwd_atomic(Q, K, V, dOut, topk_idx, lse, (int32_t)N, H, d, dv, k, scale, dQ,
-                                    dK, dV, stream);
+        e = kmip::launch_bwd_atomic(Q, K, V, dOut, topk_idx, lse, keep, keep_scale, (int32_t)N, H, d, dv, k,
+                                    scale, dQ, dK, dV, stream);
     }
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     return ok();
@@ -393,8 +414,8 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
                        const int32_t* topk_idx, const float* lse, int64_t N, int32_t H,
                        int32_t d, int32_t k, float scale, float* dQ, float* dK, float* dV,
                        int32_t variant, void* workspace, size_t workspace_bytes, void* stream) {
-    return kmip_bwd_dv(Q, K, V, dOut, topk_idx, lse, N, H, d, d, k, scale, dQ, dK, dV, variant, workspace,
-                       workspace_bytes, stream);
+    return kmip_bwd_ex(Q, K, V, dOut, topk_idx, lse, nullptr, 0.0f, N, H, d, d, k, scale, dQ, dK, dV, variant,
+                       workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -14,6 +14,10 @@
 // as the key rows when they fit in 64 registers, else right after) into a
 // DV-vector, and a transposed team reduction leaves dimensions tl, tl + 16,
 // ... on lane tl.
+//
+// Attention dropout (keep != nullptr): slot t's weight in the sum is
+// multiplied by keep_scale when keep[qh k + t] is nonzero and by 0
+// otherwise; the softmax statistics (lse) are those before dropout.
 #include "kmip_device.h"
 #include "kmip_internal.h"
 
@@ -23,8 +27,8 @@ namespace {
 template <int D, int DV, int NS>
 __global__ __launch_bounds__(256) void attend_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
-    const int32_t* __restrict__ idx, int32_t N, int32_t H, int32_t k, float scale,
-    float* __restrict__ out, float* __restrict__ lse) {
+    const int32_t* __restrict__ idx, const uint8_t* __restrict__ keep, float keep_scale, int32_t N,
+    int32_t H, int32_t k, float scale, float* __restrict__ out, float* __restrict__ lse) {
     constexpr bool kKeep = DV / 2 * NS <= 64;
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
@@ -63,6 +67,11 @@ __global__ __launch_bounds__(256) void attend_kernel(
         zs += w[s];
     }
     zs = group16_sum(zs);
+    if (keep != nullptr) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+            if (jj[s] >= 0) w[s] *= keep[(size_t)qh * k + tl + 16 * s] != 0 ? keep_scale : 0.0f;
+    }
 
     float acc[DV];
 #pragma unroll
@@ -100,28 +109,28 @@ __global__ __launch_bounds__(256) void attend_kernel(
 
 template <int D, int DV>
 void launch_attend_d(unsigned blocks, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
-                     const uint16_t* v, const int32_t* idx, int32_t N, int32_t H, int32_t k, float scale,
-                     float* out, float* lse) {
+                     const uint16_t* v, const int32_t* idx, const uint8_t* keep, float keep_scale, int32_t N,
+                     int32_t H, int32_t k, float scale, float* out, float* lse) {
     const int ns = (k + 15) / 16;
     if (ns <= 1)
-        hipLaunchKernelGGL((attend_kernel<D, DV, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H,
-                           k, scale, out, lse);
+        hipLaunchKernelGGL((attend_kernel<D, DV, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
+                           keep_scale, N, H, k, scale, out, lse);
     else if (ns <= 2)
-        hipLaunchKernelGGL((attend_kernel<D, DV, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H,
-                           k, scale, out, lse);
+        hipLaunchKernelGGL((attend_kernel<D, DV, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
+                           keep_scale, N, H, k, scale, out, lse);
     else if (ns <= 4)
-        hipLaunchKernelGGL((attend_kernel<D, DV, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H,
-                           k, scale, out, lse);
+        hipLaunchKernelGGL((attend_kernel<D, DV, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
+                           keep_scale, N, H, k, scale, out, lse);
     else
-        hipLaunchKernelGGL((attend_kernel<D, DV, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, N, H,
-                           k, scale, out, lse);
+        hipLaunchKernelGGL((attend_kernel<D, DV, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
+                           keep_scale, N, H, k, scale, out, lse);
 }
 
 }  // namespace
 
 hipError_t launch_attend(const void* Q, const void* K, const void* V, const int32_t* idx,
-                         int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* out,
-                         float* lse, hipStream_t stream) {
+                         const uint8_t* keep, float keep_scale, int32_t N, int32_t H, int32_t d, int32_t dv,
+                         int32_t k, float scale, float* out, float* lse, hipStream_t stream) {
     const int64_t nqh = (int64_t)N * H;
     if (nqh == 0) return hipSuccess;
     const unsigned blocks = (unsigned)((nqh + 15) / 16);
@@ -130,7 +139,7 @@ hipError_t launch_attend(const void* Q, const void* K, const void* V, const int3
     const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
 #define KMIP_ATTEND_CASE(DD, DVV)                                                              \
     if (d == DD && dv == DVV) {                                                                \
-        launch_attend_d<DD, DVV>(blocks, stream, q, kk, v, idx, N, H, k, scale, out, lse);    \
+        launch_attend_d<DD, DVV>(blocks, stream, q, kk, v, idx, keep, keep_scale, N, H, k, scale, out, lse); \
         return hipGetLastError();                                                              \
     }
 #define KMIP_ATTEND_D(DD) KMIP_ATTEND_CASE(DD, 16) KMIP_ATTEND_CASE(DD, 32) KMIP_ATTEND_CASE(DD, 64)

@@ -7,6 +7,9 @@
 //   dp_j = dO_i . v_j,  D_i = sum_j p_j dp_j,  g_j = p_j (dp_j - D_i)
 //   dQ_i = scale sum_j g_j k_j      (row-local, plain store)
 //   dK_j += scale g_j q_i,  dV_j += p_j dO_i   (scatter)
+// With attention dropout (keep != nullptr, f_j = keep_scale or 0 by the
+// forward's keep draw of slot j), dp_j is replaced by f_j dp_j in D_i and
+// g_j, and dV_j gets p_j f_j dO_i.
 //
 // D is the query/key width d_K, DV the value width d_V (dp_j and dV run over
 // DV dimensions, dQ and dK over D).
@@ -81,8 +84,9 @@ template <int D, int DV>
 __device__ __forceinline__ void bwd_query(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
-    int64_t qh, int h, int tl, int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ,
-    float* __restrict__ dK, float* __restrict__ dV, AggLds<D, DV>* tab) {
+    const uint8_t* __restrict__ keep, float keep_scale, int64_t qh, int h, int tl, int32_t N, int32_t H,
+    int32_t k, float scale, float* __restrict__ dQ, float* __restrict__ dK, float* __restrict__ dV,
+    AggLds<D, DV>* tab) {
     constexpr int U = D / 16;
     constexpr int UV = DV / 16;
     float q[D], g[DV];
@@ -91,13 +95,14 @@ __device__ __forceinline__ void bwd_query(
     const float l = lse[qh];
 
     const int ns = (k + 15) >> 4;
-    float p[kMaxSlotsPerLane], dp[kMaxSlotsPerLane];
+    float p[kMaxSlotsPerLane], dp[kMaxSlotsPerLane], pv[kMaxSlotsPerLane];
     int32_t jj[kMaxSlotsPerLane];
     float dsum = 0.0f;
 #pragma unroll
     for (int s = 0; s < kMaxSlotsPerLane; ++s) {
         p[s] = 0.0f;
         dp[s] = 0.0f;
+        pv[s] = 0.0f;
         jj[s] = -1;
         const int slot = tl + 16 * s;
         if (s < ns && slot < k && l != -INFINITY) {
@@ -107,6 +112,13 @@ __device__ __forceinline__ void bwd_query(
                 const float z = scale * dot_row_bf16<D>(q, K + ((size_t)j * H + h) * D);
                 p[s] = __expf(z - l);
                 dp[s] = dot_row_bf16<DV>(g, V + ((size_t)j * H + h) * DV);
+                pv[s] = p[s];
+                if (keep != nullptr) {
+                    // dropout: the gradient of p_j is f_j dp_j, and dV_j takes p_j f_j
+                    const float f = keep[(size_t)qh * k + slot] != 0 ? keep_scale : 0.0f;
+                    dp[s] *= f;
+                    pv[s] = p[s] * f;
+                }
             }
         }
         dsum = fmaf(p[s], dp[s], dsum);
@@ -137,7 +149,7 @@ __device__ __forceinline__ void bwd_query(
             for (int src = 0; src < 16; ++src) {
                 js[src] = __shfl(jj[s], src, 16);
                 gsv[src] = __shfl(gs_own, src, 16);
-                ps[src] = __shfl(p[s], src, 16);
+                ps[src] = __shfl(pv[s], src, 16);
             }
 #pragma unroll
             for (int src = 0; src < 16; ++src) {
@@ -179,11 +191,12 @@ __global__ __launch_bounds__(256) void bwd_atomic_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
     int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float* __restrict__ dK,
-    float* __restrict__ dV) {
+    float* __restrict__ dV, const uint8_t* __restrict__ keep, float keep_scale) {
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
     if (qh >= (int64_t)N * H) return;  // whole team exits together
-    bwd_query<D, DV>(Q, K, V, dO, idx, lse, qh, (int)(qh % H), tl, N, H, k, scale, dQ, dK, dV, nullptr);
+    bwd_query<D, DV>(Q, K, V, dO, idx, lse, keep, keep_scale, qh, (int)(qh % H), tl, N, H, k, scale, dQ, dK, dV,
+                     nullptr);
 }
 
 // Key-aggregated scatter: one workgroup per kAggQueries positions of head
@@ -193,7 +206,8 @@ __global__ __launch_bounds__(256) void bwd_agg_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
     const int32_t* __restrict__ perm, int32_t N, int32_t H, int32_t k, float scale,
-    float* __restrict__ dQ, float* __restrict__ dK, float* __restrict__ dV) {
+    float* __restrict__ dQ, float* __restrict__ dK, float* __restrict__ dV, const uint8_t* __restrict__ keep,
+    float keep_scale) {
     constexpr int C = AggTable<D, DV>::kSlots;
     constexpr int W = D + DV;
     __shared__ AggLds<D, DV> tab;
@@ -207,7 +221,7 @@ __global__ __launch_bounds__(256) void bwd_agg_kernel(
         const int64_t pos = (int64_t)blockIdx.x * kAggQueries + round * 16 + team;
         if (pos >= N) break;  // positions grow with round: the team is done
         const int64_t qh = (int64_t)perm[(size_t)h * N + pos] * H + h;
-        bwd_query<D, DV>(Q, K, V, dO, idx, lse, qh, h, tl, N, H, k, scale, dQ, dK, dV, &tab);
+        bwd_query<D, DV>(Q, K, V, dO, idx, lse, keep, keep_scale, qh, h, tl, N, H, k, scale, dQ, dK, dV, &tab);
     }
     __syncthreads();
     for (int e = threadIdx.x; e < C * W; e += 256) {
@@ -245,9 +259,9 @@ hipError_t launch_fill_zero(float* p, size_t n, hipStream_t stream) {
 }
 
 hipError_t launch_bwd_atomic(const void* Q, const void* K, const void* V, const void* dO,
-                             const int32_t* idx, const float* lse, int32_t N, int32_t H,
-                             int32_t d, int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV,
-                             hipStream_t stream) {
+                             const int32_t* idx, const float* lse, const uint8_t* keep, float keep_scale,
+                             int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* dQ,
+                             float* dK, float* dV, hipStream_t stream) {
     const int64_t nqh = (int64_t)N * H;
     if (nqh == 0) return hipSuccess;
     hipError_t e = launch_fill_zero(dK, (size_t)nqh * d, stream);
@@ -262,7 +276,7 @@ hipError_t launch_bwd_atomic(const void* Q, const void* K, const void* V, const 
 #define KMIP_BWD_ATOMIC_CASE(DD, DVV)                                                                  \
     if (d == DD && dv == DVV) {                                                                        \
         hipLaunchKernelGGL((bwd_atomic_kernel<DD, DVV>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, \
-                           idx, lse, N, H, k, scale, dQ, dK, dV);                                      \
+                           idx, lse, N, H, k, scale, dQ, dK, dV, keep, keep_scale);                    \
         return hipGetLastError();                                                                      \
     }
 #define KMIP_BWD_ATOMIC_D(DD) KMIP_BWD_ATOMIC_CASE(DD, 16) KMIP_BWD_ATOMIC_CASE(DD, 32) KMIP_BWD_ATOMIC_CASE(DD, 64)
@@ -281,9 +295,9 @@ namespace kmip {
 size_t bwd_agg_workspace_bytes(int32_t N, int32_t H, int32_t d) { return group_workspace_bytes(N, H, d); }
 
 hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const void* dO,
-                          const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                          int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
-                          hipStream_t stream) {
+                          const int32_t* idx, const float* lse, const uint8_t* keep, float keep_scale,
+                          int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* dQ,
+                          float* dK, float* dV, void* ws, hipStream_t stream) {
     const int64_t nqh = (int64_t)N * H;
     if (nqh == 0) return hipSuccess;
     QueryGroups groups{};
@@ -299,7 +313,7 @@ hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const voi
 #define KMIP_BWD_AGG_CASE(DD, DVV)                                                                       \
     if (d == DD && dv == DVV) {                                                                          \
         hipLaunchKernelGGL((bwd_agg_kernel<DD, DVV>), grid, dim3(256), 0, stream, q, kk, v, g, idx, lse, \
-                           groups.perm, N, H, k, scale, dQ, dK, dV);                                     \
+                           groups.perm, N, H, k, scale, dQ, dK, dV, keep, keep_scale);                   \
         return hipGetLastError();                                                                        \
     }
 #define KMIP_BWD_AGG_D(DD) KMIP_BWD_AGG_CASE(DD, 16) KMIP_BWD_AGG_CASE(DD, 32) KMIP_BWD_AGG_CASE(DD, 64)

@@ -37,11 +37,14 @@ constexpr int kChunk = 1024;         // sorted pairs per wave in the reduction
 // (QGt != nullptr, value width DV = D only) the head-major interleaved copy
 // of q_i and dO_i.  D is the query/key width, DV the value width (dp_j runs
 // over it).  Slot tl + 16 s of query-head qh leaves its key index in jj[s]
-// (-1: none) and its coefficients a = scale g, p in ca[s], cp[s].
+// (-1: none) and its coefficients a = scale g, p in ca[s], cp[s].  With
+// attention dropout (keep != nullptr, f = keep_scale or 0 by the slot's keep
+// draw) dp is replaced by f dp and the dV coefficient is p f.
 template <int D, int DV, int NS>
 __device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                                          const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
                                          const int32_t* __restrict__ idx, const float* __restrict__ lse,
+                                         const uint8_t* __restrict__ keep, float keep_scale,
                                          int32_t N, int32_t H, int32_t k, float scale, int64_t qh, int tl,
                                          float* __restrict__ dQ, uint16_t* __restrict__ QGt, int32_t (&jj)[NS],
                                          float (&ca)[NS], float (&cp)[NS]) {
@@ -60,13 +63,14 @@ __device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const u
     load_row_f32<D>(q, Q + (size_t)qh * D);
     load_row_f32<DV>(g, dO + (size_t)qh * DV);
     const float l = lse[qh];
-    float p[NS], dp[NS];
+    float p[NS], dp[NS], pv[NS];
     uint4 kw[kKeep ? NS : 1][D / 8];
     float dsum = 0.0f;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         p[s] = 0.0f;
         dp[s] = 0.0f;
+        pv[s] = 0.0f;
         jj[s] = -1;
         const int slot = tl + 16 * s;
         // a pair exists wherever its index lies in [0, N), as the counting
@@ -84,6 +88,12 @@ __device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const u
                 const float z = scale * dot_words_bf16<D>(q, w);
                 p[s] = __expf(z - l);
                 dp[s] = dot_row_bf16<DV>(g, V + ((size_t)j * H + h) * DV);
+                pv[s] = p[s];
+                if (keep != nullptr) {
+                    const float f = keep[(size_t)qh * k + slot] != 0 ? keep_scale : 0.0f;
+                    dp[s] *= f;
+                    pv[s] = p[s] * f;
+                }
             }
         }
         dsum = fmaf(p[s], dp[s], dsum);
@@ -98,7 +108,7 @@ __device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const u
     for (int s = 0; s < NS; ++s) {
         const float gs = p[s] * (dp[s] - dsum);
         ca[s] = scale * gs;
-        cp[s] = p[s];
+        cp[s] = pv[s];
         if (jj[s] >= 0 && l != -INFINITY) {
             uint4 w[D / 8];
             if constexpr (kKeep) {
@@ -130,13 +140,13 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
     int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, float2* __restrict__ coef,
-    uint16_t* __restrict__ QGt) {
+    uint16_t* __restrict__ QGt, const uint8_t* __restrict__ keep, float keep_scale) {
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
     if (qh >= (int64_t)N * H) return;  // whole team exits together
     int32_t jj[NS];
     float ca[NS], cp[NS];
-    coef_one<D, DV, NS>(Q, K, V, dO, idx, lse, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
+    coef_one<D, DV, NS>(Q, K, V, dO, idx, lse, keep, keep_scale, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         const int slot = tl + 16 * s;
@@ -148,20 +158,21 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
 template <int D, int DV>
 void launch_coef(unsigned blocks, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
                  const uint16_t* v, const uint16_t* g, const int32_t* idx, const float* lse, int32_t N,
-                 int32_t H, int32_t k, float scale, float* dQ, float2* coef, uint16_t* qg) {
+                 int32_t H, int32_t k, float scale, float* dQ, float2* coef, uint16_t* qg, const uint8_t* keep,
+                 float keep_scale) {
     const int ns = (k + 15) / 16;
     if (ns <= 1)
         hipLaunchKernelGGL((csr_coef_kernel<D, DV, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qg);
+                           N, H, k, scale, dQ, coef, qg, keep, keep_scale);
     else if (ns <= 2)
         hipLaunchKernelGGL((csr_coef_kernel<D, DV, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qg);
+                           N, H, k, scale, dQ, coef, qg, keep, keep_scale);
     else if (ns <= 4)
         hipLaunchKernelGGL((csr_coef_kernel<D, DV, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qg);
+                           N, H, k, scale, dQ, coef, qg, keep, keep_scale);
     else
         hipLaunchKernelGGL((csr_coef_kernel<D, DV, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
-                           N, H, k, scale, dQ, coef, qg);
+                           N, H, k, scale, dQ, coef, qg, keep, keep_scale);
 }
 
 // Key row of slot s of query-head qh, or -1 (padding).
@@ -565,7 +576,8 @@ __global__ __launch_bounds__(256) void coef_split_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
     int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, uint16_t* __restrict__ QGt,
-    int32_t shift, int32_t* __restrict__ supcur, PairRecord* __restrict__ mid) {
+    int32_t shift, int32_t* __restrict__ supcur, PairRecord* __restrict__ mid, const uint8_t* __restrict__ keep,
+    float keep_scale) {
     constexpr int TQ = 8 / NS;   // query-heads per team
     constexpr int R = TQ * NS;   // records per lane: 8
     static_assert(256 * R == kSplitChunk, "one staging chunk per workgroup");
@@ -585,7 +597,7 @@ __global__ __launch_bounds__(256) void coef_split_kernel(
         float ca[NS], cp[NS];
 #pragma unroll
         for (int s2 = 0; s2 < NS; ++s2) jj[s2] = -1;
-        if (qh < nh) coef_one<D, D, NS>(Q, K, V, dO, idx, lse, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
+        if (qh < nh) coef_one<D, D, NS>(Q, K, V, dO, idx, lse, keep, keep_scale, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
         const int32_t h = (int32_t)(qh % H), i = (int32_t)(qh / H);
 #pragma unroll
         for (int s2 = 0; s2 < NS; ++s2) {
@@ -630,11 +642,13 @@ template <int D>
 hipError_t launch_coef_split(int32_t nh, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
                              const uint16_t* v, const uint16_t* g, const int32_t* idx, const float* lse,
                              int32_t N, int32_t H, int32_t k, float scale, float* dQ, uint16_t* qg,
-                             int32_t shift, int32_t* supcur, PairRecord* mid) {
+                             int32_t shift, int32_t* supcur, PairRecord* mid, const uint8_t* keep,
+                             float keep_scale) {
     const int ns = (k + 15) / 16;
 #define KMIP_COEF_SPLIT(NSV)                                                                           \
     hipLaunchKernelGGL((coef_split_kernel<D, NSV>), dim3((unsigned)((nh + 128 / NSV - 1) / (128 / NSV))),   \
-                       dim3(256), 0, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur, mid)
+                       dim3(256), 0, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur, mid, \
+                       keep, keep_scale)
     if (ns <= 1)
         KMIP_COEF_SPLIT(1);
     else if (ns <= 2)
@@ -951,9 +965,9 @@ size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k) {
 }
 
 hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const void* dO,
-                             const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                             int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
-                             hipStream_t stream) {
+                             const int32_t* idx, const float* lse, const uint8_t* keep, float keep_scale,
+                             int32_t N, int32_t H, int32_t d, int32_t k, float scale, float* dQ, float* dK,
+                             float* dV, void* ws, hipStream_t stream) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };
     const int64_t nh = (int64_t)N * H;
     if (nh == 0) return hipSuccess;
@@ -1029,13 +1043,13 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     // coefficients, dQ and the interleaved copy, fused with placement pass 1
     if (d == 16)
         e = launch_coef_split<16>((int32_t)nh, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur,
-                                  mid);
+                                  mid, keep, keep_scale);
     else if (d == 32)
         e = launch_coef_split<32>((int32_t)nh, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur,
-                                  mid);
+                                  mid, keep, keep_scale);
     else
         e = launch_coef_split<64>((int32_t)nh, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur,
-                                  mid);
+                                  mid, keep, keep_scale);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(bkt_split2_kernel, dim3((unsigned)(nsup + (pairs + kSplitChunk - 1) / kSplitChunk)), dim3(256),
                        0, stream, mid, supst, pstart2, nsup, shift, gcnt, rec);
@@ -1068,9 +1082,9 @@ size_t bwd_csr_workspace_bytes(int32_t N, int32_t H, int32_t k) {
 }
 
 hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const void* dO,
-                          const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                          int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
-                          hipStream_t stream) {
+                          const int32_t* idx, const float* lse, const uint8_t* keep, float keep_scale,
+                          int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* dQ,
+                          float* dK, float* dV, void* ws, hipStream_t stream) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };
     const int64_t nh = (int64_t)N * H;
     if (nh == 0) return hipSuccess;
@@ -1098,7 +1112,8 @@ hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const voi
     bool launched = false;
 #define KMIP_CSR_COEF(DD, DVV)                                                                          \
     if (d == DD && dv == DVV) {                                                                         \
-        launch_coef<DD, DVV>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, nullptr); \
+        launch_coef<DD, DVV>(team_blocks, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, coef, nullptr, \
+                             keep, keep_scale);                                                          \
         launched = true;                                                                                \
     }
 #define KMIP_CSR_COEF_D(DD) KMIP_CSR_COEF(DD, 16) KMIP_CSR_COEF(DD, 32) KMIP_CSR_COEF(DD, 64)

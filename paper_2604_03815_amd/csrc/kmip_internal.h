@@ -116,40 +116,42 @@ hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, 
 
 // Gather-softmax-aggregate: Q, K [N,H,d] (d = d_K), V and out [N,H,dv]
 // (dv = d_V), each in {16, 32, 64}.
+// keep / keep_scale: attention dropout draws uint8 [N,H,k] and 1/(1 - rate),
+// or nullptr (no dropout), for this launcher and the backward ones.
 hipError_t launch_attend(const void* Q, const void* K, const void* V, const int32_t* idx,
-                         int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* out,
-                         float* lse, hipStream_t stream);
+                         const uint8_t* keep, float keep_scale, int32_t N, int32_t H, int32_t d, int32_t dv,
+                         int32_t k, float scale, float* out, float* lse, hipStream_t stream);
 
 // The backward launchers take the query/key width d and the value width dv
 // (each in {16, 32, 64}); the bucketed one needs dv == d.
 hipError_t launch_bwd_atomic(const void* Q, const void* K, const void* V, const void* dO,
-                             const int32_t* idx, const float* lse, int32_t N, int32_t H,
-                             int32_t d, int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV,
-                             hipStream_t stream);
+                             const int32_t* idx, const float* lse, const uint8_t* keep, float keep_scale,
+                             int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* dQ,
+                             float* dK, float* dV, hipStream_t stream);
 
 // Backward with key-aggregated scatter; ws holds bwd_agg_workspace_bytes().
 size_t bwd_agg_workspace_bytes(int32_t N, int32_t H, int32_t d);
 hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const void* dO,
-                          const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                          int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
-                          hipStream_t stream);
+                          const int32_t* idx, const float* lse, const uint8_t* keep, float keep_scale,
+                          int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* dQ,
+                          float* dK, float* dV, void* ws, hipStream_t stream);
 
 // Backward with a key-sorted segmented reduction (backward_csr.hip); ws
 // holds bwd_csr_workspace_bytes().
 size_t bwd_csr_workspace_bytes(int32_t N, int32_t H, int32_t k);
 hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const void* dO,
-                          const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                          int32_t dv, int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
-                          hipStream_t stream);
+                          const int32_t* idx, const float* lse, const uint8_t* keep, float keep_scale,
+                          int32_t N, int32_t H, int32_t d, int32_t dv, int32_t k, float scale, float* dQ,
+                          float* dK, float* dV, void* ws, hipStream_t stream);
 
 // Backward with pairs bucketed by blocks of key rows and summed in LDS
 // (backward_csr.hip); supported while N * H / (4096 / d) <= 8192.
 bool bwd_bucket_supported(int32_t N, int32_t H, int32_t d);
 size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k);
 hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const void* dO,
-                             const int32_t* idx, const float* lse, int32_t N, int32_t H, int32_t d,
-                             int32_t k, float scale, float* dQ, float* dK, float* dV, void* ws,
-                             hipStream_t stream);
+                             const int32_t* idx, const float* lse, const uint8_t* keep, float keep_scale,
+                             int32_t N, int32_t H, int32_t d, int32_t k, float scale, float* dQ, float* dK,
+                             float* dV, void* ws, hipStream_t stream);
 
 hipError_t launch_fill_zero(float* p, size_t n, hipStream_t stream);
 

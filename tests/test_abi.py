@@ -221,20 +221,29 @@ def test_noalloc_validates_before_launch(lib):
     assert lib.kmip_fwd_noalloc(None, None, None, 0, 1, 16, 4, f(1.0), None, None, None, None) == 0
 
 
-def test_value_width_entry_points_validate(lib):
+def test_extended_entry_points_validate(lib):
     f = ctypes.c_float
     # value widths outside {16, 32, 64}
-    assert lib.kmip_attend_dv(FAKE, FAKE, FAKE, 64, 1, 16, 48, 4, f(1.0), FAKE, FAKE, FAKE, None) == 2
-    assert lib.kmip_fwd_dv(FAKE, FAKE, FAKE, None, 1, 64, 1, 16, 8, 4, f(1.0), FAKE, FAKE, FAKE,
+    assert lib.kmip_attend_ex(FAKE, FAKE, FAKE, 64, 1, 16, 48, 4, f(1.0), FAKE, None, f(0.0), FAKE, FAKE,
+                              None) == 2
+    assert lib.kmip_fwd_ex(FAKE, FAKE, FAKE, None, 1, 64, 1, 16, 8, 4, f(1.0), None, f(0.0), FAKE, FAKE, FAKE,
                            FAKE, 1 << 20, None) == 2
-    args = [FAKE] * 6 + [64, 1, 32, 16, 4, f(1.0), FAKE, FAKE, FAKE]
+    args = [FAKE] * 6
+    sizes = [64, 1, 32, 16, 4, f(1.0), FAKE, FAKE, FAKE]
     # the bucketed variant needs d_V == d_K; the others take any pair
-    assert lib.kmip_bwd_dv(*args, _lib.BWD_BUCKETED, FAKE, 1 << 30, None) == 2
-    assert lib.kmip_bwd_dv_workspace_size(64, 1, 32, 16, 4, _lib.BWD_BUCKETED) == 0
-    assert lib.kmip_bwd_dv_workspace_size(64, 1, 32, 16, 4, _lib.BWD_AUTO) == \
-        lib.kmip_bwd_dv_workspace_size(64, 1, 32, 16, 4, _lib.BWD_SEGMENTED) > 0
-    assert lib.kmip_bwd_dv(*args, _lib.BWD_SEGMENTED, None, 0, None) == 3
+    assert lib.kmip_bwd_ex(*args, None, f(0.0), *sizes, _lib.BWD_BUCKETED, FAKE, 1 << 30, None) == 2
+    assert lib.kmip_bwd_ex_workspace_size(64, 1, 32, 16, 4, _lib.BWD_BUCKETED) == 0
+    assert lib.kmip_bwd_ex_workspace_size(64, 1, 32, 16, 4, _lib.BWD_AUTO) == \
+        lib.kmip_bwd_ex_workspace_size(64, 1, 32, 16, 4, _lib.BWD_SEGMENTED) > 0
+    assert lib.kmip_bwd_ex(*args, None, f(0.0), *sizes, _lib.BWD_SEGMENTED, None, 0, None) == 3
     # d_V = d_K: the plain entry points are this case
     for v in (0, 1, 2, 3, 4):
-        assert lib.kmip_bwd_dv_workspace_size(5000, 2, 32, 32, 16, v) == lib.kmip_bwd_workspace_size(5000, 2, 32, 16, v)
-    assert lib.kmip_attend_dv(FAKE, FAKE, FAKE, 64, 1, 16, 32, 4, f(-1.0), FAKE, FAKE, FAKE, None) == 1
+        assert lib.kmip_bwd_ex_workspace_size(5000, 2, 32, 32, 16, v) == lib.kmip_bwd_workspace_size(5000, 2, 32, 16, v)
+    assert lib.kmip_attend_ex(FAKE, FAKE, FAKE, 64, 1, 16, 32, 4, f(-1.0), FAKE, None, f(0.0), FAKE, FAKE,
+                              None) == 1
+    # dropout: a rate in [0, 1), and keep draws for a rate above 0
+    for rate, keep in ((1.0, FAKE), (-0.1, FAKE), (float("nan"), FAKE), (0.5, None)):
+        assert lib.kmip_attend_ex(FAKE, FAKE, FAKE, 64, 1, 16, 16, 4, f(1.0), FAKE, keep, f(rate), FAKE, FAKE,
+                                  None) == 1
+        assert lib.kmip_bwd_ex(*args, keep, f(rate), 64, 1, 16, 16, 4, f(1.0), FAKE, FAKE, FAKE, 0, None, 0,
+                               None) == 1
