@@ -756,6 +756,85 @@ __global__ __launch_bounds__(256) void sb_bounds_kernel(const uint16_t* __restri
     }
 }
 
+// One block per window w of head h: the 64 superblocks 64 w .. 64 w + 63,
+// positions 16384 w .. (positions >= N are absent).  Writes the window's row
+// of the window tiles (tile w / 32, row w % 32, same layout as the bound
+// tiles): the centre c, the mean of the window's keys rounded to bf16, and
+// R_up = bf16_up(r (1 + 2^-12) + |c| 2^-12) with r = max |k - c| over the
+// window, the construction of sb_bounds_kernel over 16384 keys instead of
+// 256.  The margin argument given there does not depend on how many keys a
+// ball holds, so q.c + |q|_up R_up bounds the MFMA score of every key of the
+// window: a window whose bound beats no query's threshold holds no key that
+// can pass the select kernel's filter.  An empty window gets c = 0, R = 0.
+template <int D>
+__global__ __launch_bounds__(256) void win_bounds_kernel(const uint16_t* __restrict__ kp, int32_t N,
+                                                         int32_t H, int32_t wctiles,
+                                                         uint16_t* __restrict__ wbounds) {
+    constexpr int NC = D / 16;
+    constexpr int WK = 64 * SBK;   // keys per window
+    __shared__ float part[4][D];
+    __shared__ float cen[D];
+    __shared__ float rpart[4];
+    const int w = blockIdx.x;
+    const int h = blockIdx.y;
+    const int t = threadIdx.x;
+    const int wave = t >> 6;
+    const int64_t p0 = (int64_t)w * WK;
+    const int64_t p1 = p0 + WK < (int64_t)N ? p0 + WK : (int64_t)N;
+    const int count = p1 > p0 ? (int)(p1 - p0) : 0;
+    float sum[D];
+#pragma unroll
+    for (int i = 0; i < D; ++i) sum[i] = 0.0f;
+    for (int64_t pos = p0 + t; pos < p1; pos += 256) {
+        float x[D];
+        load_row_f32<D>(x, kp + ((size_t)h * N + pos) * D);
+#pragma unroll
+        for (int i = 0; i < D; ++i) sum[i] += x[i];
+    }
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+        const float v = wave_sum(sum[i]);
+        if ((t & 63) == 0) part[wave][i] = v;
+    }
+    __syncthreads();
+    const int row = w & 31;
+    uint16_t* tile = wbounds + (((size_t)h * wctiles + (w >> 5)) * (NC + 1)) * 64 * 8;
+    if (t < D) {
+        const float tot = (part[0][t] + part[1][t]) + (part[2][t] + part[3][t]);
+        const uint16_t cb = count > 0 ? bf16_rne(tot / (float)count) : (uint16_t)0;
+        cen[t] = bf16_bits_to_f32(cb);
+        tile[((t >> 4) * 64 + row + 32 * ((t >> 3) & 1)) * 8 + (t & 7)] = cb;
+    }
+    __syncthreads();
+    float d2 = 0.0f;
+    for (int64_t pos = p0 + t; pos < p1; pos += 256) {
+        float x[D];
+        load_row_f32<D>(x, kp + ((size_t)h * N + pos) * D);
+        float e2 = 0.0f;
+#pragma unroll
+        for (int i = 0; i < D; ++i) {
+            const float e = x[i] - cen[i];
+            e2 = fmaf(e, e, e2);
+        }
+        d2 = fmaxf(d2, e2);
+    }
+    const float m = wave_max(d2);
+    if ((t & 63) == 0) rpart[wave] = m;
+    __syncthreads();
+    if (t >= D && t < D + 16) {
+        const int j = t - D;
+        uint16_t v = 0;
+        if (j == 0 && count > 0) {
+            float cn2 = 0.0f;
+            for (int i = 0; i < D; ++i) cn2 = fmaf(cen[i], cen[i], cn2);
+            const float r = sqrtf(fmaxf(fmaxf(rpart[0], rpart[1]), fmaxf(rpart[2], rpart[3])));
+            const float R = fmaf(r, 1.0f + 0x1p-12f, sqrtf(cn2) * 0x1p-12f);
+            v = bf16_up(R);
+        }
+        tile[(NC * 64 + row + 32 * (j >> 3)) * 8 + (j & 7)] = v;
+    }
+}
+
 // Levels of splitting for N keys: nodes of level l are split while l <
 // levels (the deepest split level has at most width nodes).
 void tree_shape(int32_t N, int32_t& levels, int32_t& width) {
@@ -783,6 +862,11 @@ int32_t key_order_ctiles(int32_t ntiles) {
     return (nsb + 63) / 64 * 2;
 }
 
+int32_t key_order_wctiles(int32_t ctiles) {
+    const int32_t nwin = ctiles / 2;   // one window per pair of bound tiles
+    return (nwin + 63) / 64 * 2;
+}
+
 size_t key_order_workspace_bytes(int32_t N, int32_t H, int32_t d) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };
     const int32_t ntiles = (N + 31) / 32;
@@ -792,8 +876,9 @@ size_t key_order_workspace_bytes(int32_t N, int32_t H, int32_t d) {
     return 2 * al((size_t)H * N * sizeof(int32_t)) + 2 * al((size_t)H * N * d * sizeof(uint16_t)) +
            al((size_t)H * N * sizeof(uint16_t)) +
            al((size_t)H * width * (2 * d + 2) * sizeof(float)) +
-           al((size_t)H * width * kNodeInts * sizeof(int32_t)) + al((size_t)H * sizeof(int32_t)) +
-           al((size_t)H * ctiles * (d / 16 + 1) * 64 * 16);
+           al((size_t)H * width * kNodeInts * sizeof(int32_t)) + al((size_t)2 * H * sizeof(int32_t)) +
+           al((size_t)H * ctiles * (d / 16 + 1) * 64 * 16) +
+           al((size_t)H * key_order_wctiles(ctiles) * (d / 16 + 1) * 64 * 16);
 }
 
 hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int32_t ntiles, void* ws,
@@ -818,11 +903,14 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
     int32_t* nodeh = reinterpret_cast<int32_t*>(p);
     p += al((size_t)H * width * kNodeInts * sizeof(int32_t));
     int32_t* votes = reinterpret_cast<int32_t*>(p);
-    p += al((size_t)H * sizeof(int32_t));
+    p += al((size_t)2 * H * sizeof(int32_t));
     uint16_t* bounds = reinterpret_cast<uint16_t*>(p);
+    p += al((size_t)H * ctiles * (d / 16 + 1) * 64 * 16);
+    uint16_t* wbounds = reinterpret_cast<uint16_t*>(p);
+    const int32_t wctiles = key_order_wctiles(ctiles);
 
     const uint16_t* k = reinterpret_cast<const uint16_t*>(K);
-    hipError_t e = launch_fill_zero(reinterpret_cast<float*>(votes), (size_t)H, stream);
+    hipError_t e = launch_fill_zero(reinterpret_cast<float*>(votes), (size_t)2 * H, stream);
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)((N + 255) / 256), (unsigned)H);
     const dim3 pgrid((unsigned)((N + kBlockPos - 1) / kBlockPos), (unsigned)H);
@@ -890,13 +978,20 @@ hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int3
     out->bounds = reinterpret_cast<const uint4*>(bounds);
     out->votes = votes;
     out->ctiles = ctiles;
+    out->wbounds = reinterpret_cast<const uint4*>(wbounds);
+    out->wctiles = wctiles;
     const dim3 sgrid((unsigned)(ctiles * 32), (unsigned)H);
-    if (d == 16)
+    const dim3 wgrid((unsigned)(wctiles * 32), (unsigned)H);
+    if (d == 16) {
         hipLaunchKernelGGL(sb_bounds_kernel<16>, sgrid, dim3(256), 0, stream, kcur, N, H, ctiles, bounds);
-    else if (d == 32)
+        hipLaunchKernelGGL(win_bounds_kernel<16>, wgrid, dim3(256), 0, stream, kcur, N, H, wctiles, wbounds);
+    } else if (d == 32) {
         hipLaunchKernelGGL(sb_bounds_kernel<32>, sgrid, dim3(256), 0, stream, kcur, N, H, ctiles, bounds);
-    else
+        hipLaunchKernelGGL(win_bounds_kernel<32>, wgrid, dim3(256), 0, stream, kcur, N, H, wctiles, wbounds);
+    } else {
         hipLaunchKernelGGL(sb_bounds_kernel<64>, sgrid, dim3(256), 0, stream, kcur, N, H, ctiles, bounds);
+        hipLaunchKernelGGL(win_bounds_kernel<64>, wgrid, dim3(256), 0, stream, kcur, N, H, wctiles, wbounds);
+    }
     return hipGetLastError();
 }
 

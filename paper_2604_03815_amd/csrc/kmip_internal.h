@@ -46,6 +46,9 @@ constexpr int kSuperTiles = 8;
 // Net votes (items finding most superblocks needed, minus the others) at
 // which a head's select items stop forming masks and scan every superblock.
 constexpr int kDenseVotes = 16;
+// Net votes (seeded items whose lower-bound pass raised no threshold, minus
+// the others) at which a head's seeded items skip that pass.
+constexpr int kLowerVotes = 16;
 
 // Device arrays of a key order:
 //   perm   [H][N]  key stored at each position;
@@ -53,17 +56,25 @@ constexpr int kDenseVotes = 16;
 //          tile s / 32, row s % 32, in the key-tile operand layout: chunks
 //          0 .. d/16-1 the bf16 center, chunk d/16 the radius R (bf16, rounded
 //          up) in dim 0;
-//   votes  [H]  dense-mode votes (zero before the select launch).
+//   votes  [2H] dense-mode votes, then lower-bound-pass votes (zero before
+//          the select launch).
+//   wbounds [H][wctiles][d/16 + 1][64] uint4: window tiles, the same kind of
+//          ball bound for each window of 64 superblocks (window w in tile
+//          w / 32, row w % 32).
 struct KeyOrder {
     const int32_t* perm;
     const uint16_t* rows;   // key rows in the stored order, head-major [H][N][d]
     const uint4* bounds;
     int32_t* votes;
     int32_t ctiles;
+    const uint4* wbounds;
+    int32_t wctiles;
 };
 
 // Bound tiles per head for ntiles key tiles: two per 64 superblocks.
 int32_t key_order_ctiles(int32_t ntiles);
+// Window tiles per head for ctiles bound tiles: two per 64 windows.
+int32_t key_order_wctiles(int32_t ctiles);
 size_t key_order_workspace_bytes(int32_t N, int32_t H, int32_t d);
 hipError_t launch_key_order(const void* K, int32_t N, int32_t H, int32_t d, int32_t ntiles, void* ws,
                             KeyOrder* out, hipStream_t stream);

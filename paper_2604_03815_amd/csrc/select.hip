@@ -225,7 +225,8 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     const uint4* __restrict__ kp, const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const Task* __restrict__ tasks, const int32_t* __restrict__ qperm,
     const uint16_t* __restrict__ qlabel, int32_t* __restrict__ seed_ref, const int32_t* __restrict__ kperm,
-    const uint4* __restrict__ bounds, int32_t* __restrict__ votes, int32_t ctiles, int32_t ntasks,
+    const uint4* __restrict__ bounds, const uint4* __restrict__ wbounds, int32_t wctiles,
+    int32_t* __restrict__ votes, int32_t ctiles, int32_t ntasks,
     int32_t N, int32_t H, int32_t k, int32_t ntiles, int32_t* __restrict__ work_ctr,
     Pacer* __restrict__ pacers, int32_t* __restrict__ topk_idx) {
     constexpr int NC = D / 16;
@@ -539,6 +540,7 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         pruned = __builtin_amdgcn_readfirstlane(v) < kDenseVotes;
     }
     const uint4* btiles = bounds != nullptr ? bounds + (size_t)head * ctiles * (NC + 1) * 64 : nullptr;
+    const uint4* wtiles = wbounds != nullptr ? wbounds + (size_t)head * wctiles * (NC + 1) * 64 : nullptr;
     uint32_t mask_lo = 0, mask_hi = 0;
     int mask_batch = -1;
     // The last masks compute_batch formed (before a warm-up replaced them):
@@ -579,6 +581,45 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         }
         uint64_t todo = whi - wlo == 64 ? ~0ull : (1ull << (whi - wlo)) - 1ull;
         if (full_batch == bt && !lower) todo &= __builtin_amdgcn_ballot_w64((full_lo | full_hi) != 0u);
+        // Windows whose own bound beats no valid query's theta hold no key
+        // that can pass the filter: their bound tiles are not scored (window
+        // tile 2 bt + ct holds windows 64 bt + 32 ct .. + 31 as its rows).
+        if (wtiles != nullptr && todo != 0ull) {
+            bf16x8 qu[QB];
+#pragma unroll
+            for (int b = 0; b < QB; ++b)
+                qu[b] = __builtin_bit_cast(bf16x8, make_uint4(half == 0 ? qn_up[b] : 0u, 0u, 0u, 0u));
+            uint64_t wneed = 0;
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                if (((todo >> (32 * ct)) & 0xFFFFFFFFull) == 0ull) continue;
+                const uint4* src = wtiles + (size_t)(2 * bt + ct) * (NC + 1) * 64 + lane;
+                uint4 wc[NC + 1];
+#pragma unroll
+                for (int c = 0; c <= NC; ++c) wc[c] = src[c * 64];
+                uint32_t lm = 0;
+                f32x16 wacc[QB];
+#pragma unroll
+                for (int b = 0; b < QB; ++b) {
+                    wacc[b] = f32x16{};
+#pragma unroll
+                    for (int c = 0; c < NC; ++c)
+                        wacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wc[c]), bq[b][c],
+                                                                          wacc[b], 0, 0, 0);
+                    wacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wc[NC]), qu[b],
+                                                                      wacc[b], 0, 0, 0);
+                }
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    uint32_t any = 0;
+#pragma unroll
+                    for (int b = 0; b < QB; ++b) any |= __float_as_uint(theta[b] - wacc[b][r]);
+                    lm = __builtin_amdgcn_alignbit(lm, any, 31);
+                }
+                wneed |= (uint64_t)half_or_rows(lm) << (32 * ct);
+            }
+            todo &= wneed;
+        }
         const int nfull = (key_hi - key_lo) / (32 * SBT);
         float low_v[QB];
 #pragma unroll
@@ -729,7 +770,30 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
 #pragma unroll
         for (int b = 0; b < QB; ++b) seeded = seeded && __builtin_amdgcn_ballot_w64(theta[b] == -INFINITY) == 0ull;
         // (superblock s holds positions 256 s .. 256 s + 255 when key_lo = 0)
-        if (key_lo == 0 && k <= 32 * SBT) compute_batch(0, false, true);
+        // With two query blocks (k <= 32), seeded items of a head skip the
+        // lower-bound pass once it has raised no threshold in nearly all
+        // seeded items of that head (their seeds, k keys of a neighbour's
+        // set, are then tighter than the balls' lower bounds): a seeded item
+        // whose pass raised nothing votes +1, one whose pass raised a
+        // threshold -8, and the pass is skipped from kLowerVotes net votes
+        // on.  The votes follow the dense-mode ones, votes[H + head].
+        if (key_lo == 0 && k <= 32 * SBT) {
+            int lv = 0;
+            if (QB == 2 && seeded && lane == 0)
+                lv = __hip_atomic_load(&votes[H + head], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__builtin_amdgcn_readfirstlane(lv) < kLowerVotes) {
+                float th0[QB];
+#pragma unroll
+                for (int b = 0; b < QB; ++b) th0[b] = theta[b];
+                compute_batch(0, false, true);
+                if (QB == 2 && seeded) {
+                    bool raised = false;
+#pragma unroll
+                    for (int b = 0; b < QB; ++b) raised = raised || __builtin_amdgcn_ballot_w64(theta[b] > th0[b]) != 0ull;
+                    if (lane == 0) atomicAdd(&votes[H + head], raised ? -8 : 1);
+                }
+            }
+        }
         const int needed = compute_batch(0, nwin <= 64, false);
         // Seeded items whose masks still keep more than half of the
         // superblocks warm up as well: a poorly seeded query widens the
@@ -1063,6 +1127,7 @@ hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const T
                        reinterpret_cast<const uint16_t*>(K), tasks, groups ? groups->perm : nullptr,
                        groups ? groups->label : nullptr, groups ? groups->seed_ref : nullptr,
                        keys ? keys->perm : nullptr, keys ? keys->bounds : nullptr,
+                       keys ? keys->wbounds : nullptr, keys ? keys->wctiles : 0,
                        keys ? keys->votes : nullptr, keys ? keys->ctiles : 0, ntasks, N, H, k, ntiles,
                        work_ctr, pacers, topk_idx);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -56,12 +56,13 @@ def test_workspace_size(lib):
     # head-major copies of the key rows in that order [H][N][d] bf16, projection
     # codes [H][N] u16, per-node data of the widest tree level (1954
     # superblocks -> 11 levels, 1024 nodes) [H][1024][2d + 2] f32 and
-    # [H][1024][520] i32, votes [H] i32 (padded to 256 B), and the bound tiles:
+    # [H][1024][520] i32, votes [2H] i32 (padded to 256 B), the bound tiles:
     # 1954 superblocks of 256 keys -> 31 windows of 64 -> 62 tiles per head of
-    # (d/16 + 1) chunks of 64 x 16 B
+    # (d/16 + 1) chunks of 64 x 16 B, and the window tiles: 31 windows -> one
+    # pair of tiles per head
     key_order = (2 * 4 * 500_000 * 4 + 2 * 4 * 500_000 * 16 * 2 + 4 * 500_000 * 2 + 4 * 1024 * 34 * 4
                  + 4 * 1024 * 520 * 4
-                 + 256 + 4 * 62 * 2 * 64 * 16)
+                 + 256 + 4 * 62 * 2 * 64 * 16 + 4 * 2 * 2 * 64 * 16)
     assert n == packed + grouping + key_order
     assert lib.kmip_topk_workspace_size(8191, 1, 16, 4, 1) == (256 + 16) * 32 * 16 * 2 + 512
     assert lib.kmip_topk_workspace_size(33, 1, 16, 4, 1) == (2 + 16) * 32 * 16 * 2 + 512
