@@ -34,8 +34,8 @@ constexpr int kChunk = 1024;         // sorted pairs per wave in the reduction
 
 // 1. Per (query, head), a team of 16 lanes with the slots on lanes, NS
 // slots per lane (k <= 16 NS): p, dp, D, g of each selected pair, dQ_i, and
-// (QGt != nullptr, value width DV = D only) the head-major interleaved copy
-// of q_i and dO_i.  D is the query/key width, DV the value width (dp_j runs
+// (QGt != nullptr, value width DV = D only) row qg_row of the interleaved
+// copy of q_i and dO_i.  D is the query/key width, DV the value width (dp_j runs
 // over it).  Slot tl + 16 s of query-head qh leaves its key index in jj[s]
 // (-1: none) and its coefficients a = scale g, p in ca[s], cp[s].  With
 // attention dropout (keep != nullptr, f = keep_scale or 0 by the slot's keep
@@ -46,18 +46,18 @@ __device__ __forceinline__ void coef_one(const uint16_t* __restrict__ Q, const u
                                          const int32_t* __restrict__ idx, const float* __restrict__ lse,
                                          const uint8_t* __restrict__ keep, float keep_scale,
                                          int32_t N, int32_t H, int32_t k, float scale, int64_t qh, int tl,
-                                         float* __restrict__ dQ, uint16_t* __restrict__ QGt, int32_t (&jj)[NS],
+                                         float* __restrict__ dQ, uint16_t* __restrict__ QGt, size_t qg_row,
+                                         int32_t (&jj)[NS],
                                          float (&ca)[NS], float (&cp)[NS]) {
     // key rows kept in registers for dQ when they take at most 64 dwords a
     // lane; otherwise read again (from cache)
     constexpr bool kKeep = D / 2 * NS <= 64;
     const int h = (int)(qh % H);
     if (DV == D && QGt != nullptr && tl < D / 4) {
-        // head-major interleaved copy [H][N][2d]: row h*N + i holds q_i then
-        // dO_i of head h, so the reduction gathers both with one load
-        const size_t ht = ((size_t)h * N + (size_t)(qh / H)) * (2 * D);
+        // interleaved copy: row qg_row holds q_i then dO_i, so the reduction
+        // gathers both with one load
         const uint16_t* src = tl < D / 8 ? Q + (size_t)qh * D : dO + (size_t)qh * D;
-        reinterpret_cast<uint4*>(QGt + ht)[tl] = reinterpret_cast<const uint4*>(src)[tl & (D / 8 - 1)];
+        reinterpret_cast<uint4*>(QGt + qg_row * (2 * D))[tl] = reinterpret_cast<const uint4*>(src)[tl & (D / 8 - 1)];
     }
     float q[D], g[DV];
     load_row_f32<D>(q, Q + (size_t)qh * D);
@@ -146,7 +146,7 @@ __global__ __launch_bounds__(256) void csr_coef_kernel(
     if (qh >= (int64_t)N * H) return;  // whole team exits together
     int32_t jj[NS];
     float ca[NS], cp[NS];
-    coef_one<D, DV, NS>(Q, K, V, dO, idx, lse, keep, keep_scale, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
+    coef_one<D, DV, NS>(Q, K, V, dO, idx, lse, keep, keep_scale, N, H, k, scale, qh, tl, dQ, QGt, 0, jj, ca, cp);
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         const int slot = tl + 16 * s;
@@ -571,13 +571,20 @@ __device__ __forceinline__ int32_t wave_rank(int32_t* ctr, int32_t digit) {
 // round for 8 rounds, ranked by ballots, staged in LDS and written as runs
 // into ranges the workgroup reserves with one atomic per super-bucket.  The
 // coefficients never go to memory.
+// The query-heads are taken in the order u = h N + p, query perm[h][p] at
+// position p of head h: with perm the grouping of the queries by direction,
+// queries that share most of their keys are processed together (their key
+// and value rows are gathered while in cache) and their rows of the
+// interleaved copy, row u, lie side by side, so the reduction's gathers for
+// one key row mostly read neighbouring rows and share cache lines.  The
+// records carry u as their query row.
 template <int D, int NS>
 __global__ __launch_bounds__(256) void coef_split_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
-    int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ, uint16_t* __restrict__ QGt,
-    int32_t shift, int32_t* __restrict__ supcur, PairRecord* __restrict__ mid, const uint8_t* __restrict__ keep,
-    float keep_scale) {
+    const int32_t* __restrict__ perm, int32_t N, int32_t H, int32_t k, float scale, float* __restrict__ dQ,
+    uint16_t* __restrict__ QGt, int32_t shift, int32_t* __restrict__ supcur, PairRecord* __restrict__ mid,
+    const uint8_t* __restrict__ keep, float keep_scale) {
     constexpr int TQ = 8 / NS;   // query-heads per team
     constexpr int R = TQ * NS;   // records per lane: 8
     static_assert(256 * R == kSplitChunk, "one staging chunk per workgroup");
@@ -592,21 +599,25 @@ __global__ __launch_bounds__(256) void coef_split_kernel(
     int32_t sup[R], slot[R];
 #pragma unroll
     for (int it = 0; it < TQ; ++it) {
-        const int64_t qh = (int64_t)blockIdx.x * (16 * TQ) + it * 16 + team;
+        const int64_t u = (int64_t)blockIdx.x * (16 * TQ) + it * 16 + team;
+        const int32_t h = u < nh ? (int32_t)(u / N) : 0;
+        const int32_t i = u < nh ? perm[u] : 0;
+        const int64_t qh = (int64_t)i * H + h;
         int32_t jj[NS];
         float ca[NS], cp[NS];
 #pragma unroll
         for (int s2 = 0; s2 < NS; ++s2) jj[s2] = -1;
-        if (qh < nh) coef_one<D, D, NS>(Q, K, V, dO, idx, lse, keep, keep_scale, N, H, k, scale, qh, tl, dQ, QGt, jj, ca, cp);
-        const int32_t h = (int32_t)(qh % H), i = (int32_t)(qh / H);
+        if (u < nh)
+            coef_one<D, D, NS>(Q, K, V, dO, idx, lse, keep, keep_scale, N, H, k, scale, qh, tl, dQ, QGt, (size_t)u, jj,
+                               ca, cp);
 #pragma unroll
         for (int s2 = 0; s2 < NS; ++s2) {
             const int r = it * NS + s2;
             sup[r] = -1;
             rr[r] = PairRecord{-1, 0, 0.0f, 0.0f};
-            if (qh < nh && jj[s2] >= 0) {
+            if (u < nh && jj[s2] >= 0) {
                 const int32_t row = jj[s2] * H + h;
-                rr[r] = PairRecord{row, h * N + i, ca[s2], cp[s2]};
+                rr[r] = PairRecord{row, (int32_t)u, ca[s2], cp[s2]};
                 sup[r] = (row >> shift) / kSupBuckets;
             }
         }
@@ -641,13 +652,13 @@ __global__ __launch_bounds__(256) void coef_split_kernel(
 template <int D>
 hipError_t launch_coef_split(int32_t nh, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
                              const uint16_t* v, const uint16_t* g, const int32_t* idx, const float* lse,
-                             int32_t N, int32_t H, int32_t k, float scale, float* dQ, uint16_t* qg,
-                             int32_t shift, int32_t* supcur, PairRecord* mid, const uint8_t* keep,
+                             const int32_t* perm, int32_t N, int32_t H, int32_t k, float scale, float* dQ,
+                             uint16_t* qg, int32_t shift, int32_t* supcur, PairRecord* mid, const uint8_t* keep,
                              float keep_scale) {
     const int ns = (k + 15) / 16;
 #define KMIP_COEF_SPLIT(NSV)                                                                           \
     hipLaunchKernelGGL((coef_split_kernel<D, NSV>), dim3((unsigned)((nh + 128 / NSV - 1) / (128 / NSV))),   \
-                       dim3(256), 0, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur, mid, \
+                       dim3(256), 0, stream, q, kk, v, g, idx, lse, perm, N, H, k, scale, dQ, qg, shift, supcur, mid, \
                        keep, keep_scale)
     if (ns <= 1)
         KMIP_COEF_SPLIT(1);
@@ -961,7 +972,7 @@ size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k) {
     const size_t nb = (nbk + 1 + kScanBlock - 1) / kScanBlock;
     return al(pairs * sizeof(BucketRecord)) + 3 * al((nbk + 1) * sizeof(int32_t)) +
            al((nb + 1) * sizeof(int32_t)) + al(nh * 2 * d * sizeof(uint16_t)) + al(pairs * sizeof(PairRecord)) +
-           3 * al((kMaxSup + 1) * sizeof(int32_t));
+           3 * al((kMaxSup + 1) * sizeof(int32_t)) + al(group_workspace_bytes(N, H, d));
 }
 
 hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const void* dO,
@@ -988,7 +999,7 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     p += al(((size_t)nbk + 1) * sizeof(int32_t));
     int32_t* sums = reinterpret_cast<int32_t*>(p);
     p += al(((size_t)nb + 1) * sizeof(int32_t));
-    uint16_t* qg = reinterpret_cast<uint16_t*>(p);   // q and dO interleaved, head-major, [H][N][2d]
+    uint16_t* qg = reinterpret_cast<uint16_t*>(p);   // q and dO interleaved, row h N + p for query perm[h][p]
     p += al((size_t)nh * 2 * d * sizeof(uint16_t));
     PairRecord* mid = reinterpret_cast<PairRecord*>(p);   // records in super-bucket order (pass 1)
     p += al(pairs * sizeof(PairRecord));
@@ -997,12 +1008,16 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     int32_t* supcur = reinterpret_cast<int32_t*>(p);
     p += al((kMaxSup + 1) * sizeof(int32_t));
     int32_t* pstart2 = reinterpret_cast<int32_t*>(p);
+    p += al((kMaxSup + 1) * sizeof(int32_t));
+    void* gws = p;   // grouping of the queries by direction (group.hip)
 
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
     const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
     const uint16_t* g = reinterpret_cast<const uint16_t*>(dO);
     hipError_t e;
+    QueryGroups groups{};
+    if ((e = launch_group_queries(Q, N, H, d, gws, &groups, stream)) != hipSuccess) return e;
     if ((e = launch_fill_zero(reinterpret_cast<float*>(gcnt), ((size_t)nbk + 1 + 3) / 4 * 4, stream)) != hipSuccess)
         return e;
     if ((e = launch_fill_zero(dK, (size_t)nh * d, stream)) != hipSuccess) return e;
@@ -1042,13 +1057,13 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // coefficients, dQ and the interleaved copy, fused with placement pass 1
     if (d == 16)
-        e = launch_coef_split<16>((int32_t)nh, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur,
+        e = launch_coef_split<16>((int32_t)nh, stream, q, kk, v, g, idx, lse, groups.perm, N, H, k, scale, dQ, qg, shift, supcur,
                                   mid, keep, keep_scale);
     else if (d == 32)
-        e = launch_coef_split<32>((int32_t)nh, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur,
+        e = launch_coef_split<32>((int32_t)nh, stream, q, kk, v, g, idx, lse, groups.perm, N, H, k, scale, dQ, qg, shift, supcur,
                                   mid, keep, keep_scale);
     else
-        e = launch_coef_split<64>((int32_t)nh, stream, q, kk, v, g, idx, lse, N, H, k, scale, dQ, qg, shift, supcur,
+        e = launch_coef_split<64>((int32_t)nh, stream, q, kk, v, g, idx, lse, groups.perm, N, H, k, scale, dQ, qg, shift, supcur,
                                   mid, keep, keep_scale);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(bkt_split2_kernel, dim3((unsigned)(nsup + (pairs + kSplitChunk - 1) / kSplitChunk)), dim3(256),

@@ -88,7 +88,9 @@ def test_workspace_size(lib):
     # interleaved copy of Q and dO (bf16, 2d per query-head)
     # ... and the records in super-bucket order between the two placement
     # passes (16 B), with three arrays of 65 super-bucket entries
-    bucket = 32000 * 12 + 3 * 256 + 256 + 2 * 2000 * 32 * 2 + 32000 * 16 + 3 * 512
+    # ... and the grouping of the queries by direction, the order in which the
+    # coefficient pass takes them (the key-aggregated variant's workspace)
+    bucket = 32000 * 12 + 3 * 256 + 256 + 2 * 2000 * 32 * 2 + 32000 * 16 + 3 * 512 + agg
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, _lib.BWD_BUCKETED) == bucket
     # the library picks the bucketed reduction where it fits
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 0) == bucket
