@@ -220,7 +220,10 @@ __device__ __forceinline__ uint64_t min_u64(uint64_t a, uint64_t b) { return b <
 
 // At least one wave per SIMD: the kernel may use the whole register file
 // rather than have the compiler trade registers for occupancy by spilling.
-template <int D, int QB, int SLOTS>
+// LBMAX: the loser trees' replay path, at least ceil(log2 k) levels (5 for
+// k <= 32, 7 for k <= 128); a longer path costs the levels it does not need
+// on every insertion.
+template <int D, int QB, int SLOTS, int LBMAX>
 __global__ __launch_bounds__(64, 1) void select_kernel(
     const uint4* __restrict__ kp, const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const Task* __restrict__ tasks, const int32_t* __restrict__ qperm,
@@ -233,8 +236,8 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     constexpr int TILE_BYTES = NC * 64 * 16;
     constexpr int SBT = kSuperTiles;
     extern __shared__ uint64_t lds[];
-    // loser trees of 2^lb leaves, lb <= LBMAX (k <= 32 with two blocks)
-    constexpr int LBMAX = QB == 2 ? 5 : 7;
+    // loser trees of 2^lb leaves, lb <= LBMAX
+    static_assert(QB == 1 || LBMAX == 5, "two query blocks take k <= 32");
     const int lb = k <= 1 ? 0 : 32 - __clz(k - 1);
     const int hrows = 1 << lb;
     const uint64_t leaf_mask = (uint64_t)(hrows - 1);
@@ -1092,7 +1095,7 @@ __global__ __launch_bounds__(256) void pack_k_kernel(const uint16_t* __restrict_
     kp[u] = v;
 }
 
-template <int D, int QB, int SLOTS>
+template <int D, int QB, int SLOTS, int LBMAX>
 hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const Task* tasks,
                            const QueryGroups* groups, const KeyOrder* keys, int32_t ntasks, int32_t N,
                            int32_t H, int32_t k, int32_t ntiles, int32_t* work_ctr, int32_t* topk_idx,
@@ -1105,14 +1108,14 @@ hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const T
     // not know about: a spill of a prefetch register would save it before its
     // load lands.  Refuse to run a build in which the kernel uses scratch.
     hipFuncAttributes fa;
-    hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(select_kernel<D, QB, SLOTS>));
+    hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(select_kernel<D, QB, SLOTS, LBMAX>));
     if (e != hipSuccess) return e;
     if (fa.localSizeBytes != 0) return hipErrorInvalidDeviceFunction;
     int dev = 0, cus = 0, per_cu = 0;
     e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_kernel<D, QB, SLOTS>, 64, lds);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_kernel<D, QB, SLOTS, LBMAX>, 64, lds);
     if (e != hipSuccess) return e;
     // work_ctr: kNumXcd item counters, then kNumXcd pacers (all fields 0).
     Pacer* pacers = reinterpret_cast<Pacer*>(work_ctr + kNumXcd);
@@ -1122,7 +1125,7 @@ hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const T
     const int64_t want = std::min<int64_t>(slots, (items + kNumXcd - 1) / kNumXcd * kNumXcd);
     const int64_t grid = std::max<int64_t>(kNumXcd, want / kNumXcd * kNumXcd);
     if (ev_start != nullptr && (e = hipEventRecord(ev_start, stream)) != hipSuccess) return e;
-    hipLaunchKernelGGL((select_kernel<D, QB, SLOTS>), dim3((unsigned)grid), dim3(64), lds, stream,
+    hipLaunchKernelGGL((select_kernel<D, QB, SLOTS, LBMAX>), dim3((unsigned)grid), dim3(64), lds, stream,
                        reinterpret_cast<const uint4*>(kp), reinterpret_cast<const uint16_t*>(Q),
                        reinterpret_cast<const uint16_t*>(K), tasks, groups ? groups->perm : nullptr,
                        groups ? groups->label : nullptr, groups ? groups->seed_ref : nullptr,
@@ -1161,13 +1164,14 @@ hipError_t launch_select(const void* kp, const void* Q, const void* K, const Tas
                          int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream,
                          hipEvent_t ev_start, hipEvent_t ev_stop) {
     if (ntasks <= 0) return hipSuccess;
-#define KMIP_SELECT_CASE(DD, QQ, SS)                                                             \
-    if (d == DD && shape.qb == QQ && shape.slots == SS)                                          \
-        return launch_select_t<DD, QQ, SS>(kp, Q, K, tasks, groups, keys, ntasks, N, H, k, ntiles, \
+#define KMIP_SELECT_CASE(DD, QQ, SS, LL)                                                         \
+    if (d == DD && shape.qb == QQ && shape.slots == SS && (k <= 32 ? 5 : 7) == LL)               \
+        return launch_select_t<DD, QQ, SS, LL>(kp, Q, K, tasks, groups, keys, ntasks, N, H, k, ntiles, \
                                            work_ctr, topk_idx, stream, ev_start, ev_stop);
 #define KMIP_SELECT_D(DD)         \
-    KMIP_SELECT_CASE(DD, 2, 4)    \
-    KMIP_SELECT_CASE(DD, 1, 8)
+    KMIP_SELECT_CASE(DD, 2, 4, 5) \
+    KMIP_SELECT_CASE(DD, 1, 8, 5) \
+    KMIP_SELECT_CASE(DD, 1, 8, 7)
     KMIP_SELECT_D(16)
     KMIP_SELECT_D(32)
     KMIP_SELECT_D(64)
