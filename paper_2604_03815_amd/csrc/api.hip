@@ -239,26 +239,34 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
     const int32_t qb = shape.qb;
 
     const kmip::Task* dtasks = nullptr;
-    int32_t ntasks = 0;
+    int32_t ntasks = 0, nsmall = 0;
     if (G > 1) {
         // Block-diagonal batch: one task per run of 32*qb queries of a graph,
-        // heaviest first (cost ~ queries x keys) to balance the tail.
+        // heaviest first (cost ~ queries x keys) to balance the tail.  The
+        // tasks of graphs of at most kSmallGraph nodes (runs of 32 queries)
+        // come first and go to the small-graph select.
         std::vector<kmip::Task> tasks;
         tasks.reserve(max_tasks(N, G));
-        const int32_t step = 32 * qb;
-        for (int32_t g = 0; g < G; ++g) {
-            const int32_t lo = graph_offsets[g], hi = graph_offsets[g + 1];
-            for (int32_t q0 = lo; q0 < hi; q0 += step)
-                tasks.push_back(kmip::Task{q0, std::min(step, hi - q0), lo, hi});
+        for (int pass = 0; pass < 2; ++pass) {
+            const size_t first = tasks.size();
+            for (int32_t g = 0; g < G; ++g) {
+                const int32_t lo = graph_offsets[g], hi = graph_offsets[g + 1];
+                const bool small = hi - lo <= kmip::kSmallGraph;
+                if (small != (pass == 0)) continue;
+                const int32_t step = small ? 32 : 32 * qb;
+                for (int32_t q0 = lo; q0 < hi; q0 += step)
+                    tasks.push_back(kmip::Task{q0, std::min(step, hi - q0), lo, hi});
+            }
+            std::stable_sort(tasks.begin() + first, tasks.end(), [](const kmip::Task& a, const kmip::Task& b) {
+                return (int64_t)a.q_count * (a.key_hi - a.key_lo) > (int64_t)b.q_count * (b.key_hi - b.key_lo);
+            });
+            if (pass == 0) nsmall = (int32_t)tasks.size();
         }
-        std::stable_sort(tasks.begin(), tasks.end(), [](const kmip::Task& a, const kmip::Task& b) {
-            return (int64_t)a.q_count * (a.key_hi - a.key_lo) > (int64_t)b.q_count * (b.key_hi - b.key_lo);
-        });
-        ntasks = (int32_t)tasks.size();
+        ntasks = (int32_t)tasks.size() - nsmall;
         void* dst = ws + tiled_bytes(N, H, d) + kCounterBytes;
         hipError_t e = upload_async(dst, tasks.data(), tasks.size() * sizeof(kmip::Task), stream);
         if (e != hipSuccess) return hip_fail(e, "work list upload");
-        dtasks = reinterpret_cast<const kmip::Task*>(dst);
+        dtasks = reinterpret_cast<const kmip::Task*>(dst) + nsmall;
     } else {
         ntasks = (int32_t)((N + 32 * qb - 1) / (32 * qb));
     }
@@ -280,11 +288,23 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
                                           stream);
     if (e != hipSuccess) return hip_fail(e, "pack_k launch");
     int32_t* work_ctr = reinterpret_cast<int32_t*>(ws + tiled_bytes(N, H, d));
-    e = kmip::launch_select(kp, Q, K, dtasks, grouped ? &groups : nullptr, grouped ? &keys : nullptr,
-                            ntasks, n32, H, d, k, ntiles, shape, work_ctr, topk_idx, stream,
-                            reinterpret_cast<hipEvent_t>(select_start),
-                            reinterpret_cast<hipEvent_t>(select_stop));
-    if (e != hipSuccess) return hip_fail(e, "select launch");
+    hipEvent_t ev_start = reinterpret_cast<hipEvent_t>(select_start);
+    hipEvent_t ev_stop = reinterpret_cast<hipEvent_t>(select_stop);
+    if (nsmall > 0) {
+        // the events bracket both select launches
+        if (ev_start != nullptr && (e = hipEventRecord(ev_start, stream)) != hipSuccess)
+            return hip_fail(e, "event record");
+        ev_start = nullptr;
+        e = kmip::launch_small_select(kp, Q, dtasks - nsmall, nsmall, n32, H, d, k, ntiles, topk_idx, stream);
+        if (e != hipSuccess) return hip_fail(e, "small-graph select launch");
+    }
+    if (ntasks > 0) {
+        e = kmip::launch_select(kp, Q, K, dtasks, grouped ? &groups : nullptr, grouped ? &keys : nullptr,
+                                ntasks, n32, H, d, k, ntiles, shape, work_ctr, topk_idx, stream, ev_start, ev_stop);
+        if (e != hipSuccess) return hip_fail(e, "select launch");
+    } else if (ev_stop != nullptr && (e = hipEventRecord(ev_stop, stream)) != hipSuccess) {
+        return hip_fail(e, "event record");
+    }
     return ok();
 }
 

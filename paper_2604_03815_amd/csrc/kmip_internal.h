@@ -114,6 +114,17 @@ hipError_t launch_select(const void* kp, const void* Q, const void* K, const Tas
 // Bytes of LDS one select workgroup uses.
 size_t select_lds_bytes(int32_t k, SelectShape shape);
 
+// Graphs of a block-diagonal batch with at most this many nodes go to the
+// small-graph select (small_select.hip), which keeps a whole graph's scores
+// of 32 queries in LDS.
+constexpr int kSmallGraph = 480;
+
+// Score + select for tasks of at most 32 queries whose graphs hold at most
+// kSmallGraph nodes (same results as launch_select).
+hipError_t launch_small_select(const void* kp, const void* Q, const Task* tasks, int32_t ntasks, int32_t N,
+                               int32_t H, int32_t d, int32_t k, int32_t ntiles, int32_t* topk_idx,
+                               hipStream_t stream);
+
 // Query grouping by direction (group.hip): reference directions per head.
 constexpr int kGroupCenters = 256;
 

@@ -171,6 +171,46 @@ def test_exact_ties_integer_inputs(d):
     np.testing.assert_array_equal(res["idx"], o_idx)
 
 
+# Block-diagonal batches of graphs of at most 480 nodes go to the small-graph
+# select (scores of a whole graph in LDS, threshold by bisection, order by
+# rank); larger graphs of the same batch to the streaming kernel.  Integer
+# inputs make ties everywhere, so rows must match the oracle's index for
+# index (tie rule and order included).
+SMALL_GRAPH_BATCHES = [
+    # (d, k, sizes)
+    (16, 1, [480, 481, 3, 0, 200]),
+    (32, 7, [5, 480, 1, 64, 479]),
+    (64, 32, [33, 31, 300, 0, 2]),
+    (16, 128, [128, 127, 129, 480, 90]),
+    (32, 16, [450] * 6 + [100] * 5),
+]
+
+
+@pytest.mark.parametrize("d,k,sizes", SMALL_GRAPH_BATCHES, ids=lambda c: str(c))
+def test_small_graph_batches_integer_ties(d, k, sizes):
+    rng = np.random.default_rng(sum(sizes) + d + k)
+    N, H = sum(sizes), 2
+    q = rng.integers(-2, 3, size=(N, H, d)).astype(np.float32)
+    kk = rng.integers(-1, 2, size=(N, H, d)).astype(np.float32)
+    v = rng.standard_normal((N, H, d)).astype(np.float32)
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    w = workloads.Workload("small_ties", N, H, d, k, 0.25, offsets, workloads.bf16_round(q),
+                           workloads.bf16_round(kk), workloads.bf16_round(v), None, False)
+    res = _run(w, backward=False)
+    Qd, Kd, Vd, _ = _f64(w)
+    _, o_idx, _ = oracle.forward(Qd, Kd, Vd, k, w.scale, offsets=offsets)
+    np.testing.assert_array_equal(res["idx"], o_idx)
+    ref_out, _ = oracle.attend(Qd, Kd, Vd, res["idx"], w.scale)
+    allclose_report("out", res["out"].reshape(-1, d), ref_out)
+
+
+def test_small_graph_batch_normal_rows():
+    # i.i.d. normal rows in graphs around the size limit: full protocol
+    sizes = [480, 479, 481, 250, 17, 0, 480]
+    w = workloads.iid(sum(sizes), 3, 32, 24, seed=480, sizes=sizes)
+    _check_all(w, _run(w))
+
+
 def test_all_scores_tied():
     # Q = 0: every score is 0, so each query keeps the k lowest indices of its graph.
     N, H, d, k = 200, 1, 32, 16
