@@ -30,8 +30,15 @@
  *  - Ties between equal scores go to the lower node id.  The query's own
  *    key is a candidate.  `scale` must be finite and > 0; selection uses the
  *    raw scores, which for scale > 0 is the same as the scaled scores.
- *  - Supported sizes: d in {16, 32, 64}; 1 <= k <= 128; H >= 1;
- *    0 <= N < 2^31 and N * H * max(d, k) < 2^31.
+ *  - Supported sizes: d in {16, 32, 64, 128}; 1 <= k <= KMIP_MAX_K (512)
+ *    for d <= 64 and 1 <= k <= KMIP_MAX_K_WIDE (128) for d = 128; H >= 1;
+ *    0 <= N < 2^31 and N * H * max(d, k) < 2^31.  (The bound on N * H * k
+ *    is also what keeps node ids below 2^(32 - ceil(log2 k)), the room the
+ *    select kernel's on-chip trees leave for an index.)  The fastest paths
+ *    are those of d <= 64 and k <= 128: the direction grouping and the key
+ *    order with bounds that let the select kernel skip key blocks are built
+ *    for d <= 64 only, and a larger k gives the kernel larger trees in LDS
+ *    (fewer resident waves).
  *  - stream: a hipStream_t (NULL = the default stream).  Every call is
  *    asynchronous on `stream`; the caller synchronises.
  *  - Ownership: the caller allocates every buffer (inputs, outputs and the
@@ -59,12 +66,13 @@ extern "C" {
 typedef enum {
     KMIP_OK = 0,
     KMIP_ERR_INVALID_ARG = 1, /* null buffer, bad size, bad offsets, bad scale */
-    KMIP_ERR_UNSUPPORTED = 2, /* d or k outside the compiled set */
+    KMIP_ERR_UNSUPPORTED = 2, /* d, d_V, k or variant outside the compiled set */
     KMIP_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
     KMIP_ERR_HIP = 4          /* a HIP launch or copy failed; see kmip_last_error() */
 } kmip_status_t;
 
-#define KMIP_MAX_K 128
+#define KMIP_MAX_K 512      /* largest k for d <= 64 */
+#define KMIP_MAX_K_WIDE 128 /* largest k for d = 128 */
 
 /*
  * Bytes of device workspace kmip_topk / kmip_fwd need for these sizes
@@ -127,7 +135,7 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
  *  - value rows of their own width (Section 3.1: W_Q and W_K project to
  *    d_K dimensions, W_V to d_V): Q and K are [N, H, d] with d = d_K, which
  *    alone decides the selection; V and out are [N, H, dv] with
- *    dv = d_V in {16, 32, 64};
+ *    dv = d_V in {16, 32, 64, 128};
  *  - attention dropout (the experimental details list an attention-dropout
  *    rate): keep is uint8 [N, H, k] device memory aligned with the topk_idx
  *    slots, drawn by the caller (nonzero keeps the slot); the kept weights
@@ -179,8 +187,8 @@ kmip_status_t kmip_fwd_ex(const void* Q, const void* K, const void* V, const int
  *                to 512 while N*H would need more than 8192 buckets; each
  *                bucket's records are sorted by key row in LDS, at most 8192
  *                at a time, and reduced as in SEGMENTED; needs
- *                N*H <= 8192*512 (else KMIP_ERR_UNSUPPORTED and workspace
- *                size 0);
+ *                N*H <= 8192*512, d <= 64 and k <= 128 (else
+ *                KMIP_ERR_UNSUPPORTED and workspace size 0);
  *            KMIP_BWD_KEY_AGGREGATED: queries are grouped by direction, each
  *                workgroup of 256 queries sums its pairs per key in LDS and
  *                adds each key's sums once;
@@ -206,7 +214,7 @@ kmip_status_t kmip_bwd(const void* Q, const void* K, const void* V, const void* 
 
 /*
  * kmip_bwd for the extended forward: value rows of width dv = d_V in
- * {16, 32, 64} (V, dOut bf16 [N, H, dv] and dV float32 [N, H, dv]; Q, K,
+ * {16, 32, 64, 128} (V, dOut bf16 [N, H, dv] and dV float32 [N, H, dv]; Q, K,
  * dQ, dK stay [N, H, d]; dp_j = dOut_i . v_j runs over the dv value
  * dimensions) and the forward's dropout draws keep / drop_rate (with
  * f_j = 1/(1 - drop_rate) for a kept slot and 0 for a dropped one, dV_j gets

@@ -18,10 +18,10 @@ from typing import Optional, Sequence
 
 import numpy as np
 
-from ._lib import KmipError, MAX_K, NOALLOC_SCRATCH_BYTES, check, load
+from ._lib import KmipError, MAX_K, MAX_K_WIDE, NOALLOC_SCRATCH_BYTES, check, load
 
 __all__ = [
-    "KmipError", "MAX_K", "NOALLOC_SCRATCH_BYTES", "topk", "attend", "fwd", "fwd_noalloc", "bwd",
+    "KmipError", "MAX_K", "MAX_K_WIDE", "NOALLOC_SCRATCH_BYTES", "topk", "attend", "fwd", "fwd_noalloc", "bwd",
     "attention", "topk_workspace_size", "bwd_workspace_size", "Workspace", "load", "KMIPAttention",
     "linear_k_schedule",
 ]

@@ -12,7 +12,8 @@ KMIP_ERR_INVALID_ARG = 1
 KMIP_ERR_UNSUPPORTED = 2
 KMIP_ERR_WORKSPACE = 3
 KMIP_ERR_HIP = 4
-MAX_K = 128
+MAX_K = 512        # largest k for d <= 64
+MAX_K_WIDE = 128   # largest k for d = 128
 
 # kmip_bwd_variant_t
 BWD_AUTO = 0

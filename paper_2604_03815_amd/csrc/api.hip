@@ -98,8 +98,10 @@ kmip_status_t check_sizes(int64_t N, int32_t H, int32_t d, int32_t k) {
     if (N < 0 || N >= (int64_t(1) << 31)) return record_error(KMIP_ERR_INVALID_ARG, "N=%lld out of range", (long long)N);
     if (H < 1) return record_error(KMIP_ERR_INVALID_ARG, "H=%d must be >= 1", H);
     if (k < 1) return record_error(KMIP_ERR_INVALID_ARG, "k=%d must be >= 1", k);
-    if (d != 16 && d != 32 && d != 64) return record_error(KMIP_ERR_UNSUPPORTED, "d=%d not in {16, 32, 64}", d);
-    if (k > KMIP_MAX_K) return record_error(KMIP_ERR_UNSUPPORTED, "k=%d exceeds %d", k, KMIP_MAX_K);
+    if (d != 16 && d != 32 && d != 64 && d != 128)
+        return record_error(KMIP_ERR_UNSUPPORTED, "d=%d not in {16, 32, 64, 128}", d);
+    const int32_t kmax = d == 128 ? KMIP_MAX_K_WIDE : KMIP_MAX_K;
+    if (k > kmax) return record_error(KMIP_ERR_UNSUPPORTED, "k=%d exceeds %d for d=%d", k, kmax, d);
     const int64_t wide = N * (int64_t)H * std::max<int64_t>(d, k);
     if (wide >= (int64_t(1) << 31)) return record_error(KMIP_ERR_INVALID_ARG, "N*H*max(d,k) >= 2^31");
     return KMIP_OK;
@@ -107,7 +109,8 @@ kmip_status_t check_sizes(int64_t N, int32_t H, int32_t d, int32_t k) {
 
 // The value width, besides the sizes check_sizes covers.
 kmip_status_t check_value_width(int64_t N, int32_t H, int32_t dv) {
-    if (dv != 16 && dv != 32 && dv != 64) return record_error(KMIP_ERR_UNSUPPORTED, "d_V=%d not in {16, 32, 64}", dv);
+    if (dv != 16 && dv != 32 && dv != 64 && dv != 128)
+        return record_error(KMIP_ERR_UNSUPPORTED, "d_V=%d not in {16, 32, 64, 128}", dv);
     if (N * (int64_t)H * dv >= (int64_t(1) << 31)) return record_error(KMIP_ERR_INVALID_ARG, "N*H*d_V >= 2^31");
     return KMIP_OK;
 }
@@ -158,20 +161,27 @@ constexpr size_t kCounterBytes = kmip::kSelectCounterBytes;
 // Upper bound on the work-list length for any query-block size.
 size_t max_tasks(int64_t N, int32_t G) { return (size_t)(N / 32 + G + 1); }
 
-// Query blocks of 32 per wave: two when k is small and there are enough
-// items to fill the chip, one otherwise (bounded by LDS per workgroup).
+// Query blocks of 32 per wave: two when k and d are small and there are
+// enough items to fill the chip, one otherwise (bounded by LDS per workgroup
+// and, at d = 128, by registers).
 // Candidate slots per lane: few, since LDS bounds the resident waves per CU
 // and occupancy pays more than the extra merges cost (4 with two blocks, 8
 // with one, measured on the 100k/500k/262k-node workloads).
-kmip::SelectShape choose_shape(int64_t N, int32_t H, int32_t k, int32_t G) {
+kmip::SelectShape choose_shape(int64_t N, int32_t H, int32_t d, int32_t k, int32_t G) {
     const int64_t items = (N + 63) / 64 * H;
-    if (k <= 32 && items >= 8192 && G == 1) return kmip::SelectShape{2, 4};
+    if (k <= 32 && d <= 64 && items >= 8192 && G == 1) return kmip::SelectShape{2, 4};
     return kmip::SelectShape{1, 8};
 }
 
-// Queries are grouped by direction (group.hip) for a single graph large
-// enough for the pre-pass to pay off.
-bool use_grouping(int64_t N, int32_t G) { return G == 1 && N >= 8192; }
+// Queries are grouped by direction (group.hip) and keys stored in bounded
+// superblocks (keyorder.hip) for a single graph large enough for the
+// pre-passes to pay off, at d <= 64 (the key-order kernels are built for
+// those widths).
+bool use_grouping(int64_t N, int32_t G, int32_t d) { return G == 1 && N >= 8192 && d <= 64; }
+
+// The small-graph select keeps up to KMIP_MAX_K_WIDE candidates per query
+// in LDS and is built for d <= 64; other tasks go to the streaming kernel.
+bool small_select_ok(int32_t d, int32_t k) { return d <= 64 && k <= KMIP_MAX_K_WIDE; }
 
 }  // namespace
 
@@ -195,7 +205,7 @@ size_t kmip_topk_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k, int3
     const int32_t G = num_graphs < 1 ? 1 : num_graphs;
     size_t bytes = tiled_bytes(N, H, d) + kCounterBytes;
     if (G > 1) bytes += align_up(max_tasks(N, G) * sizeof(kmip::Task));
-    if (use_grouping(N, G))
+    if (use_grouping(N, G, d))
         bytes += align_up(kmip::group_workspace_bytes((int32_t)N, H, d)) +
                  align_up(kmip::key_order_workspace_bytes((int32_t)N, H, d));
     return bytes;
@@ -235,7 +245,7 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
     const int32_t ntiles = num_tiles(N);
     char* ws = reinterpret_cast<char*>(workspace);
     void* kp = ws;
-    const kmip::SelectShape shape = choose_shape(N, H, k, G);
+    const kmip::SelectShape shape = choose_shape(N, H, d, k, G);
     const int32_t qb = shape.qb;
 
     const kmip::Task* dtasks = nullptr;
@@ -244,14 +254,15 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
         // Block-diagonal batch: one task per run of 32*qb queries of a graph,
         // heaviest first (cost ~ queries x keys) to balance the tail.  The
         // tasks of graphs of at most kSmallGraph nodes (runs of 32 queries)
-        // come first and go to the small-graph select.
+        // come first and go to the small-graph select (for the sizes it
+        // takes).
         std::vector<kmip::Task> tasks;
         tasks.reserve(max_tasks(N, G));
         for (int pass = 0; pass < 2; ++pass) {
             const size_t first = tasks.size();
             for (int32_t g = 0; g < G; ++g) {
                 const int32_t lo = graph_offsets[g], hi = graph_offsets[g + 1];
-                const bool small = hi - lo <= kmip::kSmallGraph;
+                const bool small = hi - lo <= kmip::kSmallGraph && small_select_ok(d, k);
                 if (small != (pass == 0)) continue;
                 const int32_t step = small ? 32 : 32 * qb;
                 for (int32_t q0 = lo; q0 < hi; q0 += step)
@@ -275,7 +286,7 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
     // superblock order with bounds.
     kmip::QueryGroups groups{};
     kmip::KeyOrder keys{};
-    const bool grouped = use_grouping(N, G);
+    const bool grouped = use_grouping(N, G, d);
     if (grouped) {
         char* gws = ws + tiled_bytes(N, H, d) + kCounterBytes;
         hipError_t e = kmip::launch_group_queries(Q, n32, H, d, gws, &groups, stream);
@@ -359,18 +370,18 @@ kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_
 }
 
 // Backward variant the library picks (KMIP_BWD_AUTO): the bucketed reduction
-// where the key rows fit its bucket table and the value width equals the
-// key width, else the full key sort.
-static int32_t default_bwd_variant(int64_t N, int32_t H, int32_t d, int32_t dv) {
-    return dv == d && kmip::bwd_bucket_supported((int32_t)N, H, d) ? KMIP_BWD_BUCKETED : KMIP_BWD_SEGMENTED;
+// where the key rows fit its bucket table, the sizes are its own and the
+// value width equals the key width, else the full key sort.
+static int32_t default_bwd_variant(int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k) {
+    return dv == d && kmip::bwd_bucket_supported((int32_t)N, H, d, k) ? KMIP_BWD_BUCKETED : KMIP_BWD_SEGMENTED;
 }
 
 size_t kmip_bwd_ex_workspace_size(int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k, int32_t variant) {
     if (check_sizes(N, H, d, k) != KMIP_OK || check_value_width(N, H, dv) != KMIP_OK) return 0;
-    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d, dv) : variant;
+    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d, dv, k) : variant;
     if (v == KMIP_BWD_KEY_AGGREGATED) return align_up(kmip::bwd_agg_workspace_bytes((int32_t)N, H, d));
     if (v == KMIP_BWD_SEGMENTED) return align_up(kmip::bwd_csr_workspace_bytes((int32_t)N, H, k));
-    if (v == KMIP_BWD_BUCKETED) return dv == d && kmip::bwd_bucket_supported((int32_t)N, H, d)
+    if (v == KMIP_BWD_BUCKETED) return dv == d && kmip::bwd_bucket_supported((int32_t)N, H, d, k)
                                          ? align_up(kmip::bwd_bucket_workspace_bytes((int32_t)N, H, d, k))
                                          : 0;
     return 0;
@@ -401,7 +412,7 @@ kmip_status_t kmip_bwd_ex(const void* Q, const void* K, const void* V, const voi
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(dOut))
         return record_error(KMIP_ERR_INVALID_ARG, "Q, K, V and dOut must be 16-byte aligned");
     if (!aligned16(dK) || !aligned16(dV)) return record_error(KMIP_ERR_INVALID_ARG, "dK and dV must be 16-byte aligned");
-    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d, dv) : variant;
+    const int32_t v = variant == KMIP_BWD_AUTO ? default_bwd_variant(N, H, d, dv, k) : variant;
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
     hipError_t e;
     if (v != KMIP_BWD_ATOMIC) {
@@ -415,8 +426,10 @@ kmip_status_t kmip_bwd_ex(const void* Q, const void* K, const void* V, const voi
         e = kmip::launch_bwd_agg(Q, K, V, dOut, topk_idx, lse, keep, keep_scale, (int32_t)N, H, d, dv, k, scale,
                                  dQ, dK, dV, workspace, stream);
     } else if (v == KMIP_BWD_BUCKETED) {
-        if (!kmip::bwd_bucket_supported((int32_t)N, H, d))
-            return record_error(KMIP_ERR_UNSUPPORTED, "the bucketed variant needs N*H <= 8192*512 (key-row buckets of at most 512 rows)");
+        if (!kmip::bwd_bucket_supported((int32_t)N, H, d, k))
+            return record_error(KMIP_ERR_UNSUPPORTED,
+                                "the bucketed variant needs d <= 64, k <= 128 and N*H <= 8192*512 (key-row "
+                                "buckets of at most 512 rows)");
         e = kmip::launch_bwd_bucket(Q, K, V, dOut, topk_idx, lse, keep, keep_scale, (int32_t)N, H, d, k, scale,
                                     dQ, dK, dV, workspace, stream);
     } else if (v == KMIP_BWD_SEGMENTED) {

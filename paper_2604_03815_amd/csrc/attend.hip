@@ -121,9 +121,18 @@ void launch_attend_d(unsigned blocks, hipStream_t stream, const uint16_t* q, con
     else if (ns <= 4)
         hipLaunchKernelGGL((attend_kernel<D, DV, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
                            keep_scale, N, H, k, scale, out, lse);
-    else
+    else if (ns <= 8)
         hipLaunchKernelGGL((attend_kernel<D, DV, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
                            keep_scale, N, H, k, scale, out, lse);
+    else if constexpr (D <= 64) {
+        // k > 128 (d <= 64 only)
+        if (ns <= 16)
+            hipLaunchKernelGGL((attend_kernel<D, DV, 16>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
+                               keep_scale, N, H, k, scale, out, lse);
+        else
+            hipLaunchKernelGGL((attend_kernel<D, DV, 32>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
+                               keep_scale, N, H, k, scale, out, lse);
+    }
 }
 
 }  // namespace
@@ -142,10 +151,12 @@ hipError_t launch_attend(const void* Q, const void* K, const void* V, const int3
         launch_attend_d<DD, DVV>(blocks, stream, q, kk, v, idx, keep, keep_scale, N, H, k, scale, out, lse); \
         return hipGetLastError();                                                              \
     }
-#define KMIP_ATTEND_D(DD) KMIP_ATTEND_CASE(DD, 16) KMIP_ATTEND_CASE(DD, 32) KMIP_ATTEND_CASE(DD, 64)
+#define KMIP_ATTEND_D(DD) \
+    KMIP_ATTEND_CASE(DD, 16) KMIP_ATTEND_CASE(DD, 32) KMIP_ATTEND_CASE(DD, 64) KMIP_ATTEND_CASE(DD, 128)
     KMIP_ATTEND_D(16)
     KMIP_ATTEND_D(32)
     KMIP_ATTEND_D(64)
+    KMIP_ATTEND_D(128)
 #undef KMIP_ATTEND_D
 #undef KMIP_ATTEND_CASE
     return hipErrorInvalidValue;

@@ -31,8 +31,6 @@
 namespace kmip {
 namespace {
 
-constexpr int kMaxSlotsPerLane = (128 + 15) / 16;
-
 // Key-aggregated scatter: a workgroup of 16 teams takes kAggQueries
 // consecutive positions of one head in the grouped query order, and sums
 // per key in a table of kSlots keys (32 KB of sums).
@@ -41,7 +39,7 @@ constexpr int kAggQueries = 256;
 template <int D, int DV>
 struct AggTable {
     // the largest power of two with kSlots (D + DV) floats <= 32 KB
-    static constexpr int kSlots = D + DV <= 32 ? 256 : D + DV <= 64 ? 128 : 64;
+    static constexpr int kSlots = D + DV <= 32 ? 256 : D + DV <= 64 ? 128 : D + DV <= 128 ? 64 : 32;
     static constexpr int kProbes = 8;
 };
 
@@ -79,8 +77,8 @@ __device__ __forceinline__ int agg_slot(AggLds<D, DV>* t, int32_t js) {
 // 16 slots is broadcast to the team, which then works with dimensions on
 // lanes.  All 16 pairs' key elements for dQ are loaded before any is used.
 // With tab != nullptr the dK/dV sums go to the workgroup's table when the
-// key has a slot there.
-template <int D, int DV>
+// key has a slot there.  MS: slots per lane the registers hold (k <= 16 MS).
+template <int D, int DV, int MS>
 __device__ __forceinline__ void bwd_query(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
@@ -95,11 +93,11 @@ __device__ __forceinline__ void bwd_query(
     const float l = lse[qh];
 
     const int ns = (k + 15) >> 4;
-    float p[kMaxSlotsPerLane], dp[kMaxSlotsPerLane], pv[kMaxSlotsPerLane];
-    int32_t jj[kMaxSlotsPerLane];
+    float p[MS], dp[MS], pv[MS];
+    int32_t jj[MS];
     float dsum = 0.0f;
 #pragma unroll
-    for (int s = 0; s < kMaxSlotsPerLane; ++s) {
+    for (int s = 0; s < MS; ++s) {
         p[s] = 0.0f;
         dp[s] = 0.0f;
         pv[s] = 0.0f;
@@ -140,7 +138,7 @@ __device__ __forceinline__ void bwd_query(
         for (int u = 0; u < UV; ++u) gd[u] = bf16_bits_to_f32(grow[16 * u]);
     }
 #pragma unroll
-    for (int s = 0; s < kMaxSlotsPerLane; ++s) {
+    for (int s = 0; s < MS; ++s) {
         if (s < ns) {
             const float gs_own = p[s] * (dp[s] - dsum);
             int32_t js[16];
@@ -186,7 +184,7 @@ __device__ __forceinline__ void bwd_query(
 }
 
 // Per-pair scatter: one team per (query, head), 16 per workgroup.
-template <int D, int DV>
+template <int D, int DV, int MS>
 __global__ __launch_bounds__(256) void bwd_atomic_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
@@ -195,13 +193,13 @@ __global__ __launch_bounds__(256) void bwd_atomic_kernel(
     const int tl = threadIdx.x & 15;
     const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
     if (qh >= (int64_t)N * H) return;  // whole team exits together
-    bwd_query<D, DV>(Q, K, V, dO, idx, lse, keep, keep_scale, qh, (int)(qh % H), tl, N, H, k, scale, dQ, dK, dV,
-                     nullptr);
+    bwd_query<D, DV, MS>(Q, K, V, dO, idx, lse, keep, keep_scale, qh, (int)(qh % H), tl, N, H, k, scale, dQ, dK,
+                         dV, nullptr);
 }
 
 // Key-aggregated scatter: one workgroup per kAggQueries positions of head
 // blockIdx.y in the grouped order.
-template <int D, int DV>
+template <int D, int DV, int MS>
 __global__ __launch_bounds__(256) void bwd_agg_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const uint16_t* __restrict__ dO, const int32_t* __restrict__ idx, const float* __restrict__ lse,
@@ -221,7 +219,7 @@ __global__ __launch_bounds__(256) void bwd_agg_kernel(
         const int64_t pos = (int64_t)blockIdx.x * kAggQueries + round * 16 + team;
         if (pos >= N) break;  // positions grow with round: the team is done
         const int64_t qh = (int64_t)perm[(size_t)h * N + pos] * H + h;
-        bwd_query<D, DV>(Q, K, V, dO, idx, lse, keep, keep_scale, qh, h, tl, N, H, k, scale, dQ, dK, dV, &tab);
+        bwd_query<D, DV, MS>(Q, K, V, dO, idx, lse, keep, keep_scale, qh, h, tl, N, H, k, scale, dQ, dK, dV, &tab);
     }
     __syncthreads();
     for (int e = threadIdx.x; e < C * W; e += 256) {
@@ -273,16 +271,26 @@ hipError_t launch_bwd_atomic(const void* Q, const void* K, const void* V, const 
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
     const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
     const uint16_t* g = reinterpret_cast<const uint16_t*>(dO);
-#define KMIP_BWD_ATOMIC_CASE(DD, DVV)                                                                  \
-    if (d == DD && dv == DVV) {                                                                        \
-        hipLaunchKernelGGL((bwd_atomic_kernel<DD, DVV>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, \
-                           idx, lse, N, H, k, scale, dQ, dK, dV, keep, keep_scale);                    \
-        return hipGetLastError();                                                                      \
+    // slots per lane: 8 up to k = 128, 32 beyond (d <= 64 only)
+#define KMIP_BWD_ATOMIC_MS(DD, DVV, MSS)                                                                  \
+    hipLaunchKernelGGL((bwd_atomic_kernel<DD, DVV, MSS>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, \
+                       idx, lse, N, H, k, scale, dQ, dK, dV, keep, keep_scale);
+#define KMIP_BWD_ATOMIC_CASE(DD, DVV)                    \
+    if (d == DD && dv == DVV) {                          \
+        if (k <= 128 || DD == 128) {                     \
+            KMIP_BWD_ATOMIC_MS(DD, DVV, 8)               \
+        } else {                                         \
+            KMIP_BWD_ATOMIC_MS(DD, DVV, (DD == 128 ? 8 : 32)) \
+        }                                                \
+        return hipGetLastError();                        \
     }
-#define KMIP_BWD_ATOMIC_D(DD) KMIP_BWD_ATOMIC_CASE(DD, 16) KMIP_BWD_ATOMIC_CASE(DD, 32) KMIP_BWD_ATOMIC_CASE(DD, 64)
+#define KMIP_BWD_ATOMIC_D(DD) \
+    KMIP_BWD_ATOMIC_CASE(DD, 16) KMIP_BWD_ATOMIC_CASE(DD, 32) KMIP_BWD_ATOMIC_CASE(DD, 64) KMIP_BWD_ATOMIC_CASE(DD, 128)
     KMIP_BWD_ATOMIC_D(16)
     KMIP_BWD_ATOMIC_D(32)
     KMIP_BWD_ATOMIC_D(64)
+    KMIP_BWD_ATOMIC_D(128)
+#undef KMIP_BWD_ATOMIC_MS
 #undef KMIP_BWD_ATOMIC_D
 #undef KMIP_BWD_ATOMIC_CASE
     return hipErrorInvalidValue;
@@ -310,16 +318,25 @@ hipError_t launch_bwd_agg(const void* Q, const void* K, const void* V, const voi
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
     const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
     const uint16_t* g = reinterpret_cast<const uint16_t*>(dO);
-#define KMIP_BWD_AGG_CASE(DD, DVV)                                                                       \
-    if (d == DD && dv == DVV) {                                                                          \
-        hipLaunchKernelGGL((bwd_agg_kernel<DD, DVV>), grid, dim3(256), 0, stream, q, kk, v, g, idx, lse, \
-                           groups.perm, N, H, k, scale, dQ, dK, dV, keep, keep_scale);                   \
-        return hipGetLastError();                                                                        \
+#define KMIP_BWD_AGG_MS(DD, DVV, MSS)                                                                         \
+    hipLaunchKernelGGL((bwd_agg_kernel<DD, DVV, MSS>), grid, dim3(256), 0, stream, q, kk, v, g, idx, lse,    \
+                       groups.perm, N, H, k, scale, dQ, dK, dV, keep, keep_scale);
+#define KMIP_BWD_AGG_CASE(DD, DVV)                     \
+    if (d == DD && dv == DVV) {                        \
+        if (k <= 128 || DD == 128) {                   \
+            KMIP_BWD_AGG_MS(DD, DVV, 8)                \
+        } else {                                       \
+            KMIP_BWD_AGG_MS(DD, DVV, (DD == 128 ? 8 : 32)) \
+        }                                              \
+        return hipGetLastError();                      \
     }
-#define KMIP_BWD_AGG_D(DD) KMIP_BWD_AGG_CASE(DD, 16) KMIP_BWD_AGG_CASE(DD, 32) KMIP_BWD_AGG_CASE(DD, 64)
+#define KMIP_BWD_AGG_D(DD) \
+    KMIP_BWD_AGG_CASE(DD, 16) KMIP_BWD_AGG_CASE(DD, 32) KMIP_BWD_AGG_CASE(DD, 64) KMIP_BWD_AGG_CASE(DD, 128)
     KMIP_BWD_AGG_D(16)
     KMIP_BWD_AGG_D(32)
     KMIP_BWD_AGG_D(64)
+    KMIP_BWD_AGG_D(128)
+#undef KMIP_BWD_AGG_MS
 #undef KMIP_BWD_AGG_D
 #undef KMIP_BWD_AGG_CASE
     return hipErrorInvalidValue;

@@ -170,9 +170,18 @@ void launch_coef(unsigned blocks, hipStream_t stream, const uint16_t* q, const u
     else if (ns <= 4)
         hipLaunchKernelGGL((csr_coef_kernel<D, DV, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
                            N, H, k, scale, dQ, coef, qg, keep, keep_scale);
-    else
+    else if (ns <= 8)
         hipLaunchKernelGGL((csr_coef_kernel<D, DV, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx, lse,
                            N, H, k, scale, dQ, coef, qg, keep, keep_scale);
+    else if constexpr (D <= 64) {
+        // k > 128 (d <= 64 only)
+        if (ns <= 16)
+            hipLaunchKernelGGL((csr_coef_kernel<D, DV, 16>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx,
+                               lse, N, H, k, scale, dQ, coef, qg, keep, keep_scale);
+        else
+            hipLaunchKernelGGL((csr_coef_kernel<D, DV, 32>), dim3(blocks), dim3(256), 0, stream, q, kk, v, g, idx,
+                               lse, N, H, k, scale, dQ, coef, qg, keep, keep_scale);
+    }
 }
 
 // Key row of slot s of query-head qh, or -1 (padding).
@@ -959,7 +968,9 @@ __global__ __launch_bounds__(256) void bkt_reduce_kernel(const uint16_t* __restr
 
 }  // namespace
 
-bool bwd_bucket_supported(int32_t N, int32_t H, int32_t d) {
+bool bwd_bucket_supported(int32_t N, int32_t H, int32_t d, int32_t k) {
+    // the coefficient pass is built for d <= 64 and at most 8 slots a lane
+    if (d > 64 || k > 128) return false;
     const int64_t nh = (int64_t)N * H;
     const int sh = bucket_shift(nh, d);
     return ((nh + (1 << sh) - 1) >> sh) <= kMaxBuckets;
@@ -1131,10 +1142,11 @@ hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const voi
                              keep, keep_scale);                                                          \
         launched = true;                                                                                \
     }
-#define KMIP_CSR_COEF_D(DD) KMIP_CSR_COEF(DD, 16) KMIP_CSR_COEF(DD, 32) KMIP_CSR_COEF(DD, 64)
+#define KMIP_CSR_COEF_D(DD) KMIP_CSR_COEF(DD, 16) KMIP_CSR_COEF(DD, 32) KMIP_CSR_COEF(DD, 64) KMIP_CSR_COEF(DD, 128)
     KMIP_CSR_COEF_D(16)
     KMIP_CSR_COEF_D(32)
     KMIP_CSR_COEF_D(64)
+    KMIP_CSR_COEF_D(128)
 #undef KMIP_CSR_COEF_D
 #undef KMIP_CSR_COEF
     if (!launched) return hipErrorInvalidValue;
@@ -1162,10 +1174,12 @@ hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const voi
     if (d == DD && dv == DVV)                                                                           \
         hipLaunchKernelGGL((csr_reduce_kernel<DD, DVV>), dim3(red_blocks), dim3(256), 0, stream, q, g, rec, \
                            total, dK, dV);
-#define KMIP_CSR_REDUCE_D(DD) KMIP_CSR_REDUCE(DD, 16) KMIP_CSR_REDUCE(DD, 32) KMIP_CSR_REDUCE(DD, 64)
+#define KMIP_CSR_REDUCE_D(DD) \
+    KMIP_CSR_REDUCE(DD, 16) KMIP_CSR_REDUCE(DD, 32) KMIP_CSR_REDUCE(DD, 64) KMIP_CSR_REDUCE(DD, 128)
     KMIP_CSR_REDUCE_D(16)
     KMIP_CSR_REDUCE_D(32)
     KMIP_CSR_REDUCE_D(64)
+    KMIP_CSR_REDUCE_D(128)
 #undef KMIP_CSR_REDUCE_D
 #undef KMIP_CSR_REDUCE
     return hipGetLastError();

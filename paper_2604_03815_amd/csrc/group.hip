@@ -201,8 +201,10 @@ hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, 
         hipLaunchKernelGGL(group_label_kernel<16>, grid, dim3(256), 0, stream, q, centers, N, H, label, hist);
     else if (d == 32)
         hipLaunchKernelGGL(group_label_kernel<32>, grid, dim3(256), 0, stream, q, centers, N, H, label, hist);
-    else
+    else if (d == 64)
         hipLaunchKernelGGL(group_label_kernel<64>, grid, dim3(256), 0, stream, q, centers, N, H, label, hist);
+    else
+        hipLaunchKernelGGL(group_label_kernel<128>, grid, dim3(256), 0, stream, q, centers, N, H, label, hist);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(group_scan_kernel, dim3(H), dim3(C), 0, stream, hist);
     if ((e = hipGetLastError()) != hipSuccess) return e;

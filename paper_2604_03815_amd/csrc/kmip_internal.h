@@ -167,8 +167,9 @@ hipError_t launch_bwd_csr(const void* Q, const void* K, const void* V, const voi
                           float* dK, float* dV, void* ws, hipStream_t stream);
 
 // Backward with pairs bucketed by blocks of key rows and summed in LDS
-// (backward_csr.hip); supported while N * H / (4096 / d) <= 8192.
-bool bwd_bucket_supported(int32_t N, int32_t H, int32_t d);
+// (backward_csr.hip); supported for d <= 64 and k <= 128 while
+// N * H / (4096 / d) <= 8192.
+bool bwd_bucket_supported(int32_t N, int32_t H, int32_t d, int32_t k);
 size_t bwd_bucket_workspace_bytes(int32_t N, int32_t H, int32_t d, int32_t k);
 hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const void* dO,
                              const int32_t* idx, const float* lse, const uint8_t* keep, float keep_scale,

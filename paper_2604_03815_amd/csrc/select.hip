@@ -221,8 +221,8 @@ __device__ __forceinline__ uint64_t min_u64(uint64_t a, uint64_t b) { return b <
 // At least one wave per SIMD: the kernel may use the whole register file
 // rather than have the compiler trade registers for occupancy by spilling.
 // LBMAX: the loser trees' replay path, at least ceil(log2 k) levels (5 for
-// k <= 32, 7 for k <= 128); a longer path costs the levels it does not need
-// on every insertion.
+// k <= 32, 7 for k <= 128, 8 for k <= 256, 9 for k <= 512); a longer path
+// costs the levels it does not need on every insertion.
 template <int D, int QB, int SLOTS, int LBMAX>
 __global__ __launch_bounds__(64, 1) void select_kernel(
     const uint4* __restrict__ kp, const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
@@ -902,8 +902,9 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
     const char* head_tiles = reinterpret_cast<const char*>(kp) + (size_t)head * (ntiles + kPadTiles) * TILE_BYTES;
     const char* graph_tiles = head_tiles + (size_t)t0 * TILE_BYTES;
 
-    // Scores of the tile in ring slot `a`; PF - 1 later tiles are in flight.
-    constexpr int PF = 8 / NC;
+    // Scores of the tile in ring slot `a`; PF - 1 later tiles are in flight
+    // (8 chunk loads in all, two whole tiles at d = 128).
+    constexpr int PF = NC >= 8 ? 2 : 8 / NC;
     static_assert(SBT % PF == 0, "ring slots must line up with superblocks");
     auto scores = [&](i32x4 (&a)[NC], f32x16 (&acc)[QB]) {
 #pragma unroll
@@ -990,6 +991,14 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
             if constexpr (NC >= 4) {
                 slot[2] = ring_load<2048>(src, lane_off);
                 slot[3] = ring_load<3072>(src, lane_off);
+            }
+            if constexpr (NC >= 8) {
+                // (the immediate offset of a global load stays below 4096)
+                const char* src2 = src + 4096;
+                slot[4] = ring_load<0>(src2, lane_off);
+                slot[5] = ring_load<1024>(src2, lane_off);
+                slot[6] = ring_load<2048>(src2, lane_off);
+                slot[7] = ring_load<3072>(src2, lane_off);
             }
             if (pos == SBT - 1 && !lex) lex = !next_sb(ls);
         };
@@ -1108,9 +1117,14 @@ hipError_t launch_select_t(const void* kp, const void* Q, const void* K, const T
     // not know about: a spill of a prefetch register would save it before its
     // load lands.  Refuse to run a build in which the kernel uses scratch.
     hipFuncAttributes fa;
-    hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(select_kernel<D, QB, SLOTS, LBMAX>));
+    const void* fn = reinterpret_cast<const void*>(select_kernel<D, QB, SLOTS, LBMAX>);
+    hipError_t e = hipFuncGetAttributes(&fa, fn);
     if (e != hipSuccess) return e;
     if (fa.localSizeBytes != 0) return hipErrorInvalidDeviceFunction;
+    // trees of k > 128 keys take more than 64 KB of LDS (up to 132 KB of
+    // the 160 KB a gfx950 workgroup may hold)
+    if (lds > 65536 && (e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess)
+        return e;
     int dev = 0, cus = 0, per_cu = 0;
     e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -1164,17 +1178,23 @@ hipError_t launch_select(const void* kp, const void* Q, const void* K, const Tas
                          int32_t* work_ctr, int32_t* topk_idx, hipStream_t stream,
                          hipEvent_t ev_start, hipEvent_t ev_stop) {
     if (ntasks <= 0) return hipSuccess;
+    const int lbmax = k <= 32 ? 5 : k <= 128 ? 7 : k <= 256 ? 8 : 9;
 #define KMIP_SELECT_CASE(DD, QQ, SS, LL)                                                         \
-    if (d == DD && shape.qb == QQ && shape.slots == SS && (k <= 32 ? 5 : 7) == LL)               \
+    if (d == DD && shape.qb == QQ && shape.slots == SS && lbmax == LL)                           \
         return launch_select_t<DD, QQ, SS, LL>(kp, Q, K, tasks, groups, keys, ntasks, N, H, k, ntiles, \
                                            work_ctr, topk_idx, stream, ev_start, ev_stop);
 #define KMIP_SELECT_D(DD)         \
     KMIP_SELECT_CASE(DD, 2, 4, 5) \
     KMIP_SELECT_CASE(DD, 1, 8, 5) \
-    KMIP_SELECT_CASE(DD, 1, 8, 7)
+    KMIP_SELECT_CASE(DD, 1, 8, 7) \
+    KMIP_SELECT_CASE(DD, 1, 8, 8) \
+    KMIP_SELECT_CASE(DD, 1, 8, 9)
     KMIP_SELECT_D(16)
     KMIP_SELECT_D(32)
     KMIP_SELECT_D(64)
+    // d = 128: one query block, k <= 128
+    KMIP_SELECT_CASE(128, 1, 8, 5)
+    KMIP_SELECT_CASE(128, 1, 8, 7)
 #undef KMIP_SELECT_D
 #undef KMIP_SELECT_CASE
     return hipErrorInvalidValue;

@@ -17,7 +17,7 @@
 //      such prefix with at least k' keys at or above it.  The keys at or
 //      above T are the candidates: the k' best and the few others that share
 //      the k'-th best's 16-bit prefix;
-//   3. when more than KMIP_MAX_K keys are candidates (many exact ties), the
+//   3. when more than kSmallKept keys are candidates (many exact ties), the
 //      low 16 bits are fixed as well, giving the k'-th best code exactly, and
 //      the candidates are the keys above it plus, at it, the ones of lowest
 //      index that the row still needs (the tie rule: score descending, index
@@ -35,6 +35,7 @@ namespace {
 
 constexpr int kSmallStride = 33;                     // LDS words per key row of scores
 constexpr int kSmallPer = (kSmallGraph + 7) / 8;     // codes per thread
+constexpr int kSmallKept = KMIP_MAX_K_WIDE;          // candidates listed per query (k <= this)
 
 __device__ __forceinline__ int small_tile_row(int r, int half) {
     return 8 * (r >> 2) + 4 * half + (r & 3);
@@ -126,7 +127,7 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
     for (int bit = 31; bit >= 16; --bit)
         if (count_at_least(T | (1u << bit)) >= kk) T |= 1u << bit;
     // 3. many candidates: the exact k'-th best code and the ties at it
-    const bool exact = count_at_least(T) > KMIP_MAX_K;
+    const bool exact = count_at_least(T) > kSmallKept;
     int m = 0;
     if (exact) {
         for (int bit = 15; bit >= 0; --bit)
@@ -167,9 +168,9 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
     __syncthreads();   // every score is in registers: the LDS is reused for the candidates
 
     // 4. the candidates of each query, listed in LDS, then placed by rank
-    uint64_t* kept = reinterpret_cast<uint64_t*>(sc);   // [32][KMIP_MAX_K] (code, ~index)
+    uint64_t* kept = reinterpret_cast<uint64_t*>(sc);   // [32][kSmallKept] (code, ~index)
     if (active) {
-        int slot = q * KMIP_MAX_K + pre - mine;
+        int slot = q * kSmallKept + pre - mine;
 #pragma unroll
         for (int i = 0; i < kSmallPer; ++i)
             if (take(i)) kept[slot++] = ((uint64_t)code[i] << 32) | (uint32_t)(~(s + 8 * i));
@@ -177,7 +178,7 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
     __syncthreads();
     if (active) {
         int32_t* dst = topk_idx + ((size_t)(tk.q_begin + q) * H + head) * k;
-        const uint64_t* row = kept + q * KMIP_MAX_K;
+        const uint64_t* row = kept + q * kSmallKept;
         for (int e = s; e < nc; e += 8) {
             const uint64_t x = row[e];
             int rank = 0;
@@ -194,8 +195,9 @@ hipError_t launch_small_select(const void* kp, const void* Q, const Task* tasks,
                                int32_t H, int32_t d, int32_t k, int32_t ntiles, int32_t* topk_idx,
                                hipStream_t stream) {
     if (ntasks <= 0) return hipSuccess;
-    static_assert((size_t)32 * KMIP_MAX_K * 8 <= sizeof(float) * kSmallGraph * kSmallStride,
+    static_assert((size_t)32 * kSmallKept * 8 <= sizeof(float) * kSmallGraph * kSmallStride,
                   "the kept keys fit the score area");
+    if (k > kSmallKept) return hipErrorInvalidValue;
     const dim3 grid((unsigned)((int64_t)ntasks * H));
     const uint4* kpp = reinterpret_cast<const uint4*>(kp);
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);

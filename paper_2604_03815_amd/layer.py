@@ -48,7 +48,7 @@ class KMIPAttention(torch.nn.Module):
     """One layer of multi-head k-MIP self-attention (Eq. 1-2, Algorithm 1).
 
     d_model: input and output width; heads: H; d_k, d_v: per-head widths of
-    queries/keys and of values (each in {16, 32, 64}); k: keys kept per
+    queries/keys and of values (each in {16, 32, 64, 128}); k: keys kept per
     query (or k_schedule).  forward(x [N, d_model], graph_offsets=None)
     returns [N, d_model] float32; graph_offsets (host int sequence [G+1])
     makes the attention block-diagonal over a batch of graphs.

@@ -102,6 +102,25 @@ def test_workspace_size(lib):
     assert (lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, 0)
             == lib.kmip_bwd_workspace_size(1_100_000, 4, 16, 16, _lib.BWD_SEGMENTED) > 0)
     assert lib.kmip_bwd_workspace_size(1000, 2, 32, 16, 5) == 0
+    # k > 128 and d = 128: the bucketed reduction is not built for them, the
+    # library picks the key sort
+    # (the key sort's arrays as above: 2000 k pairs of 8 + 16 B, each array
+    # rounded up to 256 B, 8192 B of counts and 256 B of block sums)
+    def al(x):
+        return (x + 255) // 256 * 256
+
+    for d, k in ((16, 129), (64, 512), (128, 16)):
+        csr_k = al(2000 * k * 8) + al(2000 * k * 16) + 8192 + 256
+        assert lib.kmip_bwd_workspace_size(1000, 2, d, k, _lib.BWD_BUCKETED) == 0
+        assert lib.kmip_bwd_workspace_size(1000, 2, d, k, _lib.BWD_SEGMENTED) == csr_k
+        assert lib.kmip_bwd_workspace_size(1000, 2, d, k, 0) == csr_k
+    assert lib.kmip_bwd_ex_workspace_size(1000, 2, 128, 64, 128, _lib.BWD_SEGMENTED) > 0
+    assert lib.kmip_bwd_ex_workspace_size(1000, 2, 128, 256, 16, _lib.BWD_SEGMENTED) == 0
+    # one graph of d = 128 is not grouped: tiles of K and the counters only
+    assert lib.kmip_topk_workspace_size(20000, 1, 128, 16, 1) == (625 + 16) * 32 * 128 * 2 + 512
+    assert lib.kmip_topk_workspace_size(100, 1, 128, 129, 1) == 0
+    assert lib.kmip_topk_workspace_size(100, 1, 64, 512, 1) > 0
+    assert lib.kmip_topk_workspace_size(100, 1, 64, 513, 1) == 0
 
 
 P = ctypes.c_void_p
@@ -114,7 +133,8 @@ def _topk(lib, N=64, H=1, d=16, k=4, offsets=None, G=1, ws=FAKE, ws_bytes=1 << 2
 
 
 @pytest.mark.parametrize("kw,status", [
-    (dict(N=-1), 1), (dict(H=0), 1), (dict(k=0), 1), (dict(d=24), 2), (dict(k=129), 2),
+    (dict(N=-1), 1), (dict(H=0), 1), (dict(k=0), 1), (dict(d=24), 2), (dict(d=256), 2), (dict(k=513), 2),
+    (dict(d=128, k=129), 2),
     (dict(N=1 << 31), 1), (dict(N=1 << 28, H=8, d=16), 1),
     (dict(offsets=[1, 64], G=1), 1), (dict(offsets=[0, 40, 30, 64], G=3), 1),
     (dict(offsets=[0, 32, 63], G=2), 1), (dict(offsets=[0, 64], G=0), 1),

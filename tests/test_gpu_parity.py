@@ -324,7 +324,7 @@ def test_invalid_arguments_leave_outputs_untouched():
         kmip.topk(q, k, 4, graph_offsets=[0, 30, 20, 64], idx=idx)
     assert e.value.status == 1
     with pytest.raises(kmip.KmipError) as e:
-        kmip.topk(q, k, 129, idx=torch.empty((64, 1, 129), dtype=torch.int32, device=DEV))
+        kmip.topk(q, k, 513, idx=torch.empty((64, 1, 513), dtype=torch.int32, device=DEV))
     assert e.value.status == 2
     with pytest.raises(kmip.KmipError):
         kmip.attend(q, k, v, idx, -1.0)
