@@ -50,6 +50,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--config", type=int, default=4, help="workload 1..5 (default 4: N=500k)")
     p.add_argument("--n", type=int, default=None, help="override N (c2: number of graphs)")
+    p.add_argument("--k", type=int, default=None, help="override k (configs 3 and 4)")
+    p.add_argument("--d", type=int, default=None, help="override the head width d (configs 3 and 4)")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-sample", type=int, default=2048, help="query-heads in the oracle sample")
@@ -262,7 +264,7 @@ def main():
 
     dev = torch.device("cuda:0")
     t0 = time.perf_counter()
-    w = workloads.make(args.config, seed=args.seed, n=args.n)
+    w = workloads.make(args.config, seed=args.seed, n=args.n, k=args.k, d=args.d)
     log(f"[bench] workload c{args.config}: N={w.N} H={w.H} d={w.d} k={w.k} graphs={w.num_graphs} "
         f"(generated in {time.perf_counter() - t0:.1f} s)")
 
@@ -334,7 +336,8 @@ def main():
     tflops = flops / (sel_ms * 1e-3) / 1e12
     # MFMA work the kernel actually executed (32x32x16 bf16 MFMAs counted by
     # rocprofv3 on the same sources and workload), when a counter run is on record
-    counters = measured_counters(args.config) if args.n is None and args.seed == 0 else None
+    standard = args.n is None and args.seed == 0 and args.k is None and args.d is None
+    counters = measured_counters(args.config) if standard else None
     executed = counters["mfma_flop_per_launch"] if counters else None
     exec_tflops = None if executed is None else executed / (sel_ms * 1e-3) / 1e12
     topk_ms = sum(t_topk) / len(t_topk)
@@ -416,7 +419,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": (f"c{args.config}: {w.notes}; single MI355X; "
+            "workload": (f"c{args.config}{'' if standard else ' with changed sizes'}: {w.notes}; single MI355X; "
                          f"{'forward+backward' if backward else 'forward only'}"),
             "N": N, "H": H, "d": d, "k": kk, "graphs": w.num_graphs, "score_pairs_per_head": pairs,
             "seed": args.seed, "parallelism": "single GPU",

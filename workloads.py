@@ -144,10 +144,11 @@ def _c2(seed: int, n: Optional[int]) -> Workload:
                     notes=f"{G} graphs, n_g ~ U{{100..450}}, block-diagonal")
 
 
-def _c3(seed: int, n: Optional[int], heads: Optional[int] = None) -> Workload:
+def _c3(seed: int, n: Optional[int], heads: Optional[int] = None, k: Optional[int] = None,
+        d: Optional[int] = None) -> Workload:
     rng = np.random.default_rng(seed)
     N = n or 100_000
-    H, d, F = heads or 4, 32, 32
+    H, d, F = heads or 4, d or 32, 32
     pos = rng.random((N, 2), dtype=np.float32)
     omega = _normal(rng, (2, F // 2), 8.0)
     phase = (rng.random(F // 2, dtype=np.float32) * np.float32(2 * math.pi)).astype(np.float32)
@@ -159,14 +160,15 @@ def _c3(seed: int, n: Optional[int], heads: Optional[int] = None) -> Workload:
     kk = bf16_round((X @ ws[1]).reshape(N, H, d))
     v = bf16_round((X @ ws[2]).reshape(N, H, d))
     dout = bf16_round(_normal(rng, (N, H, d)))
-    return Workload("c3", N, H, d, 32, 1.0 / math.sqrt(d), None, q, kk, v, dout, True,
+    return Workload("c3", N, H, d, k or 32, 1.0 / math.sqrt(d), None, q, kk, v, dout, True,
                     notes="2-D positions, random Fourier features + N(0,0.1^2), random projections")
 
 
-def _c4(seed: int, n: Optional[int], heads: Optional[int] = None) -> Workload:
+def _c4(seed: int, n: Optional[int], heads: Optional[int] = None, k: Optional[int] = None,
+        d: Optional[int] = None) -> Workload:
     rng = np.random.default_rng(seed)
     N = n or 500_000
-    H, d, F = heads or 4, 16, 64
+    H, d, F = heads or 4, d or 16, 64
     xyz = rng.random((N, 3), dtype=np.float32)
     P = _normal(rng, (3, F))
     X = (xyz @ P).astype(np.float32) + _normal(rng, (N, F), 0.05)
@@ -175,7 +177,7 @@ def _c4(seed: int, n: Optional[int], heads: Optional[int] = None) -> Workload:
     kk = bf16_round((X @ ws[1]).reshape(N, H, d))
     v = bf16_round((X @ ws[2]).reshape(N, H, d))
     dout = bf16_round(_normal(rng, (N, H, d)))
-    return Workload("c4", N, H, d, 32, 1.0 / math.sqrt(d), None, q, kk, v, dout, True,
+    return Workload("c4", N, H, d, k or 32, 1.0 / math.sqrt(d), None, q, kk, v, dout, True,
                     notes="xyz ~ U[0,1]^3 projected + N(0,0.05^2), random projections")
 
 
@@ -197,12 +199,14 @@ def _c5(seed: int, n: Optional[int]) -> Workload:
 CONFIGS = {1: _c1, 2: _c2, 3: _c3, 4: _c4, 5: _c5}
 
 
-def make(config: int, seed: int = 0, n: Optional[int] = None, heads: Optional[int] = None) -> Workload:
+def make(config: int, seed: int = 0, n: Optional[int] = None, heads: Optional[int] = None,
+         k: Optional[int] = None, d: Optional[int] = None) -> Workload:
     """Build workload ``config`` (1..5).  ``n`` changes N (c2: the number of
-    graphs); ``heads`` changes H of the projected-feature workloads c3 and c4
-    (the features are drawn first, so they do not depend on H)."""
-    if heads is not None:
+    graphs); ``heads``, ``k`` and ``d`` change H, k and the head width of the
+    projected-feature workloads c3 and c4 (the features are drawn first, so
+    they do not depend on H or d; the projections do)."""
+    if heads is not None or k is not None or d is not None:
         if config not in (3, 4):
-            raise ValueError("heads applies to configs 3 and 4")
-        return CONFIGS[config](seed, n, heads)
+            raise ValueError("heads, k and d apply to configs 3 and 4")
+        return CONFIGS[config](seed, n, heads, k, d)
     return CONFIGS[config](seed, n)
