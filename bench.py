@@ -52,6 +52,9 @@ def parse():
     p.add_argument("--n", type=int, default=None, help="override N (c2: number of graphs)")
     p.add_argument("--k", type=int, default=None, help="override k (configs 3 and 4)")
     p.add_argument("--d", type=int, default=None, help="override the head width d (configs 3 and 4)")
+    p.add_argument("--prefilter", action="store_true",
+                   help="score + select through the int8 prefilter with an exact re-rank "
+                        "(kmip_topk_prefilter; one graph, k <= 32); the select time is then the whole call")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-sample", type=int, default=2048, help="query-heads in the oracle sample")
@@ -281,14 +284,23 @@ def main():
     backward = w.backward and g is not None
     # one workspace, sized for the larger of the two uses, allocated up front
     ws = kmip.Workspace(dev)
-    ws.get(max(kmip.topk_workspace_size(N, H, d, kk, w.num_graphs),
+    ws.get(max(kmip.topk_prefilter_workspace_size(N, H, d, kk) if args.prefilter
+               else kmip.topk_workspace_size(N, H, d, kk, w.num_graphs),
                kmip.bwd_workspace_size(N, H, d, kk, args.bwd_variant) if backward else 0))
+    redone = torch.zeros(1, dtype=torch.int32, device=dev)
 
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        kmip.topk(q, k, kk, graph_offsets=w.offsets, idx=idx, workspace=ws,
-                  select_events=None if ev is None else (ev[4], ev[5]))
+        if args.prefilter:
+            if ev is not None:
+                ev[4].record()
+            kmip.topk_prefilter(q, k, kk, idx=idx, workspace=ws, redone=redone)
+            if ev is not None:
+                ev[5].record()
+        else:
+            kmip.topk(q, k, kk, graph_offsets=w.offsets, idx=idx, workspace=ws,
+                      select_events=None if ev is None else (ev[4], ev[5]))
         if ev is not None:
             ev[1].record()
         kmip.attend(q, k, v, idx, w.scale, out=out, lse=lse)
@@ -336,7 +348,7 @@ def main():
     tflops = flops / (sel_ms * 1e-3) / 1e12
     # MFMA work the kernel actually executed (32x32x16 bf16 MFMAs counted by
     # rocprofv3 on the same sources and workload), when a counter run is on record
-    standard = args.n is None and args.seed == 0 and args.k is None and args.d is None
+    standard = args.n is None and args.seed == 0 and args.k is None and args.d is None and not args.prefilter
     counters = measured_counters(args.config) if standard else None
     executed = counters["mfma_flop_per_launch"] if counters else None
     exec_tflops = None if executed is None else executed / (sel_ms * 1e-3) / 1e12
@@ -348,6 +360,9 @@ def main():
     nh = N * H
     att_bytes = nh * (2 * d + 4 * kk + 2 * (2 * kk * d) + 4 * d + 4)
     bwd_bytes = nh * (2 * 2 * d + 4 * kk + 4 + 2 * (2 * kk * d) + 3 * 4 * d)
+    if args.prefilter:
+        nb = (N + 31) // 32
+        log(f"[bench] prefilter: {int(redone.item())} of {nb} query blocks redone by the select kernel")
     log(f"[bench] per step: topk {topk_ms:.3f} ms (select kernel {sel_ms:.3f} ms), "
         f"attend {att_ms:.3f} ms, backward {bwd_ms:.3f} ms, "
         f"wall {ms_step:.3f} ms")
@@ -419,7 +434,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": (f"c{args.config}{'' if standard else ' with changed sizes'}: {w.notes}; single MI355X; "
+            "workload": (f"c{args.config}{'' if standard else ' with changed sizes'}"
+                         f"{'; select through the int8 prefilter' if args.prefilter else ''}: {w.notes}; single MI355X; "
                          f"{'forward+backward' if backward else 'forward only'}"),
             "N": N, "H": H, "d": d, "k": kk, "graphs": w.num_graphs, "score_pairs_per_head": pairs,
             "seed": args.seed, "parallelism": "single GPU",

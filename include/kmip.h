@@ -111,6 +111,35 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
                                     void* stream, void* select_start, void* select_stop);
 
 /*
+ * Score + select with low-precision candidate scoring (the paper names
+ * FP16/INT8 scoring on matrix cores as its next step: Appendix, comparison
+ * with FlashAttention, closing paragraph), for one graph (no
+ * graph_offsets) and k <= 32.  Same result as kmip_topk, order included:
+ *   1. Q and K are quantised to int8 with power-of-two scales (one per head
+ *      for K, one per query), and every key is scored exactly in int32 on
+ *      the matrix cores (v_mfma_i32_32x32x32_i8);
+ *   2. from the quantisation errors, a bound E + delta on the gap between
+ *      those scores and kmip_topk's fp32 scores gives each query an integer
+ *      threshold that every key of its exact top-k clears (ties included),
+ *      and a second int8 pass lists the keys that clear it (at most 512 a
+ *      query);
+ *   3. the listed keys are scored again with kmip_topk's bf16 MFMA and the
+ *      k best taken by (score descending, node id ascending).
+ *   Queries whose list would overflow (data whose top-k scores lie closer
+ *   together than the int8 error) have their blocks of 32 queries redone by
+ *   kmip_topk's select kernel on the device, so the result never depends on
+ *   the data.  k > 32 returns KMIP_ERR_UNSUPPORTED.
+ *   redone: device int32, or NULL: receives (on the stream) the number of
+ *   query blocks of 32 that the select kernel redid.
+ *   workspace: kmip_topk_prefilter_workspace_size() bytes (0 if the sizes
+ *   are not taken), 256-byte aligned; about 2 KB per query-head.
+ */
+size_t kmip_topk_prefilter_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k);
+kmip_status_t kmip_topk_prefilter(const void* Q, const void* K, int64_t N, int32_t H, int32_t d, int32_t k,
+                                  int32_t* topk_idx, int32_t* redone, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
+/*
  * Gather-softmax-aggregate (Algorithm 1: GatherRows, softmax over the k kept
  * scores divided by sqrt(d_K) -- here times `scale` -- and the einsum
  * nk,nkv->nv).  Recomputes the k kept scores in fp32 from Q and the gathered

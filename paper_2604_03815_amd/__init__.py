@@ -21,7 +21,7 @@ import numpy as np
 from ._lib import KmipError, MAX_K, MAX_K_WIDE, NOALLOC_SCRATCH_BYTES, check, load
 
 __all__ = [
-    "KmipError", "MAX_K", "MAX_K_WIDE", "NOALLOC_SCRATCH_BYTES", "topk", "attend", "fwd", "fwd_noalloc", "bwd",
+    "KmipError", "MAX_K", "MAX_K_WIDE", "NOALLOC_SCRATCH_BYTES", "topk", "topk_prefilter", "topk_prefilter_workspace_size", "attend", "fwd", "fwd_noalloc", "bwd",
     "attention", "topk_workspace_size", "bwd_workspace_size", "Workspace", "load", "KMIPAttention",
     "linear_k_schedule",
 ]
@@ -165,6 +165,32 @@ def topk(q, k_, kk: int, graph_offsets: Optional[Sequence[int]] = None, idx=None
                 ev.record()   # the event object exists only once recorded
             handles.append(ctypes.c_void_p(ev.cuda_event))
         check(load().kmip_topk_with_events(*args, *handles))
+    return idx
+
+
+def topk_prefilter_workspace_size(N: int, H: int, d: int, k: int) -> int:
+    return int(load().kmip_topk_prefilter_workspace_size(N, H, d, k))
+
+
+def topk_prefilter(q, k_, kk: int, idx=None, workspace: Optional[Workspace] = None, redone=None):
+    """Score + select of one graph through the int8 prefilter with a provable
+    bound and an exact re-rank (k <= 32): the same topk_idx as topk().
+    redone: optional int32 tensor of one element on the device, set to the
+    number of query blocks the select kernel redid."""
+    torch = _torch()
+    N, H, d = _nhd(q)
+    kk = int(kk)
+    specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d))]
+    if idx is not None:
+        specs.append((idx, "topk_idx", torch.int32, (N, H, kk)))
+    if redone is not None:
+        specs.append((redone, "redone", torch.int32, (1,)))
+    _validate(*specs)
+    if idx is None:
+        idx = torch.empty((N, H, kk), dtype=torch.int32, device=q.device)
+    buf = _workspace(workspace, topk_prefilter_workspace_size(N, H, d, kk), q.device)
+    check(load().kmip_topk_prefilter(_ptr(q), _ptr(k_), N, H, d, kk, _ptr(idx), _ptr(redone), _ptr(buf),
+                                     0 if buf is None else buf.numel(), _stream_ptr()))
     return idx
 
 

@@ -183,6 +183,36 @@ bool use_grouping(int64_t N, int32_t G, int32_t d) { return G == 1 && N >= 8192 
 // in LDS and is built for d <= 64; other tasks go to the streaming kernel.
 bool small_select_ok(int32_t d, int32_t k) { return d <= 64 && k <= KMIP_MAX_K_WIDE; }
 
+// Workspace of kmip_topk_prefilter, in order: the bf16 key tiles and the
+// select kernel's counters (for the query blocks it redoes), the int8 key
+// tiles, the per-head quantisation figures, the candidate lists and their
+// lengths, the overflow flags, the redo count and the redo task list.
+struct PrefilterLayout {
+    size_t tiles8, hstat, cand, ccount, flags, count, tasks, total;
+};
+
+PrefilterLayout prefilter_layout(int64_t N, int32_t H, int32_t d) {
+    PrefilterLayout L{};
+    const size_t nblocks = (size_t)num_tiles(N);
+    size_t off = tiled_bytes(N, H, d) + kCounterBytes;
+    L.tiles8 = off;
+    off += align_up(kmip::prefilter_tile_bytes((int32_t)N, H, d));
+    L.hstat = off;
+    off += align_up((size_t)4 * H * sizeof(uint32_t));
+    L.cand = off;
+    off += align_up((size_t)N * H * kmip::kPrefilterCap * sizeof(int32_t));
+    L.ccount = off;
+    off += align_up((size_t)N * H * 2 * sizeof(int32_t));
+    L.flags = off;
+    off += align_up((size_t)H * nblocks * sizeof(int32_t));
+    L.count = off;
+    off += align_up(sizeof(int32_t));
+    L.tasks = off;
+    off += align_up(nblocks * sizeof(kmip::Task));
+    L.total = off;
+    return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -316,6 +346,56 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
     } else if (ev_stop != nullptr && (e = hipEventRecord(ev_stop, stream)) != hipSuccess) {
         return hip_fail(e, "event record");
     }
+    return ok();
+}
+
+
+size_t kmip_topk_prefilter_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k) {
+    if (check_sizes(N, H, d, k) != KMIP_OK || k > kmip::kPrefilterMaxK) return 0;
+    return prefilter_layout(N, H, d).total;
+}
+
+kmip_status_t kmip_topk_prefilter(const void* Q, const void* K, int64_t N, int32_t H, int32_t d, int32_t k,
+                                  int32_t* topk_idx, int32_t* redone, void* workspace, size_t workspace_bytes,
+                                  void* stream_) {
+    kmip_status_t s = check_sizes(N, H, d, k);
+    if (s != KMIP_OK) return s;
+    if (k > kmip::kPrefilterMaxK)
+        return record_error(KMIP_ERR_UNSUPPORTED, "the prefilter takes k <= %d (got %d)", kmip::kPrefilterMaxK, k);
+    if (N == 0) {
+        hipError_t e = redone != nullptr ? kmip::launch_fill_zero(reinterpret_cast<float*>(redone), 1,
+                                                                 reinterpret_cast<hipStream_t>(stream_))
+                                         : hipSuccess;
+        return e == hipSuccess ? ok() : hip_fail(e, "redo count");
+    }
+    if (!Q || !K || !topk_idx) return record_error(KMIP_ERR_INVALID_ARG, "null Q, K or topk_idx");
+    if (!aligned16(Q) || !aligned16(K)) return record_error(KMIP_ERR_INVALID_ARG, "Q and K must be 16-byte aligned");
+    const PrefilterLayout L = prefilter_layout(N, H, d);
+    if (workspace == nullptr || workspace_bytes < L.total)
+        return record_error(KMIP_ERR_WORKSPACE, "workspace of %zu bytes < %zu required", workspace_bytes, L.total);
+    if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0)
+        return record_error(KMIP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    char* ws = reinterpret_cast<char*>(workspace);
+    const int32_t n32 = (int32_t)N, ntiles = num_tiles(N);
+    kmip::Task* tasks = reinterpret_cast<kmip::Task*>(ws + L.tasks);
+    hipError_t e = kmip::launch_prefilter(K, Q, n32, H, d, k, reinterpret_cast<uint32_t*>(ws + L.hstat),
+                                          reinterpret_cast<uint4*>(ws + L.tiles8), reinterpret_cast<int32_t*>(ws + L.cand),
+                                          reinterpret_cast<int32_t*>(ws + L.ccount),
+                                          reinterpret_cast<int32_t*>(ws + L.flags),
+                                          reinterpret_cast<int32_t*>(ws + L.count), tasks, topk_idx, stream);
+    if (e != hipSuccess) return hip_fail(e, "prefilter launch");
+    // the query blocks whose candidate lists overflowed, through the select
+    // kernel (every other entry of the list is a zero-query task it skips)
+    if ((e = kmip::launch_pack_k(K, nullptr, nullptr, ws, n32, H, d, ntiles, stream)) != hipSuccess)
+        return hip_fail(e, "pack_k launch");
+    int32_t* work_ctr = reinterpret_cast<int32_t*>(ws + tiled_bytes(N, H, d));
+    e = kmip::launch_select(ws, Q, K, tasks, nullptr, nullptr, ntiles, n32, H, d, k, ntiles, kmip::SelectShape{1, 8},
+                            work_ctr, topk_idx, stream, nullptr, nullptr);
+    if (e != hipSuccess) return hip_fail(e, "select launch");
+    if (redone != nullptr &&
+        (e = hipMemcpyAsync(redone, ws + L.count, sizeof(int32_t), hipMemcpyDeviceToDevice, stream)) != hipSuccess)
+        return hip_fail(e, "redo count copy");
     return ok();
 }
 

@@ -178,6 +178,22 @@ hipError_t launch_bwd_bucket(const void* Q, const void* K, const void* V, const 
 
 hipError_t launch_fill_zero(float* p, size_t n, hipStream_t stream);
 
+// Int8 prefilter with a provable bound and exact re-rank (prefilter.hip), for
+// one graph and k <= 32.  Candidates listed per query-head (two halves).
+constexpr int kPrefilterCap = 1024;
+constexpr int kPrefilterMaxK = 32;
+// Bytes of the int8 key tiles: H x (ceil(N/32) + kPadTiles) tiles of
+// ceil(d/32) chunks of 1 KB.
+size_t prefilter_tile_bytes(int32_t N, int32_t H, int32_t d);
+// Writes topk_idx for every query-head whose candidate list fits; the query
+// blocks of the others are listed in fb_tasks[0 .. *fb_count) (the rest of
+// fb_tasks, ceil(N/32) entries, holds zero-query tasks) for the select
+// kernel to redo.  hstat: 4 H words; cand: N H kPrefilterCap ints; ccount:
+// 2 N H ints; flags: H ceil(N/32) ints.
+hipError_t launch_prefilter(const void* K, const void* Q, int32_t N, int32_t H, int32_t d, int32_t k,
+                            uint32_t* hstat, uint4* kp8, int32_t* cand, int32_t* ccount, int32_t* flags,
+                            int32_t* fb_count, Task* fb_tasks, int32_t* topk_idx, hipStream_t stream);
+
 // Sets the calling thread's kmip_last_error() text (printf-style) and
 // returns s.
 kmip_status_t record_error(kmip_status_t s, const char* fmt, ...);

@@ -306,6 +306,9 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
         key_lo = 0;
         key_hi = N;
     }
+    // a task without queries (the unused tail of a list filled on the
+    // device) has nothing to select
+    if (q_count <= 0) continue;
 
     const int lane = threadIdx.x;
     const int col = lane & 31;

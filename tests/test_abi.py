@@ -270,3 +270,25 @@ def test_extended_entry_points_validate(lib):
                                   None) == 1
         assert lib.kmip_bwd_ex(*args, keep, f(rate), 64, 1, 16, 16, 4, f(1.0), FAKE, FAKE, FAKE, 0, None, 0,
                                None) == 1
+
+
+def test_prefilter_sizes_and_rejects(lib):
+    # the select's tiles and counters, then the int8 tiles (H x (ceil(N/32)
+    # + 16) tiles of ceil(d/32) 1 KB chunks), 4 words a head, 1024 candidates
+    # and 2 lengths per query-head, a flag per (head, block), the redo count
+    # and one task per block, each rounded up to 256 bytes
+    def al(x):
+        return (x + 255) // 256 * 256
+
+    N, H, d, k = 1000, 2, 32, 16
+    nb = 32
+    want = (al(H * (nb + 16) * 32 * d * 2) + 512 + al(H * (nb + 16) * 1024) + 256 + al(N * H * 1024 * 4)
+            + al(N * H * 2 * 4) + al(H * nb * 4) + 256 + al(nb * 16))
+    assert lib.kmip_topk_prefilter_workspace_size(N, H, d, k) == want
+    assert lib.kmip_topk_prefilter_workspace_size(N, H, d, 33) == 0      # k <= 32 only
+    assert lib.kmip_topk_prefilter_workspace_size(N, H, 24, 16) == 0     # unsupported d
+    assert lib.kmip_topk_prefilter(FAKE, FAKE, 64, 1, 16, 33, FAKE, None, FAKE, 1 << 30, None) == 2
+    assert lib.kmip_topk_prefilter(FAKE, FAKE, 64, 1, 16, 8, FAKE, None, FAKE, 10, None) == 3
+    assert lib.kmip_topk_prefilter(FAKE, FAKE, 64, 1, 16, 8, FAKE, None, P(256 + 16), 1 << 30, None) == 3
+    assert lib.kmip_topk_prefilter(None, FAKE, 64, 1, 16, 8, FAKE, None, FAKE, 1 << 30, None) == 1
+    assert lib.kmip_topk_prefilter(None, None, 0, 1, 16, 8, None, None, None, 0, None) == 0
