@@ -4,14 +4,14 @@
 // at most kSmallGraph nodes.  There a query keeps a large share of its graph
 // (k / n of several percent), so a running threshold filters little and the
 // streaming kernel spends its time inserting into its trees.  Instead, a
-// workgroup of 256 threads takes one task (up to 32 queries of one graph and
+// workgroup of 512 threads takes one task (up to 32 queries of one graph and
 // one head):
-//   1. its four waves form the scores of the 32 queries against every key
+//   1. its eight waves form the scores of the 32 queries against every key
 //      of the graph with the streaming kernel's MFMA on the same tiled key
 //      operands, so the fp32 scores are the same values, and keep them in LDS
 //      ([key][query], row stride 33 words: the stores of a wave and the reads
 //      of a query's threads are free of bank conflicts);
-//   2. eight threads per query hold its scores as order-preserving 32-bit
+//   2. sixteen threads per query hold its scores as order-preserving 32-bit
 //      codes (larger score, larger code) and fix the top 16 bits of the code
 //      T of the k'-th best key, k' = min(k, n), bit by bit: T is the largest
 //      such prefix with at least k' keys at or above it.  The keys at or
@@ -34,30 +34,32 @@ namespace kmip {
 namespace {
 
 constexpr int kSmallStride = 33;                     // LDS words per key row of scores
-constexpr int kSmallPer = (kSmallGraph + 7) / 8;     // codes per thread
 constexpr int kSmallKept = KMIP_MAX_K_WIDE;          // candidates listed per query (k <= this)
+constexpr int kSmallTpq = 16;                        // threads per query
+constexpr int kSmallThreads = 32 * kSmallTpq;
+constexpr int kSmallPer = (kSmallGraph + kSmallTpq - 1) / kSmallTpq;   // codes per thread
 
 __device__ __forceinline__ int small_tile_row(int r, int half) {
     return 8 * (r >> 2) + 4 * half + (r & 3);
 }
 
-// Sum over the 8 threads of a query (aligned groups of 8 lanes).
-__device__ __forceinline__ int group8_sum(int v) {
-    v += __shfl_xor(v, 1, 8);
-    v += __shfl_xor(v, 2, 8);
-    v += __shfl_xor(v, 4, 8);
+// Sum over the kSmallTpq threads of a query (aligned groups of lanes).
+__device__ __forceinline__ int group_sum(int v) {
+#pragma unroll
+    for (int m = 1; m < kSmallTpq; m <<= 1) v += __shfl_xor(v, m, kSmallTpq);
     return v;
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restrict__ kp, const uint16_t* __restrict__ Q,
+__global__ __launch_bounds__(kSmallThreads) void small_select_kernel(const uint4* __restrict__ kp, const uint16_t* __restrict__ Q,
                                                            const Task* __restrict__ tasks, int32_t ntasks, int32_t N,
                                                            int32_t H, int32_t k, int32_t ntiles,
                                                            int32_t* __restrict__ topk_idx) {
     constexpr int NC = D / 16;
     constexpr int TILE_BYTES = NC * 64 * 16;
     constexpr int kMaxTiles = kSmallGraph / 32 + 1;   // tiles a graph can touch
-    constexpr int kWaveTiles = (kMaxTiles + 3) / 4;
+    constexpr int kWaves = kSmallThreads / 64;
+    constexpr int kWaveTiles = (kMaxTiles + kWaves - 1) / kWaves;
     __shared__ float sc[kSmallGraph * kSmallStride];
     const int t = threadIdx.x;
     const int wave = t >> 6, lane = t & 63;
@@ -82,7 +84,7 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
     uint4 tw[kWaveTiles][NC];   // this wave's tiles, all loads in flight together
 #pragma unroll
     for (int u = 0; u < kWaveTiles; ++u) {
-        const int tt = wave + 4 * u;
+        const int tt = wave + kWaves * u;
         if (tt < nt) {
             const uint4* src = reinterpret_cast<const uint4*>(head_tiles + (size_t)(t0 + tt) * TILE_BYTES) + lane;
 #pragma unroll
@@ -91,7 +93,7 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
     }
 #pragma unroll
     for (int u = 0; u < kWaveTiles; ++u) {
-        const int tt = wave + 4 * u;
+        const int tt = wave + kWaves * u;
         if (tt < nt) {
             f32x16 acc = f32x16{};
 #pragma unroll
@@ -106,13 +108,13 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
     }
     __syncthreads();
 
-    // 2. codes of the row, eight threads per query, and the top half of T
-    const int q = t >> 3, s = t & 7;
+    // 2. codes of the row, kSmallTpq threads per query, and the top half of T
+    const int q = t / kSmallTpq, s = t % kSmallTpq;
     const bool active = q < tk.q_count;
     uint32_t code[kSmallPer];
 #pragma unroll
     for (int i = 0; i < kSmallPer; ++i) {
-        const int j = s + 8 * i;
+        const int j = s + kSmallTpq * i;
         // 0 lies below every score's code (that of -inf is 0x007FFFFF)
         code[i] = active && j < n ? score_code(sc[j * kSmallStride + q]) : 0u;
     }
@@ -121,7 +123,7 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
         int c = 0;
 #pragma unroll
         for (int i = 0; i < kSmallPer; ++i) c += code[i] >= x ? 1 : 0;
-        return group8_sum(c);
+        return group_sum(c);
     };
     uint32_t T = 0;
     for (int bit = 31; bit >= 16; --bit)
@@ -135,7 +137,7 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
         int above = 0;
 #pragma unroll
         for (int i = 0; i < kSmallPer; ++i) above += code[i] > T ? 1 : 0;
-        const int need = kk - group8_sum(above);
+        const int need = kk - group_sum(above);
         if (need > 0) {
             // the smallest m such that the keys at T with index below m
             // complete the row
@@ -144,27 +146,27 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
                 const int mid = (lo + hi) >> 1;
                 int c = 0;
 #pragma unroll
-                for (int i = 0; i < kSmallPer; ++i) c += (code[i] == T && s + 8 * i < mid) ? 1 : 0;
-                if (group8_sum(c) >= need) hi = mid; else lo = mid;
+                for (int i = 0; i < kSmallPer; ++i) c += (code[i] == T && s + kSmallTpq * i < mid) ? 1 : 0;
+                if (group_sum(c) >= need) hi = mid; else lo = mid;
             }
             m = hi;
         }
     }
     auto take = [&](int i) {
-        const int j = s + 8 * i;
+        const int j = s + kSmallTpq * i;
         return exact ? (code[i] > T || (code[i] == T && code[i] != 0u && j < m)) : (code[i] >= T && code[i] != 0u);
     };
     int mine = 0;
 #pragma unroll
     for (int i = 0; i < kSmallPer; ++i) mine += take(i) ? 1 : 0;
-    // inclusive prefix sum over the query's 8 threads
+    // inclusive prefix sum over the query's threads
     int pre = mine;
 #pragma unroll
-    for (int o = 1; o < 8; o <<= 1) {
-        const int y = __shfl_up(pre, o, 8);
+    for (int o = 1; o < kSmallTpq; o <<= 1) {
+        const int y = __shfl_up(pre, o, kSmallTpq);
         if (s >= o) pre += y;
     }
-    const int nc = __shfl(pre, 7, 8);
+    const int nc = __shfl(pre, kSmallTpq - 1, kSmallTpq);
     __syncthreads();   // every score is in registers: the LDS is reused for the candidates
 
     // 4. the candidates of each query, listed in LDS, then placed by rank
@@ -173,19 +175,19 @@ __global__ __launch_bounds__(256) void small_select_kernel(const uint4* __restri
         int slot = q * kSmallKept + pre - mine;
 #pragma unroll
         for (int i = 0; i < kSmallPer; ++i)
-            if (take(i)) kept[slot++] = ((uint64_t)code[i] << 32) | (uint32_t)(~(s + 8 * i));
+            if (take(i)) kept[slot++] = ((uint64_t)code[i] << 32) | (uint32_t)(~(s + kSmallTpq * i));
     }
     __syncthreads();
     if (active) {
         int32_t* dst = topk_idx + ((size_t)(tk.q_begin + q) * H + head) * k;
         const uint64_t* row = kept + q * kSmallKept;
-        for (int e = s; e < nc; e += 8) {
+        for (int e = s; e < nc; e += kSmallTpq) {
             const uint64_t x = row[e];
             int rank = 0;
             for (int f = 0; f < nc; ++f) rank += row[f] > x ? 1 : 0;
             if (rank < kk) dst[rank] = tk.key_lo + key_index(x);
         }
-        for (int p = kk + s; p < k; p += 8) dst[p] = -1;
+        for (int p = kk + s; p < k; p += kSmallTpq) dst[p] = -1;
     }
 }
 
@@ -203,15 +205,15 @@ hipError_t launch_small_select(const void* kp, const void* Q, const Task* tasks,
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
     switch (d) {
         case 16:
-            hipLaunchKernelGGL(small_select_kernel<16>, grid, dim3(256), 0, stream, kpp, q, tasks, ntasks, N, H, k,
+            hipLaunchKernelGGL(small_select_kernel<16>, grid, dim3(kSmallThreads), 0, stream, kpp, q, tasks, ntasks, N, H, k,
                                ntiles, topk_idx);
             break;
         case 32:
-            hipLaunchKernelGGL(small_select_kernel<32>, grid, dim3(256), 0, stream, kpp, q, tasks, ntasks, N, H, k,
+            hipLaunchKernelGGL(small_select_kernel<32>, grid, dim3(kSmallThreads), 0, stream, kpp, q, tasks, ntasks, N, H, k,
                                ntiles, topk_idx);
             break;
         case 64:
-            hipLaunchKernelGGL(small_select_kernel<64>, grid, dim3(256), 0, stream, kpp, q, tasks, ntasks, N, H, k,
+            hipLaunchKernelGGL(small_select_kernel<64>, grid, dim3(kSmallThreads), 0, stream, kpp, q, tasks, ntasks, N, H, k,
                                ntiles, topk_idx);
             break;
         default:
