@@ -43,10 +43,27 @@ __device__ __forceinline__ int small_tile_row(int r, int half) {
     return 8 * (r >> 2) + 4 * half + (r & 3);
 }
 
-// Sum over the kSmallTpq threads of a query (aligned groups of lanes).
+// The threads of a query are one row of 16 lanes, so their sums and scans
+// use DPP row operations (a VALU modifier) rather than LDS permutes.
+static_assert(kSmallTpq == 16, "a query's threads are one DPP row");
+
+// Sum over the 16 threads of a query: quad swaps, then the half-row and row
+// mirrors (each pairs lanes of the two halves it joins).
 __device__ __forceinline__ int group_sum(int v) {
-#pragma unroll
-    for (int m = 1; m < kSmallTpq; m <<= 1) v += __shfl_xor(v, m, kSmallTpq);
+    v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);    // quad_perm [1,0,3,2]
+    v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);    // quad_perm [2,3,0,1]
+    v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);   // row_half_mirror
+    v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);   // row_mirror
+    return v;
+}
+
+// Inclusive prefix sum over the 16 threads of a query (row shifts, zero
+// shifted in).
+__device__ __forceinline__ int group_scan(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true);    // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true);    // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true);    // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true);    // row_shr:8
     return v;
 }
 
@@ -159,14 +176,9 @@ __global__ __launch_bounds__(kSmallThreads) void small_select_kernel(const uint4
     int mine = 0;
 #pragma unroll
     for (int i = 0; i < kSmallPer; ++i) mine += take(i) ? 1 : 0;
-    // inclusive prefix sum over the query's threads
-    int pre = mine;
-#pragma unroll
-    for (int o = 1; o < kSmallTpq; o <<= 1) {
-        const int y = __shfl_up(pre, o, kSmallTpq);
-        if (s >= o) pre += y;
-    }
-    const int nc = __shfl(pre, kSmallTpq - 1, kSmallTpq);
+    // inclusive prefix sum over the query's threads, and their total
+    const int pre = group_scan(mine);
+    const int nc = group_sum(mine);
     __syncthreads();   // every score is in registers: the LDS is reused for the candidates
 
     // 4. the candidates of each query, listed in LDS, then placed by rank
