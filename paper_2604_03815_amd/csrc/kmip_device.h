@@ -88,35 +88,64 @@ __device__ __forceinline__ void load_row_f32(float (&q)[D], const uint16_t* __re
     }
 }
 
-// Reductions over aligned groups of 16 lanes.
+// Reductions over aligned groups of 16 lanes.  A group is one DPP row, so
+// the exchanges are DPP row permutes (a modifier of the VALU instruction)
+// rather than LDS permutes: row_mirror pairs lane i with 15 - i,
+// row_half_mirror with 7 - i (within each half), and the quad permutes with
+// i ^ 2 and i ^ 1.  Each of these pairs lanes that differ in the bit of the
+// step (8, 4, 2, 1) and agree in every higher bit, which is all a butterfly
+// needs.
+template <int CTRL>
+__device__ __forceinline__ float row_perm(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+constexpr int kDppRowMirror = 0x140;
+constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm [2, 3, 0, 1]
+constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm [1, 0, 3, 2]
+
+// The partner of the butterfly step with bit m (8, 4, 2, 1).
+template <int M>
+__device__ __forceinline__ float step_partner(float v) {
+    static_assert(M == 8 || M == 4 || M == 2 || M == 1, "steps of a 16-lane group");
+    return row_perm<M == 8 ? kDppRowMirror : M == 4 ? kDppRowHalfMirror : M == 2 ? kDppQuadSwap2 : kDppQuadSwap1>(v);
+}
+
 __device__ __forceinline__ float group16_max(float v) {
-#pragma unroll
-    for (int m = 8; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 16));
+    v = fmaxf(v, step_partner<8>(v));
+    v = fmaxf(v, step_partner<4>(v));
+    v = fmaxf(v, step_partner<2>(v));
+    v = fmaxf(v, step_partner<1>(v));
     return v;
 }
 
 __device__ __forceinline__ float group16_sum(float v) {
-#pragma unroll
-    for (int m = 8; m >= 1; m >>= 1) v += __shfl_xor(v, m, 16);
+    v += step_partner<8>(v);
+    v += step_partner<4>(v);
+    v += step_partner<2>(v);
+    v += step_partner<1>(v);
     return v;
 }
 
 // Sum of a D-vector over the 16 lanes of a team, transposed: out[u] of lane
 // tl receives the team sum of dimension 16u + tl.  Recursive halving: at the
-// step with partner tl ^ m (m = 8, 4, 2, 1) a lane keeps the half of its
-// dimensions whose bit m matches its own and adds the partner's values of
-// that half, so the step exchanges half of what is left (15 shuffles per 16
-// dimensions, against 64 for a full butterfly per dimension).
-template <int N>
-__device__ __forceinline__ void halve_step(const float* in, float* outv, int tl, int m) {
-    const bool hi = (tl & m) != 0;
+// step with bit m (m = 8, 4, 2, 1) a lane keeps the half of its dimensions
+// whose bit m matches its own and adds its partner's values of that half
+// (the partner has the other bit m and the same higher bits, so it kept the
+// same dimensions so far), so the step exchanges half of what is left (15
+// exchanges per 16 dimensions, against 64 for a full butterfly per
+// dimension).
+template <int N, int M>
+__device__ __forceinline__ void halve_step(const float* in, float* outv, int tl) {
+    const bool hi = (tl & M) != 0;
 #pragma unroll
-    for (int b = 0; b < N; b += 2 * m) {
+    for (int b = 0; b < N; b += 2 * M) {
 #pragma unroll
-        for (int j = 0; j < m; ++j) {
-            const float lo_v = in[b + j], hi_v = in[b + m + j];
+        for (int j = 0; j < M; ++j) {
+            const float lo_v = in[b + j], hi_v = in[b + M + j];
             const float own = hi ? hi_v : lo_v, other = hi ? lo_v : hi_v;
-            outv[b / 2 + j] = own + __shfl_xor(other, m, 16);
+            outv[b / 2 + j] = own + step_partner<M>(other);
         }
     }
 }
@@ -124,10 +153,10 @@ __device__ __forceinline__ void halve_step(const float* in, float* outv, int tl,
 template <int D>
 __device__ __forceinline__ void team_sum_transpose(const float (&acc)[D], float (&out)[D / 16], int tl) {
     float a8[D / 2], a4[D / 4], a2[D / 8];
-    halve_step<D>(acc, a8, tl, 8);
-    halve_step<D / 2>(a8, a4, tl, 4);
-    halve_step<D / 4>(a4, a2, tl, 2);
-    halve_step<D / 8>(a2, out, tl, 1);
+    halve_step<D, 8>(acc, a8, tl);
+    halve_step<D / 2, 4>(a8, a4, tl);
+    halve_step<D / 4, 2>(a4, a2, tl);
+    halve_step<D / 8, 1>(a2, out, tl);
 }
 
 }  // namespace kmip
