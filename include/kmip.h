@@ -121,7 +121,7 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
  *   2. from the quantisation errors, a bound E + delta on the gap between
  *      those scores and kmip_topk's fp32 scores gives each query an integer
  *      threshold that every key of its exact top-k clears (ties included),
- *      and a second int8 pass lists the keys that clear it (at most 512 a
+ *      and a second int8 pass lists the keys that clear it (at most 1024 a
  *      query);
  *   3. the listed keys are scored again with kmip_topk's bf16 MFMA and the
  *      k best taken by (score descending, node id ascending).
@@ -132,7 +132,7 @@ kmip_status_t kmip_topk_with_events(const void* Q, const void* K, const int32_t*
  *   redone: device int32, or NULL: receives (on the stream) the number of
  *   query blocks of 32 that the select kernel redid.
  *   workspace: kmip_topk_prefilter_workspace_size() bytes (0 if the sizes
- *   are not taken), 256-byte aligned; about 2 KB per query-head.
+ *   are not taken), 256-byte aligned; about 4 KB per query-head.
  */
 size_t kmip_topk_prefilter_workspace_size(int64_t N, int32_t H, int32_t d, int32_t k);
 kmip_status_t kmip_topk_prefilter(const void* Q, const void* K, int64_t N, int32_t H, int32_t d, int32_t k,
