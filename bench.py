@@ -298,12 +298,14 @@ def main():
             kmip.topk_prefilter(q, k, kk, idx=idx, workspace=ws, redone=redone)
             if ev is not None:
                 ev[5].record()
+                ev[1].record()
+            kmip.attend(q, k, v, idx, w.scale, out=out, lse=lse)
         else:
-            kmip.topk(q, k, kk, graph_offsets=w.offsets, idx=idx, workspace=ws,
-                      select_events=None if ev is None else (ev[4], ev[5]))
-        if ev is not None:
-            ev[1].record()
-        kmip.attend(q, k, v, idx, w.scale, out=out, lse=lse)
+            # the whole forward in one call (its aggregate takes the queries
+            # in the select's grouped order); the library records the select
+            # kernel's events and the start of the aggregate
+            kmip.fwd(q, k, v, kk, w.scale, graph_offsets=w.offsets, workspace=ws, out=out, idx=idx, lse=lse,
+                     events=None if ev is None else (ev[4], ev[5], ev[1]))
         if ev is not None:
             ev[2].record()
         if backward:
@@ -327,8 +329,8 @@ def main():
     # per step: topk start/end, attend end, backward end, select kernel start/end
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
     for e in evs:
-        for x in e[4:]:
-            x.record()   # creates the events the library records around the select kernel
+        for x in e:
+            x.record()   # creates the events (the library records some of them)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):

@@ -184,6 +184,21 @@ kmip_status_t kmip_fwd_ex(const void* Q, const void* K, const void* V, const int
                           float* lse, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * kmip_fwd_ex, recording caller events for timing: select_start and
+ * select_stop as kmip_topk_with_events does (around the score+select
+ * kernel alone), attend_start right before the aggregate.  Each may be NULL
+ * to record nothing.  In every kmip_fwd* call on one graph that the library
+ * groups by direction (at least 8192 nodes, d <= 64) the aggregate takes
+ * the query-heads in that grouped order, so that the queries of a
+ * workgroup share their keys' rows; results do not depend on the order.
+ */
+kmip_status_t kmip_fwd_ex_with_events(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
+                                      int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k,
+                                      float scale, const uint8_t* keep, float drop_rate, float* out,
+                                      int32_t* topk_idx, float* lse, void* workspace, size_t workspace_bytes,
+                                      void* stream, void* select_start, void* select_stop, void* attend_start);
+
+/*
  * Backward with the forward's index set held fixed (Section 3.1, last
  * paragraph, and Appendix E, last paragraph: the top-k indices are reused,
  * so only the k selected pairs of each query carry gradient).  With p_j the

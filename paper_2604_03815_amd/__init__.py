@@ -217,25 +217,54 @@ def attend(q, k_, v, idx, scale: float, out=None, lse=None, keep=None, drop_rate
     return out, lse
 
 
+def _event_handles(events):
+    handles = []
+    for ev in events:
+        if ev is None:
+            handles.append(ctypes.c_void_p(0))
+            continue
+        if not ev.cuda_event:
+            ev.record()   # the event object exists only once recorded
+        handles.append(ctypes.c_void_p(ev.cuda_event))
+    return handles
+
+
 def fwd(q, k_, v, kk: int, scale: float, graph_offsets=None, workspace=None, keep=None,
-        drop_rate: float = 0.0):
-    """Full forward: returns (out, topk_idx, lse)."""
+        drop_rate: float = 0.0, out=None, idx=None, lse=None, events=None):
+    """Full forward: returns (out, topk_idx, lse).
+
+    out, idx, lse: optional outputs to write into.  events: optional triple
+    of torch.cuda.Event (or None entries) recorded around the score+select
+    kernel and right before the aggregate."""
     torch = _torch()
     N, H, d = _nhd(q)
     dv = _dv(v, N, H)
     kk = int(kk)
-    _validate((q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d)),
-              (v, "V", torch.bfloat16, (N, H, dv)), *_keep_spec(keep, N, H, kk))
+    specs = [(q, "Q", torch.bfloat16, None), (k_, "K", torch.bfloat16, (N, H, d)),
+             (v, "V", torch.bfloat16, (N, H, dv)), *_keep_spec(keep, N, H, kk)]
+    for t, name, dt, shp in ((out, "out", torch.float32, (N, H, dv)), (idx, "topk_idx", torch.int32, (N, H, kk)),
+                             (lse, "lse", torch.float32, (N, H))):
+        if t is not None:
+            specs.append((t, name, dt, shp))
+    _validate(*specs)
     o, optr, G = _offsets(graph_offsets)
     if o is not None and (o.ndim != 1 or len(o) < 2):
         raise ValueError("graph_offsets must be a 1-D sequence of at least two entries")
-    out = torch.empty((N, H, dv), dtype=torch.float32, device=q.device)
-    idx = torch.empty((N, H, kk), dtype=torch.int32, device=q.device)
-    lse = torch.empty((N, H), dtype=torch.float32, device=q.device)
+    if out is None:
+        out = torch.empty((N, H, dv), dtype=torch.float32, device=q.device)
+    if idx is None:
+        idx = torch.empty((N, H, kk), dtype=torch.int32, device=q.device)
+    if lse is None:
+        lse = torch.empty((N, H), dtype=torch.float32, device=q.device)
     buf = _workspace(workspace, topk_workspace_size(N, H, d, kk, G), q.device)
-    check(load().kmip_fwd_ex(_ptr(q), _ptr(k_), _ptr(v), optr, G, N, H, d, dv, kk, float(scale), _ptr(keep),
-                             float(drop_rate), _ptr(out), _ptr(idx), _ptr(lse), _ptr(buf),
-                             0 if buf is None else buf.numel(), _stream_ptr()))
+    args = (_ptr(q), _ptr(k_), _ptr(v), optr, G, N, H, d, dv, kk, float(scale), _ptr(keep), float(drop_rate),
+            _ptr(out), _ptr(idx), _ptr(lse), _ptr(buf), 0 if buf is None else buf.numel(), _stream_ptr())
+    if events is None:
+        check(load().kmip_fwd_ex(*args))
+    else:
+        if len(events) != 3:
+            raise ValueError("events must be (select_start, select_stop, attend_start)")
+        check(load().kmip_fwd_ex_with_events(*args, *_event_handles(events)))
     return out, idx, lse
 
 

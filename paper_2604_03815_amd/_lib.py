@@ -25,7 +25,7 @@ BWD_KEY_AGGREGATED = 4
 # Every symbol declared in include/kmip.h.
 EXPORTS = (
     "kmip_topk_workspace_size", "kmip_topk", "kmip_topk_with_events", "kmip_attend", "kmip_fwd_workspace_size",
-    "kmip_fwd", "kmip_attend_ex", "kmip_fwd_ex", "kmip_bwd_workspace_size", "kmip_bwd",
+    "kmip_fwd", "kmip_attend_ex", "kmip_fwd_ex", "kmip_fwd_ex_with_events", "kmip_bwd_workspace_size", "kmip_bwd",
     "kmip_bwd_ex_workspace_size", "kmip_bwd_ex", "kmip_fwd_noalloc", "kmip_topk_prefilter_workspace_size",
     "kmip_topk_prefilter", "kmip_status_string", "kmip_last_error",
 )
@@ -70,12 +70,15 @@ def load(path: str = LIB_PATH):
     lib.kmip_fwd_noalloc.argtypes = [P, P, P, i64, i32, i32, i32, f32, P, P, P, P]
     lib.kmip_attend_ex.argtypes = [P, P, P, i64, i32, i32, i32, i32, f32, P, P, f32, P, P, P]
     lib.kmip_fwd_ex.argtypes = [P, P, P, P, i32, i64, i32, i32, i32, i32, f32, P, f32, P, P, P, P, sz, P]
+    lib.kmip_fwd_ex_with_events.argtypes = [P, P, P, P, i32, i64, i32, i32, i32, i32, f32, P, f32, P, P, P, P, sz, P,
+                                            P, P, P]
     lib.kmip_bwd_ex.argtypes = [P, P, P, P, P, P, P, f32, i64, i32, i32, i32, i32, f32, P, P, P, i32, P, sz, P]
     lib.kmip_topk_prefilter_workspace_size.argtypes = [i64, i32, i32, i32]
     lib.kmip_topk_prefilter_workspace_size.restype = sz
     lib.kmip_topk_prefilter.argtypes = [P, P, i64, i32, i32, i32, P, P, P, sz, P]
     for f in ("kmip_topk", "kmip_topk_with_events", "kmip_attend", "kmip_fwd", "kmip_bwd",
-              "kmip_fwd_noalloc", "kmip_attend_ex", "kmip_fwd_ex", "kmip_bwd_ex", "kmip_topk_prefilter"):
+              "kmip_fwd_noalloc", "kmip_attend_ex", "kmip_fwd_ex", "kmip_fwd_ex_with_events", "kmip_bwd_ex",
+              "kmip_topk_prefilter"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kmip_status_string.argtypes = [ctypes.c_int]
     lib.kmip_status_string.restype = ctypes.c_char_p

@@ -213,6 +213,27 @@ PrefilterLayout prefilter_layout(int64_t N, int32_t H, int32_t d) {
     return L;
 }
 
+// kmip_attend_ex with an optional query order (perm [H][N], the forward's
+// grouping, or nullptr) for the order the aggregate takes query-heads in.
+kmip_status_t attend_checked(const void* Q, const void* K, const void* V, int64_t N, int32_t H, int32_t d,
+                             int32_t dv, int32_t k, float scale, const int32_t* topk_idx, const uint8_t* keep,
+                             float drop_rate, const int32_t* perm, float* out, float* lse, void* stream_) {
+    kmip_status_t s = check_sizes(N, H, d, k);
+    if (s != KMIP_OK) return s;
+    if ((s = check_value_width(N, H, dv)) != KMIP_OK) return s;
+    if ((s = check_scale(scale)) != KMIP_OK) return s;
+    if ((s = check_dropout(keep, drop_rate)) != KMIP_OK) return s;
+    if (N == 0) return ok();
+    if (!Q || !K || !V || !topk_idx || !out || !lse)
+        return record_error(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_attend");
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V))
+        return record_error(KMIP_ERR_INVALID_ARG, "Q, K and V must be 16-byte aligned");
+    hipError_t e = kmip::launch_attend(Q, K, V, topk_idx, keep, 1.0f / (1.0f - drop_rate), (int32_t)N, H, d, dv,
+                                       k, scale, perm, out, lse, reinterpret_cast<hipStream_t>(stream_));
+    if (e != hipSuccess) return hip_fail(e, "attend launch");
+    return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -402,20 +423,7 @@ kmip_status_t kmip_topk_prefilter(const void* Q, const void* K, int64_t N, int32
 kmip_status_t kmip_attend_ex(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
                              int32_t d, int32_t dv, int32_t k, float scale, const int32_t* topk_idx,
                              const uint8_t* keep, float drop_rate, float* out, float* lse, void* stream_) {
-    kmip_status_t s = check_sizes(N, H, d, k);
-    if (s != KMIP_OK) return s;
-    if ((s = check_value_width(N, H, dv)) != KMIP_OK) return s;
-    if ((s = check_scale(scale)) != KMIP_OK) return s;
-    if ((s = check_dropout(keep, drop_rate)) != KMIP_OK) return s;
-    if (N == 0) return ok();
-    if (!Q || !K || !V || !topk_idx || !out || !lse)
-        return record_error(KMIP_ERR_INVALID_ARG, "null buffer passed to kmip_attend");
-    if (!aligned16(Q) || !aligned16(K) || !aligned16(V))
-        return record_error(KMIP_ERR_INVALID_ARG, "Q, K and V must be 16-byte aligned");
-    hipError_t e = kmip::launch_attend(Q, K, V, topk_idx, keep, 1.0f / (1.0f - drop_rate), (int32_t)N, H, d, dv,
-                                       k, scale, out, lse, reinterpret_cast<hipStream_t>(stream_));
-    if (e != hipSuccess) return hip_fail(e, "attend launch");
-    return ok();
+    return attend_checked(Q, K, V, N, H, d, dv, k, scale, topk_idx, keep, drop_rate, nullptr, out, lse, stream_);
 }
 
 kmip_status_t kmip_attend(const void* Q, const void* K, const void* V, int64_t N, int32_t H,
@@ -428,6 +436,15 @@ kmip_status_t kmip_fwd_ex(const void* Q, const void* K, const void* V, const int
                           int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k,
                           float scale, const uint8_t* keep, float drop_rate, float* out, int32_t* topk_idx,
                           float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+    return kmip_fwd_ex_with_events(Q, K, V, graph_offsets, num_graphs, N, H, d, dv, k, scale, keep, drop_rate, out,
+                                   topk_idx, lse, workspace, workspace_bytes, stream, nullptr, nullptr, nullptr);
+}
+
+kmip_status_t kmip_fwd_ex_with_events(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,
+                                      int32_t num_graphs, int64_t N, int32_t H, int32_t d, int32_t dv, int32_t k,
+                                      float scale, const uint8_t* keep, float drop_rate, float* out,
+                                      int32_t* topk_idx, float* lse, void* workspace, size_t workspace_bytes,
+                                      void* stream, void* select_start, void* select_stop, void* attend_start) {
     kmip_status_t s = check_sizes(N, H, d, k);
     if (s != KMIP_OK) return s;
     if ((s = check_value_width(N, H, dv)) != KMIP_OK) return s;
@@ -435,10 +452,22 @@ kmip_status_t kmip_fwd_ex(const void* Q, const void* K, const void* V, const int
     if ((s = check_dropout(keep, drop_rate)) != KMIP_OK) return s;
     if (N > 0 && (!V || !out || !lse)) return record_error(KMIP_ERR_INVALID_ARG, "null V, out or lse");
     if (N > 0 && !aligned16(V)) return record_error(KMIP_ERR_INVALID_ARG, "V must be 16-byte aligned");
-    s = kmip_topk(Q, K, graph_offsets, num_graphs, N, H, d, k, topk_idx, workspace,
-                  workspace_bytes, stream);
+    s = kmip_topk_with_events(Q, K, graph_offsets, num_graphs, N, H, d, k, topk_idx, workspace,
+                              workspace_bytes, stream, select_start, select_stop);
     if (s != KMIP_OK) return s;
-    return kmip_attend_ex(Q, K, V, N, H, d, dv, k, scale, topk_idx, keep, drop_rate, out, lse, stream);
+    if (N > 0 && attend_start != nullptr) {
+        const hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(attend_start),
+                                            reinterpret_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return hip_fail(e, "event record");
+    }
+    // one graph grouped by direction: the aggregate takes the queries in
+    // that order too (the grouping is still in the workspace)
+    const int32_t G = graph_offsets ? num_graphs : 1;
+    const int32_t* perm = nullptr;
+    if (N > 0 && use_grouping(N, G, d))
+        perm = kmip::group_perm_in(reinterpret_cast<char*>(workspace) + tiled_bytes(N, H, d) + kCounterBytes,
+                                   (int32_t)N, H, d);
+    return attend_checked(Q, K, V, N, H, d, dv, k, scale, topk_idx, keep, drop_rate, perm, out, lse, stream);
 }
 
 kmip_status_t kmip_fwd(const void* Q, const void* K, const void* V, const int32_t* graph_offsets,

@@ -18,6 +18,12 @@
 // Attention dropout (keep != nullptr): slot t's weight in the sum is
 // multiplied by keep_scale when keep[qh k + t] is nonzero and by 0
 // otherwise; the softmax statistics (lse) are those before dropout.
+//
+// Order: with perm == nullptr, team t of block b takes query-head
+// 16 b + t.  With a query order perm [H][N] (the forward's grouping of the
+// queries by direction), block (b, h) takes positions 16 b .. 16 b + 15 of
+// head h in that order: queries of one group select mostly the same keys,
+// so the teams of a workgroup gather the same rows.
 #include "kmip_device.h"
 #include "kmip_internal.h"
 
@@ -28,12 +34,22 @@ template <int D, int DV, int NS>
 __global__ __launch_bounds__(256) void attend_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     const int32_t* __restrict__ idx, const uint8_t* __restrict__ keep, float keep_scale, int32_t N,
-    int32_t H, int32_t k, float scale, float* __restrict__ out, float* __restrict__ lse) {
+    int32_t H, int32_t k, float scale, const int32_t* __restrict__ perm, float* __restrict__ out,
+    float* __restrict__ lse) {
     constexpr bool kKeep = DV / 2 * NS <= 64;
     const int tl = threadIdx.x & 15;
-    const int64_t qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
-    if (qh >= (int64_t)N * H) return;  // whole team exits together
-    const int h = (int)(qh % H);
+    int64_t qh;
+    int h;
+    if (perm != nullptr) {
+        h = blockIdx.y;
+        const int64_t p = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+        if (p >= N) return;  // whole team exits together
+        qh = (int64_t)perm[(size_t)h * N + p] * H + h;
+    } else {
+        qh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+        if (qh >= (int64_t)N * H) return;  // whole team exits together
+        h = (int)(qh % H);
+    }
 
     float q[D];
     load_row_f32<D>(q, Q + (size_t)qh * D);
@@ -108,30 +124,30 @@ __global__ __launch_bounds__(256) void attend_kernel(
 }
 
 template <int D, int DV>
-void launch_attend_d(unsigned blocks, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
+void launch_attend_d(dim3 blocks, hipStream_t stream, const uint16_t* q, const uint16_t* kk,
                      const uint16_t* v, const int32_t* idx, const uint8_t* keep, float keep_scale, int32_t N,
-                     int32_t H, int32_t k, float scale, float* out, float* lse) {
+                     int32_t H, int32_t k, float scale, const int32_t* perm, float* out, float* lse) {
     const int ns = (k + 15) / 16;
     if (ns <= 1)
         hipLaunchKernelGGL((attend_kernel<D, DV, 1>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
-                           keep_scale, N, H, k, scale, out, lse);
+                           keep_scale, N, H, k, scale, perm, out, lse);
     else if (ns <= 2)
         hipLaunchKernelGGL((attend_kernel<D, DV, 2>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
-                           keep_scale, N, H, k, scale, out, lse);
+                           keep_scale, N, H, k, scale, perm, out, lse);
     else if (ns <= 4)
         hipLaunchKernelGGL((attend_kernel<D, DV, 4>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
-                           keep_scale, N, H, k, scale, out, lse);
+                           keep_scale, N, H, k, scale, perm, out, lse);
     else if (ns <= 8)
         hipLaunchKernelGGL((attend_kernel<D, DV, 8>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
-                           keep_scale, N, H, k, scale, out, lse);
+                           keep_scale, N, H, k, scale, perm, out, lse);
     else if constexpr (D <= 64) {
         // k > 128 (d <= 64 only)
         if (ns <= 16)
             hipLaunchKernelGGL((attend_kernel<D, DV, 16>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
-                               keep_scale, N, H, k, scale, out, lse);
+                               keep_scale, N, H, k, scale, perm, out, lse);
         else
             hipLaunchKernelGGL((attend_kernel<D, DV, 32>), dim3(blocks), dim3(256), 0, stream, q, kk, v, idx, keep,
-                               keep_scale, N, H, k, scale, out, lse);
+                               keep_scale, N, H, k, scale, perm, out, lse);
     }
 }
 
@@ -139,16 +155,18 @@ void launch_attend_d(unsigned blocks, hipStream_t stream, const uint16_t* q, con
 
 hipError_t launch_attend(const void* Q, const void* K, const void* V, const int32_t* idx,
                          const uint8_t* keep, float keep_scale, int32_t N, int32_t H, int32_t d, int32_t dv,
-                         int32_t k, float scale, float* out, float* lse, hipStream_t stream) {
+                         int32_t k, float scale, const int32_t* perm, float* out, float* lse,
+                         hipStream_t stream) {
     const int64_t nqh = (int64_t)N * H;
     if (nqh == 0) return hipSuccess;
-    const unsigned blocks = (unsigned)((nqh + 15) / 16);
+    const dim3 blocks = perm != nullptr ? dim3((unsigned)((N + 15) / 16), (unsigned)H)
+                                        : dim3((unsigned)((nqh + 15) / 16));
     const uint16_t* q = reinterpret_cast<const uint16_t*>(Q);
     const uint16_t* kk = reinterpret_cast<const uint16_t*>(K);
     const uint16_t* v = reinterpret_cast<const uint16_t*>(V);
 #define KMIP_ATTEND_CASE(DD, DVV)                                                              \
     if (d == DD && dv == DVV) {                                                                \
-        launch_attend_d<DD, DVV>(blocks, stream, q, kk, v, idx, keep, keep_scale, N, H, k, scale, out, lse); \
+        launch_attend_d<DD, DVV>(blocks, stream, q, kk, v, idx, keep, keep_scale, N, H, k, scale, perm, out, lse); \
         return hipGetLastError();                                                              \
     }
 #define KMIP_ATTEND_D(DD) \

@@ -175,6 +175,14 @@ size_t group_workspace_bytes(int32_t N, int32_t H, int32_t d) {
            al((size_t)2 * H * C * sizeof(int32_t)) + al((size_t)H * N * sizeof(int32_t));
 }
 
+const int32_t* group_perm_in(const void* ws, int32_t N, int32_t H, int32_t d) {
+    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+    const char* p = reinterpret_cast<const char*>(ws);
+    p += al((size_t)H * C * d * sizeof(uint16_t)) + al((size_t)H * N * sizeof(uint16_t)) +
+         al((size_t)2 * H * C * sizeof(int32_t));
+    return reinterpret_cast<const int32_t*>(p);
+}
+
 hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, void* ws,
                                 QueryGroups* out, hipStream_t stream) {
     auto al = [](size_t x) { return (x + 255) / 256 * 256; };

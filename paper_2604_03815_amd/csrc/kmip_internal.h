@@ -133,6 +133,9 @@ size_t group_workspace_bytes(int32_t N, int32_t H, int32_t d);
 
 // Groups the queries of each head by direction into ws and describes the
 // result in *out.
+// The query order [H][N] a grouping workspace holds after
+// launch_group_queries (the same address QueryGroups::perm was given).
+const int32_t* group_perm_in(const void* ws, int32_t N, int32_t H, int32_t d);
 hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, void* ws,
                                 QueryGroups* out, hipStream_t stream);
 
@@ -142,7 +145,8 @@ hipError_t launch_group_queries(const void* Q, int32_t N, int32_t H, int32_t d, 
 // or nullptr (no dropout), for this launcher and the backward ones.
 hipError_t launch_attend(const void* Q, const void* K, const void* V, const int32_t* idx,
                          const uint8_t* keep, float keep_scale, int32_t N, int32_t H, int32_t d, int32_t dv,
-                         int32_t k, float scale, float* out, float* lse, hipStream_t stream);
+                         int32_t k, float scale, const int32_t* perm, float* out, float* lse,
+                         hipStream_t stream);
 
 // The backward launchers take the query/key width d and the value width dv
 // (each in {16, 32, 64}); the bucketed one needs dv == d.

@@ -515,3 +515,21 @@ def test_peak_memory_linear_in_n():
         print(f"N={n}: {per_node[n]:.0f} peak bytes per node", flush=True)
     assert per_node[500_000] <= 1.1 * per_node[125_000]
     assert per_node[500_000] < 8192
+
+
+def test_fwd_grouped_order_matches_separate_calls():
+    # kmip_fwd on one grouped graph takes the aggregate in the grouped query
+    # order; the rows must be those of kmip_topk + kmip_attend, bit for bit,
+    # and the recorded events must bracket the select kernel and the
+    # aggregate in that order.
+    w = workloads.iid(12000, 2, 16, 16, seed=12)
+    q, k, v = _dev(w.q), _dev(w.kk), _dev(w.v)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    out, idx, lse = kmip.fwd(q, k, v, w.k, w.scale, events=ev)
+    end = torch.cuda.Event(enable_timing=True)
+    end.record()
+    idx2 = kmip.topk(q, k, w.k)
+    out2, lse2 = kmip.attend(q, k, v, idx2, w.scale)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx2) and torch.equal(out, out2) and torch.equal(lse, lse2)
+    assert ev[0].elapsed_time(ev[1]) > 0 and ev[1].elapsed_time(ev[2]) >= 0 and ev[2].elapsed_time(end) > 0
