@@ -14,9 +14,14 @@
 //   2. sixteen threads per query hold its scores as order-preserving 32-bit
 //      codes (larger score, larger code) and fix the top 16 bits of the code
 //      T of the k'-th best key, k' = min(k, n), bit by bit: T is the largest
-//      such prefix with at least k' keys at or above it.  The keys at or
-//      above T are the candidates: the k' best and the few others that share
-//      the k'-th best's 16-bit prefix;
+//      such prefix with at least k' keys at or above it.  The leading bits
+//      that the largest code and a lower bound L of the k'-th best share (for
+//      k' <= 16 the k'-th largest of the threads' own maxima) are fixed at
+//      once, and when at most kSmallList keys reach L with its low 16 bits
+//      cleared (every candidate does), the threads list those keys in LDS,
+//      seven a thread, and the search and the steps below run on the list.
+//      The keys at or above T are the candidates: the k' best and the few
+//      others that share the k'-th best's 16-bit prefix;
 //   3. when more than kSmallKept keys are candidates (many exact ties), the
 //      low 16 bits are fixed as well, giving the k'-th best code exactly, and
 //      the candidates are the keys above it plus, at it, the ones of lowest
@@ -35,6 +40,7 @@ namespace {
 
 constexpr int kSmallStride = 33;                     // LDS words per key row of scores
 constexpr int kSmallKept = KMIP_MAX_K_WIDE;          // candidates listed per query (k <= this)
+constexpr int kSmallList = 112;                      // keys listed per query above the lower bound
 constexpr int kSmallTpq = 16;                        // threads per query
 constexpr int kSmallThreads = 32 * kSmallTpq;
 constexpr int kSmallPer = (kSmallGraph + kSmallTpq - 1) / kSmallTpq;   // codes per thread
@@ -65,6 +71,32 @@ __device__ __forceinline__ int group_scan(int v) {
     v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true);    // row_shr:4
     v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true);    // row_shr:8
     return v;
+}
+
+// Largest value over the 16 threads of a query, with the same row operations.
+__device__ __forceinline__ uint32_t group_max(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));
+    return v;
+}
+
+// The kk-th largest of the 16 threads' values v (kk <= 16): the value of the
+// threads with fewer than kk values above theirs and at least kk at or
+// above (row rotations bring every other thread's value).
+__device__ __forceinline__ uint32_t group_kth(uint32_t v, int kk) {
+    int gt = 0, ge = 1;
+#define KMIP_ROR(R)                                                                       \
+    {                                                                                     \
+        const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x120 + R, 0xF, 0xF, false); \
+        gt += o > v ? 1 : 0;                                                              \
+        ge += o >= v ? 1 : 0;                                                             \
+    }
+    KMIP_ROR(1) KMIP_ROR(2) KMIP_ROR(3) KMIP_ROR(4) KMIP_ROR(5) KMIP_ROR(6) KMIP_ROR(7) KMIP_ROR(8)
+    KMIP_ROR(9) KMIP_ROR(10) KMIP_ROR(11) KMIP_ROR(12) KMIP_ROR(13) KMIP_ROR(14) KMIP_ROR(15)
+#undef KMIP_ROR
+    return group_max(gt < kk && ge >= kk ? v : 0u);
 }
 
 template <int D>
@@ -142,52 +174,111 @@ __global__ __launch_bounds__(kSmallThreads) void small_select_kernel(const uint4
         for (int i = 0; i < kSmallPer; ++i) c += code[i] >= x ? 1 : 0;
         return group_sum(c);
     };
-    uint32_t T = 0;
-    for (int bit = 31; bit >= 16; --bit)
-        if (count_at_least(T | (1u << bit)) >= kk) T |= 1u << bit;
-    // 3. many candidates: the exact k'-th best code and the ties at it
-    const bool exact = count_at_least(T) > kSmallKept;
-    int m = 0;
-    if (exact) {
-        for (int bit = 15; bit >= 0; --bit)
-            if (count_at_least(T | (1u << bit)) >= kk) T |= 1u << bit;
-        int above = 0;
+    // The k'-th best code lies between a lower bound L (for k' <= 16 the
+    // k'-th largest of the threads' maxima, which k' keys reach; else 0) and
+    // the largest code U, so it shares their common leading bits, and the
+    // bit-by-bit search starts below them.
+    uint32_t mx = 0;
 #pragma unroll
-        for (int i = 0; i < kSmallPer; ++i) above += code[i] > T ? 1 : 0;
-        const int need = kk - group_sum(above);
-        if (need > 0) {
-            // the smallest m such that the keys at T with index below m
-            // complete the row
-            int lo = 0, hi = n;
-            while (hi - lo > 1) {
-                const int mid = (lo + hi) >> 1;
-                int c = 0;
+    for (int i = 0; i < kSmallPer; ++i) mx = max(mx, code[i]);
+    const uint32_t U = group_max(mx);
+    const uint32_t L = kk <= kSmallTpq ? group_kth(mx, kk) : 0u;
+    const uint32_t diff = L ^ U;
+    const int top = diff == 0u ? -1 : 31 - __clz(diff);
+    uint32_t T = top < 0 ? U : top >= 31 ? 0u : U & ~((2u << top) - 1u);
+    T &= 0xFFFF0000u;
+    // Every candidate's code is at least T >= L with its low 16 bits
+    // cleared.  When at most kSmallList keys reach that, the query's threads
+    // list them (7 a thread) and search and select on the list alone.
+    const uint32_t Lc = L & 0xFFFF0000u;
+    int lm = 0;
 #pragma unroll
-                for (int i = 0; i < kSmallPer; ++i) c += (code[i] == T && s + kSmallTpq * i < mid) ? 1 : 0;
-                if (group_sum(c) >= need) hi = mid; else lo = mid;
-            }
-            m = hi;
-        }
-    }
-    auto take = [&](int i) {
-        const int j = s + kSmallTpq * i;
-        return exact ? (code[i] > T || (code[i] == T && code[i] != 0u && j < m)) : (code[i] >= T && code[i] != 0u);
-    };
-    int mine = 0;
-#pragma unroll
-    for (int i = 0; i < kSmallPer; ++i) mine += take(i) ? 1 : 0;
-    // inclusive prefix sum over the query's threads, and their total
-    const int pre = group_scan(mine);
-    const int nc = group_sum(mine);
-    __syncthreads();   // every score is in registers: the LDS is reused for the candidates
+    for (int i = 0; i < kSmallPer; ++i) lm += code[i] >= Lc && code[i] != 0u ? 1 : 0;
+    const int lpre = group_scan(lm);
+    const bool use_list = group_sum(lm) <= kSmallList;   // the same for a query's threads
+    __syncthreads();   // every score is in registers: the LDS is reused
 
     // 4. the candidates of each query, listed in LDS, then placed by rank
     uint64_t* kept = reinterpret_cast<uint64_t*>(sc);   // [32][kSmallKept] (code, ~index)
-    if (active) {
-        int slot = q * kSmallKept + pre - mine;
+    uint64_t* lst = kept + 32 * kSmallKept;             // [32][kSmallList]
+    if (use_list) {
+        int slot = q * kSmallList + lpre - lm;
 #pragma unroll
         for (int i = 0; i < kSmallPer; ++i)
-            if (take(i)) kept[slot++] = ((uint64_t)code[i] << 32) | (uint32_t)(~(s + kSmallTpq * i));
+            if (code[i] >= Lc && code[i] != 0u)
+                lst[slot++] = ((uint64_t)code[i] << 32) | (uint32_t)(~(s + kSmallTpq * i));
+    }
+    __syncthreads();
+    int nc = 0;
+    if (use_list) {
+        const int m = group_sum(lm);
+        uint64_t e[kSmallList / kSmallTpq];
+#pragma unroll
+        for (int r = 0; r < kSmallList / kSmallTpq; ++r)
+            e[r] = s + kSmallTpq * r < m ? lst[q * kSmallList + s + kSmallTpq * r] : 0ull;
+        auto list_at_least = [&](uint32_t x) {
+            int c = 0;
+#pragma unroll
+            for (int r = 0; r < kSmallList / kSmallTpq; ++r) c += (uint32_t)(e[r] >> 32) >= x ? 1 : 0;
+            return group_sum(c);
+        };
+        for (int bit = min(top, 31); bit >= 16; --bit)
+            if (list_at_least(T | (1u << bit)) >= kk) T |= 1u << bit;
+        // at most kSmallList keys reach T: no exact pass
+        int mine = 0;
+#pragma unroll
+        for (int r = 0; r < kSmallList / kSmallTpq; ++r) mine += (uint32_t)(e[r] >> 32) >= T && e[r] != 0ull ? 1 : 0;
+        const int pre = group_scan(mine);
+        nc = group_sum(mine);
+        if (active) {
+            int slot = q * kSmallKept + pre - mine;
+#pragma unroll
+            for (int r = 0; r < kSmallList / kSmallTpq; ++r)
+                if ((uint32_t)(e[r] >> 32) >= T && e[r] != 0ull) kept[slot++] = e[r];
+        }
+    } else {
+        for (int bit = min(top, 31); bit >= 16; --bit)
+            if (count_at_least(T | (1u << bit)) >= kk) T |= 1u << bit;
+        // 3. many candidates: the exact k'-th best code and the ties at it
+        const bool exact = count_at_least(T) > kSmallKept;
+        int m = 0;
+        if (exact) {
+            for (int bit = 15; bit >= 0; --bit)
+                if (count_at_least(T | (1u << bit)) >= kk) T |= 1u << bit;
+            int above = 0;
+#pragma unroll
+            for (int i = 0; i < kSmallPer; ++i) above += code[i] > T ? 1 : 0;
+            const int need = kk - group_sum(above);
+            if (need > 0) {
+                // the smallest m such that the keys at T with index below m
+                // complete the row
+                int lo = 0, hi = n;
+                while (hi - lo > 1) {
+                    const int mid = (lo + hi) >> 1;
+                    int c = 0;
+#pragma unroll
+                    for (int i = 0; i < kSmallPer; ++i) c += (code[i] == T && s + kSmallTpq * i < mid) ? 1 : 0;
+                    if (group_sum(c) >= need) hi = mid; else lo = mid;
+                }
+                m = hi;
+            }
+        }
+        auto take = [&](int i) {
+            const int j = s + kSmallTpq * i;
+            return exact ? (code[i] > T || (code[i] == T && code[i] != 0u && j < m)) : (code[i] >= T && code[i] != 0u);
+        };
+        int mine = 0;
+#pragma unroll
+        for (int i = 0; i < kSmallPer; ++i) mine += take(i) ? 1 : 0;
+        // inclusive prefix sum over the query's threads, and their total
+        const int pre = group_scan(mine);
+        nc = group_sum(mine);
+        if (active) {
+            int slot = q * kSmallKept + pre - mine;
+#pragma unroll
+            for (int i = 0; i < kSmallPer; ++i)
+                if (take(i)) kept[slot++] = ((uint64_t)code[i] << 32) | (uint32_t)(~(s + kSmallTpq * i));
+        }
     }
     __syncthreads();
     if (active) {
@@ -209,8 +300,8 @@ hipError_t launch_small_select(const void* kp, const void* Q, const Task* tasks,
                                int32_t H, int32_t d, int32_t k, int32_t ntiles, int32_t* topk_idx,
                                hipStream_t stream) {
     if (ntasks <= 0) return hipSuccess;
-    static_assert((size_t)32 * kSmallKept * 8 <= sizeof(float) * kSmallGraph * kSmallStride,
-                  "the kept keys fit the score area");
+    static_assert((size_t)32 * (kSmallKept + kSmallList) * 8 <= sizeof(float) * kSmallGraph * kSmallStride,
+                  "the kept keys and the lists fit the score area");
     if (k > kSmallKept) return hipErrorInvalidValue;
     const dim3 grid((unsigned)((int64_t)ntasks * H));
     const uint4* kpp = reinterpret_cast<const uint4*>(kp);
