@@ -573,6 +573,147 @@ __device__ __forceinline__ int32_t wave_rank(int32_t* ctr, int32_t digit) {
     return base + (int32_t)__popcll(same & ((1ull << lane) - 1ull));
 }
 
+// Inputs of one query-head of the coefficient pass, fetched one query-head
+// ahead (coef_fetch) so that their loads overlap the previous query-head's
+// arithmetic (coef_compute).
+template <int D, int NS>
+struct CoefIn {
+    int32_t j[NS];       // this lane's key slots tl + 16 s (-1: none)
+    uint4 qw[D / 8];     // q_i and dO_i as bf16 words
+    uint4 gw[D / 8];
+    float l;             // lse (-inf: no key kept, or no query-head)
+    int64_t qh;
+    bool valid;          // u < N H
+};
+
+template <int D, int NS>
+__device__ __forceinline__ void coef_fetch(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ dO,
+                                           const int32_t* __restrict__ idx, const float* __restrict__ lse,
+                                           int32_t N, int32_t H, int32_t k, int64_t u, int64_t nh, int32_t i, int tl,
+                                           CoefIn<D, NS>& in) {
+    in.valid = u < nh;
+    const int32_t h = in.valid ? (int32_t)(u / N) : 0;
+    in.qh = (int64_t)i * H + h;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const int slot = tl + 16 * s;
+        in.j[s] = in.valid && slot < k ? idx[(size_t)in.qh * k + slot] : -1;
+    }
+    if (in.valid) {
+        load_row_words<D>(in.qw, Q + (size_t)in.qh * D);
+        load_row_words<D>(in.gw, dO + (size_t)in.qh * D);
+        in.l = lse[in.qh];
+    } else {
+#pragma unroll
+        for (int c = 0; c < D / 8; ++c) in.qw[c] = in.gw[c] = make_uint4(0, 0, 0, 0);
+        in.l = -INFINITY;
+    }
+}
+
+// coef_one's arithmetic (value width D, with the interleaved copy) on
+// fetched inputs: the same operations in the same order, so the same bits.
+template <int D, int NS>
+__device__ __forceinline__ void coef_compute(const CoefIn<D, NS>& in, const uint16_t* __restrict__ K,
+                                             const uint16_t* __restrict__ V, const uint8_t* __restrict__ keep,
+                                             float keep_scale, int32_t N, int32_t H, int32_t k, float scale,
+                                             int tl, float* __restrict__ dQ, uint16_t* __restrict__ QGt,
+                                             size_t qg_row, int32_t (&jj)[NS], float (&ca)[NS], float (&cp)[NS]) {
+    constexpr bool kKeep = D / 2 * NS <= 64;
+    const int64_t qh = in.qh;
+    const int h = (int)(qh % H);
+    if (in.valid && tl < D / 4) {
+        // row qg_row of the interleaved copy: lane tl < D / 8 writes chunk tl
+        // of q_i, lane D / 8 + c chunk c of dO_i
+        uint4 v = in.qw[0];
+#pragma unroll
+        for (int c = 1; c < D / 8; ++c)
+            if (tl == c) v = in.qw[c];
+#pragma unroll
+        for (int c = 0; c < D / 8; ++c)
+            if (tl == D / 8 + c) v = in.gw[c];
+        reinterpret_cast<uint4*>(QGt + qg_row * (2 * D))[tl] = v;
+    }
+    float q[D], g[D];
+#pragma unroll
+    for (int c = 0; c < D / 8; ++c) {
+        const uint32_t wq[4] = {in.qw[c].x, in.qw[c].y, in.qw[c].z, in.qw[c].w};
+        const uint32_t wg[4] = {in.gw[c].x, in.gw[c].y, in.gw[c].z, in.gw[c].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            q[8 * c + 2 * e] = bf16_bits_to_f32(wq[e] & 0xFFFFu);
+            q[8 * c + 2 * e + 1] = bf16_bits_to_f32(wq[e] >> 16);
+            g[8 * c + 2 * e] = bf16_bits_to_f32(wg[e] & 0xFFFFu);
+            g[8 * c + 2 * e + 1] = bf16_bits_to_f32(wg[e] >> 16);
+        }
+    }
+    const float l = in.l;
+    float p[NS], dp[NS], pv[NS];
+    uint4 kw[kKeep ? NS : 1][D / 8];
+    float dsum = 0.0f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        p[s] = 0.0f;
+        dp[s] = 0.0f;
+        pv[s] = 0.0f;
+        jj[s] = -1;
+        const int slot = tl + 16 * s;
+        const int32_t j = in.j[s];
+        if (j >= 0 && j < N) jj[s] = j;
+        if (j >= 0 && j < N && l != -INFINITY) {
+            uint4 w[D / 8];
+            load_row_words<D>(w, K + ((size_t)j * H + h) * D);
+            if constexpr (kKeep) {
+#pragma unroll
+                for (int c = 0; c < D / 8; ++c) kw[s][c] = w[c];
+            }
+            const float z = scale * dot_words_bf16<D>(q, w);
+            p[s] = __expf(z - l);
+            dp[s] = dot_row_bf16<D>(g, V + ((size_t)j * H + h) * D);
+            pv[s] = p[s];
+            if (keep != nullptr) {
+                const float f = keep[(size_t)qh * k + slot] != 0 ? keep_scale : 0.0f;
+                dp[s] *= f;
+                pv[s] = p[s] * f;
+            }
+        }
+        dsum = fmaf(p[s], dp[s], dsum);
+    }
+    dsum = group16_sum(dsum);
+    float acc[D];
+#pragma unroll
+    for (int t = 0; t < D; ++t) acc[t] = 0.0f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const float gs = p[s] * (dp[s] - dsum);
+        ca[s] = scale * gs;
+        cp[s] = pv[s];
+        if (jj[s] >= 0 && l != -INFINITY) {
+            uint4 w[D / 8];
+            if constexpr (kKeep) {
+#pragma unroll
+                for (int c = 0; c < D / 8; ++c) w[c] = kw[s][c];
+            } else {
+                load_row_words<D>(w, K + ((size_t)jj[s] * H + h) * D);
+            }
+#pragma unroll
+            for (int c = 0; c < D / 8; ++c) {
+                const uint32_t ww[4] = {w[c].x, w[c].y, w[c].z, w[c].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[8 * c + 2 * e] = fmaf(gs, bf16_bits_to_f32(ww[e] & 0xFFFFu), acc[8 * c + 2 * e]);
+                    acc[8 * c + 2 * e + 1] = fmaf(gs, bf16_bits_to_f32(ww[e] >> 16), acc[8 * c + 2 * e + 1]);
+                }
+            }
+        }
+    }
+    float out[D / 16];
+    team_sum_transpose<D>(acc, out, tl);
+    if (in.valid) {
+#pragma unroll
+        for (int u = 0; u < D / 16; ++u) dQ[(size_t)qh * D + 16 * u + tl] = scale * out[u];
+    }
+}
+
 // The coefficient pass fused with placement pass 1: a
 // workgroup takes 128 / NS query-heads (8 / NS per team, at most 2048
 // pairs), computes their coefficients, dQ and the interleaved copy, and
@@ -606,19 +747,40 @@ __global__ __launch_bounds__(256) void coef_split_kernel(
     if (t < kMaxSup) cnt[t] = 0;
     PairRecord rr[R];
     int32_t sup[R], slot[R];
+    // With narrow rows the inputs of a team's next query-head are fetched
+    // while the current one computes (the query rows of all of them first);
+    // wider rows would not leave the registers for it.
+    constexpr bool kAhead = D == 16 || (D == 32 && NS == 1);
+    int32_t qrow[TQ];
+    CoefIn<D, NS> nxt;
+    if constexpr (kAhead) {
+#pragma unroll
+        for (int it = 0; it < TQ; ++it) {
+            const int64_t u = (int64_t)blockIdx.x * (16 * TQ) + it * 16 + team;
+            qrow[it] = u < nh ? perm[u] : 0;
+        }
+        coef_fetch<D, NS>(Q, dO, idx, lse, N, H, k, (int64_t)blockIdx.x * (16 * TQ) + team, nh, qrow[0], tl, nxt);
+    }
 #pragma unroll
     for (int it = 0; it < TQ; ++it) {
         const int64_t u = (int64_t)blockIdx.x * (16 * TQ) + it * 16 + team;
         const int32_t h = u < nh ? (int32_t)(u / N) : 0;
-        const int32_t i = u < nh ? perm[u] : 0;
-        const int64_t qh = (int64_t)i * H + h;
         int32_t jj[NS];
         float ca[NS], cp[NS];
+        if constexpr (kAhead) {
+            const CoefIn<D, NS> cur = nxt;
+            if (it + 1 < TQ)
+                coef_fetch<D, NS>(Q, dO, idx, lse, N, H, k, u + 16, nh, qrow[it + 1], tl, nxt);
+            coef_compute<D, NS>(cur, K, V, keep, keep_scale, N, H, k, scale, tl, dQ, QGt, (size_t)u, jj, ca, cp);
+        } else {
+            const int32_t i = u < nh ? perm[u] : 0;
+            const int64_t qh = (int64_t)i * H + h;
 #pragma unroll
-        for (int s2 = 0; s2 < NS; ++s2) jj[s2] = -1;
-        if (u < nh)
-            coef_one<D, D, NS>(Q, K, V, dO, idx, lse, keep, keep_scale, N, H, k, scale, qh, tl, dQ, QGt, (size_t)u, jj,
-                               ca, cp);
+            for (int s2 = 0; s2 < NS; ++s2) jj[s2] = -1;
+            if (u < nh)
+                coef_one<D, D, NS>(Q, K, V, dO, idx, lse, keep, keep_scale, N, H, k, scale, qh, tl, dQ, QGt,
+                                   (size_t)u, jj, ca, cp);
+        }
 #pragma unroll
         for (int s2 = 0; s2 < NS; ++s2) {
             const int r = it * NS + s2;
