@@ -614,7 +614,7 @@ __device__ __forceinline__ void coef_fetch(const uint16_t* __restrict__ Q, const
 // fetched inputs: the same operations in the same order, so the same bits.
 // (A coef_one built from coef_fetch and coef_compute, which would leave one
 // copy of the arithmetic, made the code the compiler emits for width 32
-// slower: the coefficient pass went from 1.10 to 1.39 ms on a 100k-node
+// slower: the backward went from 1.10 to 1.39 ms on a 100k-node
 // graph at d = 32, so the two stay apart.)
 template <int D, int NS>
 __device__ __forceinline__ void coef_compute(const CoefIn<D, NS>& in, const uint16_t* __restrict__ K,
