@@ -533,3 +533,33 @@ def test_fwd_grouped_order_matches_separate_calls():
     torch.cuda.synchronize()
     assert torch.equal(idx, idx2) and torch.equal(out, out2) and torch.equal(lse, lse2)
     assert ev[0].elapsed_time(ev[1]) > 0 and ev[1].elapsed_time(ev[2]) >= 0 and ev[2].elapsed_time(end) > 0
+
+
+@pytest.mark.parametrize("k", [1, 8, 16])
+def test_small_graph_lists_and_full_rows_in_one_wave(k):
+    # The small-graph select lists, per query, the keys that reach a lower
+    # bound of its k-th best (k <= 16) and selects on the list when at most
+    # 112 keys do; otherwise it searches all of the row.  Here a quarter of
+    # the queries are zero (every score ties at 0: all n keys reach the
+    # bound, so n > 112 takes the full row) next to queries with integer
+    # rows (short lists), so the four queries of a wave mix both paths.
+    # Integer inputs make the scores exact: every row, order included, must
+    # be the oracle's.
+    rng = np.random.default_rng(77 + k)
+    sizes = [480, 113, 112, 300, 17, 479, 250]
+    N, H, d = sum(sizes), 2, 32
+    q = rng.integers(-2, 3, size=(N, H, d)).astype(np.float32)
+    q[rng.random(N) < 0.25] = 0.0
+    kk = rng.integers(-2, 3, size=(N, H, d)).astype(np.float32)
+    v = rng.standard_normal((N, H, d)).astype(np.float32)
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    w = workloads.Workload("small_mixed", N, H, d, k, 0.25, offsets, workloads.bf16_round(q),
+                           workloads.bf16_round(kk), workloads.bf16_round(v), None, False)
+    print(f"[case] small-graph lists k={k} sizes={sizes}", flush=True)
+    res = _run(w, backward=False)
+    Qd, Kd, Vd, _ = _f64(w)
+    _, o_idx, _ = oracle.forward(Qd, Kd, Vd, k, w.scale, offsets=offsets)
+    np.testing.assert_array_equal(res["idx"], o_idx)
+    ref_out, ref_lse = oracle.attend(Qd, Kd, Vd, res["idx"], w.scale)
+    allclose_report("out", res["out"].reshape(-1, d), ref_out)
+    allclose_report("lse", res["lse"].reshape(-1), ref_lse)
