@@ -187,9 +187,12 @@ __global__ __launch_bounds__(kSmallThreads) void small_select_kernel(const uint4
     const int top = diff == 0u ? -1 : 31 - __clz(diff);
     uint32_t T = top < 0 ? U : top >= 31 ? 0u : U & ~((2u << top) - 1u);
     T &= 0xFFFF0000u;
-    // Every candidate's code is at least T >= L with its low 16 bits
-    // cleared.  When at most kSmallList keys reach that, the query's threads
-    // list them (7 a thread) and search and select on the list alone.
+    // T is the k'-th best code's 16-bit prefix and that code is at least L,
+    // so T, and with it every candidate's code, is at least L with its low
+    // 16 bits cleared (Lc).  When at most kSmallList keys reach Lc, the
+    // query's threads list them (7 a thread) and search and select on the
+    // list alone: for any x >= Lc the list holds every code >= x, and below
+    // Lc both counts reach k'.
     const uint32_t Lc = L & 0xFFFF0000u;
     int lm = 0;
 #pragma unroll
