@@ -701,15 +701,39 @@ __global__ __launch_bounds__(64, 1) void select_kernel(
                 }
                 const uint32_t bits = half_or_rows(lm);
                 if (track) {
+                    // Each query's superblock of largest bound so far (the
+                    // first in visiting order among equal ones).  In a tile
+                    // of whole superblocks: the largest of the lane's 16
+                    // rows by a max3 tree and the first row that holds it;
+                    // in the last, row by row, valid rows only.
                     const int sb0 = 64 * w + 32 * ct;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int sb = sb0 + tile_row(r, half);
+                    if (sb0 + 32 <= nsb) {
 #pragma unroll
                         for (int b = 0; b < QB; ++b) {
-                            const bool better = sb < nsb && theta[b] != INFINITY && bacc[b][r] > best_v[b];
-                            best_v[b] = better ? bacc[b][r] : best_v[b];
-                            best_sb[b] = better ? sb : best_sb[b];
+                            const f32x16& a = bacc[b];
+                            const float l0 = fmaxf(fmaxf(a[0], a[1]), a[2]);
+                            const float l1 = fmaxf(fmaxf(a[3], a[4]), a[5]);
+                            const float l2 = fmaxf(fmaxf(a[6], a[7]), a[8]);
+                            const float l3 = fmaxf(fmaxf(a[9], a[10]), a[11]);
+                            const float l4 = fmaxf(fmaxf(a[12], a[13]), a[14]);
+                            const float mx = fmaxf(fmaxf(fmaxf(l0, l1), l2), fmaxf(fmaxf(l3, l4), a[15]));
+                            int pick = 15;
+#pragma unroll
+                            for (int r = 14; r >= 0; --r) pick = a[r] == mx ? r : pick;
+                            const bool better = theta[b] != INFINITY && mx > best_v[b];
+                            best_v[b] = better ? mx : best_v[b];
+                            best_sb[b] = better ? sb0 + tile_row(pick, half) : best_sb[b];
+                        }
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) {
+                            const int sb = sb0 + tile_row(r, half);
+#pragma unroll
+                            for (int b = 0; b < QB; ++b) {
+                                const bool better = sb < nsb && theta[b] != INFINITY && bacc[b][r] > best_v[b];
+                                best_v[b] = better ? bacc[b][r] : best_v[b];
+                                best_sb[b] = better ? sb : best_sb[b];
+                            }
                         }
                     }
                 }
